@@ -1,0 +1,133 @@
+/*
+ * ffn_oracle.c -- reference oracle for the activation-sparse gated FFN forward pass.
+ *
+ * TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.  Only the test suite, the smoke
+ * check and the benchmark's CPU-baseline leg load this file's library.  It shares
+ * no code, header, table or helper with the GPU library; it is deliberately plain
+ * and slow: fp64 arithmetic, straight ascending loops, no blocking, no SIMD.
+ *
+ * What it computes (paper: "Model casting & Low-parameter gating: towards more
+ * sparsely activated FFNs"):
+ *
+ *   Gated FFN, Section 3.1, Eq. (ffn):  y = W2 ( A(W1 x) (*) (W3 x) ),
+ *     with W1 = W_gate, W3 = W_up, W2 = W_down; W2 is passed transposed
+ *     (w_down_t[i][:] = column i of W2 = the output vector of hidden neuron i).
+ *   Activation A: shifted ReLU, A(h) = max(h - t, 0) (the "shifted ReLU" of the
+ *     activation ablation, Appendix M), so neuron i is active iff h_i > t.
+ *   Exploitable zeros, Section 3.1 ("FFN FLOP-ratio"): a zero of A(W1 x) is known
+ *     before W3 is applied, so the sparse method skips row i of W3 and column i
+ *     of W2 for every inactive i, while W1 x is always computed in full.
+ *   LoPA gating, Section 3.3, Eq. (lopaapprox): W1 = G + U V with U (H x r),
+ *     V (r x D).  This oracle implements the low-rank product only, h = U (V x),
+ *     with V = lopa_a [r][d] and U = lopa_b [d_ff][r]; the fixed term G is zero.
+ *   FLOP accounting, Section 3.1 Eq. (flops_ratio) and Section 3.3: the oracle
+ *     counts every multiply-add it executes, so that the count can be compared
+ *     with the paper's cost model: standard d*d_ff + 2|S|d, LoPA r(d + d_ff) + 2|S|d,
+ *     dense 3 d d_ff (LoPA dense: r(d + d_ff) + 2 d d_ff).
+ *
+ * Inputs are exactly the bit patterns the GPU receives: x is fp32, weights are
+ * fp32 (wdt = 0) or bfloat16 bit patterns (wdt = 1); both widen to double
+ * exactly.  t is the same fp32 value, widened.
+ */
+#include <stdint.h>
+#include <stddef.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* element k of a weight matrix, widened exactly to double */
+static double weight_at(const void* w, int wdt, size_t k) {
+  if (wdt == 0) return (double)((const float*)w)[k];
+  uint32_t bits = ((uint32_t)((const uint16_t*)w)[k]) << 16; /* bf16 = top half of an fp32 */
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return (double)f;
+}
+
+/* <row i of an [n][len] matrix, v>, ascending j, counting multiply-adds */
+static double row_dot(const void* w, int wdt, size_t i, int len, const double* v, int64_t* macs) {
+  double s = 0.0;
+  for (int j = 0; j < len; ++j) s += weight_at(w, wdt, i * (size_t)len + (size_t)j) * v[j];
+  *macs += len;
+  return s;
+}
+
+/*
+ * oracle_ffn -- one FFN forward pass per token, tokens independent.
+ *
+ *   gating        0: standard, h = W_gate x          (w_gate [d_ff][d])
+ *                 1: LoPA,     h = B (A x)           (lopa_a [r][d], lopa_b [d_ff][r])
+ *   skip_inactive 1: the sparse method (inactive neurons' W_up rows and W_down
+ *                    columns are never read)
+ *                 0: the dense FFN (every neuron evaluated, inactive ones weigh 0)
+ *   wdt           weight storage: 0 = fp32, 1 = bf16 bit patterns
+ *   x             [T][d] fp32
+ *   t             activation threshold (shift of the ReLU)
+ * Outputs (any may be NULL):
+ *   h_out         [T][d_ff] gate pre-activations, fp64
+ *   z_out         [T][r] LoPA intermediate V x, fp64 (LoPA only)
+ *   active_out    [T][d_ff] 1 if h > t else 0
+ *   y_out         [T][d] fp64
+ *   macs_out      [T] multiply-adds executed for that token
+ * Returns 0, or -1 on a bad argument.
+ */
+int oracle_ffn(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
+               const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
+               const void* w_up, const void* w_down_t, float t,
+               double* h_out, double* z_out, uint8_t* active_out, double* y_out, int64_t* macs_out) {
+  if (T < 1 || d < 1 || d_ff < 1 || (wdt != 0 && wdt != 1) || !x || !w_up || !w_down_t) return -1;
+  if (gating == 0 && !w_gate) return -1;
+  if (gating == 1 && (r < 1 || !lopa_a || !lopa_b)) return -1;
+  if (gating != 0 && gating != 1) return -1;
+
+  const double tt = (double)t;
+  int zlen = gating == 1 ? r : 1;
+
+  /* per-call scratch; the oracle is not a hot path */
+  double* xv = (double*)malloc(sizeof(double) * (size_t)d);
+  double* zv = (double*)malloc(sizeof(double) * (size_t)zlen);
+  if (!xv || !zv) {
+    free(xv);
+    free(zv);
+    return -1;
+  }
+
+  for (int tok = 0; tok < T; ++tok) {
+    int64_t macs = 0;
+    for (int j = 0; j < d; ++j) xv[j] = (double)x[(size_t)tok * d + j];
+
+    /* LoPA: the low-rank intermediate z = V x = A x */
+    if (gating == 1) {
+      for (int k = 0; k < r; ++k) zv[k] = row_dot(lopa_a, wdt, (size_t)k, d, xv, &macs);
+      if (z_out)
+        for (int k = 0; k < r; ++k) z_out[(size_t)tok * r + k] = zv[k];
+    }
+
+    double* y = y_out ? y_out + (size_t)tok * d : NULL;
+    if (y)
+      for (int j = 0; j < d; ++j) y[j] = 0.0;
+
+    for (int i = 0; i < d_ff; ++i) {
+      /* gate pre-activation, computed for every neuron */
+      double h = gating == 0 ? row_dot(w_gate, wdt, (size_t)i, d, xv, &macs)
+                             : row_dot(lopa_b, wdt, (size_t)i, r, zv, &macs);
+      int active = h > tt; /* strict: A(h) = max(h - t, 0) is 0 at h == t; NaN is inactive */
+      if (h_out) h_out[(size_t)tok * d_ff + i] = h;
+      if (active_out) active_out[(size_t)tok * d_ff + i] = (uint8_t)active;
+      if (skip_inactive && !active) continue;
+
+      double a = active ? h - tt : 0.0;                  /* A(W1 x)_i */
+      double v = row_dot(w_up, wdt, (size_t)i, d, xv, &macs); /* (W3 x)_i */
+      double zi = a * v;
+      /* y += zi * (column i of W2) = zi * w_down_t[i][:] */
+      for (int j = 0; j < d; ++j) {
+        double wd = weight_at(w_down_t, wdt, (size_t)i * d + (size_t)j);
+        if (y) y[j] += zi * wd;
+      }
+      macs += d;
+    }
+    if (macs_out) macs_out[tok] = macs;
+  }
+  free(xv);
+  free(zv);
+  return 0;
+}

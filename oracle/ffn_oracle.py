@@ -1,0 +1,119 @@
+"""Python front end of the reference oracle (test infrastructure, not product).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this module.  It builds ``ffn_oracle.c`` with gcc into
+``oracle/_build/`` and calls it through ctypes.  Nothing here is shared with the
+GPU library: no headers, no helpers, no constants.
+
+The computation (gated FFN of Section 3.1, Eq. (ffn); shifted-ReLU activation;
+skipping of inactive neurons per Section 3.1 "FFN FLOP-ratio"; LoPA gate
+h = U (V x) of Section 3.3, Eq. (lopaapprox)) is documented in ``ffn_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ffn_oracle.c")
+_BUILD = os.path.join(_HERE, "_build")
+_LIB_PATH = os.path.join(_BUILD, "libffn_oracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain -O2, no fast-math, no FMA contraction)."""
+    os.makedirs(_BUILD, exist_ok=True)
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
+                               "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB_PATH)
+        vp = ctypes.c_void_p
+        lib.oracle_ffn.restype = ctypes.c_int
+        lib.oracle_ffn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                   ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_float,
+                                   vp, vp, vp, vp, vp]
+        _lib = lib
+    return _lib
+
+
+@dataclass
+class OracleResult:
+    h: np.ndarray        # [T, d_ff] fp64 gate pre-activations
+    active: np.ndarray   # [T, d_ff] bool, h > t
+    y: np.ndarray        # [T, d] fp64
+    macs: np.ndarray     # [T] int64 multiply-adds executed
+    z: np.ndarray | None  # [T, r] fp64 (LoPA only)
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _weights(w, wdt):
+    if w is None:
+        return None
+    want = np.float32 if wdt == 0 else np.uint16
+    w = np.ascontiguousarray(w)
+    if w.dtype != want:
+        raise TypeError(f"weights must be {want.__name__} for wdt={wdt}, got {w.dtype}")
+    return w
+
+
+def ffn(x, *, w_up, w_down_t, t, wdt, w_gate=None, lopa_a=None, lopa_b=None,
+        skip_inactive=True) -> OracleResult:
+    """Run the oracle on every token of ``x`` ([T, d] float32).
+
+    Weights: float32 arrays (wdt=0) or uint16 arrays holding bfloat16 bit patterns
+    (wdt=1), row-major: w_gate/w_up/w_down_t [d_ff, d], lopa_a [r, d], lopa_b [d_ff, r].
+    Exactly one of ``w_gate`` (standard gating) or ``lopa_a``+``lopa_b`` (LoPA) is given.
+    ``skip_inactive`` selects the sparse method (True) or the dense FFN (False).
+    """
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    T, d = x.shape
+    w_up = _weights(w_up, wdt)
+    w_down_t = _weights(w_down_t, wdt)
+    d_ff = w_up.shape[0]
+    lopa = lopa_a is not None
+    if lopa == (w_gate is not None):
+        raise ValueError("give exactly one of w_gate or (lopa_a, lopa_b)")
+    w_gate = _weights(w_gate, wdt)
+    lopa_a = _weights(lopa_a, wdt)
+    lopa_b = _weights(lopa_b, wdt)
+    r = lopa_a.shape[0] if lopa else 0
+    if w_up.shape != (d_ff, d) or w_down_t.shape != (d_ff, d):
+        raise ValueError("w_up and w_down_t must be [d_ff, d]")
+    if not lopa and w_gate.shape != (d_ff, d):
+        raise ValueError("w_gate must be [d_ff, d]")
+    if lopa and (lopa_a.shape != (r, d) or lopa_b.shape != (d_ff, r)):
+        raise ValueError("lopa_a must be [r, d] and lopa_b [d_ff, r]")
+
+    h = np.empty((T, d_ff), np.float64)
+    act = np.empty((T, d_ff), np.uint8)
+    y = np.empty((T, d), np.float64)
+    macs = np.empty((T,), np.int64)
+    z = np.empty((T, r), np.float64) if lopa else None
+    rc = lib.oracle_ffn(1 if lopa else 0, 1 if skip_inactive else 0, wdt, T, d, d_ff, r,
+                        _ptr(x), _ptr(w_gate), _ptr(lopa_a), _ptr(lopa_b), _ptr(w_up), _ptr(w_down_t),
+                        ctypes.c_float(np.float32(t)), _ptr(h), _ptr(z), _ptr(act), _ptr(y), _ptr(macs))
+    if rc != 0:
+        raise ValueError(f"oracle_ffn rejected its arguments (rc={rc})")
+    return OracleResult(h=h, active=act.astype(bool), y=y, macs=macs, z=z)

@@ -1,0 +1,143 @@
+"""Seeded synthetic inputs for the sparse-FFN kernels and for their oracle.
+
+This module holds no FFN arithmetic: it only draws Gaussian tensors, encodes them
+as fp32 or bfloat16 bit patterns and names the workload shapes.  Both the GPU
+tests/benchmark and the CPU oracle take their inputs from here, so the two sides
+see bit-identical data.
+
+Recipe (per weight set, ``seed``):
+  numpy ``SeedSequence(seed).spawn(5)`` -> one PCG64 stream per tensor, in the order
+  x, (W_gate | A), B, W_up, W_down^T.  Values are float32 standard normals scaled by
+  the standard deviation below, then (bf16 weights) rounded to nearest-even bf16.
+    x        [T, d]      N(0, 1)
+    W_gate   [d_ff, d]   N(0, 1/d)       standard gating
+    A        [r, d]      N(0, 1/d)       LoPA V factor
+    B        [d_ff, r]   N(0, 1/r)       LoPA U factor
+    W_up     [d_ff, d]   N(0, 1/d)
+    W_down^T [d_ff, d]   N(0, 1/d_ff)    (row i = output vector of neuron i)
+With these scales every gate pre-activation is close to N(0, 1), so the threshold
+t = Phi^-1(s) gives sparsity s: 0, 0.8416, 1.2816, 1.6449 for 50/80/90/95%.
+The paper timed trained checkpoints, which are not available; these Gaussian
+weights reproduce the sparsity level but not the correlation of real masks, so
+the batched union here is the iid worst case.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+F32 = 0
+BF16 = 1
+
+# activation thresholds for a target sparsity under N(0, 1) gate pre-activations
+THRESHOLD = {0.50: 0.0, 0.80: 0.8416, 0.90: 1.2816, 0.95: 1.6449}
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round finite float32 values to the nearest bfloat16 (ties to even); returns uint16 bits."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Exact widening of bfloat16 bit patterns to float32."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
+    a = rng.standard_normal(size=shape, dtype=np.float32)
+    a *= np.float32(std)
+    return a
+
+
+def _encode(a: np.ndarray, wdt: int) -> np.ndarray:
+    return a if wdt == F32 else f32_to_bf16_bits(a)
+
+
+@dataclass
+class FFNInputs:
+    x: np.ndarray                  # [T, d] float32
+    w_up: np.ndarray               # [d_ff, d] float32 or uint16 (bf16 bits)
+    w_down_t: np.ndarray           # [d_ff, d]
+    w_gate: np.ndarray | None = None   # [d_ff, d] (standard gating)
+    lopa_a: np.ndarray | None = None   # [r, d] (LoPA)
+    lopa_b: np.ndarray | None = None   # [d_ff, r] (LoPA)
+    wdt: int = BF16
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def T(self):
+        return self.x.shape[0]
+
+    @property
+    def d(self):
+        return self.x.shape[1]
+
+    @property
+    def d_ff(self):
+        return self.w_up.shape[0]
+
+    @property
+    def r(self):
+        return 0 if self.lopa_a is None else self.lopa_a.shape[0]
+
+
+def make_inputs(seed: int, T: int, d: int, d_ff: int, *, r: int = 0, wdt: int = BF16) -> FFNInputs:
+    """One weight set plus T input tokens; r > 0 selects LoPA factors instead of W_gate."""
+    s_x, s_g, s_b, s_u, s_d = (np.random.Generator(np.random.PCG64(s))
+                               for s in np.random.SeedSequence(seed).spawn(5))
+    x = _normal(s_x, (T, d), 1.0)
+    if r > 0:
+        lopa_a = _encode(_normal(s_g, (r, d), d ** -0.5), wdt)
+        lopa_b = _encode(_normal(s_b, (d_ff, r), r ** -0.5), wdt)
+        w_gate = None
+    else:
+        w_gate = _encode(_normal(s_g, (d_ff, d), d ** -0.5), wdt)
+        lopa_a = lopa_b = None
+    w_up = _encode(_normal(s_u, (d_ff, d), d ** -0.5), wdt)
+    w_down_t = _encode(_normal(s_d, (d_ff, d), d_ff ** -0.5), wdt)
+    return FFNInputs(x=x, w_up=w_up, w_down_t=w_down_t, w_gate=w_gate, lopa_a=lopa_a, lopa_b=lopa_b,
+                     wdt=wdt, meta=dict(seed=seed))
+
+
+def make_tokens(seed: int, T: int, d: int) -> np.ndarray:
+    """A separate pool of iid N(0, 1) tokens [T, d] (its own stream, independent of weights)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0x70C3])))
+    return _normal(rng, (T, d), 1.0)
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    d: int
+    d_ff: int
+    r: int            # 0 = standard gating
+    T: int
+    wdt: int
+    t: float
+    seed: int
+    n_sets: int
+
+
+# The five workload families; every (sparsity, T) point is its own entry.
+def workloads() -> list[Workload]:
+    out = [Workload("tiny_f32_std_s90", 256, 1024, 0, 1, F32, THRESHOLD[0.90], 0, 1)]
+    for s in (0.50, 0.80, 0.90, 0.95):
+        out.append(Workload(f"8b_std_s{int(s * 100)}", 4096, 14336, 0, 1, BF16, THRESHOLD[s], 1000, 4))
+    for s in (0.90, 0.95):
+        out.append(Workload(f"8b_lopa512_s{int(s * 100)}", 4096, 14336, 512, 1, BF16, THRESHOLD[s], 2000, 4))
+    for T in (1, 4, 16, 64):
+        out.append(Workload(f"8b_lopa512_s90_T{T}", 4096, 14336, 512, T, BF16, THRESHOLD[0.90], 3000, 4))
+    for T in (1, 8):
+        out.append(Workload(f"70b_std_s90_T{T}", 8192, 28672, 0, T, BF16, THRESHOLD[0.90], 4000, 2))
+        out.append(Workload(f"70b_lopa1024_s90_T{T}", 8192, 28672, 1024, T, BF16, THRESHOLD[0.90], 5000, 2))
+    return out
+
+
+def workload(name: str) -> Workload:
+    for w in workloads():
+        if w.name == name:
+            return w
+    raise KeyError(name)

@@ -1,0 +1,306 @@
+"""Pins of the reference oracle to facts outside itself (CPU only).
+
+Each test checks the oracle against something it does not compute itself: a result
+worked out by hand, a library routine (BLAS matrix products), an algebraic identity
+of the method, or a number printed in the paper.  Together they catch a dropped
+term, a wrong sign, a wrong index or a transposed operand anywhere in it.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ffn_oracle, flop_model
+from paper_2609_31975_amd import workloads as wl
+
+GOLDEN = __file__.replace("test_oracle.py", "golden/flop_model_printed.txt")
+
+
+def _widen(w, wdt):
+    return (w if wdt == wl.F32 else wl.bf16_bits_to_f32(w)).astype(np.float64)
+
+
+def _enc(a, wdt):
+    a = np.asarray(a, np.float32)
+    return a if wdt == wl.F32 else wl.f32_to_bf16_bits(a)
+
+
+# ---------------------------------------------------------------- worked examples
+# Hand-built gated FFN, d=4, d_ff=6 (all values exact in fp32 and bf16).
+#   x = (1, -2, 3, 0.5);  gate rows e0, -e1, e2, e3, -e0, 2e2  ->  h = (1, 2, 3, 0.5, -1, 6)
+#   t = 1: active = {1, 2, 5}; neuron 0 sits exactly on the threshold and is inactive.
+#   a = h - t = (1, 2, 5) on {1, 2, 5};  up rows 1: e3, 2: e0+e1, 5: 2e2 -> v = (0.5, -1, 6)
+#   a*v = (0.5, -2, 30);  down rows 1: e0, 2: e1+e2, 5: 0.5 e3
+#   y = 0.5 e0 - 2 (e1 + e2) + 15 e3 = (0.5, -2, -2, 15);  MACs = 6*4 + 2*3*4 = 48.
+# Inactive rows of W_up / W_down^T hold NaN: the sparse method never reads them.
+NAN = float("nan")
+
+
+def _worked_standard():
+    x = np.array([[1, -2, 3, 0.5]], np.float32)
+    g = np.array([[1, 0, 0, 0], [0, -1, 0, 0], [0, 0, 1, 0], [0, 0, 0, 1], [-1, 0, 0, 0], [0, 0, 2, 0]])
+    up = np.full((6, 4), NAN)
+    up[1] = [0, 0, 0, 1]
+    up[2] = [1, 1, 0, 0]
+    up[5] = [0, 0, 2, 0]
+    dn = np.full((6, 4), NAN)
+    dn[1] = [1, 0, 0, 0]
+    dn[2] = [0, 1, 1, 0]
+    dn[5] = [0, 0, 0, 0.5]
+    return x, g, up, dn
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_worked_example_standard(wdt):
+    x, g, up, dn = _worked_standard()
+    res = ffn_oracle.ffn(x, w_gate=_enc(g, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt), t=1.0, wdt=wdt)
+    assert res.h.tolist() == [[1, 2, 3, 0.5, -1, 6]]
+    assert np.flatnonzero(res.active[0]).tolist() == [1, 2, 5]
+    assert res.y.tolist() == [[0.5, -2, -2, 15]]
+    assert res.macs.tolist() == [48]
+
+
+# LoPA, d=4, d_ff=6, r=2:  A rows e0, e2 -> z = (1, 3)
+#   B rows (1,0), (0,1), (1,1), (-1,0), (.5,.5), (2,-1) -> h = (1, 3, 4, -1, 2, -1)
+#   t = 1.5: active = {1, 2, 4}, a = (1.5, 2.5, 0.5)
+#   up rows 1: e0, 2: e1, 4: e2+e3 -> v = (1, -2, 3.5);  a*v = (1.5, -5, 1.75)
+#   down rows 1: 2e3, 2: e0, 4: 4e1 -> y = (-5, 7, 0, 3);  MACs = 2*4 + 6*2 + 2*3*4 = 44.
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_worked_example_lopa(wdt):
+    x = np.array([[1, -2, 3, 0.5]], np.float32)
+    A = np.array([[1, 0, 0, 0], [0, 0, 1, 0]])
+    B = np.array([[1, 0], [0, 1], [1, 1], [-1, 0], [0.5, 0.5], [2, -1]])
+    up = np.full((6, 4), NAN)
+    up[1] = [1, 0, 0, 0]
+    up[2] = [0, 1, 0, 0]
+    up[4] = [0, 0, 1, 1]
+    dn = np.full((6, 4), NAN)
+    dn[1] = [0, 0, 0, 2]
+    dn[2] = [1, 0, 0, 0]
+    dn[4] = [0, 4, 0, 0]
+    res = ffn_oracle.ffn(x, lopa_a=_enc(A, wdt), lopa_b=_enc(B, wdt), w_up=_enc(up, wdt),
+                         w_down_t=_enc(dn, wdt), t=1.5, wdt=wdt)
+    assert res.z.tolist() == [[1, 3]]
+    assert res.h.tolist() == [[1, 3, 4, -1, 2, -1]]
+    assert np.flatnonzero(res.active[0]).tolist() == [1, 2, 4]
+    assert res.y.tolist() == [[-5, 7, 0, 3]]
+    assert res.macs.tolist() == [44]
+
+
+# ---------------------------------------------------------------- library routine
+SHAPES = [(3, 24, 80, 0), (2, 40, 56, 8), (1, 17, 33, 0), (2, 17, 33, 5)]
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("T,d,d_ff,r", SHAPES)
+def test_dense_matches_blas(wdt, T, d, d_ff, r):
+    """Dense FFN y = W2 (relu(W1 x - t) * (W3 x)) against numpy fp64 matrix products."""
+    inp = wl.make_inputs(7, T, d, d_ff, r=r, wdt=wdt)
+    t = 0.3
+    kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    res = ffn_oracle.ffn(inp.x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wdt, skip_inactive=False, **kw)
+    X = inp.x.astype(np.float64).T                      # [d, T] column vectors
+    if r == 0:
+        H = _widen(inp.w_gate, wdt) @ X                 # [d_ff, T]
+    else:
+        Z = _widen(inp.lopa_a, wdt) @ X                 # [r, T]
+        np.testing.assert_allclose(res.z, Z.T, rtol=1e-12, atol=1e-13)
+        H = _widen(inp.lopa_b, wdt) @ Z
+    V = _widen(inp.w_up, wdt) @ X
+    W2 = _widen(inp.w_down_t, wdt).T                    # [d, d_ff]
+    Y = W2 @ (np.maximum(H - np.float64(np.float32(t)), 0.0) * V)
+    np.testing.assert_allclose(res.h, H.T, rtol=1e-12, atol=1e-13)
+    assert (res.active == (H.T > np.float32(t))).all()
+    np.testing.assert_allclose(res.y, Y.T, rtol=1e-11, atol=1e-13)
+    assert (res.active.sum(1) > 0).all() and (~res.active).sum() > 0
+
+
+# ---------------------------------------------------------------- identities of the method
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("T,d,d_ff,r", SHAPES)
+def test_sparse_equals_dense(wdt, T, d, d_ff, r):
+    """Skipping inactive neurons changes no output bit (Section 3.1): their terms are exact zeros."""
+    inp = wl.make_inputs(11, T, d, d_ff, r=r, wdt=wdt)
+    kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    common = dict(w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.5, wdt=wdt, **kw)
+    sp = ffn_oracle.ffn(inp.x, skip_inactive=True, **common)
+    de = ffn_oracle.ffn(inp.x, skip_inactive=False, **common)
+    assert np.array_equal(sp.h, de.h) and np.array_equal(sp.active, de.active)
+    assert np.array_equal(sp.y + 0.0, de.y + 0.0)
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_sparse_never_reads_inactive_rows(wdt):
+    """Poison inactive rows of W_up and W_down^T with NaN: the sparse result is unchanged, the dense is NaN."""
+    inp = wl.make_inputs(12, 1, 32, 96, wdt=wdt)
+    t = 1.0
+    clean = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wdt)
+    off = ~clean.active[0]
+    nan_bits = np.float32(np.nan) if wdt == wl.F32 else np.uint16(0x7FC0)
+    up, dn = inp.w_up.copy(), inp.w_down_t.copy()
+    up[off] = nan_bits
+    dn[off] = nan_bits
+    pois = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=up, w_down_t=dn, t=t, wdt=wdt)
+    assert np.array_equal(pois.y, clean.y)
+    dense = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=up, w_down_t=dn, t=t, wdt=wdt, skip_inactive=False)
+    assert np.isnan(dense.y).all()
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_lopa_with_identity_factor_is_standard_gating(wdt):
+    """LoPA with r = d, A = I and B = W_gate is standard gating, bit for bit (Eq. lopaapprox with G = 0)."""
+    inp = wl.make_inputs(13, 2, 48, 120, wdt=wdt)
+    eye = _enc(np.eye(48), wdt)
+    common = dict(w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.8, wdt=wdt)
+    std = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, **common)
+    lop = ffn_oracle.ffn(inp.x, lopa_a=eye, lopa_b=inp.w_gate, **common)
+    assert np.array_equal(lop.z, inp.x.astype(np.float64))
+    assert np.array_equal(lop.h, std.h) and np.array_equal(lop.active, std.active)
+    assert np.array_equal(lop.y, std.y)
+    d, d_ff = 48, 120
+    assert (lop.macs - std.macs).tolist() == [d * d] * 2      # the extra A x product
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_lopa_signed_permutation(wdt):
+    """A = signed permutation P, B = W_gate P^T (exact in any format): same gate up to summation order."""
+    d, d_ff = 40, 100
+    inp = wl.make_inputs(14, 3, d, d_ff, wdt=wdt)
+    rng = np.random.default_rng(5)
+    perm = rng.permutation(d)
+    sign = rng.choice([-1.0, 1.0], d)
+    P = np.zeros((d, d))
+    P[np.arange(d), perm] = sign                    # (P x)_k = sign_k x_perm(k)
+    Wg = _widen(inp.w_gate, wdt)
+    B = Wg @ P.T                                    # exact: a column permutation with sign flips
+    common = dict(w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.7, wdt=wdt)
+    std = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, **common)
+    lop = ffn_oracle.ffn(inp.x, lopa_a=_enc(P, wdt), lopa_b=_enc(B, wdt), **common)
+    np.testing.assert_allclose(lop.h, std.h, rtol=1e-13, atol=1e-14)
+    assert np.array_equal(lop.active, std.active)
+    np.testing.assert_allclose(lop.y, std.y, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_tokens_are_independent(wdt):
+    inp = wl.make_inputs(15, 4, 24, 64, r=6, wdt=wdt)
+    common = dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b, w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.2, wdt=wdt)
+    batch = ffn_oracle.ffn(inp.x, **common)
+    for k in range(4):
+        one = ffn_oracle.ffn(inp.x[k:k + 1], **common)
+        assert np.array_equal(one.y[0], batch.y[k]) and np.array_equal(one.h[0], batch.h[k])
+
+
+def test_degenerate_thresholds():
+    inp = wl.make_inputs(16, 2, 32, 64, wdt=wl.BF16)
+    common = dict(w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=inp.w_down_t, wdt=wl.BF16)
+    none = ffn_oracle.ffn(inp.x, t=1e30, **common)             # nothing active
+    assert not none.active.any() and (none.y == 0).all()
+    assert none.macs.tolist() == [32 * 64] * 2
+    every = ffn_oracle.ffn(inp.x, t=-100.0, **common)          # everything active
+    dense = ffn_oracle.ffn(inp.x, t=-100.0, skip_inactive=False, **common)
+    assert every.active.all() and np.array_equal(every.y, dense.y)
+    assert every.macs.tolist() == [3 * 32 * 64] * 2
+
+
+def test_nan_gate_is_inactive():
+    inp = wl.make_inputs(17, 1, 16, 8, wdt=wl.F32)
+    g = inp.w_gate.copy()
+    g[3, 0] = np.nan
+    res = ffn_oracle.ffn(inp.x, w_gate=g, w_up=inp.w_up, w_down_t=inp.w_down_t, t=-100.0, wdt=wl.F32)
+    assert np.isnan(res.h[0, 3]) and not res.active[0, 3] and res.active[0].sum() == 7
+    assert np.isfinite(res.y).all()
+
+
+# ---------------------------------------------------------------- cost model
+@pytest.mark.parametrize("r", [0, 8])
+def test_mac_counter_matches_cost_model(r):
+    T, d, d_ff = 3, 64, 160
+    inp = wl.make_inputs(18, T, d, d_ff, r=r, wdt=wl.BF16)
+    kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    for t in (-100.0, 0.0, 1.2816, 1e30):
+        sp = ffn_oracle.ffn(inp.x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wl.BF16, **kw)
+        de = ffn_oracle.ffn(inp.x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wl.BF16,
+                            skip_inactive=False, **kw)
+        n = sp.active.sum(1)
+        if r == 0:
+            want = [flop_model.standard_cost(d, d_ff, k) for k in n]
+            assert de.macs.tolist() == [flop_model.dense_cost(d, d_ff)] * T
+        else:
+            want = [flop_model.lopa_cost(d, d_ff, r, k) for k in n]
+            assert de.macs.tolist() == [flop_model.lopa_cost(d, d_ff, r, d_ff)] * T
+        assert sp.macs.tolist() == want
+        if r == 0:   # the ratio follows Eq. (flops_ratio) at the realized sparsity
+            for k, m in zip(n, sp.macs):
+                s = 1 - k / d_ff
+                assert math.isclose(flop_model.dense_cost(d, d_ff) / m, flop_model.flop_ratio_standard(s))
+
+
+def _printed_rows():
+    rows = []
+    for line in open(GOLDEN):
+        if line.startswith("#") or not line.strip():
+            continue
+        f = line.split()
+        rows.append(dict(kind=f[0], D=int(f[1]), H=int(f[2]), alpha=None if f[3] == "-" else float(f[3]),
+                         s=float(f[4]), hw=float(f[5]), printed=float(f[6]), strict=f[7] == "1",
+                         source=" ".join(f[8:])))
+    return rows
+
+
+@pytest.mark.parametrize("row", _printed_rows(), ids=lambda r: f"{r['kind']}-{r['s']}-{r['printed']}")
+def test_printed_flop_ratios(row):
+    def model(s):
+        if row["kind"] == "std":
+            return flop_model.flop_ratio_standard(s)
+        if row["kind"] == "lopa":
+            return flop_model.flop_ratio_lopa_cast(row["D"], row["H"], row["alpha"], s)
+        return flop_model.flop_ratio_arch_cast(row["D"], row["H"], row["alpha"] * row["D"], s)
+
+    lo, hi = model(row["s"] - row["hw"]), model(min(1.0, row["s"] + row["hw"]))
+    p = row["printed"]
+    if row["strict"]:
+        assert lo - 0.005 <= p <= hi + 0.005, (lo, hi, p)
+    else:
+        assert min(abs(p - lo), abs(p - hi)) / p < 0.01 or lo <= p <= hi, (lo, hi, p)
+
+
+def test_lopa_ratio_identities():
+    # Section 3.3: at H/D = 8/3 the LoPA numerator equals 3HD (parameter-count matching)
+    D, H = 3840.0, 10240.0
+    r = D / 8
+    Hp = flop_model.lopa_hidden_dim(D, H, r)
+    assert math.isclose(r * (D + Hp) + 2 * D * Hp, 3 * H * D, rel_tol=1e-12)
+    # closed form at alpha = 1/8, s -> 1: 136/10
+    assert math.isclose(flop_model.flop_ratio_lopa_cast(D, H, 0.125, 1.0), 13.6, rel_tol=1e-12)
+    # standard gating caps at 3 (Section 3.3 opening)
+    assert flop_model.flop_ratio_standard(1.0) == 3.0
+
+
+def test_printed_adapted_hidden_dim():
+    # Figure ffn_cost caption: D=2560, H=7168, r=400 gives H' = 9787
+    assert round(flop_model.lopa_hidden_dim(2560, 7168, 400)) == 9787
+
+
+# ---------------------------------------------------------------- inputs
+def test_bf16_encoding():
+    vals = np.array([1.0, -2.0, 0.5, 1.00390625, 1.01171875, 3.0e38, 1e-40], np.float32)
+    bits = wl.f32_to_bf16_bits(vals)
+    # 1 + 2^-8 is a tie -> even (1.0); 1 + 3*2^-8 is a tie -> even (1 + 2^-6)
+    assert bits.tolist() == [0x3F80, 0xC000, 0x3F00, 0x3F80, 0x3F82, 0x7F62, 0x0001]
+    assert np.array_equal(wl.bf16_bits_to_f32(bits[:3]), vals[:3])
+
+
+@pytest.mark.parametrize("r", [0, 32])
+def test_threshold_gives_target_sparsity(r):
+    """Gate pre-activations are ~N(0, sigma^2) with sigma^2 = |x|^2/d (standard) or |Ax|^2/r (LoPA)."""
+    d, d_ff = 256, 4096
+    inp = wl.make_inputs(19, 1, d, d_ff, r=r, wdt=wl.F32)
+    t = wl.THRESHOLD[0.90]
+    kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    res = ffn_oracle.ffn(inp.x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wl.F32, **kw)
+    sigma = math.sqrt(float((inp.x.astype(np.float64) ** 2).sum()) / d) if r == 0 else \
+        math.sqrt(float((res.z ** 2).sum()) / r)
+    p = 0.5 * math.erfc(t / sigma / math.sqrt(2))
+    n = int(res.active.sum())
+    assert abs(n - p * d_ff) < 4 * math.sqrt(d_ff * p * (1 - p)), (n, p * d_ff)
