@@ -1,0 +1,114 @@
+/*
+ * ffn_sparse.h -- C ABI of the MI355X (gfx950) activation-sparse FFN forward pass.
+ *
+ * Operation (paper: "Model casting & Low-parameter gating: towards more sparsely
+ * activated FFNs"):
+ *   Gated FFN, Section 3.1 Eq. (ffn):  y = W2 ( A(W1 x) (*) (W3 x) )
+ *   with the shifted ReLU A(h) = max(h - t, 0) (Appendix M), so hidden neuron i is
+ *   active iff h_i > t.  A zero of A(W1 x) is known before W3 is applied
+ *   (Section 3.1, "FFN FLOP-ratio"), so the sparse method computes the gate h = W1 x
+ *   in full and then reads only the active neurons' rows of W3 and columns of W2:
+ *       y = sum over active i of (h_i - t) * <w_up[i], x> * w_down_t[i]
+ *   LoPA gating (Section 3.3, Eq. (lopaapprox)): W1 = G + U V; this library computes
+ *   the low-rank product h = B (A x), B = U [d_ff][r], A = V [r][d] (G = 0).
+ *   A batch of T tokens (Section 5.3) reads the rows of the union of the tokens'
+ *   active sets once; each token is still its own FFN pass (a neuron that is inactive
+ *   for a token contributes nothing to that token's output).
+ *
+ * Naming: W1 = w_gate, W3 = w_up, W2 = w_down (stored transposed, see layouts).
+ *
+ * Layouts (all row-major, all pointers are DEVICE pointers, 16-byte aligned):
+ *   x          [T][d]      fp32   input tokens
+ *   y          [T][d]      fp32   output; fully overwritten (never accumulated into)
+ *   w_gate     [d_ff][d]   weights (standard gating)
+ *   lopa_a     [r][d]      weights (LoPA V factor)
+ *   lopa_b     [d_ff][r]   weights (LoPA U factor)
+ *   w_up       [d_ff][d]   weights
+ *   w_down_t   [d_ff][d]   weights, W2 transposed: row i = output vector of neuron i
+ *   ws         workspace of at least ffn_workspace_bytes(...) bytes
+ * Weights are fp32 (FFN_F32) or bfloat16 (FFN_BF16, raw 16-bit patterns); x, y and
+ * every accumulation are fp32.  t is a host fp32 scalar.
+ *
+ * Ownership: the caller allocates and owns every buffer.  The forward calls never
+ * allocate, free or synchronize; they enqueue kernels on `stream` and return.  Calls
+ * that share a workspace must be ordered (same stream); distinct workspaces may run
+ * concurrently.  Results are deterministic: identical inputs give identical bits.
+ *
+ * Errors: arguments are checked on the host before anything is enqueued; on a
+ * negative return nothing was enqueued.  A launch failure returns FFN_ERR_HIP.
+ * Faults during execution surface at the caller's next synchronization of `stream`.
+ *
+ * Semantics of special values: a NaN gate value is inactive (h > t is false).
+ * Inf/NaN in the w_up / w_down_t rows of a neuron that is active for any token of
+ * the batch propagate into every token's output (the row is read for the union).
+ */
+#ifndef FFN_SPARSE_H
+#define FFN_SPARSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { FFN_F32 = 0, FFN_BF16 = 1 } ffn_dtype_t;
+
+enum {
+  FFN_OK = 0,
+  FFN_ERR_NULL = -1,      /* a required pointer is NULL */
+  FFN_ERR_SHAPE = -2,     /* T, d, d_ff < 1, or r < 1 for LoPA, or a size overflows int32 indexing */
+  FFN_ERR_DTYPE = -3,     /* weight dtype is not FFN_F32 / FFN_BF16 */
+  FFN_ERR_ALIGN = -4,     /* a pointer is not 16-byte aligned */
+  FFN_ERR_WORKSPACE = -5, /* ws_bytes < ffn_workspace_bytes(...) */
+  FFN_ERR_HIP = -6        /* a HIP launch failed */
+};
+
+/* Bytes of workspace the forward calls need for this shape (r = 0 for standard gating).
+ * Returns 0 for an invalid shape. */
+size_t ffn_workspace_bytes(int T, int d, int d_ff, int r);
+
+/* Dense gated FFN (Section 3.1 Eq. (ffn)) with standard gating: every neuron is
+ * evaluated.  The speedup baseline. */
+int ffn_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                      const void* w_up, const void* w_down_t, float t, float* y, void* ws,
+                      size_t ws_bytes, hipStream_t stream);
+
+/* Sparse method, standard gating: gate in full, then only active neurons' rows of
+ * w_up and w_down_t (Section 3.1). */
+int ffn_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                       const void* w_up, const void* w_down_t, float t, float* y, void* ws,
+                       size_t ws_bytes, hipStream_t stream);
+
+/* Sparse method, LoPA gating h = B (A x) (Section 3.3). */
+int ffn_lopa_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                            const void* lopa_a, const void* lopa_b, const void* w_up,
+                            const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* LoPA gating with every neuron evaluated (no skipping): a baseline. */
+int ffn_lopa_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                           const void* lopa_a, const void* lopa_b, const void* w_up,
+                           const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/* Inspection hook for tests and the benchmark (not on the hot path).  Synchronizes
+ * `stream`, then copies the active set of the last forward call made with this
+ * workspace and the same (T, d, d_ff, r) to host memory:
+ *   *n_union        number of neurons active for at least one token
+ *   idx_host        [d_ff] int32: those neurons, ascending (first *n_union entries)
+ *   act_host        [T][d_ff] fp32 (may be NULL): act_host[tau][k] = h - t of neuron
+ *                   idx_host[k] for token tau, or 0 where that token is inactive
+ * For a dense call every neuron is listed.  Returns FFN_OK or an error code. */
+int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
+                   float* act_host, hipStream_t stream);
+
+/* Human-readable text for a status code. */
+const char* ffn_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FFN_SPARSE_H */

@@ -1,0 +1,182 @@
+// Host side of the C ABI declared in include/ffn_sparse.h: argument checks,
+// workspace carve-up and kernel sequencing.  No allocation, no synchronization on the
+// forward path.
+#include <stdint.h>
+#include <string.h>
+
+#include <vector>
+
+#include "ffn_internal.h"
+#include "ffn_sparse.h"
+
+namespace ffn {
+
+namespace {
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxElems = (int64_t)1 << 31;  // kernels index rows with 32-bit chunk counts
+
+size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+}  // namespace
+
+size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out) {
+  (void)d;
+  Workspace w{};
+  w.nseg = (d_ff + kSeg - 1) / kSeg;
+  w.slots = w.nseg * kSeg;
+  w.tc = T < kTokChunk ? T : kTokChunk;
+  w.r = r;
+  size_t off = 0;
+  char* b = static_cast<char*>(base);
+  auto take = [&](size_t bytes) {
+    char* p = b ? b + off : nullptr;
+    off += round_up(bytes);
+    return p;
+  };
+  w.seg_count = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.nseg));
+  w.seg_idx = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.slots));
+  w.seg_act = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
+  w.seg_zval = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
+  w.z = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * (r > 0 ? r : 1)));
+  if (out) *out = w;
+  return off;
+}
+
+namespace {
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_shape(int T, int d, int d_ff, int r, bool lopa) {
+  if (T < 1 || d < 1 || d_ff < 1 || (lopa && r < 1)) return FFN_ERR_SHAPE;
+  if ((int64_t)d_ff * d >= kMaxElems || (int64_t)T * d >= kMaxElems) return FFN_ERR_SHAPE;
+  if (lopa && ((int64_t)r * d >= kMaxElems || (int64_t)d_ff * r >= kMaxElems)) return FFN_ERR_SHAPE;
+  // the down kernel keeps one prefix entry per segment in LDS
+  if (d_ff > (1 << 20)) return FFN_ERR_SHAPE;
+  return FFN_OK;
+}
+
+struct Call {
+  ffn_dtype_t wdt;
+  int T, d, d_ff, r;  // r = 0: standard gating
+  bool dense;
+  const float* x;
+  const void* gate;   // w_gate, or lopa_b for LoPA
+  const void* lopa_a;
+  const void* w_up;
+  const void* w_down_t;
+  float t;
+  float* y;
+  void* ws;
+  size_t ws_bytes;
+  hipStream_t stream;
+};
+
+int run(const Call& c) {
+  const bool lopa = c.r > 0;
+  if (!c.x || !c.gate || !c.w_up || !c.w_down_t || !c.y || !c.ws || (lopa && !c.lopa_a)) return FFN_ERR_NULL;
+  if (c.wdt != FFN_F32 && c.wdt != FFN_BF16) return FFN_ERR_DTYPE;
+  const int sc = check_shape(c.T, c.d, c.d_ff, c.r, lopa);
+  if (sc != FFN_OK) return sc;
+  if (!aligned(c.x) || !aligned(c.gate) || !aligned(c.w_up) || !aligned(c.w_down_t) || !aligned(c.y) ||
+      !aligned(c.ws) || (lopa && !aligned(c.lopa_a)))
+    return FFN_ERR_ALIGN;
+  Workspace ws;
+  if (c.ws_bytes < workspace_layout(c.T, c.d, c.d_ff, c.r, c.ws, &ws)) return FFN_ERR_WORKSPACE;
+
+  // tokens run in passes of up to kTokChunk; each pass is an independent FFN call
+  for (int t0 = 0; t0 < c.T; t0 += kTokChunk) {
+    Shape sh{c.T - t0 < kTokChunk ? c.T - t0 : kTokChunk, c.d, c.d_ff, c.r, c.wdt == FFN_BF16 ? 1 : 0};
+    const float* x = c.x + (size_t)t0 * c.d;
+    float* y = c.y + (size_t)t0 * c.d;
+    hipError_t e = hipSuccess;
+    if (lopa) e = launch_lopa_z(sh, x, c.lopa_a, ws, c.stream);
+    if (e == hipSuccess)
+      e = launch_gate_up(sh, lopa ? Gate::LoPA : Gate::Standard, c.dense, x, c.gate, c.w_up, c.t, ws, c.stream);
+    if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
+    if (e != hipSuccess) return FFN_ERR_HIP;
+  }
+  return FFN_OK;
+}
+
+}  // namespace
+}  // namespace ffn
+
+using ffn::Call;
+
+extern "C" {
+
+size_t ffn_workspace_bytes(int T, int d, int d_ff, int r) {
+  if (ffn::check_shape(T, d, d_ff, r, r > 0) != FFN_OK || r < 0) return 0;
+  return ffn::workspace_layout(T, d, d_ff, r, nullptr, nullptr);
+}
+
+int ffn_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                      const void* w_up, const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
+                      hipStream_t stream) {
+  return ffn::run(Call{wdt, T, d, d_ff, 0, true, x, w_gate, nullptr, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+}
+
+int ffn_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                       const void* w_up, const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+  return ffn::run(Call{wdt, T, d, d_ff, 0, false, x, w_gate, nullptr, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+}
+
+int ffn_lopa_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x, const void* lopa_a,
+                            const void* lopa_b, const void* w_up, const void* w_down_t, float t, float* y, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  if (r < 1) return FFN_ERR_SHAPE;
+  return ffn::run(Call{wdt, T, d, d_ff, r, false, x, lopa_b, lopa_a, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+}
+
+int ffn_lopa_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x, const void* lopa_a,
+                           const void* lopa_b, const void* w_up, const void* w_down_t, float t, float* y, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (r < 1) return FFN_ERR_SHAPE;
+  return ffn::run(Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+}
+
+int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
+                   float* act_host, hipStream_t stream) {
+  if (!ws || !n_union || !idx_host) return FFN_ERR_NULL;
+  if (r < 0 || ffn::check_shape(T, d, d_ff, r, r > 0) != FFN_OK || T > ffn::kTokChunk) return FFN_ERR_SHAPE;
+  ffn::Workspace w;
+  ffn::workspace_layout(T, d, d_ff, r, const_cast<void*>(ws), &w);
+  if (hipStreamSynchronize(stream) != hipSuccess) return FFN_ERR_HIP;
+  std::vector<int32_t> cnt(w.nseg), idx(w.slots);
+  std::vector<float> act;
+  if (hipMemcpy(cnt.data(), w.seg_count, sizeof(int32_t) * w.nseg, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(idx.data(), w.seg_idx, sizeof(int32_t) * w.slots, hipMemcpyDeviceToHost) != hipSuccess)
+    return FFN_ERR_HIP;
+  if (act_host) {
+    act.resize((size_t)T * w.slots);
+    if (hipMemcpy(act.data(), w.seg_act, sizeof(float) * act.size(), hipMemcpyDeviceToHost) != hipSuccess)
+      return FFN_ERR_HIP;
+  }
+  int n = 0;
+  for (int s = 0; s < w.nseg; ++s) {
+    if (cnt[s] < 0 || cnt[s] > ffn::kSeg) return FFN_ERR_HIP;  // workspace does not hold a finished call
+    for (int e = 0; e < cnt[s]; ++e) {
+      const int slot = s * ffn::kSeg + e;
+      if (act_host)
+        for (int tau = 0; tau < T; ++tau) act_host[(size_t)tau * d_ff + n] = act[(size_t)tau * w.slots + slot];
+      idx_host[n++] = idx[slot];
+    }
+  }
+  *n_union = n;
+  return FFN_OK;
+}
+
+const char* ffn_status_string(int status) {
+  switch (status) {
+    case FFN_OK: return "ok";
+    case FFN_ERR_NULL: return "null pointer argument";
+    case FFN_ERR_SHAPE: return "invalid shape";
+    case FFN_ERR_DTYPE: return "invalid weight dtype";
+    case FFN_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case FFN_ERR_WORKSPACE: return "workspace too small";
+    case FFN_ERR_HIP: return "HIP launch or copy failed";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,50 @@
+// Internal declarations shared by the kernels and the host dispatcher of the
+// sparse-FFN library (gfx950).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ffn {
+
+constexpr int kWave = 64;
+constexpr int kSeg = 32;          // gate rows per workgroup = one compaction segment
+constexpr int kBlock = 256;       // threads per workgroup for every kernel
+constexpr int kTokChunk = 64;     // tokens per pass; a larger batch runs as several passes
+constexpr int kListWindow = 1024; // active entries staged in LDS at a time by the down kernel
+
+// Workspace carve-up for one pass of up to `tc` tokens.  Every region starts on a
+// 256-byte boundary.  "slots" = nseg * kSeg: slot s*kSeg + e holds the e-th active
+// neuron (ascending) of segment s, for e < seg_count[s].
+struct Workspace {
+  int nseg;
+  int slots;
+  int tc;
+  int r;
+  int32_t* seg_count;  // [nseg]
+  int32_t* seg_idx;    // [slots]          neuron index
+  float* seg_act;      // [tc][slots]      h - t for the token, 0 where inactive
+  float* seg_zval;     // [tc][slots]      act * <w_up[i], x_tau>
+  float* z;            // [tc][r]          LoPA intermediate A x (LoPA only)
+};
+
+size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out);
+
+// Kernel launch parameters decided on the host.
+struct Shape {
+  int T, d, d_ff, r;
+  int wdt;  // 0 fp32, 1 bf16
+};
+
+enum class Gate { Standard, LoPA };
+
+// Launchers (return hipSuccess or the launch error).  Every launcher enqueues on `s`.
+hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
+                         hipStream_t s);
+hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w,
+                          const void* w_up, float t, const Workspace& ws, hipStream_t s);
+hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
+                       hipStream_t s);
+
+}  // namespace ffn

@@ -1,0 +1,163 @@
+"""Thin ctypes binding of ``include/ffn_sparse.h`` (argument marshalling only).
+
+Every function takes torch device tensors, checks nothing the library does not
+check itself beyond dtype/shape bookkeeping, and passes raw device pointers plus
+the current HIP stream to the C ABI.  All arithmetic runs in the gfx950 kernels of
+``libffn_sparse.so``; there is no fallback: if the library is missing this module
+raises on first use.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libffn_sparse.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "ffn_sparse.h")
+
+FFN_F32 = 0
+FFN_BF16 = 1
+
+STATUS = {0: "FFN_OK", -1: "FFN_ERR_NULL", -2: "FFN_ERR_SHAPE", -3: "FFN_ERR_DTYPE", -4: "FFN_ERR_ALIGN",
+          -5: "FFN_ERR_WORKSPACE", -6: "FFN_ERR_HIP"}
+
+
+class FFNError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} failed: {STATUS.get(code, code)}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2609_31975_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        i, f, vp, sz = ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+        L.ffn_workspace_bytes.restype = sz
+        L.ffn_workspace_bytes.argtypes = [i, i, i, i]
+        std = [i, i, i, i, vp, vp, vp, vp, f, vp, vp, sz, vp]
+        lop = [i, i, i, i, i, vp, vp, vp, vp, vp, f, vp, vp, sz, vp]
+        for name, args in (("ffn_dense_forward", std), ("ffn_sparse_forward", std),
+                           ("ffn_lopa_sparse_forward", lop), ("ffn_lopa_dense_forward", lop)):
+            getattr(L, name).restype = i
+            getattr(L, name).argtypes = args
+        L.ffn_active_set.restype = i
+        L.ffn_active_set.argtypes = [vp, i, i, i, i, vp, vp, vp, vp]
+        L.ffn_status_string.restype = ctypes.c_char_p
+        L.ffn_status_string.argtypes = [i]
+        _lib = L
+    return _lib
+
+
+def declared_functions() -> list[str]:
+    """Names of the functions the public header declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+[\s*]+(ffn_\w+)\s*\(", text, re.M)))
+
+
+# ---------------------------------------------------------------- marshalling helpers
+def _torch():
+    import torch
+    return torch
+
+
+def weight_dtype(w) -> int:
+    torch = _torch()
+    if w.dtype == torch.bfloat16:
+        return FFN_BF16
+    if w.dtype == torch.float32:
+        return FFN_F32
+    raise TypeError(f"weights must be bfloat16 or float32, got {w.dtype}")
+
+
+def _dev(t, what):
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous device tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(fn, rc):
+    if rc != 0:
+        raise FFNError(fn, rc)
+
+
+def workspace_bytes(T: int, d: int, d_ff: int, r: int = 0) -> int:
+    return int(lib().ffn_workspace_bytes(T, d, d_ff, r))
+
+
+def alloc_workspace(T: int, d: int, d_ff: int, r: int = 0, device="cuda"):
+    torch = _torch()
+    n = workspace_bytes(T, d, d_ff, r)
+    if n == 0:
+        raise FFNError("ffn_workspace_bytes", -2)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _std_call(name, x, w_gate, w_up, w_down_t, t, y, ws, stream):
+    T, d = x.shape
+    d_ff = w_up.shape[0]
+    rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, _dev(x, "x"), _dev(w_gate, "w_gate"),
+                              _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t), _dev(y, "y"),
+                              _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+    _check(name, rc)
+    return y
+
+
+def _lopa_call(name, x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream):
+    T, d = x.shape
+    d_ff, r = lopa_b.shape
+    rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, r, _dev(x, "x"), _dev(lopa_a, "lopa_a"),
+                              _dev(lopa_b, "lopa_b"), _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"),
+                              ctypes.c_float(t), _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(),
+                              _stream(stream))
+    _check(name, rc)
+    return y
+
+
+# ---------------------------------------------------------------- the C ABI, by name
+def ffn_dense_forward(x, w_gate, w_up, w_down_t, t, y, ws, stream=None):
+    return _std_call("ffn_dense_forward", x, w_gate, w_up, w_down_t, t, y, ws, stream)
+
+
+def ffn_sparse_forward(x, w_gate, w_up, w_down_t, t, y, ws, stream=None):
+    return _std_call("ffn_sparse_forward", x, w_gate, w_up, w_down_t, t, y, ws, stream)
+
+
+def ffn_lopa_sparse_forward(x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream=None):
+    return _lopa_call("ffn_lopa_sparse_forward", x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream)
+
+
+def ffn_lopa_dense_forward(x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream=None):
+    return _lopa_call("ffn_lopa_dense_forward", x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream)
+
+
+def ffn_active_set(ws, T, d, d_ff, r=0, stream=None, with_act=True):
+    """Returns (idx [n] int32 numpy, act [T, n] float32 numpy or None) of the last call."""
+    import numpy as np
+    n = ctypes.c_int32(0)
+    idx = np.empty(d_ff, np.int32)
+    act = np.empty((T, d_ff), np.float32) if with_act else None
+    rc = lib().ffn_active_set(_dev(ws, "ws"), T, d, d_ff, r, ctypes.byref(n), idx.ctypes.data_as(ctypes.c_void_p),
+                              None if act is None else act.ctypes.data_as(ctypes.c_void_p), _stream(stream))
+    _check("ffn_active_set", rc)
+    k = n.value
+    return idx[:k].copy(), (None if act is None else act[:, :k].copy())
+
+
+def ffn_status_string(code: int) -> str:
+    return lib().ffn_status_string(code).decode()

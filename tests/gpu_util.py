@@ -1,0 +1,121 @@
+"""Helpers shared by the GPU tests: move seeded inputs to the device, run a library
+entry point through the C ABI, and compare against the oracle with the parity rule:
+
+* active sets: bit-exact for every neuron whose oracle gate value is at least
+  BAND = 1e-3 away from the threshold (inside the band both decisions are valid);
+* outputs: ||y - y_ref|| / ||y_ref|| <= 1e-5 (fp32 weights) or 2e-3 (bf16 weights),
+  per token; an all-zero reference requires an exactly zero output.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import ffn_oracle
+from paper_2609_31975_amd import ffn
+from paper_2609_31975_amd import workloads as wl
+
+BAND = 1e-3
+TOL = {wl.F32: 1e-5, wl.BF16: 2e-3}
+
+
+def torch():
+    import torch as _t
+    return _t
+
+
+def to_dev(a: np.ndarray, wdt: int | None = None):
+    """numpy -> device tensor; uint16 arrays are bfloat16 bit patterns."""
+    t = torch()
+    if a is None:
+        return None
+    if a.dtype == np.uint16:
+        return t.from_numpy(a.view(np.int16)).to("cuda").view(t.bfloat16)
+    return t.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+class DevInputs:
+    def __init__(self, inp: wl.FFNInputs):
+        self.inp = inp
+        self.x = to_dev(inp.x)
+        self.w_gate = to_dev(inp.w_gate)
+        self.lopa_a = to_dev(inp.lopa_a)
+        self.lopa_b = to_dev(inp.lopa_b)
+        self.w_up = to_dev(inp.w_up)
+        self.w_down_t = to_dev(inp.w_down_t)
+
+
+def run_gpu(dev: DevInputs, t: float, dense: bool = False, x=None):
+    """Run the matching entry point; returns (y numpy [T, d], idx, act, ws)."""
+    tch = torch()
+    inp = dev.inp
+    x = dev.x if x is None else x
+    T, d = x.shape
+    ws = ffn.alloc_workspace(T, d, inp.d_ff, inp.r)
+    y = tch.full((T, d), float("nan"), dtype=tch.float32, device="cuda")
+    if inp.r:
+        fn = ffn.ffn_lopa_dense_forward if dense else ffn.ffn_lopa_sparse_forward
+        fn(x, dev.lopa_a, dev.lopa_b, dev.w_up, dev.w_down_t, t, y, ws)
+    else:
+        fn = ffn.ffn_dense_forward if dense else ffn.ffn_sparse_forward
+        fn(x, dev.w_gate, dev.w_up, dev.w_down_t, t, y, ws)
+    tch.cuda.synchronize()
+    idx, act = (None, None)
+    if T <= 64:
+        idx, act = ffn.ffn_active_set(ws, T, d, inp.d_ff, inp.r)
+    return y.cpu().numpy(), idx, act, ws
+
+
+def run_oracle(inp: wl.FFNInputs, t: float, dense: bool = False, x=None):
+    x = inp.x if x is None else x
+    kw = dict(w_gate=inp.w_gate) if inp.r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    return ffn_oracle.ffn(x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=inp.wdt, skip_inactive=not dense, **kw)
+
+
+def rel_err(y, y_ref):
+    y_ref = np.asarray(y_ref, np.float64)
+    nrm = np.linalg.norm(y_ref)
+    if nrm == 0:
+        return 0.0 if np.all(y == 0) else np.inf
+    return float(np.linalg.norm(np.asarray(y, np.float64) - y_ref) / nrm)
+
+
+def check_parity(res, y, idx, act, t, wdt, dense=False, what=""):
+    """Assert the parity rule; returns a dict of figures for reporting."""
+    T, d_ff = res.h.shape
+    tol = TOL[wdt]
+    out = dict(max_rel_err=0.0, n_union=None, n_active=[], band_flips=0)
+    assert np.isfinite(y).all() or not np.isfinite(res.y).all(), f"{what}: non-finite output"
+    for tau in range(T):
+        e = rel_err(y[tau], res.y[tau])
+        assert e <= tol, f"{what}: token {tau} relative error {e:.3e} > {tol}"
+        out["max_rel_err"] = max(out["max_rel_err"], e)
+    if idx is None:
+        return out
+    assert np.all(np.diff(idx) > 0), f"{what}: active list not strictly ascending"
+    out["n_union"] = len(idx)
+    if dense:
+        assert idx.tolist() == list(range(d_ff)), f"{what}: dense call must list every neuron"
+    h = res.h
+    band = np.abs(h - np.float64(np.float32(t))) < BAND
+    union = np.zeros(d_ff, bool)
+    for tau in range(T):
+        on = np.zeros(d_ff, bool)
+        on[idx] = act[tau] > 0
+        union |= on
+        ref = res.active[tau]
+        bad = (on != ref) & ~band[tau]
+        assert not bad.any(), f"{what}: token {tau} active-set mismatch outside the band at {np.flatnonzero(bad)[:10]}"
+        out["band_flips"] += int((on != ref).sum())
+        out["n_active"].append(int(on.sum()))
+        # the activation values themselves: h - t within fp32 gate accuracy
+        ok = on & ref
+        if ok.any():
+            ref_act = h[tau][ok] - np.float64(np.float32(t))
+            got = np.zeros(d_ff)
+            got[idx] = act[tau]
+            assert np.allclose(got[ok], ref_act, rtol=1e-4, atol=1e-4), f"{what}: activation values differ"
+    if not dense:
+        listed = np.zeros(d_ff, bool)
+        listed[idx] = True
+        assert np.array_equal(listed, union), f"{what}: listed neurons are not the union of the active sets"
+    return out

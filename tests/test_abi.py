@@ -1,0 +1,98 @@
+"""The C ABI library: loads, exports what the header declares, and rejects bad
+arguments on the host before anything is enqueued (CPU only: every call here fails
+validation, so no kernel is ever launched)."""
+import ctypes
+
+import pytest
+
+from paper_2609_31975_amd import ffn
+
+L = None
+
+
+def setup_module(_):
+    global L
+    L = ffn.lib()
+
+
+def test_exports_every_declared_function():
+    names = ffn.declared_functions()
+    assert set(names) >= {"ffn_workspace_bytes", "ffn_dense_forward", "ffn_sparse_forward",
+                          "ffn_lopa_sparse_forward", "ffn_lopa_dense_forward", "ffn_active_set",
+                          "ffn_status_string"}
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code, name in ffn.STATUS.items():
+        assert ffn.ffn_status_string(code) and ffn.ffn_status_string(code) != "unknown status", name
+    assert ffn.ffn_status_string(123) == "unknown status"
+
+
+def test_workspace_bytes():
+    a = ffn.workspace_bytes(1, 4096, 14336, 0)
+    b = ffn.workspace_bytes(1, 4096, 14336, 512)
+    c = ffn.workspace_bytes(8, 4096, 14336, 512)
+    assert 0 < a <= b < c
+    assert a % 256 == 0
+    # per-token state grows linearly with tokens up to the 64-token pass size, then stops
+    assert ffn.workspace_bytes(64, 64, 100, 0) == ffn.workspace_bytes(500, 64, 100, 0)
+    for bad in [(0, 8, 8, 0), (1, 0, 8, 0), (1, 8, 0, 0), (1, 8, 8, -1), (1, 1 << 20, 1 << 12, 0)]:
+        assert ffn.workspace_bytes(*bad) == 0, bad
+
+
+A = 1 << 20                     # a 16-byte-aligned address that is never dereferenced
+MIS = A + 4                     # misaligned
+
+
+def _std(fn="ffn_sparse_forward", wdt=1, T=1, d=64, d_ff=128, x=A, g=A, u=A, dn=A, y=A, ws=A, ws_bytes=1 << 30):
+    return getattr(L, fn)(wdt, T, d, d_ff, x, g, u, dn, ctypes.c_float(0.5), y, ws, ws_bytes, None)
+
+
+def _lopa(fn="ffn_lopa_sparse_forward", wdt=1, T=1, d=64, d_ff=128, r=8, x=A, a=A, b=A, u=A, dn=A, y=A, ws=A,
+          ws_bytes=1 << 30):
+    return getattr(L, fn)(wdt, T, d, d_ff, r, x, a, b, u, dn, ctypes.c_float(0.5), y, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("fn", ["ffn_sparse_forward", "ffn_dense_forward"])
+def test_standard_argument_errors(fn):
+    assert _std(fn, x=None) == -1
+    assert _std(fn, g=None) == -1
+    assert _std(fn, dn=None) == -1
+    assert _std(fn, y=None) == -1
+    assert _std(fn, ws=None) == -1
+    assert _std(fn, wdt=7) == -3
+    assert _std(fn, T=0) == -2
+    assert _std(fn, d=-1) == -2
+    assert _std(fn, d_ff=0) == -2
+    assert _std(fn, d=1 << 16, d_ff=1 << 15) == -2
+    assert _std(fn, x=MIS) == -4
+    assert _std(fn, u=MIS) == -4
+    assert _std(fn, ws=MIS) == -4
+    assert _std(fn, ws_bytes=ffn.workspace_bytes(1, 64, 128, 0) - 1) == -5
+
+
+@pytest.mark.parametrize("fn", ["ffn_lopa_sparse_forward", "ffn_lopa_dense_forward"])
+def test_lopa_argument_errors(fn):
+    assert _lopa(fn, a=None) == -1
+    assert _lopa(fn, b=None) == -1
+    assert _lopa(fn, r=0) == -2
+    assert _lopa(fn, wdt=-1) == -3
+    assert _lopa(fn, a=MIS) == -4
+    assert _lopa(fn, b=MIS) == -4
+    assert _lopa(fn, ws_bytes=ffn.workspace_bytes(1, 64, 128, 8) - 256) == -5
+
+
+def test_active_set_argument_errors():
+    n = ctypes.c_int32()
+    assert L.ffn_active_set(None, 1, 64, 128, 0, ctypes.byref(n), A, None, None) == -1
+    assert L.ffn_active_set(A, 65, 64, 128, 0, ctypes.byref(n), A, None, None) == -2
+    assert L.ffn_active_set(A, 1, 64, 128, -1, ctypes.byref(n), A, None, None) == -2
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(ffn, "_lib", None)
+    monkeypatch.setattr(ffn, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        ffn.lib()

@@ -1,0 +1,155 @@
+"""GPU parity: every entry point of the C ABI against the oracle on the same seeded
+inputs (element-wise outputs, exact active sets outside the 1e-3 band).
+
+Small shapes exercise every kernel variant with ragged tails; the full-size cases
+are the workloads the benchmark times, in the same launch configuration.
+"""
+import numpy as np
+import pytest
+
+from paper_2609_31975_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16 = wl.F32, wl.BF16
+
+
+@pytest.fixture(scope="module")
+def gu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from tests import gpu_util
+    return gpu_util
+
+
+# name, T, d, d_ff, r, wdt, t
+SMALL = [
+    ("tiny_f32_workload", 1, 256, 1024, 0, F32, 1.2816),   # the tiny fp32 workload, seed 0
+    ("std_bf16_ragged", 1, 264, 1000, 0, BF16, 1.0),       # 33 chunks per row, last segment 8 rows
+    ("std_bf16_long_rows", 1, 4104, 300, 0, BF16, 1.0),    # 513 chunks per row: 16 chunks per lane
+    ("std_f32_ragged", 1, 260, 999, 0, F32, 0.8),
+    ("std_bf16_odd_d", 1, 100, 77, 0, BF16, 0.5),          # d not a multiple of 8: element-wise kernels
+    ("std_f32_odd_d", 1, 102, 130, 0, F32, 0.5),
+    ("std_bf16_T3", 3, 264, 1000, 0, BF16, 1.0),           # union of 3 active sets
+    ("std_f32_T70", 70, 64, 200, 0, F32, 1.0),             # two token passes (64 + 6)
+    ("lopa_bf16", 1, 264, 1000, 40, BF16, 1.0),
+    ("lopa_bf16_odd_r", 1, 264, 1000, 36, BF16, 1.0),
+    ("lopa_f32", 1, 256, 1024, 32, F32, 1.2816),
+    ("lopa_bf16_T5", 5, 264, 1000, 40, BF16, 1.0),
+    ("very_small", 1, 8, 3, 0, BF16, 0.0),
+    ("d_is_1", 1, 1, 5, 0, F32, 0.0),
+    ("lopa_r_is_1", 2, 16, 40, 1, F32, 0.1),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+@pytest.mark.parametrize("dense", [False, True], ids=["sparse", "dense"])
+def test_small_shapes(gu, case, dense):
+    name, T, d, d_ff, r, wdt, t = case
+    inp = wl.make_inputs(101, T, d, d_ff, r=r, wdt=wdt)
+    dev = gu.DevInputs(inp)
+    y, idx, act, _ = gu.run_gpu(dev, t, dense=dense)
+    res = gu.run_oracle(inp, t, dense=dense)
+    gu.check_parity(res, y, idx, act, t, wdt, dense=dense, what=name)
+
+
+# ---------------------------------------------------------------- full-size workloads
+_cache = {}
+
+
+def _inputs(key, T, d, d_ff, r, seed):
+    if key not in _cache:
+        _cache.clear()
+        _cache[key] = wl.make_inputs(seed, T, d, d_ff, r=r, wdt=BF16)
+    return _cache[key]
+
+
+FULL = [w for w in wl.workloads() if w.name != "tiny_f32_std_s90"]
+
+
+@pytest.mark.parametrize("w", FULL, ids=[w.name for w in FULL])
+def test_full_size_workloads(gu, w):
+    inp = _inputs((w.d, w.d_ff, w.r, w.T, w.seed), w.T, w.d, w.d_ff, w.r, w.seed)
+    dev = gu.DevInputs(inp)
+    y, idx, act, _ = gu.run_gpu(dev, w.t)
+    res = gu.run_oracle(inp, w.t)
+    fig = gu.check_parity(res, y, idx, act, w.t, w.wdt, what=w.name)
+    print(w.name, fig["max_rel_err"], fig["n_union"], fig["band_flips"], flush=True)
+
+
+@pytest.mark.parametrize("r", [0, 512], ids=["standard", "lopa512"])
+def test_full_size_dense(gu, r):
+    inp = _inputs((4096, 14336, r, 1, 1000 + r), 1, 4096, 14336, r, 1000 + r)
+    dev = gu.DevInputs(inp)
+    y, idx, act, _ = gu.run_gpu(dev, 1.2816, dense=True)
+    res = gu.run_oracle(inp, 1.2816, dense=True)
+    gu.check_parity(res, y, idx, act, 1.2816, BF16, dense=True, what=f"dense r={r}")
+
+
+# ---------------------------------------------------------------- edge cases
+EDGE_SHAPES = [(1, 264, 1000, 0, BF16), (1, 100, 77, 0, BF16), (1, 264, 1000, 40, BF16), (4, 64, 200, 0, F32)]
+
+
+@pytest.mark.parametrize("shape", EDGE_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
+def test_nothing_active(gu, shape):
+    T, d, d_ff, r, wdt = shape
+    inp = wl.make_inputs(102, T, d, d_ff, r=r, wdt=wdt)
+    y, idx, act, _ = gu.run_gpu(gu.DevInputs(inp), 1e30)
+    assert len(idx) == 0 and np.all(y == 0)
+
+
+@pytest.mark.parametrize("shape", EDGE_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
+def test_everything_active_equals_dense(gu, shape):
+    T, d, d_ff, r, wdt = shape
+    inp = wl.make_inputs(103, T, d, d_ff, r=r, wdt=wdt)
+    dev = gu.DevInputs(inp)
+    ys, idx, _, _ = gu.run_gpu(dev, -100.0)
+    yd, _, _, _ = gu.run_gpu(dev, -100.0, dense=True)
+    assert idx.tolist() == list(range(d_ff))
+    assert np.array_equal(ys, yd)
+    gu.check_parity(gu.run_oracle(inp, -100.0), ys, None, None, -100.0, wdt)
+
+
+@pytest.mark.parametrize("shape", EDGE_SHAPES[:3], ids=lambda s: f"d{s[1]}_dff{s[2]}_r{s[3]}")
+def test_inactive_rows_are_never_read(gu, shape):
+    """NaN in every W_up / W_down^T row that no token activates: the output is unchanged."""
+    T, d, d_ff, r, wdt = shape
+    inp = wl.make_inputs(104, T, d, d_ff, r=r, wdt=wdt)
+    t = 1.0
+    res = gu.run_oracle(inp, t)
+    off = ~res.active.any(0)
+    near = (np.abs(res.h - t) < gu.BAND).any(0)
+    poison = off & ~near
+    assert poison.sum() > d_ff // 2
+    up, dn = inp.w_up.copy(), inp.w_down_t.copy()
+    nan = np.uint16(0x7FC0) if wdt == BF16 else np.float32(np.nan)
+    up[poison] = nan
+    dn[poison] = nan
+    pinp = wl.FFNInputs(x=inp.x, w_up=up, w_down_t=dn, w_gate=inp.w_gate, lopa_a=inp.lopa_a, lopa_b=inp.lopa_b,
+                        wdt=wdt)
+    y, idx, act, _ = gu.run_gpu(gu.DevInputs(pinp), t)
+    assert np.isfinite(y).all()
+    gu.check_parity(res, y, idx, act, t, wdt, what="poisoned")
+
+
+@pytest.mark.parametrize("wdt", [F32, BF16])
+def test_worked_example_on_gpu(gu, wdt):
+    """The hand-worked example of the oracle pins (exact arithmetic; neuron 0 sits on the threshold)."""
+    from tests.test_oracle import _enc, _worked_standard
+    x, g, up, dn = _worked_standard()
+    up = np.nan_to_num(up, nan=0.0)
+    dn = np.nan_to_num(dn, nan=0.0)
+    inp = wl.FFNInputs(x=x, w_gate=_enc(g, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt), wdt=wdt)
+    y, idx, act, _ = gu.run_gpu(gu.DevInputs(inp), 1.0)
+    assert y.tolist() == [[0.5, -2, -2, 15]]
+    assert idx.tolist() == [1, 2, 5] and act.tolist() == [[1, 2, 5]]
+
+
+@pytest.mark.parametrize("r", [0, 512])
+def test_bitwise_reproducible(gu, r):
+    inp = wl.make_inputs(105, 1, 4096, 14336, r=r, wdt=BF16)
+    dev = gu.DevInputs(inp)
+    y1, i1, a1, _ = gu.run_gpu(dev, 1.2816)
+    y2, i2, a2, _ = gu.run_gpu(dev, 1.2816)
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+    assert np.array_equal(i1, i2) and np.array_equal(a1, a2)
