@@ -32,7 +32,11 @@
  * Ownership: the caller allocates and owns every buffer.  The forward calls never
  * allocate, free or synchronize; they enqueue kernels on `stream` and return.  Calls
  * that share a workspace must be ordered (same stream); distinct workspaces may run
- * concurrently.  Results are deterministic: identical inputs give identical bits.
+ * concurrently.  y must not overlap x, the weights or the workspace.
+ *
+ * Determinism: the active set and the activations are bit-reproducible.  For one
+ * token the output is summed over row chunks with fp32 atomic adds, so its last bits
+ * may differ between runs (the order of the additions is not fixed).
  *
  * Errors: arguments are checked on the host before anything is enqueued; on a
  * negative return nothing was enqueued.  A launch failure returns FFN_ERR_HIP.
@@ -103,6 +107,15 @@ int ffn_lopa_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const
  * For a dense call every neuron is listed.  Returns FFN_OK or an error code. */
 int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
                    float* act_host, hipStream_t stream);
+
+/* Benchmark hook (eager launches only, not for graph capture): the next forward call
+ * made by this host thread launches its gate kernel -- gate GEMV, threshold,
+ * compaction and the W_up dot products of the active neurons, the call's dominant
+ * kernel -- with `start` / `stop` recorded at that kernel's start and end
+ * (hipExtLaunchKernel semantics), so hipEventElapsedTime(start, stop) is its
+ * execution time.  One call consumes the pair; NULL, NULL cancels.  Returns FFN_OK,
+ * or FFN_ERR_NULL if exactly one event is NULL. */
+int ffn_time_next_gate_kernel(hipEvent_t start, hipEvent_t stop);
 
 /* Human-readable text for a status code. */
 const char* ffn_status_string(int status);

@@ -11,6 +11,8 @@
 
 namespace ffn {
 
+thread_local GateTiming g_gate_timing;
+
 namespace {
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxElems = (int64_t)1 << 31;  // kernels index rows with 32-bit chunk counts
@@ -21,8 +23,8 @@ size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out) {
   (void)d;
   Workspace w{};
-  w.nseg = (d_ff + kSeg - 1) / kSeg;
-  w.slots = w.nseg * kSeg;
+  w.nseg = 0;
+  w.slots = d_ff;
   w.tc = T < kTokChunk ? T : kTokChunk;
   w.r = r;
   size_t off = 0;
@@ -32,7 +34,8 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
     off += round_up(bytes);
     return p;
   };
-  w.seg_count = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.nseg));
+  w.meta = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 64));
+  w.seg_count = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)d_ff));
   w.seg_idx = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.slots));
   w.seg_act = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
   w.seg_zval = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
@@ -90,7 +93,7 @@ int run(const Call& c) {
     hipError_t e = hipSuccess;
     if (lopa) e = launch_lopa_z(sh, x, c.lopa_a, ws, c.stream);
     if (e == hipSuccess)
-      e = launch_gate_up(sh, lopa ? Gate::LoPA : Gate::Standard, c.dense, x, c.gate, c.w_up, c.t, ws, c.stream);
+      e = launch_gate_up(sh, lopa ? Gate::LoPA : Gate::Standard, c.dense, x, c.gate, c.w_up, c.t, ws, y, c.stream);
     if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
     if (e != hipSuccess) return FFN_ERR_HIP;
   }
@@ -142,9 +145,12 @@ int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_uni
   ffn::Workspace w;
   ffn::workspace_layout(T, d, d_ff, r, const_cast<void*>(ws), &w);
   if (hipStreamSynchronize(stream) != hipSuccess) return FFN_ERR_HIP;
-  std::vector<int32_t> cnt(w.nseg), idx(w.slots);
+  int32_t nseg = 0;
+  if (hipMemcpy(&nseg, w.meta, sizeof nseg, hipMemcpyDeviceToHost) != hipSuccess) return FFN_ERR_HIP;
+  if (nseg < 1 || nseg > d_ff) return FFN_ERR_HIP;  // workspace does not hold a finished call
+  std::vector<int32_t> cnt(nseg), idx(w.slots);
   std::vector<float> act;
-  if (hipMemcpy(cnt.data(), w.seg_count, sizeof(int32_t) * w.nseg, hipMemcpyDeviceToHost) != hipSuccess ||
+  if (hipMemcpy(cnt.data(), w.seg_count, sizeof(int32_t) * nseg, hipMemcpyDeviceToHost) != hipSuccess ||
       hipMemcpy(idx.data(), w.seg_idx, sizeof(int32_t) * w.slots, hipMemcpyDeviceToHost) != hipSuccess)
     return FFN_ERR_HIP;
   if (act_host) {
@@ -153,16 +159,23 @@ int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_uni
       return FFN_ERR_HIP;
   }
   int n = 0;
-  for (int s = 0; s < w.nseg; ++s) {
-    if (cnt[s] < 0 || cnt[s] > ffn::kSeg) return FFN_ERR_HIP;  // workspace does not hold a finished call
+  for (int s = 0; s < nseg; ++s) {
+    const int row0 = (int)(((int64_t)s * d_ff) / nseg), row1 = (int)(((int64_t)(s + 1) * d_ff) / nseg);
+    if (cnt[s] < 0 || cnt[s] > row1 - row0) return FFN_ERR_HIP;  // workspace does not hold a finished call
     for (int e = 0; e < cnt[s]; ++e) {
-      const int slot = s * ffn::kSeg + e;
+      const int slot = row0 + e;
       if (act_host)
         for (int tau = 0; tau < T; ++tau) act_host[(size_t)tau * d_ff + n] = act[(size_t)tau * w.slots + slot];
       idx_host[n++] = idx[slot];
     }
   }
   *n_union = n;
+  return FFN_OK;
+}
+
+int ffn_time_next_gate_kernel(hipEvent_t start, hipEvent_t stop) {
+  if ((start == nullptr) != (stop == nullptr)) return FFN_ERR_NULL;
+  ffn::g_gate_timing = ffn::GateTiming{start, stop};
   return FFN_OK;
 }
 

@@ -9,20 +9,25 @@
 namespace ffn {
 
 constexpr int kWave = 64;
-constexpr int kSeg = 32;          // gate rows per workgroup = one compaction segment
+constexpr int kSegMax = 64;       // most gate rows per segment (one 64-lane ballot)
+constexpr int kSegGeneric = 32;   // rows per segment of the element-wise kernels
 constexpr int kBlock = 256;       // threads per workgroup for every kernel
 constexpr int kTokChunk = 64;     // tokens per pass; a larger batch runs as several passes
 constexpr int kListWindow = 1024; // active entries staged in LDS at a time by the down kernel
 
 // Workspace carve-up for one pass of up to `tc` tokens.  Every region starts on a
-// 256-byte boundary.  "slots" = nseg * kSeg: slot s*kSeg + e holds the e-th active
-// neuron (ascending) of segment s, for e < seg_count[s].
+// 256-byte boundary.  The neurons are split into nseg row-balanced segments (chosen
+// per call by the gate launcher and recorded in meta[0]); segment w covers rows
+// [w d_ff / nseg, (w+1) d_ff / nseg), and its active neurons occupy the slots from
+// its first row on: slot w d_ff / nseg + e holds its e-th active neuron (ascending),
+// for e < seg_count[w].  slots = d_ff.
 struct Workspace {
   int nseg;
   int slots;
   int tc;
   int r;
-  int32_t* seg_count;  // [nseg]
+  int32_t* meta;       // [64]             meta[0] = nseg of the last call
+  int32_t* seg_count;  // [d_ff]           (at most d_ff segments)
   int32_t* seg_idx;    // [slots]          neuron index
   float* seg_act;      // [tc][slots]      h - t for the token, 0 where inactive
   float* seg_zval;     // [tc][slots]      act * <w_up[i], x_tau>
@@ -39,11 +44,19 @@ struct Shape {
 
 enum class Gate { Standard, LoPA };
 
+// Events for the next gate-kernel launch on this host thread (benchmark hook).
+struct GateTiming {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+extern thread_local GateTiming g_gate_timing;
+
 // Launchers (return hipSuccess or the launch error).  Every launcher enqueues on `s`.
 hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
                          hipStream_t s);
+// Also clears y[0 .. T*d) and sets ws.nseg / meta[0] for the down kernel.
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w,
-                          const void* w_up, float t, const Workspace& ws, hipStream_t s);
+                          const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s);
 

@@ -4,18 +4,21 @@
 // A(W1 x) are known before W3 and W2 are touched; Section 3.3: LoPA gate B (A x)):
 //
 //   [LoPA only] k_lopa_z*     z = A x                               -> ws.z
-//   k_gate_up*                per workgroup = one segment of kSeg consecutive
-//                             neurons: h = W_gate x (or B z), ballot compaction of
-//                             the neurons with h > t (union over tokens), then the
-//                             W_up row dot products of exactly those neurons:
+//   k_gate_up*                one workgroup per row-balanced segment of neurons:
+//                             h = W_gate x (or B z), 64-lane ballot compaction of the
+//                             neurons with h > t (union over tokens), then the W_up
+//                             row dot products of exactly those neurons:
 //                             act = h - t, zval = act * <w_up[i], x>
-//                             -> seg_count / seg_idx / seg_act / seg_zval
-//   k_down*                   y = sum_k zval_k * w_down_t[idx_k], each workgroup
-//                             owning a 16-column slice of y for all active rows;
-//                             prefix sums of seg_count give the ascending list.
+//                             -> seg_count / seg_idx / seg_act / seg_zval; clears y
+//   k_down*                   y += zval_k * w_down_t[idx_k] over the listed neurons;
+//                             one workgroup per (row chunk, 1 KB column slice), fp32
+//                             atomics into y across row chunks.
 //
-// No atomics and no inter-workgroup waits: every output element is written by one
-// thread after a fixed-order reduction, so results are bit-reproducible.
+// The compaction needs no atomics and no inter-workgroup waits: each segment writes
+// its own count and an ascending list, and readers find a segment's list from its
+// first row.
+#include <hip/hip_ext.h>
+
 #include "ffn_internal.h"
 
 namespace ffn {
@@ -126,8 +129,15 @@ __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const float (&v
   return acc0 + acc1;
 }
 
-// Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n): waves take
-// passes of 64/lpr rows, two passes in flight; `sink(k, value)` runs on lane q == 0.
+// Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n): each wave takes
+// passes of 64/lpr rows (passes wave, wave + 4, ...); with kPipeline the loads of its
+// next pass are issued before the current pass is reduced.  `sink(k, value)` runs on
+// lane q == 0.
+#ifndef FFN_GATE_PIPE
+#define FFN_GATE_PIPE 0
+#endif
+constexpr bool kPipeline = FFN_GATE_PIPE != 0;
+
 template <class W, int CPL, class RowOf, class Sink>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, int C, int lpr, int lpr_log2, int n,
                                          const float (&v)[CPL][W::EPC], RowOf row_of, Sink sink) {
@@ -136,34 +146,45 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, int C, i
   const int q = lane & (lpr - 1), p = lane >> lpr_log2;
   const int rpp = kWave >> lpr_log2;
   const int npass = (n + rpp - 1) / rpp;
-  for (int pass = wave; pass < npass; pass += 2 * kWaves) {
-    const int k0 = pass * rpp + p;
-    const int k1 = (pass + kWaves) * rpp + p;
-    const bool v0 = k0 < n, v1 = k1 < n;
-    uint4 b0[CPL], b1[CPL];
-    load_row<CPL>(mat + (size_t)row_of(v0 ? k0 : 0) * C, v0, C, q, lpr, b0);
-    load_row<CPL>(mat + (size_t)row_of(v1 ? k1 : 0) * C, v1, C, q, lpr, b1);
-    const float s0 = group_sum(lane_dot<W, CPL>(b0, v), lpr);
-    const float s1 = group_sum(lane_dot<W, CPL>(b1, v), lpr);
-    if (q == 0) {
-      if (v0) sink(k0, s0);
-      if (v1) sink(k1, s1);
+  int pass = wave;
+  if (pass >= npass) return;
+  int k = pass * rpp + p;
+  bool ok = k < n;
+  uint4 cur[CPL];
+  load_row<CPL>(mat + (size_t)row_of(ok ? k : 0) * C, ok, C, q, lpr, cur);
+  while (true) {
+    const int pass_n = pass + kWaves;
+    const int k_n = pass_n * rpp + p;
+    const bool more = pass_n < npass;
+    const bool ok_n = more && k_n < n;
+    uint4 nxt[CPL];
+    float sum;
+    if constexpr (kPipeline) {
+      if (more) load_row<CPL>(mat + (size_t)row_of(ok_n ? k_n : 0) * C, ok_n, C, q, lpr, nxt);
+      sum = group_sum(lane_dot<W, CPL>(cur, v), lpr);
+    } else {
+      sum = group_sum(lane_dot<W, CPL>(cur, v), lpr);
+      if (more) load_row<CPL>(mat + (size_t)row_of(ok_n ? k_n : 0) * C, ok_n, C, q, lpr, nxt);
     }
+    if (q == 0 && ok) sink(k, sum);
+    if (!more) break;
+    pass = pass_n;
+    k = k_n;
+    ok = ok_n;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) cur[c] = nxt[c];
   }
 }
 
-// ------------------------------------------------------------------ fast kernels, T = 1
-// z = A x for one token (rows of A: C chunks).
-template <class W, int CPL>
-__global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ x, const uint4* __restrict__ A,
-                                                      int C, int lpr, int lpr_log2, int r, float* __restrict__ z) {
-  float xr[CPL][W::EPC];
-  load_vec<W, CPL>(x, C, lane_id() & (lpr - 1), lpr, xr);
-  const int rows_per_block = (kBlock / kWave) * 2 * (kWave >> lpr_log2);
-  const int k0 = blockIdx.x * rows_per_block;
-  const int n = min(rows_per_block, r - k0);
-  dot_rows<W, CPL>(A, C, lpr, lpr_log2, n, xr, [&](int k) { return k0 + k; },
-                   [&](int k, float s) { z[k0 + k] = s; });
+// ------------------------------------------------------------------ segments
+// The d_ff neurons are split into nseg row-balanced segments; segment w covers rows
+// [seg_row(w), seg_row(w + 1)) (at most kSegMax of them).  Its active neurons occupy
+// slots seg_row(w) .. seg_row(w) + seg_count[w] - 1, in ascending neuron order.
+__device__ __forceinline__ int seg_row(int w, int d_ff, int nseg) { return (int)(((int64_t)w * d_ff) / nseg); }
+
+// the segment that contains `row`: the largest w with seg_row(w) <= row
+__device__ __forceinline__ int seg_of_row(int row, int d_ff, int nseg) {
+  return (int)((((int64_t)row + 1) * nseg + d_ff - 1) / d_ff) - 1;
 }
 
 // Ballot compaction of one segment (run by the first wave): neurons whose gate value
@@ -195,25 +216,47 @@ __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int
   }
 }
 
-// One segment of kSeg neurons: gate, compaction, W_up dots of the selected neurons.
+// The gate kernels clear y (the down kernel accumulates into it) and record the
+// segment count for the inspection hook.
+__device__ __forceinline__ void clear_output(float* __restrict__ y, int n, int32_t* meta, int nseg) {
+  for (int j = blockIdx.x * kBlock + threadIdx.x; j < n; j += gridDim.x * kBlock) y[j] = 0.f;
+  if (blockIdx.x == 0 && threadIdx.x == 0) meta[0] = nseg;
+}
+
+// ------------------------------------------------------------------ fast kernels, T = 1
+// z = A x for one token (rows of A: C chunks); one pass of 64/lpr rows per wave.
+template <class W, int CPL>
+__global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ x, const uint4* __restrict__ A,
+                                                      int C, int lpr, int lpr_log2, int r, float* __restrict__ z) {
+  float xr[CPL][W::EPC];
+  load_vec<W, CPL>(x, C, lane_id() & (lpr - 1), lpr, xr);
+  const int rows_per_block = (kBlock / kWave) * (kWave >> lpr_log2);
+  const int k0 = blockIdx.x * rows_per_block;
+  const int n = min(rows_per_block, r - k0);
+  dot_rows<W, CPL>(A, C, lpr, lpr_log2, n, xr, [&](int k) { return k0 + k; },
+                   [&](int k, float s) { z[k0 + k] = s; });
+}
+
+// One segment: gate values, compaction, W_up dots of the selected neurons.
 // LOPA: the gate rows are B [d_ff][r] against z; otherwise W_gate [d_ff][d] against x.
 // DENSE: every neuron of the segment is selected (act = max(h - t, 0)).
 template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU>
 __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__ x, const float* __restrict__ z,
                                                        const uint4* __restrict__ gate_w, int Cg, int lprg,
                                                        int lprg_log2, const uint4* __restrict__ w_up, int Cu,
-                                                       int lpru, int lpru_log2, int d_ff, float t,
-                                                       int32_t* __restrict__ seg_count,
+                                                       int lpru, int lpru_log2, int d_ff, int nseg, float t,
+                                                       int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                                        int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
-                                                       float* __restrict__ seg_zval) {
-  __shared__ float s_h[kSeg];
-  __shared__ int s_list[kSeg];
-  __shared__ float s_act[kSeg];
+                                                       float* __restrict__ seg_zval, float* __restrict__ y, int d) {
+  __shared__ float s_h[kSegMax];
+  __shared__ int s_list[kSegMax];
+  __shared__ float s_act[kSegMax];
   __shared__ int s_cnt;
 
   const int seg = blockIdx.x;
-  const int row0 = seg * kSeg;
-  const int nrows = min(kSeg, d_ff - row0);
+  const int row0 = seg_row(seg, d_ff, nseg);
+  const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;
+  clear_output(y, d, meta, nseg);
   auto gate_sink = [&](int k, float s) { s_h[k] = s; };
   auto gate_row = [&](int k) { return row0 + k; };
   auto up_row = [&](int e) { return row0 + s_list[e]; };
@@ -243,129 +286,109 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
   }
 }
 
-// ------------------------------------------------------------------ down projection
-// Exclusive prefix sum of s[0..n) in place, s[n] = total; all kBlock threads call it.
-__device__ void block_exclusive_scan(int* s, int n) {
-  __shared__ int s_wsum[kBlock / kWave];
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  const int per = (n + kBlock - 1) / kBlock;
-  const int b = min((int)threadIdx.x * per, n), e = min(b + per, n);
-  int local = 0;
-  for (int i = b; i < e; ++i) local += s[i];
-  int v = local;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int u = __shfl_up(v, o);
-    if (lane >= o) v += u;
-  }
-  if (lane == kWave - 1) s_wsum[wave] = v;
-  __syncthreads();
-  int excl = v - local;
-  for (int w = 0; w < wave; ++w) excl += s_wsum[w];
-  for (int i = b; i < e; ++i) {
-    const int c = s[i];
-    s[i] = excl;
-    excl += c;
-  }
-  if (threadIdx.x == kBlock - 1) s[n] = excl;
-  __syncthreads();
-}
-
-// Load segment counts and turn them into ascending-list offsets; returns the total.
-__device__ int segment_offsets(const int32_t* __restrict__ seg_count, int nseg, int* s_pre) {
-  for (int s = threadIdx.x; s < nseg; s += kBlock) s_pre[s] = seg_count[s];
-  __syncthreads();
-  block_exclusive_scan(s_pre, nseg);
-  return s_pre[nseg];
-}
-
-// Stage list entries [base, base + wn) into LDS as slot numbers.
-__device__ void stage_window(const int* s_pre, int nseg, int base, int wn, int* s_slot) {
-  for (int s = threadIdx.x; s < nseg; s += kBlock) {
-    const int k0 = s_pre[s], k1 = s_pre[s + 1];
-    const int lo = max(k0, base), hi = min(k1, base + wn);
-    for (int k = lo; k < hi; ++k) s_slot[k - base] = s * kSeg + (k - k0);
-  }
-}
-
-// Map workgroup -> column slice so that neighbouring slices (which share 128-byte
-// lines of each weight row) run on the same XCD: workgroups are dealt round-robin
-// over the 8 XCDs, so group b % 8 gets a contiguous range of slices.
-__device__ __forceinline__ int xcd_slice(int b, int nslices) {
-  return (nslices % 8 == 0) ? (b % 8) * (nslices / 8) + b / 8 : b;
-}
-
-// y (one token) = sum over listed neurons of zval * w_down_t[row]; the workgroup owns
-// CPW chunks (16 columns) of y and reduces its row groups in a fixed order.
-template <class W, int CPW, bool DENSE>
+// y += sum over the listed neurons of a row chunk of zval * w_down_t[neuron], for one
+// 64-chunk column slice (1 KB of every bf16 row, read by one wave instruction).
+// Workgroup b covers column slice b % S of the neurons in segments [c nseg/R,
+// (c+1) nseg/R), c = b / S.  Its four waves take the chunk's active rows in turn;
+// their partial sums are added in a fixed order and then into y with one atomic
+// per column (y was cleared by the gate kernel).
+template <class W, bool DENSE>
 __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ seg_count,
                                                     const int32_t* __restrict__ seg_idx,
-                                                    const float* __restrict__ seg_zval, int nseg, int d_ff,
+                                                    const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
                                                     const uint4* __restrict__ w_down_t, int C, int d,
                                                     float* __restrict__ y) {
-  extern __shared__ int s_pre[];  // [nseg + 1]
-  __shared__ int s_slot[kListWindow];
-  constexpr int EPC = W::EPC, NRG = kBlock / CPW, OUT = CPW * EPC, NB = kBlock / OUT;
-  __shared__ float s_red[kBlock * EPC];
-  __shared__ float s_red2[kBlock];
-  constexpr int U = 8;
+  constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave;
+  extern __shared__ int s_dyn[];  // raw slots, then the compacted list (sparse only)
+  __shared__ int s_cnt[kWave];
+  __shared__ int s_off[kWave + 1];
+  __shared__ float s_red[kWaves][kWave * EPC];
 
-  const int nslices = (C + CPW - 1) / CPW;
-  const int slice = xcd_slice(blockIdx.x, nslices);
-  const int cc = threadIdx.x % CPW, rg = threadIdx.x / CPW;
-  const int ch = slice * CPW + cc;
+  const int S = (C + kWave - 1) / kWave;
+  const int chunk = blockIdx.x / S, slice = blockIdx.x % S;
+  const int seg_lo = (int)(((int64_t)chunk * nseg) / R), seg_hi = (int)(((int64_t)(chunk + 1) * nseg) / R);
+  const int row_lo = seg_row(seg_lo, d_ff, nseg), row_hi = seg_row(seg_hi, d_ff, nseg);
+  const int raw_n = row_hi - row_lo;
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+
+  int n = raw_n;
+  int* l_idx = nullptr;
+  float* l_z = nullptr;
+  if constexpr (!DENSE) {
+    int* raw_idx = s_dyn;
+    float* raw_z = reinterpret_cast<float*>(s_dyn + raw_n);
+    l_idx = s_dyn + 2 * raw_n;
+    l_z = reinterpret_cast<float*>(s_dyn + 3 * raw_n);
+    // one round trip: every slot of the chunk plus the segment counts
+    for (int p = threadIdx.x; p < raw_n; p += kBlock) {
+      raw_idx[p] = seg_idx[row_lo + p];
+      raw_z[p] = seg_zval[row_lo + p];
+    }
+    if (wave == 0) {
+      const int nsc = seg_hi - seg_lo;  // <= 64, guaranteed by the host
+      const int c = lane < nsc ? seg_count[seg_lo + lane] : 0;
+      int v = c;
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int u = __shfl_up(v, o);
+        if (lane >= o) v += u;
+      }
+      s_cnt[lane] = c;
+      s_off[lane] = v - c;
+      if (lane == kWave - 1) s_off[kWave] = v;
+    }
+    __syncthreads();
+    n = s_off[kWave];
+    for (int p = threadIdx.x; p < raw_n; p += kBlock) {
+      const int row = row_lo + p;
+      const int w = seg_of_row(row, d_ff, nseg) - seg_lo;
+      const int e = row - seg_row(seg_lo + w, d_ff, nseg);
+      if (e < s_cnt[w]) {
+        l_idx[s_off[w] + e] = raw_idx[p];
+        l_z[s_off[w] + e] = raw_z[p];
+      }
+    }
+    __syncthreads();
+  }
+
+  const int ch = slice * kWave + lane;
   const bool cvalid = ch < C;
-
   float acc[EPC];
 #pragma unroll
   for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-
-  const int n = DENSE ? d_ff : segment_offsets(seg_count, nseg, s_pre);
-  for (int base = 0; base < n; base += kListWindow) {
-    const int wn = min(kListWindow, n - base);
-    if (!DENSE) {
-      stage_window(s_pre, nseg, base, wn, s_slot);
-      __syncthreads();
-    }
-    for (int k = rg; k < wn; k += NRG * U) {
-      uint4 wv[U];
-      float zz[U];
+  for (int k = wave; k < n; k += kWaves * U) {
+    uint4 wv[U];
+    float zz[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int kk = k + u * NRG;
-        const bool ok = kk < wn;
-        const int slot = ok ? (DENSE ? base + kk : s_slot[kk]) : 0;
-        const int row = DENSE ? slot : (ok ? seg_idx[slot] : 0);
-        zz[u] = ok ? seg_zval[slot] : 0.f;
-        wv[u] = (ok && cvalid) ? ld_weights(w_down_t + (size_t)row * C + ch) : make_uint4(0u, 0u, 0u, 0u);
+    for (int u = 0; u < U; ++u) {
+      const int kk = k + u * kWaves;
+      const bool ok = kk < n;
+      int row;
+      if constexpr (DENSE) {
+        row = row_lo + kk;
+        zz[u] = ok ? seg_zval[row] : 0.f;
+      } else {
+        row = ok ? l_idx[kk] : 0;
+        zz[u] = ok ? l_z[kk] : 0.f;
       }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        float f[EPC];
-        unpack(W{}, wv[u], f);
-#pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[e] = fmaf(zz[u], f[e], acc[e]);
-      }
+      wv[u] = (ok && cvalid) ? ld_weights(w_down_t + (size_t)row * C + ch) : make_uint4(0u, 0u, 0u, 0u);
     }
-    if (!DENSE) __syncthreads();
-  }
-
-  // fixed-order reduction over the NRG row groups: [rg][cc][e] -> NB partials -> 1
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) s_red[(rg * CPW + cc) * EPC + e] = acc[e];
-  __syncthreads();
-  {
-    const int o = threadIdx.x % OUT, blk = threadIdx.x / OUT;
-    constexpr int PER = NRG / NB;
-    float s = 0.f;
-    for (int g = blk * PER; g < (blk + 1) * PER; ++g) s += s_red[g * OUT + o];
-    s_red2[blk * OUT + o] = s;
+    for (int u = 0; u < U; ++u) {
+      float f[EPC];
+      unpack(W{}, wv[u], f);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) acc[e] = fmaf(zz[u], f[e], acc[e]);
+    }
   }
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) s_red[wave][lane * EPC + e] = acc[e];
   __syncthreads();
-  if (threadIdx.x < OUT) {
-    float s = 0.f;
-    for (int b2 = 0; b2 < NB; ++b2) s += s_red2[b2 * OUT + threadIdx.x];
-    const int col = slice * OUT + threadIdx.x;
-    if (col < d) y[col] = s;
+  for (int o = threadIdx.x; o < kWave * EPC; o += kBlock) {
+    float s = s_red[0][o];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) s += s_red[w][o];
+    const int col = slice * kWave * EPC + o;
+    if (col < d) unsafeAtomicAdd(y + col, s);
   }
 }
 
@@ -390,18 +413,22 @@ template <class W, bool LOPA, bool DENSE>
 __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restrict__ x, const float* __restrict__ z,
                                                             const void* __restrict__ gate_w,
                                                             const void* __restrict__ w_up, int T, int d, int d_ff,
-                                                            int r, float t, int slots, int32_t* __restrict__ seg_count,
+                                                            int r, int nseg, float t, int slots,
+                                                            int32_t* __restrict__ meta,
+                                                            int32_t* __restrict__ seg_count,
                                                             int32_t* __restrict__ seg_idx,
                                                             float* __restrict__ seg_act,
-                                                            float* __restrict__ seg_zval) {
-  __shared__ float s_h[kSeg][kTokChunk];
-  __shared__ int s_list[kSeg];
+                                                            float* __restrict__ seg_zval, float* __restrict__ y) {
+  __shared__ float s_h[kSegMax][kTokChunk];
+  __shared__ int s_list[kSegMax];
   __shared__ int s_cnt;
-  const int seg = blockIdx.x, row0 = seg * kSeg, nrows = min(kSeg, d_ff - row0);
+  const int seg = blockIdx.x;
+  const int row0 = seg_row(seg, d_ff, nseg), nrows = seg_row(seg + 1, d_ff, nseg) - row0;
   const int lane = lane_id(), wave = threadIdx.x / kWave;
   constexpr int kWaves = kBlock / kWave;
   const int len = LOPA ? r : d;
   const float* vec = LOPA ? z : x;
+  clear_output(y, T * d, meta, nseg);
 
   for (int k = wave; k < nrows; k += kWaves) {
     const size_t rowoff = (size_t)(row0 + k) * len;
@@ -452,18 +479,50 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   }
 }
 
-// thread per output column; tokens in groups of 8 accumulators
+// Exclusive prefix sum of s[0..n) in place, s[n] = total; all kBlock threads call it.
+__device__ void block_exclusive_scan(int* s, int n) {
+  __shared__ int s_wsum[kBlock / kWave];
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const int per = (n + kBlock - 1) / kBlock;
+  const int b = min((int)threadIdx.x * per, n), e = min(b + per, n);
+  int local = 0;
+  for (int i = b; i < e; ++i) local += s[i];
+  int v = local;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int u = __shfl_up(v, o);
+    if (lane >= o) v += u;
+  }
+  if (lane == kWave - 1) s_wsum[wave] = v;
+  __syncthreads();
+  int excl = v - local;
+  for (int w = 0; w < wave; ++w) excl += s_wsum[w];
+  for (int i = b; i < e; ++i) {
+    const int c = s[i];
+    s[i] = excl;
+    excl += c;
+  }
+  if (threadIdx.x == kBlock - 1) s[n] = excl;
+  __syncthreads();
+}
+
+// thread per output column; tokens in groups of 8 accumulators; y written directly
 template <class W, bool DENSE>
 __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restrict__ seg_count,
                                                          const int32_t* __restrict__ seg_idx,
                                                          const float* __restrict__ seg_zval, int nseg, int d_ff,
                                                          int slots, const void* __restrict__ w_down_t, int T, int d,
                                                          float* __restrict__ y) {
-  extern __shared__ int s_pre[];
+  extern __shared__ int s_pre[];  // [nseg + 1] list offsets (sparse only)
   __shared__ int s_slot[kListWindow];
   const int col = blockIdx.x * kBlock + threadIdx.x;
   const bool cvalid = col < d;
-  const int n = DENSE ? d_ff : segment_offsets(seg_count, nseg, s_pre);
+  int n = d_ff;
+  if (!DENSE) {
+    for (int s = threadIdx.x; s < nseg; s += kBlock) s_pre[s] = seg_count[s];
+    __syncthreads();
+    block_exclusive_scan(s_pre, nseg);
+    n = s_pre[nseg];
+  }
   for (int tg = 0; tg < T; tg += 8) {
     const int tn = min(8, T - tg);
     float acc[8];
@@ -472,7 +531,12 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
     for (int base = 0; base < n; base += kListWindow) {
       const int wn = min(kListWindow, n - base);
       if (!DENSE) {
-        stage_window(s_pre, nseg, base, wn, s_slot);
+        for (int s = threadIdx.x; s < nseg; s += kBlock) {
+          const int k0 = s_pre[s], k1 = s_pre[s + 1];
+          const int lo = max(k0, base), hi = min(k1, base + wn);
+          const int slot0 = seg_row(s, d_ff, nseg);
+          for (int k = lo; k < hi; ++k) s_slot[k - base] = slot0 + (k - k0);
+        }
         __syncthreads();
       }
       if (cvalid) {
@@ -493,6 +557,20 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
 }
 
 // ------------------------------------------------------------------ launch helpers
+// Launch a gate kernel; if the benchmark hook armed a pair of events, the launch
+// records them at the kernel's start and end and disarms the hook.
+template <class K, class... Args>
+hipError_t launch_gate_kernel(K kernel, int grid, hipStream_t s, Args... args) {
+  GateTiming ev = g_gate_timing;
+  if (ev.start) {
+    g_gate_timing = GateTiming{};
+    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, s, ev.start, ev.stop, 0, args...);
+  } else {
+    kernel<<<grid, kBlock, 0, s>>>(args...);
+  }
+  return hipGetLastError();
+}
+
 int ilog2(int v) {
   int l = 0;
   while ((1 << l) < v) ++l;
@@ -508,6 +586,36 @@ int lanes_per_row(int C, int cpl) {
 
 int cpl_for(int C) { return C <= 8 * kWave ? 8 : (C <= 16 * kWave ? 16 : 0); }
 
+int cu_count() {
+  static int cus[16] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+  const int slot = dev & 15;
+  if (cus[slot] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[slot] = n;
+  }
+  return cus[slot];
+}
+
+// Segments for the T = 1 gate kernel: one row-balanced segment per workgroup the GPU
+// can hold at once (so every CU gets the same number of rows), never more than
+// kSegMax rows per segment.  `per_cu` caches the kernel's occupancy.
+template <class K>
+int resident_segments(K kernel, int* per_cu, int d_ff) {
+  if (*per_cu == 0) {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kBlock, 0) != hipSuccess || n <= 0) n = 1;
+    *per_cu = n;
+  }
+  int g = cu_count() * *per_cu;
+  const int lo = (d_ff + kSegMax - 1) / kSegMax;
+  if (g < lo) g = lo;
+  if (g > d_ff) g = d_ff;
+  return g;
+}
+
 bool fast_ok(const Shape& sh, Gate g) {
   const int epc_ = sh.wdt == 1 ? WBf16::EPC : WF32::EPC;
   if (sh.T != 1 || sh.d % epc_ != 0 || cpl_for(sh.d / epc_) == 0) return false;
@@ -516,39 +624,41 @@ bool fast_ok(const Shape& sh, Gate g) {
 }
 
 template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU>
-hipError_t go_gate_up_t1(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t,
-                         const Workspace& ws, hipStream_t s) {
+hipError_t go_gate_up_t1(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
+                         float* y, hipStream_t s) {
   const int Cu = sh.d / W::EPC, Cg = LOPA ? sh.r / W::EPC : Cu;
   const int lpru = lanes_per_row(Cu, CPLU), lprg = lanes_per_row(Cg, CPLG);
-  k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU><<<ws.nseg, kBlock, 0, s>>>(
-      x, ws.z, static_cast<const uint4*>(gate_w), Cg, lprg, ilog2(lprg), static_cast<const uint4*>(w_up), Cu, lpru,
-      ilog2(lpru), sh.d_ff, t, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval);
-  return hipGetLastError();
+  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU>;
+  static int per_cu = 0;  // one cache per instantiation
+  ws.nseg = resident_segments(kernel, &per_cu, sh.d_ff);
+  return launch_gate_kernel(kernel, ws.nseg, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg, lprg,
+                            ilog2(lprg), static_cast<const uint4*>(w_up), Cu, lpru, ilog2(lpru), sh.d_ff, ws.nseg, t,
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d);
 }
 
 template <class W, bool LOPA, bool DENSE>
-hipError_t gate_up_fast(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t,
-                        const Workspace& ws, hipStream_t s) {
+hipError_t gate_up_fast(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
+                        float* y, hipStream_t s) {
   const int cplu = cpl_for(sh.d / W::EPC);
   if constexpr (LOPA) {
     const int cplg = cpl_for(sh.r / W::EPC);
-    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, 8, 8>(sh, x, gate_w, w_up, t, ws, s);
-    if (cplg == 8 && cplu == 16) return go_gate_up_t1<W, true, DENSE, 8, 16>(sh, x, gate_w, w_up, t, ws, s);
-    if (cplg == 16 && cplu == 8) return go_gate_up_t1<W, true, DENSE, 16, 8>(sh, x, gate_w, w_up, t, ws, s);
-    return go_gate_up_t1<W, true, DENSE, 16, 16>(sh, x, gate_w, w_up, t, ws, s);
+    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, 8, 8>(sh, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == 8 && cplu == 16) return go_gate_up_t1<W, true, DENSE, 8, 16>(sh, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == 16 && cplu == 8) return go_gate_up_t1<W, true, DENSE, 16, 8>(sh, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, true, DENSE, 16, 16>(sh, x, gate_w, w_up, t, ws, y, s);
   } else {
-    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, 8, 8>(sh, x, gate_w, w_up, t, ws, s);
-    return go_gate_up_t1<W, false, DENSE, 16, 16>(sh, x, gate_w, w_up, t, ws, s);
+    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, 8, 8>(sh, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, false, DENSE, 16, 16>(sh, x, gate_w, w_up, t, ws, y, s);
   }
 }
 
 template <class W, bool LOPA, bool DENSE>
 hipError_t gate_up_generic(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t,
-                           const Workspace& ws, hipStream_t s) {
-  k_gate_up_generic<W, LOPA, DENSE><<<ws.nseg, kBlock, 0, s>>>(x, ws.z, gate_w, w_up, sh.T, sh.d, sh.d_ff, sh.r, t,
-                                                               ws.slots, ws.seg_count, ws.seg_idx, ws.seg_act,
-                                                               ws.seg_zval);
-  return hipGetLastError();
+                           Workspace& ws, float* y, hipStream_t s) {
+  ws.nseg = (sh.d_ff + kSegGeneric - 1) / kSegGeneric;
+  return launch_gate_kernel(k_gate_up_generic<W, LOPA, DENSE>, ws.nseg, s, x, (const float*)ws.z, gate_w, w_up, sh.T,
+                            sh.d, sh.d_ff, sh.r, ws.nseg, t, ws.slots, ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act,
+                            ws.seg_zval, y);
 }
 
 template <class W>
@@ -556,7 +666,7 @@ hipError_t lopa_z(const Shape& sh, const float* x, const void* A, const Workspac
   if (fast_ok(sh, Gate::LoPA)) {
     const int C = sh.d / W::EPC;
     const int cpl = cpl_for(C), lpr = lanes_per_row(C, cpl), lg = ilog2(lpr);
-    const int rows_per_block = (kBlock / kWave) * 2 * (kWave >> lg);
+    const int rows_per_block = (kBlock / kWave) * (kWave >> lg);
     const int grid = (sh.r + rows_per_block - 1) / rows_per_block;
     if (cpl == 8)
       k_lopa_z_t1<W, 8><<<grid, kBlock, 0, s>>>(x, static_cast<const uint4*>(A), C, lpr, lg, sh.r, ws.z);
@@ -569,16 +679,37 @@ hipError_t lopa_z(const Shape& sh, const float* x, const void* A, const Workspac
   return hipGetLastError();
 }
 
+// Down-projection grid for T = 1: S column slices x R row chunks, about
+// kDownWgPerCu workgroups per CU, at most 64 segments per chunk.
+#ifndef FFN_DOWN_WG_PER_CU
+#define FFN_DOWN_WG_PER_CU 2
+#endif
+constexpr int kDownWgPerCu = FFN_DOWN_WG_PER_CU;
+
+void down_grid(int C, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
+  *S = (C + kWave - 1) / kWave;
+  int r = (kDownWgPerCu * cu_count() + *S - 1) / *S;
+  const int rmin = (nseg + kWave - 1) / kWave;
+  if (r < rmin) r = rmin;
+  if (r > nseg) r = nseg;
+  *R = r;
+  // largest row range of a chunk: ceil(nseg / R) segments of at most ceil(d_ff / nseg) rows
+  *shmem_rows = (size_t)((nseg + r - 1) / r) * (size_t)((d_ff + nseg - 1) / nseg);
+}
+
 template <class W, bool DENSE>
 hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
-  const size_t shmem = DENSE ? 0 : sizeof(int) * (size_t)(ws.nseg + 1);
   if (sh.T == 1 && sh.d % W::EPC == 0) {
-    constexpr int CPW = 16 / W::EPC;  // 16 output columns per workgroup
     const int C = sh.d / W::EPC;
-    const int grid = (C + CPW - 1) / CPW;
-    k_down_t1<W, CPW, DENSE><<<grid, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
-                                                        static_cast<const uint4*>(w_down_t), C, sh.d, y);
+    int S, R;
+    size_t rows;
+    down_grid(C, ws.nseg, sh.d_ff, &S, &R, &rows);
+    const size_t shmem = DENSE ? 0 : 4 * sizeof(int) * rows;
+    if (shmem > 96 * 1024) return hipErrorInvalidValue;
+    k_down_t1<W, DENSE><<<S * R, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R,
+                                                      static_cast<const uint4*>(w_down_t), C, sh.d, y);
   } else {
+    const size_t shmem = DENSE ? 0 : sizeof(int) * (size_t)(ws.nseg + 1);
     const int grid = (sh.d + kBlock - 1) / kBlock;
     k_down_generic<W, DENSE><<<grid, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
                                                         ws.slots, w_down_t, sh.T, sh.d, y);
@@ -594,12 +725,12 @@ hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, co
 }
 
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w, const void* w_up,
-                          float t, const Workspace& ws, hipStream_t s) {
+                          float t, Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
   const bool fast = fast_ok(sh, g);
 #define FFN_GU(W, L, D)                                                                     \
-  return fast ? gate_up_fast<W, L, D>(sh, x, gate_w, w_up, t, ws, s)                       \
-              : gate_up_generic<W, L, D>(sh, x, gate_w, w_up, t, ws, s)
+  return fast ? gate_up_fast<W, L, D>(sh, x, gate_w, w_up, t, ws, y, s)                    \
+              : gate_up_generic<W, L, D>(sh, x, gate_w, w_up, t, ws, y, s)
   if (sh.wdt == 1) {
     if (lopa) {
       if (dense) FFN_GU(WBf16, true, true);

@@ -50,6 +50,8 @@ def lib() -> ctypes.CDLL:
             getattr(L, name).argtypes = args
         L.ffn_active_set.restype = i
         L.ffn_active_set.argtypes = [vp, i, i, i, i, vp, vp, vp, vp]
+        L.ffn_time_next_gate_kernel.restype = i
+        L.ffn_time_next_gate_kernel.argtypes = [vp, vp]
         L.ffn_status_string.restype = ctypes.c_char_p
         L.ffn_status_string.argtypes = [i]
         _lib = L
@@ -157,6 +159,12 @@ def ffn_active_set(ws, T, d, d_ff, r=0, stream=None, with_act=True):
     _check("ffn_active_set", rc)
     k = n.value
     return idx[:k].copy(), (None if act is None else act[:, :k].copy())
+
+
+def ffn_time_next_gate_kernel(start, stop):
+    """Arm torch.cuda.Event pair (enable_timing=True) for the next call's gate kernel."""
+    rc = lib().ffn_time_next_gate_kernel(ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event))
+    _check("ffn_time_next_gate_kernel", rc)
 
 
 def ffn_status_string(code: int) -> str:

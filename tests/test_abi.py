@@ -19,7 +19,7 @@ def test_exports_every_declared_function():
     names = ffn.declared_functions()
     assert set(names) >= {"ffn_workspace_bytes", "ffn_dense_forward", "ffn_sparse_forward",
                           "ffn_lopa_sparse_forward", "ffn_lopa_dense_forward", "ffn_active_set",
-                          "ffn_status_string"}
+                          "ffn_status_string", "ffn_time_next_gate_kernel"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -89,6 +89,12 @@ def test_active_set_argument_errors():
     assert L.ffn_active_set(None, 1, 64, 128, 0, ctypes.byref(n), A, None, None) == -1
     assert L.ffn_active_set(A, 65, 64, 128, 0, ctypes.byref(n), A, None, None) == -2
     assert L.ffn_active_set(A, 1, 64, 128, -1, ctypes.byref(n), A, None, None) == -2
+
+
+def test_timing_hook_argument_errors():
+    assert L.ffn_time_next_gate_kernel(A, None) == -1
+    assert L.ffn_time_next_gate_kernel(None, A) == -1
+    assert L.ffn_time_next_gate_kernel(None, None) == 0
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
