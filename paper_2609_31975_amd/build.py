@@ -12,8 +12,9 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("ffn_api.hip", "ffn_kernels.hip")]
-HEADERS = [os.path.join(ROOT, "include", "ffn_sparse.h"), os.path.join(PKG, "csrc", "ffn_internal.h")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("ffn_api.hip", "ffn_kernels.hip", "ffn_batched.hip")]
+HEADERS = [os.path.join(ROOT, "include", "ffn_sparse.h")] + [os.path.join(PKG, "csrc", f) for f in
+                                                             ("ffn_internal.h", "ffn_device.h")]
 LIB = os.path.join(PKG, "libffn_sparse.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -60,4 +60,13 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, c
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s);
 
+// Matrix-core kernels for batches of 2..64 tokens with bf16 weights (ffn_batched.hip).
+bool batched_ok(const Shape& sh, Gate g);
+bool batched_down_ok(const Shape& sh);
+hipError_t launch_lopa_z_batched(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
+                                 hipStream_t s);
+hipError_t launch_gate_up_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w,
+                                  const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
+hipError_t launch_down_batched(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s);
+
 }  // namespace ffn

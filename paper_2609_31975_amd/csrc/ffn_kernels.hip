@@ -19,63 +19,11 @@
 // first row.
 #include <hip/hip_ext.h>
 
+#include "ffn_device.h"
 #include "ffn_internal.h"
 
 namespace ffn {
 namespace {
-
-// ------------------------------------------------------------------ weight formats
-struct WBf16 {
-  static constexpr int EPC = 8;  // elements per 16-byte chunk
-};
-struct WF32 {
-  static constexpr int EPC = 4;
-};
-
-__device__ __forceinline__ void unpack(WBf16, const uint4& v, float (&f)[8]) {
-  // a bf16 is the high half of an fp32: shift the low element up, mask the high one
-  f[0] = __uint_as_float(v.x << 16);
-  f[1] = __uint_as_float(v.x & 0xffff0000u);
-  f[2] = __uint_as_float(v.y << 16);
-  f[3] = __uint_as_float(v.y & 0xffff0000u);
-  f[4] = __uint_as_float(v.z << 16);
-  f[5] = __uint_as_float(v.z & 0xffff0000u);
-  f[6] = __uint_as_float(v.w << 16);
-  f[7] = __uint_as_float(v.w & 0xffff0000u);
-}
-__device__ __forceinline__ void unpack(WF32, const uint4& v, float (&f)[4]) {
-  f[0] = __uint_as_float(v.x);
-  f[1] = __uint_as_float(v.y);
-  f[2] = __uint_as_float(v.z);
-  f[3] = __uint_as_float(v.w);
-}
-
-__device__ __forceinline__ float welem(WBf16, const void* w, size_t k) {
-  return __uint_as_float((uint32_t)(static_cast<const uint16_t*>(w)[k]) << 16);
-}
-__device__ __forceinline__ float welem(WF32, const void* w, size_t k) {
-  return static_cast<const float*>(w)[k];
-}
-
-// Weights are read once per call: stream them past the caches.
-__device__ __forceinline__ uint4 ld_weights(const uint4* p) {
-  typedef unsigned u4v __attribute__((ext_vector_type(4)));
-  u4v t = __builtin_nontemporal_load(reinterpret_cast<const u4v*>(p));
-  return make_uint4(t.x, t.y, t.z, t.w);
-}
-
-__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
-
-// sum over aligned groups of `width` lanes (width a power of two <= 64)
-__device__ __forceinline__ float group_sum(float v, int width) {
-  for (int o = width >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) { return group_sum(v, kWave); }
-
-__device__ __forceinline__ int rank_in_mask(uint64_t m) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-}
 
 // ------------------------------------------------------------------ row-dot helpers
 // A row of C 16-byte chunks is covered by a group of `lpr` lanes; lane q of the group
@@ -176,17 +124,6 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, int C, i
   }
 }
 
-// ------------------------------------------------------------------ segments
-// The d_ff neurons are split into nseg row-balanced segments; segment w covers rows
-// [seg_row(w), seg_row(w + 1)) (at most kSegMax of them).  Its active neurons occupy
-// slots seg_row(w) .. seg_row(w) + seg_count[w] - 1, in ascending neuron order.
-__device__ __forceinline__ int seg_row(int w, int d_ff, int nseg) { return (int)(((int64_t)w * d_ff) / nseg); }
-
-// the segment that contains `row`: the largest w with seg_row(w) <= row
-__device__ __forceinline__ int seg_of_row(int row, int d_ff, int nseg) {
-  return (int)((((int64_t)row + 1) * nseg + d_ff - 1) / d_ff) - 1;
-}
-
 // Ballot compaction of one segment (run by the first wave): neurons whose gate value
 // exceeds t (all neurons if `all`) get ascending ranks; their activation h - t is
 // kept in LDS for the W_up phase and published with the neuron index.
@@ -214,13 +151,6 @@ __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int
       seg_count[seg] = cnt;
     }
   }
-}
-
-// The gate kernels clear y (the down kernel accumulates into it) and record the
-// segment count for the inspection hook.
-__device__ __forceinline__ void clear_output(float* __restrict__ y, int n, int32_t* meta, int nseg) {
-  for (int j = blockIdx.x * kBlock + threadIdx.x; j < n; j += gridDim.x * kBlock) y[j] = 0.f;
-  if (blockIdx.x == 0 && threadIdx.x == 0) meta[0] = nseg;
 }
 
 // ------------------------------------------------------------------ fast kernels, T = 1
@@ -479,32 +409,6 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   }
 }
 
-// Exclusive prefix sum of s[0..n) in place, s[n] = total; all kBlock threads call it.
-__device__ void block_exclusive_scan(int* s, int n) {
-  __shared__ int s_wsum[kBlock / kWave];
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  const int per = (n + kBlock - 1) / kBlock;
-  const int b = min((int)threadIdx.x * per, n), e = min(b + per, n);
-  int local = 0;
-  for (int i = b; i < e; ++i) local += s[i];
-  int v = local;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int u = __shfl_up(v, o);
-    if (lane >= o) v += u;
-  }
-  if (lane == kWave - 1) s_wsum[wave] = v;
-  __syncthreads();
-  int excl = v - local;
-  for (int w = 0; w < wave; ++w) excl += s_wsum[w];
-  for (int i = b; i < e; ++i) {
-    const int c = s[i];
-    s[i] = excl;
-    excl += c;
-  }
-  if (threadIdx.x == kBlock - 1) s[n] = excl;
-  __syncthreads();
-}
-
 // thread per output column; tokens in groups of 8 accumulators; y written directly
 template <class W, bool DENSE>
 __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restrict__ seg_count,
@@ -557,20 +461,6 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
 }
 
 // ------------------------------------------------------------------ launch helpers
-// Launch a gate kernel; if the benchmark hook armed a pair of events, the launch
-// records them at the kernel's start and end and disarms the hook.
-template <class K, class... Args>
-hipError_t launch_gate_kernel(K kernel, int grid, hipStream_t s, Args... args) {
-  GateTiming ev = g_gate_timing;
-  if (ev.start) {
-    g_gate_timing = GateTiming{};
-    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, s, ev.start, ev.stop, 0, args...);
-  } else {
-    kernel<<<grid, kBlock, 0, s>>>(args...);
-  }
-  return hipGetLastError();
-}
-
 int ilog2(int v) {
   int l = 0;
   while ((1 << l) < v) ++l;
@@ -599,9 +489,13 @@ int cu_count() {
   return cus[slot];
 }
 
-// Segments for the T = 1 gate kernel: one row-balanced segment per workgroup the GPU
-// can hold at once (so every CU gets the same number of rows), never more than
-// kSegMax rows per segment.  `per_cu` caches the kernel's occupancy.
+// Segments for the T = 1 gate kernel: kSegWaves row-balanced segments per workgroup
+// slot the GPU holds at once (so every CU gets the same number of rows), never more
+// than kSegMax rows per segment.  `per_cu` caches the kernel's occupancy.
+#ifndef FFN_SEG_WAVES
+#define FFN_SEG_WAVES 1
+#endif
+constexpr int kSegWaves = FFN_SEG_WAVES;
 template <class K>
 int resident_segments(K kernel, int* per_cu, int d_ff) {
   if (*per_cu == 0) {
@@ -609,7 +503,7 @@ int resident_segments(K kernel, int* per_cu, int d_ff) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kBlock, 0) != hipSuccess || n <= 0) n = 1;
     *per_cu = n;
   }
-  int g = cu_count() * *per_cu;
+  int g = cu_count() * *per_cu * kSegWaves;
   const int lo = (d_ff + kSegMax - 1) / kSegMax;
   if (g < lo) g = lo;
   if (g > d_ff) g = d_ff;
@@ -721,12 +615,14 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
 
 // ------------------------------------------------------------------ launchers
 hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
+  if (batched_ok(sh, Gate::LoPA)) return launch_lopa_z_batched(sh, x, lopa_a, ws, s);
   return sh.wdt == 1 ? lopa_z<WBf16>(sh, x, lopa_a, ws, s) : lopa_z<WF32>(sh, x, lopa_a, ws, s);
 }
 
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w, const void* w_up,
                           float t, Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
+  if (batched_ok(sh, g)) return launch_gate_up_batched(sh, g, dense, x, gate_w, w_up, t, ws, y, s);
   const bool fast = fast_ok(sh, g);
 #define FFN_GU(W, L, D)                                                                     \
   return fast ? gate_up_fast<W, L, D>(sh, x, gate_w, w_up, t, ws, y, s)                    \
@@ -750,6 +646,7 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, c
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s) {
+  if (batched_down_ok(sh)) return launch_down_batched(sh, w_down_t, ws, y, s);
   if (sh.wdt == 1) return dense ? down<WBf16, true>(sh, w_down_t, ws, y, s) : down<WBf16, false>(sh, w_down_t, ws, y, s);
   return dense ? down<WF32, true>(sh, w_down_t, ws, y, s) : down<WF32, false>(sh, w_down_t, ws, y, s);
 }

@@ -36,6 +36,12 @@ SMALL = [
     ("lopa_bf16_odd_r", 1, 264, 1000, 36, BF16, 1.0),
     ("lopa_f32", 1, 256, 1024, 32, F32, 1.2816),
     ("lopa_bf16_T5", 5, 264, 1000, 40, BF16, 1.0),
+    ("std_bf16_T2", 2, 264, 1000, 0, BF16, 1.0),            # matrix-core gate, vector down (2 tokens)
+    ("std_bf16_T8", 8, 264, 1000, 0, BF16, 1.2),
+    ("std_bf16_T12", 12, 264, 1000, 0, BF16, 1.2),          # matrix-core down, one token tile
+    ("lopa_bf16_T20", 20, 264, 1000, 40, BF16, 1.3),        # two token tiles
+    ("std_bf16_T40", 40, 136, 300, 0, BF16, 1.5),           # four token tiles, short rows
+    ("std_bf16_T64", 64, 264, 1000, 0, BF16, 1.6),
     ("very_small", 1, 8, 3, 0, BF16, 0.0),
     ("d_is_1", 1, 1, 5, 0, F32, 0.0),
     ("lopa_r_is_1", 2, 16, 40, 1, F32, 0.1),
