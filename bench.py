@@ -320,16 +320,26 @@ def copy_calibration(K):
     return dict(kernel="neg", bytes_read=n, bytes_written=n, launches=K)
 
 
+def kernel_source_digest():
+    """sha256 over every GPU source and header of the library (in a fixed order): a
+    counter profile holds for the kernels it was taken on only."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2609_31975_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode() + b"\0" + open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
 def recorded_traffic(workload):
     """HBM bytes per launch of the dominant kernel from the committed counter profile
     (profiles/<kernel>_<workload>_pmc.json), or None if the kernels changed since."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", f"k_gate_up_t1_{workload}_pmc.json")
     if not os.path.exists(path):
         return None, None
     rec = json.load(open(path))
-    src = open(os.path.join(ROOT, "paper_2609_31975_amd", "csrc", "ffn_kernels.hip"), "rb").read()
-    if rec.get("kernel_source_sha256") != hashlib.sha256(src).hexdigest():
+    if rec.get("kernel_source_sha256") != kernel_source_digest():
         return None, path
     return int(rec["traffic_bytes"]), path
 

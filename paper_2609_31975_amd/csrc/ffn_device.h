@@ -53,9 +53,28 @@ __device__ __forceinline__ uint4 ld_weights(const uint4* p) {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
-// sum over aligned groups of `width` lanes (width a power of two <= 64)
+// Cross-lane moves within a row of 16 lanes (DPP: a modifier of one VALU op, no LDS
+// round trip).  After xor-1 and xor-2 steps every lane of a quad holds the quad's sum;
+// mirroring within 8 lanes then pairs quad 0 with quad 1, mirroring within 16 pairs
+// the two halves of the row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm 1,0,3,2
+constexpr int kDppXor2 = 0x4E;        // quad_perm 2,3,0,1
+constexpr int kDppHalfMirror = 0x141; // row_half_mirror
+constexpr int kDppMirror = 0x140;     // row_mirror
+
+// sum over aligned groups of `width` lanes (width a power of two <= 64); every lane of
+// a group ends with the group's sum
 __device__ __forceinline__ float group_sum(float v, int width) {
-  for (int o = width >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if (width >= 2) v += dpp_move<kDppXor1>(v);
+  if (width >= 4) v += dpp_move<kDppXor2>(v);
+  if (width >= 8) v += dpp_move<kDppHalfMirror>(v);
+  if (width >= 16) v += dpp_move<kDppMirror>(v);
+  if (width >= 32) v += __shfl_xor(v, 16);
+  if (width >= 64) v += __shfl_xor(v, 32);
   return v;
 }
 __device__ __forceinline__ float wave_sum(float v) { return group_sum(v, kWave); }
