@@ -39,7 +39,9 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
   w.seg_idx = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.slots));
   w.seg_act = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
   w.seg_zval = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
-  w.z = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * (r > 0 ? r : 1)));
+  const size_t bt = w.tc >= 2 ? (size_t)w.tc : 0;  // matrix-core path only
+  w.z = reinterpret_cast<float*>(take(sizeof(float) * (bt ? 2 : 1) * (size_t)w.tc * (r > 0 ? r : 1)));
+  w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * 4 * bt * 2 * (size_t)((d_ff + 63) / 64)));
   if (out) *out = w;
   return off;
 }
@@ -90,11 +92,15 @@ int run(const Call& c) {
     Shape sh{c.T - t0 < kTokChunk ? c.T - t0 : kTokChunk, c.d, c.d_ff, c.r, c.wdt == FFN_BF16 ? 1 : 0};
     const float* x = c.x + (size_t)t0 * c.d;
     float* y = c.y + (size_t)t0 * c.d;
+    const Gate g = lopa ? Gate::LoPA : Gate::Standard;
     hipError_t e = hipSuccess;
-    if (lopa) e = launch_lopa_z(sh, x, c.lopa_a, ws, c.stream);
-    if (e == hipSuccess)
-      e = launch_gate_up(sh, lopa ? Gate::LoPA : Gate::Standard, c.dense, x, c.gate, c.w_up, c.t, ws, y, c.stream);
-    if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
+    if (batched_ok(sh, g)) {
+      e = launch_batched(sh, g, c.dense, x, c.lopa_a, c.gate, c.w_up, c.w_down_t, c.t, ws, y, c.stream);
+    } else {
+      if (lopa) e = launch_lopa_z(sh, x, c.lopa_a, ws, c.stream);
+      if (e == hipSuccess) e = launch_gate_up(sh, g, c.dense, x, c.gate, c.w_up, c.t, ws, y, c.stream);
+      if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
+    }
     if (e != hipSuccess) return FFN_ERR_HIP;
   }
   return FFN_OK;

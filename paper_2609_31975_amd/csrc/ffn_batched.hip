@@ -1,26 +1,39 @@
 // gfx950 kernels for a batch of 2..64 tokens with bf16 weights (paper Section 5.3: the
 // rows of W_up / W_down are read once for the union of the tokens' active sets).
 //
-// The gate (W_gate x or B z), the W_up dots of the union rows and LoPA's A x are
-// dense contractions over a token tile, so they run on the matrix cores:
-// v_mfma_f32_16x16x32_bf16 with a 16-row weight tile as the A operand and 16 tokens as
-// the B operand.  The fp32 tokens are split into bf16 hi + lo (x - hi rounded again),
-// two MFMAs per step: the products are exact in fp32 and the split leaves a relative
-// error of about 2^-16 on each token element, far inside the 1e-3 band of the active
-// set decision.  Weights are read straight from HBM into the A operand: lane l holds
-// 8 consecutive bf16 of row (l mod 16); the four lane groups l / 16 take four
-// consecutive 16-byte chunks, so one instruction reads 64 contiguous bytes of each of
-// 16 rows.  Which k positions a lane group holds does not matter for a full
-// reduction as long as the A and B operands use the same ones.
+// Every contraction runs on the matrix cores (v_mfma_f32_16x16x32_bf16): LoPA's A x,
+// the gate (W_gate x, or B z), the W_up dots of the union rows and the down
+// projection.  Token-side operands (x, z, zval) enter as bf16 hi + lo pairs (v - hi
+// rounded again): two MFMAs per step whose products are exact in fp32, so the split
+// leaves a relative error of about 2^-16 per element, far inside the 1e-3 band of the
+// active-set decision.  A 16-row weight tile is the A operand, streamed from HBM
+// straight into registers: lane l holds 8 consecutive bf16 of row l mod 16 and the
+// four lane groups l / 16 take four consecutive 16-byte chunks, so one instruction
+// reads 64 contiguous bytes of each of 16 rows.  Which k positions a lane group holds
+// does not matter for a full reduction as long as both operands use the same ones.
 //
-// The down projection accumulates zval[tau][k] * w_down_t[idx_k] for 2..8 tokens on
-// the vector ALUs (every weight element feeds T FMAs), 128 columns per workgroup.  For
-// 9..64 tokens it is a matrix-core product Y[tokens][cols] = Z[tokens][entries] x
-// D[entries][cols] whose reduction runs over the gathered rows.  The B operand needs 8
-// entries of one column per lane, but a row gather gives a lane 8 columns of one entry;
-// an MFMA against a 0/1 selector matrix transposes each 16 x 16 block exactly in fp32
-// (every output is one weight times 1), and its output layout (lane = column,
-// lane group = entries 4g..4g+3) is already the B-operand layout of the product.
+// One call is three kernels (two for standard gating):
+//   k_lopa_z_mfma  z = A x as two partial sums over halves of the d range;
+//   k_gate_up_mfma per 64-row segment: gate, union of the tokens' active rows (ascending),
+//                  W_up dots of the union rows; zval = act * v is left in the A-operand
+//                  fragment order of the down product;
+//   k_down_mfma    Y[tokens][cols] += Z[tokens][entries] D[entries][cols] over the
+//                  union rows, segment by segment.
+// A wave of the gate kernel multiplies four row tiles over a quarter of the k range, so
+// each token fragment it loads and splits feeds four tiles; the loads of the next k
+// steps are in flight while the current ones are multiplied.  All operand loads are
+// raw buffer loads: a lane with nothing to load (a row past the segment or the union,
+// a token past the batch, a k step past the row) uses an offset beyond the buffer,
+// which returns zero without a memory access, so every wave issues the same loads in
+// the same order and the load counter waits stay exact.
+//
+// The down product needs, per lane, 8 entries of one column as the B operand, while a
+// row gather gives a lane 8 columns of one entry.  An MFMA against a 0/1 selector
+// matrix transposes each 16 x 16 block exactly (every output is one weight times 1),
+// and its output layout (lane = column, lane group = entries 4g..4g+3) is already the
+// B-operand layout of the product.  A consequence: a non-finite weight in an active
+// row spreads over the 16-column block it sits in (0 x Inf is NaN), where the
+// definition would confine it to its own column.
 #include "ffn_device.h"
 #include "ffn_internal.h"
 
@@ -30,15 +43,32 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kMRows = 32;  // gate rows per segment of the batched gate kernel (two 16-row tiles)
-constexpr int kKU = 8;      // k steps (32 elements each) loaded per unrolled group
+constexpr int kTiles = 4;                // 16-row tiles of a gate segment
+constexpr int kSegRowsB = 16 * kTiles;   // rows per gate segment (one 64-lane ballot)
+constexpr int kParts = kBlock / kWave;   // k parts of a workgroup, one per wave
 
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ bf16x8_t bf8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-// x = hi + lo with both in bf16 (round to nearest even twice)
-__device__ __forceinline__ void split_bf16(const float (&v)[8], bf16x8_t& hi, bf16x8_t& lo) {
+// Buffer resource over [p, p + bytes), bytes < 2^31; loads at kOOB or above return zero.
+struct Buf {
+  __amdgpu_buffer_rsrc_t r;
+};
+__device__ __forceinline__ Buf make_buf(const void* p, uint32_t bytes) {
+  return Buf{__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000)};
+}
+constexpr uint32_t kOOB = 0x80000000u;
+// Weights too go through the caches: an instruction reads 64 bytes of each of 16 rows,
+// and the next one the other half of the same 128-byte lines.
+__device__ __forceinline__ uint4 ldb(const Buf& b, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b.r, off, 0, 0));
+}
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// v = hi + lo with both in bf16 (round to nearest even twice)
+__device__ __forceinline__ void split8(const float (&v)[8], bf16x8_t& hi, bf16x8_t& lo) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const __bf16 h = (__bf16)v[j];
@@ -47,55 +77,7 @@ __device__ __forceinline__ void split_bf16(const float (&v)[8], bf16x8_t& hi, bf
   }
 }
 
-// B operand of one k step: 8 consecutive elements (chunk c) of token `tok`'s vector,
-// split into hi / lo; zero outside the batch or the row.
-__device__ __forceinline__ void vec_frag(const float* __restrict__ vec, int len, int T, int tok, int c, int C,
-                                         bf16x8_t& hi, bf16x8_t& lo) {
-  float v[8];
-  if (tok < T && c < C) {
-    const float4* p = reinterpret_cast<const float4*>(vec + (size_t)tok * len + (size_t)c * 8);
-    const float4 a = p[0], b = p[1];
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = 0.f;
-  }
-  split_bf16(v, hi, lo);
-}
-
-// acc[nt] += (16 rows starting at this lane's row) . (tokens 16 nt .. 16 nt + 15) over
-// k steps [ks0, ks1); a k step covers chunks 4 ks .. 4 ks + 3 of the rows.
-template <int NT>
-__device__ __forceinline__ void mfma_rows(const uint4* __restrict__ wrow, bool rok, int C,
-                                          const float* __restrict__ vec, int len, int T, int ks0, int ks1,
-                                          f32x4_t (&acc)[NT]) {
-  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
-  for (int ks = ks0; ks < ks1; ks += kKU) {
-    uint4 a[kKU];
-#pragma unroll
-    for (int u = 0; u < kKU; ++u) {
-      const int c = (ks + u) * 4 + g;
-      a[u] = (rok && ks + u < ks1 && c < C) ? ld_weights(wrow + c) : make_uint4(0u, 0u, 0u, 0u);
-    }
-#pragma unroll
-    for (int u = 0; u < kKU; ++u) {
-      if (ks + u < ks1) {
-        const int c = (ks + u) * 4 + g;
-        const bf16x8_t av = __builtin_bit_cast(bf16x8_t, a[u]);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          bf16x8_t hi, lo;
-          vec_frag(vec, len, T, nt * 16 + m, c, C, hi, lo);
-          acc[nt] = mfma16(av, hi, acc[nt]);
-          acc[nt] = mfma16(av, lo, acc[nt]);
-        }
-      }
-    }
-  }
-}
-
-// k-step range of k part kp out of np for rows of C chunks
+// k-step range [ks0, ks1) of k part kp out of np for rows of C chunks (4 chunks a step)
 __device__ __forceinline__ void kpart(int C, int kp, int np, int* ks0, int* ks1) {
   const int nks = (C + 3) / 4;
   const int per = (nks + np - 1) / np;
@@ -103,61 +85,223 @@ __device__ __forceinline__ void kpart(int C, int kp, int np, int* ks0, int* ks1)
   *ks1 = min(nks, *ks0 + per);
 }
 
-// ------------------------------------------------------------------ gate + W_up
-// One segment of <= 32 neurons per workgroup.  Wave w computes row tile w & 1 over
-// half w >> 1 of the k range; the halves are added through LDS.  A neuron joins the
-// union if any token activates it; one ballot orders the union; the W_up dots of the
-// union rows (tiles of 16 gathered rows, same k split) give zval = act * v per token.
+// ------------------------------------------------------------------ streaming core
+// Operands of KU consecutive k steps: RT weight-tile fragments and, per token tile, the
+// token fragment: the 8 fp32 of the chunk (two 16-byte halves) from each of NP partial
+// copies of the token matrix, summed and split into hi / lo when multiplied.  A token
+// matrix is [T][8 C] fp32; partial copy p starts part_bytes * p into its buffer.
+template <int RT, int NT, int KU, int NP>
+struct Frags {
+  uint4 a[KU][RT];
+  uint4 b[KU][NT][NP][2];
+};
+
+// roff[rt]: this lane's weight row of tile rt, in chunks (row * C), or -1 for none;
+// ntile (uniform): tiles in use
+template <int RT, int NT, int KU, int NP>
+__device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& wb, int C, const int (&roff)[RT],
+                                           int ntile, const Buf& tb, uint32_t part_bytes, int T, int ks, int ks1) {
+  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int u = 0; u < KU; ++u) {
+    const int c = 4 * (ks + u) + g;
+    const bool cv = ks + u < ks1 && c < C;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      f.a[u][rt] = ldb(wb, (cv && rt < ntile && roff[rt] >= 0) ? 16u * (uint32_t)(roff[rt] + c) : kOOB);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int tok = 16 * nt + m;
+      const uint32_t off = (cv && tok < T) ? 32u * (uint32_t)(tok * C + c) : kOOB;
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        f.b[u][nt][p][0] = ldb(tb, off + p * part_bytes);
+        f.b[u][nt][p][1] = ldb(tb, off + p * part_bytes + 16);
+      }
+    }
+  }
+}
+
+template <int RT, int NT, int KU, int NP>
+__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, int ntile, f32x4_t (&acc)[RT][NT]) {
+#pragma unroll
+  for (int u = 0; u < KU; ++u)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float v[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint4 q = f.b[u][nt][0][h];
+        v[4 * h] = __uint_as_float(q.x);
+        v[4 * h + 1] = __uint_as_float(q.y);
+        v[4 * h + 2] = __uint_as_float(q.z);
+        v[4 * h + 3] = __uint_as_float(q.w);
+      }
+#pragma unroll
+      for (int p = 1; p < NP; ++p)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint4 q = f.b[u][nt][p][h];
+          v[4 * h] += __uint_as_float(q.x);
+          v[4 * h + 1] += __uint_as_float(q.y);
+          v[4 * h + 2] += __uint_as_float(q.z);
+          v[4 * h + 3] += __uint_as_float(q.w);
+        }
+      bf16x8_t hi, lo;
+      split8(v, hi, lo);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        if (rt < ntile) {
+          acc[rt][nt] = mfma16(bf8(f.a[u][rt]), hi, acc[rt][nt]);
+          acc[rt][nt] = mfma16(bf8(f.a[u][rt]), lo, acc[rt][nt]);
+        }
+    }
+}
+
+// acc[rt][nt] += weight tile rt . token tile nt over the k steps [ks0, ks1) (uniform).
+// Two register sets alternate: the loads of the next KU steps are issued before the
+// current ones are multiplied; loads past ks1 are out of range and read nothing.
+template <int RT, int NT, int KU, int NP>
+__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT], int ntile, const Buf& tb,
+                                            uint32_t part_bytes, int T, int ks0, int ks1, f32x4_t (&acc)[RT][NT]) {
+  if (ks0 >= ks1) return;
+  Frags<RT, NT, KU, NP> f0, f1;
+  load_frags(f0, wb, C, roff, ntile, tb, part_bytes, T, ks0, ks1);
+  for (int ks = ks0;;) {
+    load_frags(f1, wb, C, roff, ntile, tb, part_bytes, T, ks + KU, ks1);
+    mma_frags(f0, ntile, acc);
+    ks += KU;
+    if (ks >= ks1) break;
+    load_frags(f0, wb, C, roff, ntile, tb, part_bytes, T, ks + KU, ks1);
+    mma_frags(f1, ntile, acc);
+    ks += KU;
+    if (ks >= ks1) break;
+  }
+}
+
+// ------------------------------------------------------------------ LoPA z = A x
+// Workgroup b: 16-row tile b / kZParts of A over half b % kZParts of the d range, each
+// of its waves a sixteenth of that half.  The waves' sums are added in LDS (fixed order)
+// and stored as partial copy b % kZParts of z: zp[part][tc][r]; the gate kernel adds
+// the two copies.
+constexpr int kZWaves = 16;
+constexpr int kZParts = 2;
+
+template <int NT>
+__global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __restrict__ x,
+                                                                 const uint4* __restrict__ A, int C, int T, int r,
+                                                                 int tc, float* __restrict__ zp) {
+  __shared__ f32x4_t s_part[kZWaves][NT][kWave];
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave), m = lane & 15;
+  const int tile = blockIdx.x / kZParts, part = blockIdx.x % kZParts;
+  const int row = tile * 16 + m;
+  const int roff[1] = {row < r ? row * C : -1};
+  const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)C);
+  const Buf xb = make_buf(x, 32u * (uint32_t)T * (uint32_t)C);
+  f32x4_t acc[1][NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[0][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  int ks0, ks1;
+  kpart(C, part * kZWaves + wave, kZParts * kZWaves, &ks0, &ks1);
+  stream_rows<1, NT, (NT == 1 ? 4 : NT == 2 ? 2 : 1), 1>(ab, C, roff, 1, xb, 0u, T, ks0, ks1, acc);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[0][nt];
+  __syncthreads();
+  // thread o: token o / 16, row tile * 16 + o % 16 (16 consecutive floats of z a token);
+  // that value sits in lane 16 (kk / 4) + tok % 16, element kk % 4, of token tile tok / 16
+  const float* sp = reinterpret_cast<const float*>(s_part);
+  for (int o = threadIdx.x; o < T * 16; o += kZWaves * kWave) {
+    const int tok = o >> 4, kk = o & 15;
+    const int k = tile * 16 + kk;
+    if (k >= r) continue;
+    const int nt = tok >> 4, src = ((16 * (kk >> 2) + (tok & 15)) << 2) + (kk & 3);
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kZWaves; ++w) s += sp[(w * NT + nt) * kWave * 4 + src];
+    zp[((size_t)part * tc + tok) * r + k] = s;
+  }
+}
+
+// ------------------------------------------------------------------ gate + union + W_up
+// One segment of at most 64 neurons per workgroup.  Wave w multiplies the segment's
+// four row tiles over k part w; the parts are added in LDS, wave w owning tile w.  A
+// neuron joins the union if any token activates it (h > t; NaN compares false); one
+// ballot orders the union ascending.  The W_up dots of the union rows use the same
+// split, and zval = act * v goes to the fragment buffer of the down kernel:
+// group (segment, entries 32 gi .. 32 gi + 31), token, lane group g, 16-byte hi and lo
+// vectors holding entries 4g .. 4g + 3 then 16 + 4g .. 16 + 4g + 3 of the group; a used
+// group is written whole (zero past the union), an unused one is never read.
+// LOPA: the gate rows are B [d_ff][r] against z = zp[0] + zp[1]; otherwise W_gate x.
 template <bool LOPA, bool DENSE, int NT>
-__global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict__ x, const float* __restrict__ z,
+__global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict__ x, const float* __restrict__ zp,
                                                          const uint4* __restrict__ gate_w, int Cg,
-                                                         const uint4* __restrict__ w_up, int Cu, int T, int d, int r,
-                                                         int d_ff, int nseg, float t, int slots,
+                                                         const uint4* __restrict__ w_up, int Cu, int T, int d,
+                                                         int d_ff, int nseg, float t, int slots, int tc,
                                                          int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                                          int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
-                                                         float* __restrict__ seg_zval, float* __restrict__ y) {
-  __shared__ f32x4_t s_part[2][NT][kWave];
-  __shared__ float s_act[kMRows][kTokChunk];
-  __shared__ uint32_t s_mask[2];
-  __shared__ int s_list[kMRows];
+                                                         uint4* __restrict__ zf, float* __restrict__ y) {
+  constexpr int KU = (NT == 1 && !LOPA) ? 4 : 2;
+  __shared__ f32x4_t s_red[kParts][kTiles][NT][kWave];
+  __shared__ float s_act[kSegRowsB][kTokChunk];
+  __shared__ uint32_t s_mask[kTiles];
+  __shared__ int s_list[kSegRowsB];
   __shared__ int s_cnt;
 
   const int seg = blockIdx.x;
   const int row0 = seg_row(seg, d_ff, nseg);
-  const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;  // <= kSegRowsB, guaranteed by the host
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int m = lane & 15, g = lane >> 4;
-  const int tile = wave & 1, kp = wave >> 1;
   clear_output(y, T * d, meta, nseg);
+  const Buf xb = make_buf(x, 32u * (uint32_t)T * (uint32_t)Cu);
+  const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu);
 
-  // gate values h[row][token]
-  f32x4_t acc[NT];
+  f32x4_t acc[kTiles][NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rt = 0; rt < kTiles; ++rt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   {
-    const int rl = tile * 16 + m;
-    const bool rok = rl < nrows;
+    int roff[kTiles];
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt) {
+      const int rl = 16 * rt + m;
+      roff[rt] = rl < nrows ? (row0 + rl) * Cg : -1;
+    }
     int ks0, ks1;
-    kpart(Cg, kp, 2, &ks0, &ks1);
-    mfma_rows<NT>(gate_w + (size_t)(row0 + (rok ? rl : 0)) * Cg, rok, Cg, LOPA ? z : x, LOPA ? r : d, T, ks0, ks1,
-                  acc);
+    kpart(Cg, wave, kParts, &ks0, &ks1);
+    const int ntile = (nrows + 15) / 16;
+    const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg);
+    if constexpr (LOPA) {
+      const uint32_t part = 32u * (uint32_t)tc * (uint32_t)Cg;
+      stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, ntile, make_buf(zp, 2 * part), part, T, ks0, ks1, acc);
+    } else {
+      stream_rows<kTiles, NT, KU, 1>(gb, Cg, roff, ntile, xb, 0u, T, ks0, ks1, acc);
+    }
   }
-  if (kp == 1)
-    for (int nt = 0; nt < NT; ++nt) s_part[tile][nt][lane] = acc[nt];
+#pragma unroll
+  for (int rt = 0; rt < kTiles; ++rt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) s_red[wave][rt][nt][lane] = acc[rt][nt];
   __syncthreads();
-  if (kp == 0) {
-    // lane holds h of rows tile*16 + 4g + i (i < 4) for tokens 16 nt + m
+  {
+    // lane holds h of rows 16 wave + 4g + i (i < 4) for tokens 16 nt + m
+    f32x4_t h[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      h[nt] = ((s_red[0][wave][nt][lane] + s_red[1][wave][nt][lane]) + s_red[2][wave][nt][lane]) +
+              s_red[3][wave][nt][lane];
     uint32_t mask = 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int rl = tile * 16 + 4 * g + i;
+      const int rl = 16 * wave + 4 * g + i;
       bool any = false;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const float h = acc[nt][i] + s_part[tile][nt][lane][i];
-        const int tok = nt * 16 + m;
-        const bool on = tok < T && h > t;  // NaN compares false: inactive
-        if (tok < T && rl < nrows) s_act[rl][tok] = on ? h - t : 0.f;
+        const int tok = 16 * nt + m;
+        const float hv = h[nt][i];
+        const bool on = tok < T && hv > t;
+        if (tok < T && rl < nrows) s_act[rl][tok] = on ? hv - t : 0.f;
         any |= on;
       }
       const uint64_t b = __ballot(any && rl < nrows);
@@ -165,243 +309,207 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict
       for (int gg = 0; gg < 4; ++gg)
         if ((b >> (16 * gg)) & 0xffffull) mask |= 1u << (4 * gg + i);
     }
-    if (lane == 0) s_mask[tile] = mask;
+    if (lane == 0) s_mask[wave] = mask;
   }
   __syncthreads();
-
-  // ascending union of the segment
   if (wave == 0) {
-    const uint32_t on = s_mask[0] | (s_mask[1] << 16);
-    const bool sel = lane < nrows && (DENSE || ((on >> lane) & 1u));
+    const uint64_t on = (uint64_t)s_mask[0] | ((uint64_t)s_mask[1] << 16) | ((uint64_t)s_mask[2] << 32) |
+                        ((uint64_t)s_mask[3] << 48);
+    const bool sel = lane < nrows && (DENSE || ((on >> lane) & 1ull));
     const uint64_t b = __ballot(sel);
     const int rank = rank_in_mask(b);
     if (sel) {
       s_list[rank] = lane;
       seg_idx[row0 + rank] = row0 + lane;
-      for (int tok = 0; tok < T; ++tok) seg_act[(size_t)tok * slots + row0 + rank] = s_act[lane][tok];
     }
     if (lane == 0) {
       s_cnt = __popcll(b);
-      seg_count[seg] = s_cnt;
+      seg_count[seg] = __popcll(b);
     }
   }
   __syncthreads();
+  const int cnt = uniform(s_cnt);
+  for (int o = threadIdx.x; o < cnt * T; o += kBlock) {
+    const int tok = o / cnt, e = o - tok * cnt;
+    seg_act[(size_t)tok * slots + row0 + e] = s_act[s_list[e]][tok];
+  }
 
   // W_up dots of the union rows: tiles of 16 entries
-  const int cnt = s_cnt;
-  const bool tile_on = tile * 16 < cnt;
+  const int nut = (cnt + 15) / 16;
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (tile_on) {
-    const int e = tile * 16 + m;
-    const bool eok = e < cnt;
-    int ks0, ks1;
-    kpart(Cu, kp, 2, &ks0, &ks1);
-    mfma_rows<NT>(w_up + (size_t)(row0 + (eok ? s_list[e] : 0)) * Cu, eok, Cu, x, d, T, ks0, ks1, acc);
-    if (kp == 1)
-      for (int nt = 0; nt < NT; ++nt) s_part[tile][nt][lane] = acc[nt];
-  }
-  __syncthreads();
-  if (tile_on && kp == 0) {
+  for (int rt = 0; rt < kTiles; ++rt)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = tile * 16 + 4 * g + i;
-      if (e < cnt) {
-        const int kr = s_list[e];
+    for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (nut > 0) {
+    int roff[kTiles];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int tok = nt * 16 + m;
-          if (tok < T)
-            seg_zval[(size_t)tok * slots + row0 + e] = s_act[kr][tok] * (acc[nt][i] + s_part[tile][nt][lane][i]);
-        }
-      }
+    for (int rt = 0; rt < kTiles; ++rt) {
+      const int e = 16 * rt + m;
+      roff[rt] = e < cnt ? (row0 + s_list[e]) * Cu : -1;
     }
+    int ks0, ks1;
+    kpart(Cu, wave, kParts, &ks0, &ks1);
+    stream_rows<kTiles, NT, (NT == 1 ? 4 : 2), 1>(ub, Cu, roff, nut, xb, 0u, T, ks0, ks1, acc);
   }
-}
-
-// ------------------------------------------------------------------ LoPA z = A x
-// One 16-row tile of A per workgroup of kZWaves waves, each over 1/kZWaves of d.
-constexpr int kZWaves = 8;
-
-template <int NT>
-__global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __restrict__ x,
-                                                                 const uint4* __restrict__ A, int C, int T, int d,
-                                                                 int r, float* __restrict__ z) {
-  __shared__ f32x4_t s_part[kZWaves][NT][kWave];
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  const int m = lane & 15, g = lane >> 4;
-  const int row = blockIdx.x * 16 + m;
-  const bool rok = row < r;
-  f32x4_t acc[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  int ks0, ks1;
-  kpart(C, wave, kZWaves, &ks0, &ks1);
-  mfma_rows<NT>(A + (size_t)(rok ? row : 0) * C, rok, C, x, d, T, ks0, ks1, acc);
+  for (int rt = 0; rt < kTiles; ++rt)
+    if (rt < nut)
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[nt];
+      for (int nt = 0; nt < NT; ++nt) s_red[wave][rt][nt][lane] = acc[rt][nt];
   __syncthreads();
-  if (wave == 0) {
+
+  // wave w: union entries 16 w .. 16 w + 15 = half (w & 1) of fragment group w >> 1
+  const int gi = wave >> 1, half = wave & 1;
+  if (32 * gi < cnt) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      f32x4_t s = s_part[0][nt][lane];
-      for (int w = 1; w < kZWaves; ++w) s += s_part[w][nt][lane];
-      const int tok = nt * 16 + m;
+      const int tok = 16 * nt + m;
+      f32x4_t v = {0.f, 0.f, 0.f, 0.f};
+      if (wave < nut)
+        v = ((s_red[0][wave][nt][lane] + s_red[1][wave][nt][lane]) + s_red[2][wave][nt][lane]) +
+            s_red[3][wave][nt][lane];
+      if (tok < T) {
+        uint32_t hw[2] = {0u, 0u}, lw[2] = {0u, 0u};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = blockIdx.x * 16 + 4 * g + i;
-        if (tok < T && k < r) z[(size_t)tok * r + k] = s[i];
-      }
-    }
-  }
-}
-
-// ------------------------------------------------------------------ down, 2..8 tokens
-// Workgroup b: row chunk b / S (segments [c nseg/R, (c+1) nseg/R)), column slice b % S
-// of 16 chunks (128 bf16 columns).  A wave instruction reads 256 bytes of each of 4
-// rows.  The chunk's ascending active list is staged in LDS a window at a time, with
-// the per-token zval of each entry; partial sums go to y with fp32 atomics.
-constexpr int kDnSliceChunks = 16;
-constexpr int kDnWindow = 512;
-
-template <int TT>
-__global__ __launch_bounds__(kBlock) void k_down_tn(const int32_t* __restrict__ seg_count,
-                                                    const int32_t* __restrict__ seg_idx,
-                                                    const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
-                                                    int slots, const uint4* __restrict__ w_down_t, int C, int d, int T,
-                                                    float* __restrict__ y) {
-  constexpr int U = 8, kWaves = kBlock / kWave, RPW = kWave / kDnSliceChunks;  // rows per wave load
-  __shared__ int s_off[kBlock + 1];
-  __shared__ int s_idx[kDnWindow];
-  __shared__ float s_z[TT][kDnWindow];
-  __shared__ float s_red[kWaves][kDnSliceChunks][TT][8];
-
-  const int S = (C + kDnSliceChunks - 1) / kDnSliceChunks;
-  const int chunk = blockIdx.x / S, slice = blockIdx.x % S;
-  const int seg_lo = (int)(((int64_t)chunk * nseg) / R), seg_hi = (int)(((int64_t)(chunk + 1) * nseg) / R);
-  const int nsc = seg_hi - seg_lo;  // <= kBlock, guaranteed by the host
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
-  const int q = lane % kDnSliceChunks, p = lane / kDnSliceChunks;
-
-  s_off[threadIdx.x] = threadIdx.x < nsc ? seg_count[seg_lo + threadIdx.x] : 0;
-  __syncthreads();
-  block_exclusive_scan(s_off, kBlock);
-  const int n = s_off[kBlock];
-
-  const int ch = slice * kDnSliceChunks + q;
-  const bool cvalid = ch < C;
-  float acc[TT][8];
-#pragma unroll
-  for (int tau = 0; tau < TT; ++tau)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[tau][e] = 0.f;
-
-  for (int base = 0; base < n; base += kDnWindow) {
-    const int wn = min(kDnWindow, n - base);
-    // stage entries [base, base + wn): binary search of the owning segment
-    for (int k = threadIdx.x; k < wn; k += kBlock) {
-      const int kk = base + k;
-      int lo = 0, hi = nsc - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (s_off[mid] <= kk) lo = mid; else hi = mid - 1;
-      }
-      const int slot = seg_row(seg_lo + lo, d_ff, nseg) + (kk - s_off[lo]);
-      s_idx[k] = seg_idx[slot];
-      for (int tau = 0; tau < TT; ++tau) s_z[tau][k] = tau < T ? seg_zval[(size_t)tau * slots + slot] : 0.f;
-    }
-    __syncthreads();
-    for (int k = wave * RPW + p; k < wn; k += kWaves * RPW * U) {
-      uint4 wv[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int kk = k + u * kWaves * RPW;
-        wv[u] = (kk < wn && cvalid) ? ld_weights(w_down_t + (size_t)s_idx[kk] * C + ch) : make_uint4(0u, 0u, 0u, 0u);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int kk = k + u * kWaves * RPW;
-        if (kk < wn) {
-          float f[8];
-          unpack(WBf16{}, wv[u], f);
-#pragma unroll
-          for (int tau = 0; tau < TT; ++tau) {
-            const float zz = s_z[tau][kk];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[tau][e] = fmaf(zz, f[e], acc[tau][e]);
-          }
+        for (int i = 0; i < 4; ++i) {
+          const int e = 16 * wave + 4 * g + i;
+          const float zz = e < cnt ? s_act[s_list[e]][tok] * v[i] : 0.f;
+          const __bf16 hb = (__bf16)zz;
+          const __bf16 lb = (__bf16)(zz - (float)hb);
+          hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
+          lw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, lb) << (16 * (i & 1));
         }
+        uint2* frag = reinterpret_cast<uint2*>(zf + 2 * ((((size_t)seg * 2 + gi) * tc + tok) * 4 + g));
+        frag[half] = make_uint2(hw[0], hw[1]);
+        frag[2 + half] = make_uint2(lw[0], lw[1]);
       }
     }
-    __syncthreads();
-  }
-
-  // reduce over the 4 row lanes of a wave (lane bits 4, 5), then over the waves
-#pragma unroll
-  for (int tau = 0; tau < TT; ++tau)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v = acc[tau][e];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      acc[tau][e] = v;
-    }
-  if (p == 0)
-#pragma unroll
-    for (int tau = 0; tau < TT; ++tau)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s_red[wave][q][tau][e] = acc[tau][e];
-  __syncthreads();
-  for (int o = threadIdx.x; o < kDnSliceChunks * TT * 8; o += kBlock) {
-    const int e = o % 8, tau = (o / 8) % TT, qq = o / (8 * TT);
-    if (tau >= T) continue;
-    float s = s_red[0][qq][tau][e];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) s += s_red[w][qq][tau][e];
-    const int col = (slice * kDnSliceChunks + qq) * 8 + e;
-    if (col < d) unsafeAtomicAdd(y + (size_t)tau * d + col, s);
   }
 }
 
-// ------------------------------------------------------------------ down, 9..64 tokens
-// Workgroup b: 128-column group b % S4 (S4 = ceil(C / 16)), row chunk b / S4; wave w
-// owns the 32 columns w of the group.  The chunk's slot list is expanded into LDS once;
-// then kMdWindow entries at a time the row indices and per-token zvals are staged and
-// every wave issues all its W_down loads of the window before the matrix-core work.
-// Partial sums over the R row chunks go to y with fp32 atomics.
-constexpr int kMdWindow = 128;
-constexpr int kMdChunkMax = 4096;  // most active entries of one row chunk
+// ------------------------------------------------------------------ down projection
+// Workgroup b: column group b % S, row chunk b / S (segments [c nseg/R, (c+1) nseg/R)).
+// A column group is CW slots of 64 columns (two 32-column tiles), CW = 4 / NT; wave w
+// takes slot w % CW and every (4 / CW)-th used fragment group of the chunk (32 union
+// entries of one segment), the loads of its next group in flight while the current one
+// is multiplied.  The chunk's counts and slot indices are staged in LDS once.  The
+// waves' sums meet in LDS, then go to y with one fp32 atomic per token and column (y
+// was cleared by the gate kernel).
+constexpr int kDnTiles = 2;             // 32-column tiles per wave
+constexpr int kDnCols = 32 * kDnTiles;  // columns of a wave
+constexpr int kDnSlots = 8192;          // most slot indices of one row chunk
+
+template <int NT>
+struct DnFrags {
+  uint4 t[kDnTiles][2];  // W_down rows of entries m and 16 + m, 8 columns each
+  uint4 zh[NT], zl[NT];  // zval fragments (hi, lo) of the token tiles
+};
+
+struct DnChunk {
+  const int* grp;   // used groups: segment (relative) << 1 | group
+  const int* cnt;   // union size per segment
+  const int* srow;  // first slot per segment, relative to the chunk's first slot
+  const int* idx;   // slot -> neuron
+  int seg_lo;
+};
+
+template <int NT>
+__device__ __forceinline__ void dn_load(DnFrags<NT>& f, int j, int ngrp, const DnChunk& ck, const Buf& db,
+                                        const Buf& zb, int C, int cg0, int T, int tc) {
+  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+  const bool jv = j < ngrp;  // past the last group: out-of-range loads, nothing read
+  const int sg = uniform(jv ? ck.grp[j] : 0), sl = sg >> 1, gi = sg & 1;
+  const int cnt = uniform(ck.cnt[sl]), srow = uniform(ck.srow[sl]);
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const int e = 32 * gi + 16 * hh + m;
+    const bool ok = jv && e < cnt;
+    const int idx = ok ? ck.idx[srow + e] : 0;
+#pragma unroll
+    for (int ct = 0; ct < kDnTiles; ++ct) {
+      const int ch = cg0 + 4 * ct + g;
+      f.t[ct][hh] = ldb(db, (ok && ch < C) ? 16u * (uint32_t)(idx * C + ch) : kOOB);
+    }
+  }
+  const uint32_t zg = (uint32_t)((ck.seg_lo + sl) * 2 + gi) * (uint32_t)tc;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int tok = 16 * nt + m;
+    const uint32_t off = (jv && tok < T) ? 32u * ((zg + tok) * 4 + g) : kOOB;
+    f.zh[nt] = ldb(zb, off);
+    f.zl[nt] = ldb(zb, off + 16);
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, const bf16x8_t (&sel)[2],
+                                       f32x4_t (&acc)[kDnTiles][2][NT]) {
+#pragma unroll
+  for (int ct = 0; ct < kDnTiles; ++ct) {
+    const bf16x8_t t0 = bf8(f.t[ct][0]), t1 = bf8(f.t[ct][1]);
+    bf16x8_t bfrag[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+      const f32x4_t c0 = mfma16(t0, sel[h], zero);  // entries 4g..4g+3 of column 16h + m
+      const f32x4_t c1 = mfma16(t1, sel[h], zero);  // entries 16+4g..16+4g+3
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        bfrag[h][j] = (__bf16)c0[j];
+        bfrag[h][4 + j] = (__bf16)c1[j];
+      }
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        acc[ct][h][nt] = mfma16(bf8(f.zh[nt]), bfrag[h], acc[ct][h][nt]);
+        acc[ct][h][nt] = mfma16(bf8(f.zl[nt]), bfrag[h], acc[ct][h][nt]);
+      }
+  }
+}
 
 template <int NT>
 __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict__ seg_count,
                                                       const int32_t* __restrict__ seg_idx,
-                                                      const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
-                                                      int slots, const uint4* __restrict__ w_down_t, int C, int d,
-                                                      int T, float* __restrict__ y) {
-  constexpr int KG = kMdWindow / 32;  // 32-entry k groups per window
-  __shared__ int s_off[kBlock + 1];
-  __shared__ int s_slot[kMdChunkMax];
-  __shared__ int s_idx[kMdWindow];
-  __shared__ float s_z[NT * 16][kMdWindow + 4];
+                                                      const uint4* __restrict__ zf, int nseg, int d_ff, int R, int tc,
+                                                      const uint4* __restrict__ w_down_t, int C, int d, int T,
+                                                      float* __restrict__ y) {
+  constexpr int CW = 4 / NT, GS = kParts / CW, WCOLS = kDnCols * CW;
+  const Buf db = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
+  const Buf zb = make_buf(zf, 256u * (uint32_t)nseg * (uint32_t)tc);
+  __shared__ int s_cnt[kBlock];
+  __shared__ int s_srow[kBlock];
+  __shared__ int s_goff[kBlock + 1];
+  __shared__ int s_grp[2 * kBlock];
+  __shared__ int s_idx[kDnSlots];
+  __shared__ float s_y[16 * NT * WCOLS];
 
-  const int S4 = (C + 15) / 16;
-  const int chunk = blockIdx.x / S4, cgrp = blockIdx.x % S4;
+  const int S = (C * 8 + WCOLS - 1) / WCOLS;
+  const int chunk = blockIdx.x / S, cgrp = blockIdx.x % S;
   const int seg_lo = (int)(((int64_t)chunk * nseg) / R), seg_hi = (int)(((int64_t)(chunk + 1) * nseg) / R);
   const int nsc = seg_hi - seg_lo;  // <= kBlock, guaranteed by the host
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const int row_lo = seg_row(seg_lo, d_ff, nseg);
+  const int nslot = seg_row(seg_hi, d_ff, nseg) - row_lo;  // <= kDnSlots, guaranteed by the host
+  const int tid = threadIdx.x, lane = lane_id(), wave = uniform(tid / kWave);
   const int m = lane & 15, g = lane >> 4;
-  const int ch = cgrp * 16 + wave * 4 + g;  // this lane's 8 columns in the transposition tiles
-  const bool cvalid = ch < C;
+  const int slot_w = wave % CW, phase = wave / CW;
 
-  s_off[threadIdx.x] = threadIdx.x < nsc ? seg_count[seg_lo + threadIdx.x] : 0;
+  const int c = tid < nsc ? seg_count[seg_lo + tid] : 0;
+  s_cnt[tid] = c;
+  s_srow[tid] = tid < nsc ? seg_row(seg_lo + tid, d_ff, nseg) - row_lo : 0;
+  s_goff[tid] = (c > 0) + (c > 32);
+  for (int o = tid; o < nslot; o += kBlock) s_idx[o] = seg_idx[row_lo + o];
+  for (int o = tid; o < T * WCOLS; o += kBlock) s_y[o] = 0.f;
   __syncthreads();
-  block_exclusive_scan(s_off, kBlock);
-  const int n = min(s_off[kBlock], kMdChunkMax);
-  if (threadIdx.x < nsc) {
-    const int k0 = s_off[threadIdx.x], k1 = min(s_off[threadIdx.x + 1], kMdChunkMax);
-    const int slot0 = seg_row(seg_lo + threadIdx.x, d_ff, nseg);
-    for (int k = k0; k < k1; ++k) s_slot[k] = slot0 + (k - k0);
+  block_exclusive_scan(s_goff, kBlock);
+  if (tid < nsc) {
+    const int b = s_goff[tid];
+    if (c > 0) s_grp[b] = tid << 1;
+    if (c > 32) s_grp[b + 1] = (tid << 1) | 1;
   }
+  __syncthreads();
+  const int ngrp = uniform(s_goff[kBlock]);
 
   // 0/1 selectors: column 16 h + m of the 32-column tile
   bf16x8_t sel[2];
@@ -410,180 +518,139 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
 #pragma unroll
     for (int j = 0; j < 8; ++j) sel[h][j] = (__bf16)((8 * g + j == 16 * h + m) ? 1.f : 0.f);
 
-  f32x4_t acc[2][NT];
+  f32x4_t acc[kDnTiles][2][NT];
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+  for (int ct = 0; ct < kDnTiles; ++ct)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[ct][h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int base = 0; base < n; base += kMdWindow) {
-    const int wn = min(kMdWindow, n - base);
-    __syncthreads();  // slot list ready / previous window consumed
-    for (int o = threadIdx.x; o < kMdWindow * (NT * 16 + 1); o += kBlock) {
-      const int k = o % kMdWindow, row = o / kMdWindow;  // row 0: index, rows 1..: tokens
-      const bool ok = k < wn;
-      const int slot = ok ? s_slot[base + k] : 0;
-      if (row == 0) {
-        s_idx[k] = ok ? seg_idx[slot] : 0;
-      } else {
-        const int tau = row - 1;
-        s_z[tau][k] = (ok && tau < T) ? seg_zval[(size_t)tau * slots + slot] : 0.f;
-      }
-    }
-    __syncthreads();
-    uint4 a[KG][2];
-#pragma unroll
-    for (int kg = 0; kg < KG; ++kg)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int e = kg * 32 + hh * 16 + m;
-        a[kg][hh] = (e < wn && cvalid) ? ld_weights(w_down_t + (size_t)s_idx[e] * C + ch) : make_uint4(0u, 0u, 0u, 0u);
-      }
-#pragma unroll
-    for (int kg = 0; kg < KG; ++kg) {
-      if (kg * 32 >= wn) break;
-      const bf16x8_t t0 = __builtin_bit_cast(bf16x8_t, a[kg][0]), t1 = __builtin_bit_cast(bf16x8_t, a[kg][1]);
-      bf16x8_t bfrag[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
-        const f32x4_t c0 = mfma16(t0, sel[h], zero);  // entries 4g..4g+3 of column 16h + m
-        const f32x4_t c1 = mfma16(t1, sel[h], zero);  // entries 16+4g..16+4g+3
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          bfrag[h][j] = (__bf16)c0[j];
-          bfrag[h][4 + j] = (__bf16)c1[j];
-        }
-      }
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const float* zr = &s_z[nt * 16 + m][kg * 32];
-        float v[8];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          v[j] = zr[4 * g + j];
-          v[4 + j] = zr[16 + 4 * g + j];
-        }
-        bf16x8_t zhi, zlo;
-        split_bf16(v, zhi, zlo);
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          acc[h][nt] = mfma16(zhi, bfrag[h], acc[h][nt]);
-          acc[h][nt] = mfma16(zlo, bfrag[h], acc[h][nt]);
-        }
-      }
+  const DnChunk ck{s_grp, s_cnt, s_srow, s_idx, seg_lo};
+  const int cg0 = (cgrp * WCOLS + slot_w * kDnCols) / 8;  // first chunk of this wave's columns
+  if (phase < ngrp) {
+    // two register sets alternate; loads past the last group read nothing
+    DnFrags<NT> f0, f1;
+    dn_load(f0, phase, ngrp, ck, db, zb, C, cg0, T, tc);
+    for (int j = phase;;) {
+      dn_load(f1, j + GS, ngrp, ck, db, zb, C, cg0, T, tc);
+      dn_mma(f0, sel, acc);
+      j += GS;
+      if (j >= ngrp) break;
+      dn_load(f0, j + GS, ngrp, ck, db, zb, C, cg0, T, tc);
+      dn_mma(f1, sel, acc);
+      j += GS;
+      if (j >= ngrp) break;
     }
   }
-
+  // lane holds tokens 16 nt + 4g + i of column 32 ct + 16 h + m of its slot
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int col = (cgrp * 16 + wave * 4) * 8 + 16 * h + m;
+  for (int ct = 0; ct < kDnTiles; ++ct)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tau = nt * 16 + 4 * g + i;
-        if (tau < T && col < d) unsafeAtomicAdd(y + (size_t)tau * d + col, acc[h][nt][i]);
-      }
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 16 * nt + 4 * g + i;
+          if (tok < T) atomicAdd(&s_y[tok * WCOLS + slot_w * kDnCols + 32 * ct + 16 * h + m], acc[ct][h][nt][i]);
+        }
+  __syncthreads();
+  for (int o = tid; o < T * WCOLS; o += kBlock) {
+    const int tok = o / WCOLS, col = cgrp * WCOLS + (o - tok * WCOLS);
+    if (col < d) unsafeAtomicAdd(y + (size_t)tok * d + col, s_y[o]);
   }
+}
+
+// ------------------------------------------------------------------ host side
+template <int NT>
+hipError_t z_mfma(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
+  const int C = sh.d / 8, grid = ((sh.r + 15) / 16) * kZParts;
+  k_lopa_z_mfma<NT><<<grid, kZWaves * kWave, 0, s>>>(x, static_cast<const uint4*>(lopa_a), C, sh.T, sh.r, ws.tc,
+                                                      ws.z);
+  return hipGetLastError();
+}
+
+template <bool LOPA, bool DENSE, int NT>
+hipError_t gate_mfma(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
+                     float* y, hipStream_t s) {
+  const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
+  return launch_gate_kernel(k_gate_up_mfma<LOPA, DENSE, NT>, ws.nseg, s, x, (const float*)ws.z,
+                            static_cast<const uint4*>(gate_w), Cg, static_cast<const uint4*>(w_up), Cu, sh.T, sh.d,
+                            sh.d_ff, ws.nseg, t, ws.slots, ws.tc, ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act,
+                            ws.zf, y);
+}
+
+template <bool LOPA, bool DENSE>
+hipError_t gate_nt(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
+                   float* y, hipStream_t s) {
+  if (sh.T <= 16) return gate_mfma<LOPA, DENSE, 1>(sh, x, gate_w, w_up, t, ws, y, s);
+  if (sh.T <= 32) return gate_mfma<LOPA, DENSE, 2>(sh, x, gate_w, w_up, t, ws, y, s);
+  return gate_mfma<LOPA, DENSE, 4>(sh, x, gate_w, w_up, t, ws, y, s);
+}
+
+// Down grid: S column groups x R row chunks, about kDnWgTarget workgroups, at most
+// kDnAtomicsMax fp32 atomics into y (half that for 64-token tiles, whose workgroups
+// carry four times the zval traffic), every chunk within the LDS slot and segment limits.
+constexpr int kDnWgTarget = 512;
+constexpr int64_t kDnAtomicsMax = 2 << 20;
+
+template <int NT>
+hipError_t down_mfma(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
+  const int C = sh.d / 8;
+  const int64_t wcols = kDnCols * (4 / NT);
+  const int64_t S = ((int64_t)sh.d + wcols - 1) / wcols;
+  int64_t R = (kDnWgTarget + S - 1) / S;
+  const int64_t amax = (NT == 4 ? kDnAtomicsMax / 2 : kDnAtomicsMax) / ((int64_t)sh.T * sh.d);
+  if (R > amax) R = amax;
+  const int64_t rmin = (ws.nseg + kBlock - 1) / kBlock;
+  if (R < rmin) R = rmin;
+  if (R > ws.nseg) R = ws.nseg;
+  if (R < 1) R = 1;
+  const int64_t rows_per_seg = (sh.d_ff + ws.nseg - 1) / ws.nseg;
+  while (R < ws.nseg && ((ws.nseg + R - 1) / R) * rows_per_seg > kDnSlots) ++R;
+  if (((ws.nseg + R - 1) / R) * rows_per_seg > kDnSlots || S * R > INT32_MAX) return hipErrorInvalidValue;
+  k_down_mfma<NT><<<(int)(S * R), kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.zf, ws.nseg, sh.d_ff, (int)R, ws.tc,
+                                                  static_cast<const uint4*>(w_down_t), C, sh.d, sh.T, y);
+  return hipGetLastError();
 }
 
 }  // namespace
 
-// ------------------------------------------------------------------ launchers
+// The matrix-core path addresses every operand with 32-bit byte offsets below 2^31.
 bool batched_ok(const Shape& sh, Gate g) {
   if (sh.wdt != 1 || sh.T < 2 || sh.T > kTokChunk || sh.d % 8 != 0) return false;
-  if (g == Gate::LoPA && sh.r % 8 != 0) return false;
+  const int64_t lim = int64_t(1) << 31;
+  if (2 * (int64_t)sh.d_ff * sh.d >= lim || 4 * (int64_t)kTokChunk * sh.d >= lim) return false;
+  if ((int64_t)((sh.d_ff + kSegRowsB - 1) / kSegRowsB) * 256 * kTokChunk >= lim) return false;
+  if (g == Gate::LoPA && (sh.r % 8 != 0 || 2 * (int64_t)sh.d_ff * sh.r >= lim || 2 * (int64_t)sh.r * sh.d >= lim))
+    return false;
   return true;
 }
 
-bool batched_down_ok(const Shape& sh) { return sh.wdt == 1 && sh.T >= 2 && sh.T <= kTokChunk && sh.d % 8 == 0; }
+int batched_segments(int d_ff) { return (d_ff + kSegRowsB - 1) / kSegRowsB; }
 
-int batched_segments(int d_ff) { return (d_ff + kMRows - 1) / kMRows; }
-
-hipError_t launch_lopa_z_batched(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
-                                 hipStream_t s) {
-  const int C = sh.d / 8, grid = (sh.r + 15) / 16;
-  const uint4* A = static_cast<const uint4*>(lopa_a);
-  if (sh.T <= 16)
-    k_lopa_z_mfma<1><<<grid, kZWaves * kWave, 0, s>>>(x, A, C, sh.T, sh.d, sh.r, ws.z);
-  else if (sh.T <= 32)
-    k_lopa_z_mfma<2><<<grid, kZWaves * kWave, 0, s>>>(x, A, C, sh.T, sh.d, sh.r, ws.z);
-  else
-    k_lopa_z_mfma<4><<<grid, kZWaves * kWave, 0, s>>>(x, A, C, sh.T, sh.d, sh.r, ws.z);
-  return hipGetLastError();
-}
-
-template <bool LOPA, bool DENSE>
-hipError_t gate_up_batched(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t,
-                           Workspace& ws, float* y, hipStream_t s) {
-  ws.nseg = batched_segments(sh.d_ff);
-  const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
-  const uint4* G = static_cast<const uint4*>(gate_w);
-  const uint4* U = static_cast<const uint4*>(w_up);
-#define FFN_GUB(NT)                                                                                              \
-  return launch_gate_kernel(k_gate_up_mfma<LOPA, DENSE, NT>, ws.nseg, s, x, (const float*)ws.z, G, Cg, U, Cu, sh.T, \
-                            sh.d, sh.r, sh.d_ff, ws.nseg, t, ws.slots, ws.meta, ws.seg_count, ws.seg_idx,         \
-                            ws.seg_act, ws.seg_zval, y)
-  if (sh.T <= 16) FFN_GUB(1);
-  if (sh.T <= 32) FFN_GUB(2);
-  FFN_GUB(4);
-#undef FFN_GUB
-}
-
-hipError_t launch_gate_up_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w,
-                                  const void* w_up, float t, Workspace& ws, float* y, hipStream_t s) {
-  if (g == Gate::LoPA)
-    return dense ? gate_up_batched<true, true>(sh, x, gate_w, w_up, t, ws, y, s)
-                 : gate_up_batched<true, false>(sh, x, gate_w, w_up, t, ws, y, s);
-  return dense ? gate_up_batched<false, true>(sh, x, gate_w, w_up, t, ws, y, s)
-               : gate_up_batched<false, false>(sh, x, gate_w, w_up, t, ws, y, s);
-}
-
-// about kDownAtomics fp32 atomics per call into y; at most kBlock segments per chunk
-constexpr int64_t kDownAtomics = 512 * 1024;
-
-hipError_t launch_down_batched(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
-  const int C = sh.d / 8;
-  const int S = (C + kDnSliceChunks - 1) / kDnSliceChunks;
-  int R = (int)(kDownAtomics / ((int64_t)sh.T * sh.d));
-  const int rmin = (ws.nseg + kBlock - 1) / kBlock;
-  if (R < rmin) R = rmin;
-  if (R > ws.nseg) R = ws.nseg;
-  if (R < 1) R = 1;
-  const uint4* D = static_cast<const uint4*>(w_down_t);
-  if (sh.T > 8) {
-    // row chunks: enough workgroups to cover the GPU, each chunk's rows fit the LDS slot list
-    const int S4 = (C + 15) / 16;
-    int Rm = (2 * 256 + S4 - 1) / S4;
-    const int rows_per_seg = (sh.d_ff + ws.nseg - 1) / ws.nseg;
-    const int rcap = (sh.d_ff + kMdChunkMax - 1) / kMdChunkMax + 1;
-    if (Rm < rcap) Rm = rcap;
-    if (Rm < rmin) Rm = rmin;
-    while (Rm < ws.nseg && ((ws.nseg + Rm - 1) / Rm) * rows_per_seg > kMdChunkMax) ++Rm;
-    if (Rm > ws.nseg) Rm = ws.nseg;
-#define FFN_DM(NT)                                                                                                 \
-  k_down_mfma<NT><<<S4 * Rm, kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, Rm, ws.slots, \
-                                            D, C, sh.d, sh.T, y)
-    if (sh.T <= 16)
-      FFN_DM(1);
-    else if (sh.T <= 32)
-      FFN_DM(2);
-    else
-      FFN_DM(4);
-#undef FFN_DM
-    return hipGetLastError();
+hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
+                          const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
+                          float* y, hipStream_t s) {
+  const bool lopa = g == Gate::LoPA;
+  hipError_t e = hipSuccess;
+  if (lopa) {
+    e = sh.T <= 16 ? z_mfma<1>(sh, x, lopa_a, ws, s)
+                   : sh.T <= 32 ? z_mfma<2>(sh, x, lopa_a, ws, s) : z_mfma<4>(sh, x, lopa_a, ws, s);
+    if (e != hipSuccess) return e;
   }
-  if (sh.T <= 2)
-    k_down_tn<2><<<S * R, kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R, ws.slots, D, C,
-                                          sh.d, sh.T, y);
-  else if (sh.T <= 4)
-    k_down_tn<4><<<S * R, kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R, ws.slots, D, C,
-                                          sh.d, sh.T, y);
+  ws.nseg = batched_segments(sh.d_ff);
+  if (lopa)
+    e = dense ? gate_nt<true, true>(sh, x, gate_w, w_up, t, ws, y, s)
+              : gate_nt<true, false>(sh, x, gate_w, w_up, t, ws, y, s);
   else
-    k_down_tn<8><<<S * R, kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R, ws.slots, D, C,
-                                          sh.d, sh.T, y);
-  return hipGetLastError();
+    e = dense ? gate_nt<false, true>(sh, x, gate_w, w_up, t, ws, y, s)
+              : gate_nt<false, false>(sh, x, gate_w, w_up, t, ws, y, s);
+  if (e != hipSuccess) return e;
+  if (sh.T <= 16) return down_mfma<1>(sh, w_down_t, ws, y, s);
+  if (sh.T <= 32) return down_mfma<2>(sh, w_down_t, ws, y, s);
+  return down_mfma<4>(sh, w_down_t, ws, y, s);
 }
 
 }  // namespace ffn

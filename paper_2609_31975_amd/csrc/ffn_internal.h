@@ -31,7 +31,10 @@ struct Workspace {
   int32_t* seg_idx;    // [slots]          neuron index
   float* seg_act;      // [tc][slots]      h - t for the token, 0 where inactive
   float* seg_zval;     // [tc][slots]      act * <w_up[i], x_tau>
-  float* z;            // [tc][r]          LoPA intermediate A x (LoPA only)
+  float* z;            // [tc][r]          LoPA intermediate A x (LoPA only); for tc >= 2
+                       //                  two partial copies [2][tc][r]
+  uint4* zf;           // [2 ceil(d_ff / 64)][tc][4][2]  zval fragments of the down product
+                       //                  (matrix-core path, tc >= 2; empty for tc = 1)
 };
 
 size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out);
@@ -60,13 +63,11 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, c
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s);
 
-// Matrix-core kernels for batches of 2..64 tokens with bf16 weights (ffn_batched.hip).
+// Matrix-core path for batches of 2..64 tokens with bf16 weights (ffn_batched.hip):
+// the whole call (LoPA z, gate + union + W_up, down), clearing y first.
 bool batched_ok(const Shape& sh, Gate g);
-bool batched_down_ok(const Shape& sh);
-hipError_t launch_lopa_z_batched(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
-                                 hipStream_t s);
-hipError_t launch_gate_up_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w,
-                                  const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
-hipError_t launch_down_batched(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s);
+hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
+                          const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
+                          float* y, hipStream_t s);
 
 }  // namespace ffn

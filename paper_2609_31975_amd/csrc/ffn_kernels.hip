@@ -615,14 +615,12 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
 
 // ------------------------------------------------------------------ launchers
 hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
-  if (batched_ok(sh, Gate::LoPA)) return launch_lopa_z_batched(sh, x, lopa_a, ws, s);
   return sh.wdt == 1 ? lopa_z<WBf16>(sh, x, lopa_a, ws, s) : lopa_z<WF32>(sh, x, lopa_a, ws, s);
 }
 
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w, const void* w_up,
                           float t, Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
-  if (batched_ok(sh, g)) return launch_gate_up_batched(sh, g, dense, x, gate_w, w_up, t, ws, y, s);
   const bool fast = fast_ok(sh, g);
 #define FFN_GU(W, L, D)                                                                     \
   return fast ? gate_up_fast<W, L, D>(sh, x, gate_w, w_up, t, ws, y, s)                    \
@@ -646,7 +644,6 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, c
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s) {
-  if (batched_down_ok(sh)) return launch_down_batched(sh, w_down_t, ws, y, s);
   if (sh.wdt == 1) return dense ? down<WBf16, true>(sh, w_down_t, ws, y, s) : down<WBf16, false>(sh, w_down_t, ws, y, s);
   return dense ? down<WF32, true>(sh, w_down_t, ws, y, s) : down<WF32, false>(sh, w_down_t, ws, y, s);
 }

@@ -93,7 +93,9 @@ def test_full_size_dense(gu, r):
 
 
 # ---------------------------------------------------------------- edge cases
-EDGE_SHAPES = [(1, 264, 1000, 0, BF16), (1, 100, 77, 0, BF16), (1, 264, 1000, 40, BF16), (4, 64, 200, 0, F32)]
+EDGE_SHAPES = [(1, 264, 1000, 0, BF16), (1, 100, 77, 0, BF16), (1, 264, 1000, 40, BF16), (4, 64, 200, 0, F32),
+               (4, 264, 1000, 0, BF16), (16, 264, 1000, 40, BF16), (64, 136, 300, 0, BF16)]  # matrix-core batches
+POISON_SHAPES = EDGE_SHAPES[:3] + [(2, 264, 1000, 0, BF16), (2, 264, 1000, 40, BF16)]
 
 
 @pytest.mark.parametrize("shape", EDGE_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
@@ -116,7 +118,7 @@ def test_everything_active_equals_dense(gu, shape):
     gu.check_parity(gu.run_oracle(inp, -100.0), ys, None, None, -100.0, wdt)
 
 
-@pytest.mark.parametrize("shape", EDGE_SHAPES[:3], ids=lambda s: f"d{s[1]}_dff{s[2]}_r{s[3]}")
+@pytest.mark.parametrize("shape", POISON_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}")
 def test_inactive_rows_are_never_read(gu, shape):
     """NaN in every W_up / W_down^T row that no token activates: the output is unchanged."""
     T, d, d_ff, r, wdt = shape
