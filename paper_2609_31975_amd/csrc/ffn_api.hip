@@ -41,7 +41,7 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
   w.seg_zval = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
   const size_t bt = w.tc >= 2 ? (size_t)w.tc : 0;  // matrix-core path only
   w.z = reinterpret_cast<float*>(take(sizeof(float) * (bt ? 2 : 1) * (size_t)w.tc * (r > 0 ? r : 1)));
-  w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * 4 * bt * 2 * (size_t)((d_ff + 63) / 64)));
+  w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * 4 * bt * 2 * (size_t)batched_segments(d_ff)));
   if (out) *out = w;
   return off;
 }

@@ -46,26 +46,12 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kTiles = 4;                // 16-row tiles of a gate segment
 constexpr int kSegRowsB = 16 * kTiles;   // rows per gate segment (one 64-lane ballot)
 constexpr int kParts = kBlock / kWave;   // k parts of a workgroup, one per wave
+constexpr int kSegGrid = 256;            // most workgroups of the gate kernel (one per CU)
 
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ bf16x8_t bf8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
-
-// Buffer resource over [p, p + bytes), bytes < 2^31; loads at kOOB or above return zero.
-struct Buf {
-  __amdgpu_buffer_rsrc_t r;
-};
-__device__ __forceinline__ Buf make_buf(const void* p, uint32_t bytes) {
-  return Buf{__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000)};
-}
-constexpr uint32_t kOOB = 0x80000000u;
-// Weights too go through the caches: an instruction reads 64 bytes of each of 16 rows,
-// and the next one the other half of the same 128-byte lines.
-__device__ __forceinline__ uint4 ldb(const Buf& b, uint32_t off) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b.r, off, 0, 0));
-}
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // v = hi + lo with both in bf16 (round to nearest even twice)
 __device__ __forceinline__ void split8(const float (&v)[8], bf16x8_t& hi, bf16x8_t& lo) {
@@ -86,29 +72,62 @@ __device__ __forceinline__ void kpart(int C, int kp, int np, int* ks0, int* ks1)
 }
 
 // ------------------------------------------------------------------ streaming core
-// Operands of KU consecutive k steps: RT weight-tile fragments and, per token tile, the
+// A group of KU consecutive k steps covers 16 RT weight rows x 4 KU chunks.  The group
+// is read row by row, LPR = 4 KU lanes per row and 64 / LPR rows per instruction (256
+// contiguous bytes per row for KU = 4), streamed past the caches, and reshaped into MFMA
+// operands through a wave-private LDS tile: row br of the group sits at br * PITCH, one
+// pad chunk per row keeping the operand reads free of bank conflicts.  (Loading the
+// operand layout directly reads 64 bytes of each of 16 rows per instruction, which
+// streams about 25% slower.)
+template <int RT, int KU>
+struct WStage {
+  static constexpr int LPR = 4 * KU;          // lanes per row of a load instruction
+  static constexpr int RPI = kWave / LPR;     // rows per load instruction
+  static constexpr int NI = RT * KU;          // load instructions per group
+  static constexpr int PITCH = LPR + 1;       // 16-byte chunks per LDS row
+  static constexpr int WORDS = 16 * RT * PITCH;  // uint4 of one wave's tile
+};
+
+// Rows of this lane's load instructions: roff[i] = row_of(i RPI + lane / LPR) * C, or -1
+// where row_of gives no row (-1).
+template <int RT, int KU, class RowOf>
+__device__ __forceinline__ void stage_rows(int (&roff)[RT * KU], int C, RowOf row_of) {
+  using S = WStage<RT, KU>;
+  const int lane = lane_id();
+#pragma unroll
+  for (int i = 0; i < S::NI; ++i) {
+    const int r = row_of(i * S::RPI + lane / S::LPR);
+    roff[i] = r >= 0 ? r * C : -1;
+  }
+}
+
+// Operands of one group: the weight chunks as loaded and, per k step and token tile, the
 // token fragment: the 8 fp32 of the chunk (two 16-byte halves) from each of NP partial
 // copies of the token matrix, summed and split into hi / lo when multiplied.  A token
 // matrix is [T][8 C] fp32; partial copy p starts part_bytes * p into its buffer.
 template <int RT, int NT, int KU, int NP>
 struct Frags {
-  uint4 a[KU][RT];
+  uint4 a[RT * KU];
   uint4 b[KU][NT][NP][2];
 };
 
-// roff[rt]: this lane's weight row of tile rt, in chunks (row * C), or -1 for none;
-// ntile (uniform): tiles in use
 template <int RT, int NT, int KU, int NP>
-__device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& wb, int C, const int (&roff)[RT],
-                                           int ntile, const Buf& tb, uint32_t part_bytes, int T, int ks, int ks1) {
+__device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& wb, int C,
+                                           const int (&roff)[RT * KU], const Buf& tb, uint32_t part_bytes,
+                                           int T, int ks, int ks1) {
+  using S = WStage<RT, KU>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+  {
+    const int gc = lane % S::LPR, c = 4 * ks + gc;
+    const bool cv = ks + (gc >> 2) < ks1 && c < C;
+#pragma unroll
+    for (int i = 0; i < S::NI; ++i)
+      f.a[i] = ldb_nt(wb, (cv && roff[i] >= 0) ? 16u * (uint32_t)(roff[i] + c) : kOOB);
+  }
 #pragma unroll
   for (int u = 0; u < KU; ++u) {
     const int c = 4 * (ks + u) + g;
     const bool cv = ks + u < ks1 && c < C;
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-      f.a[u][rt] = ldb(wb, (cv && rt < ntile && roff[rt] >= 0) ? 16u * (uint32_t)(roff[rt] + c) : kOOB);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int tok = 16 * nt + m;
@@ -122,8 +141,15 @@ __device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& 
   }
 }
 
+// tile: this wave's LDS tile (Stage::WORDS uint4); ntile (uniform): row tiles in use
 template <int RT, int NT, int KU, int NP>
-__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, int ntile, f32x4_t (&acc)[RT][NT]) {
+__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, int ntile, uint4* tile,
+                                          f32x4_t (&acc)[RT][NT]) {
+  using S = WStage<RT, KU>;
+  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < S::NI; ++i) tile[(i * S::RPI + lane / S::LPR) * S::PITCH + lane % S::LPR] = f.a[i];
+  __builtin_amdgcn_wave_barrier();  // LDS operations of a wave complete in order
 #pragma unroll
   for (int u = 0; u < KU; ++u)
 #pragma unroll
@@ -152,28 +178,31 @@ __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, int nt
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
         if (rt < ntile) {
-          acc[rt][nt] = mfma16(bf8(f.a[u][rt]), hi, acc[rt][nt]);
-          acc[rt][nt] = mfma16(bf8(f.a[u][rt]), lo, acc[rt][nt]);
+          const bf16x8_t a = bf8(tile[(16 * rt + m) * S::PITCH + 4 * u + g]);
+          acc[rt][nt] = mfma16(a, hi, acc[rt][nt]);
+          acc[rt][nt] = mfma16(a, lo, acc[rt][nt]);
         }
     }
+  __builtin_amdgcn_wave_barrier();
 }
 
 // acc[rt][nt] += weight tile rt . token tile nt over the k steps [ks0, ks1) (uniform).
 // Two register sets alternate: the loads of the next KU steps are issued before the
 // current ones are multiplied; loads past ks1 are out of range and read nothing.
 template <int RT, int NT, int KU, int NP>
-__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT], int ntile, const Buf& tb,
-                                            uint32_t part_bytes, int T, int ks0, int ks1, f32x4_t (&acc)[RT][NT]) {
+__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT * KU], int ntile,
+                                            uint4* tile, const Buf& tb, uint32_t part_bytes, int T, int ks0, int ks1,
+                                            f32x4_t (&acc)[RT][NT]) {
   if (ks0 >= ks1) return;
   Frags<RT, NT, KU, NP> f0, f1;
-  load_frags(f0, wb, C, roff, ntile, tb, part_bytes, T, ks0, ks1);
+  load_frags(f0, wb, C, roff, tb, part_bytes, T, ks0, ks1);
   for (int ks = ks0;;) {
-    load_frags(f1, wb, C, roff, ntile, tb, part_bytes, T, ks + KU, ks1);
-    mma_frags(f0, ntile, acc);
+    load_frags(f1, wb, C, roff, tb, part_bytes, T, ks + KU, ks1);
+    mma_frags(f0, ntile, tile, acc);
     ks += KU;
     if (ks >= ks1) break;
-    load_frags(f0, wb, C, roff, ntile, tb, part_bytes, T, ks + KU, ks1);
-    mma_frags(f1, ntile, acc);
+    load_frags(f0, wb, C, roff, tb, part_bytes, T, ks + KU, ks1);
+    mma_frags(f1, ntile, tile, acc);
     ks += KU;
     if (ks >= ks1) break;
   }
@@ -192,10 +221,12 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
                                                                  const uint4* __restrict__ A, int C, int T, int r,
                                                                  int tc, float* __restrict__ zp) {
   __shared__ f32x4_t s_part[kZWaves][NT][kWave];
-  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave), m = lane & 15;
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int tile = blockIdx.x / kZParts, part = blockIdx.x % kZParts;
-  const int row = tile * 16 + m;
-  const int roff[1] = {row < r ? row * C : -1};
+  constexpr int KU = NT == 1 ? 4 : NT == 2 ? 2 : 1;
+  __shared__ uint4 s_stage[kZWaves][WStage<1, KU>::WORDS];
+  int roff[KU];
+  stage_rows<1, KU>(roff, C, [&](int br) { return tile * 16 + br < r ? tile * 16 + br : -1; });
   const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)C);
   const Buf xb = make_buf(x, 32u * (uint32_t)T * (uint32_t)C);
   f32x4_t acc[1][NT];
@@ -203,7 +234,7 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
   for (int nt = 0; nt < NT; ++nt) acc[0][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   int ks0, ks1;
   kpart(C, part * kZWaves + wave, kZParts * kZWaves, &ks0, &ks1);
-  stream_rows<1, NT, (NT == 1 ? 4 : NT == 2 ? 2 : 1), 1>(ab, C, roff, 1, xb, 0u, T, ks0, ks1, acc);
+  stream_rows<1, NT, KU, 1>(ab, C, roff, 1, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[0][nt];
   __syncthreads();
@@ -223,7 +254,8 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 }
 
 // ------------------------------------------------------------------ gate + union + W_up
-// One segment of at most 64 neurons per workgroup.  Wave w multiplies the segment's
+// Segments of at most 64 neurons, each workgroup taking every gridDim.x-th one.  Wave w
+// multiplies the segment's
 // four row tiles over k part w; the parts are added in LDS, wave w owning tile w.  A
 // neuron joins the union if any token activates it (h > t; NaN compares false); one
 // ballot orders the union ascending.  The W_up dots of the union rows use the same
@@ -240,148 +272,148 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict
                                                          int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                                          int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                                          uint4* __restrict__ zf, float* __restrict__ y) {
-  constexpr int KU = (NT == 1 && !LOPA) ? 4 : 2;
+  constexpr int KU = (NT == 1 && !LOPA) ? 4 : 2;  // gate rows
+  constexpr int KUU = NT == 1 ? 4 : 2;               // W_up rows
+  constexpr int STAGE = WStage<kTiles, (KU > KUU ? KU : KUU)>::WORDS;
+  __shared__ uint4 s_stage[kParts][STAGE];
   __shared__ f32x4_t s_red[kParts][kTiles][NT][kWave];
-  __shared__ float s_act[kSegRowsB][kTokChunk];
+  __shared__ float s_act[kSegRowsB][16 * NT];
   __shared__ uint32_t s_mask[kTiles];
   __shared__ int s_list[kSegRowsB];
   __shared__ int s_cnt;
 
-  const int seg = blockIdx.x;
-  const int row0 = seg_row(seg, d_ff, nseg);
-  const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;  // <= kSegRowsB, guaranteed by the host
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int m = lane & 15, g = lane >> 4;
   clear_output(y, T * d, meta, nseg);
   const Buf xb = make_buf(x, 32u * (uint32_t)T * (uint32_t)Cu);
   const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu);
 
-  f32x4_t acc[kTiles][NT];
+  // segments blockIdx.x, blockIdx.x + gridDim.x, ... (the host makes the counts equal)
+  for (int seg = blockIdx.x; seg < nseg; seg += gridDim.x) {
+    if (seg != (int)blockIdx.x) __syncthreads();  // the previous segment's LDS reads are done
+    const int row0 = seg_row(seg, d_ff, nseg);
+    const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;  // <= kSegRowsB, guaranteed by the host
+
+    f32x4_t acc[kTiles][NT];
 #pragma unroll
-  for (int rt = 0; rt < kTiles; ++rt)
+    for (int rt = 0; rt < kTiles; ++rt)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  {
-    int roff[kTiles];
-#pragma unroll
-    for (int rt = 0; rt < kTiles; ++rt) {
-      const int rl = 16 * rt + m;
-      roff[rt] = rl < nrows ? (row0 + rl) * Cg : -1;
+      for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    {
+      int roff[kTiles * KU];
+      stage_rows<kTiles, KU>(roff, Cg, [&](int br) { return br < nrows ? row0 + br : -1; });
+      int ks0, ks1;
+      kpart(Cg, wave, kParts, &ks0, &ks1);
+      const int ntile = (nrows + 15) / 16;
+      const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg);
+      if constexpr (LOPA) {
+        const uint32_t part = 32u * (uint32_t)tc * (uint32_t)Cg;
+        stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, ntile, s_stage[wave], make_buf(zp, 2 * part), part, T, ks0, ks1,
+                                       acc);
+      } else {
+        stream_rows<kTiles, NT, KU, 1>(gb, Cg, roff, ntile, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+      }
     }
-    int ks0, ks1;
-    kpart(Cg, wave, kParts, &ks0, &ks1);
-    const int ntile = (nrows + 15) / 16;
-    const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg);
-    if constexpr (LOPA) {
-      const uint32_t part = 32u * (uint32_t)tc * (uint32_t)Cg;
-      stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, ntile, make_buf(zp, 2 * part), part, T, ks0, ks1, acc);
-    } else {
-      stream_rows<kTiles, NT, KU, 1>(gb, Cg, roff, ntile, xb, 0u, T, ks0, ks1, acc);
+#pragma unroll
+    for (int rt = 0; rt < kTiles; ++rt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) s_red[wave][rt][nt][lane] = acc[rt][nt];
+    __syncthreads();
+    {
+      // lane holds h of rows 16 wave + 4g + i (i < 4) for tokens 16 nt + m
+      f32x4_t h[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        h[nt] = ((s_red[0][wave][nt][lane] + s_red[1][wave][nt][lane]) + s_red[2][wave][nt][lane]) +
+                s_red[3][wave][nt][lane];
+      uint32_t mask = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rl = 16 * wave + 4 * g + i;
+        bool any = false;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int tok = 16 * nt + m;
+          const float hv = h[nt][i];
+          const bool on = tok < T && hv > t;
+          if (tok < T && rl < nrows) s_act[rl][tok] = on ? hv - t : 0.f;
+          any |= on;
+        }
+        const uint64_t b = __ballot(any && rl < nrows);
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg)
+          if ((b >> (16 * gg)) & 0xffffull) mask |= 1u << (4 * gg + i);
+      }
+      if (lane == 0) s_mask[wave] = mask;
     }
-  }
+    __syncthreads();
+    if (wave == 0) {
+      const uint64_t on = (uint64_t)s_mask[0] | ((uint64_t)s_mask[1] << 16) | ((uint64_t)s_mask[2] << 32) |
+                          ((uint64_t)s_mask[3] << 48);
+      const bool sel = lane < nrows && (DENSE || ((on >> lane) & 1ull));
+      const uint64_t b = __ballot(sel);
+      const int rank = rank_in_mask(b);
+      if (sel) {
+        s_list[rank] = lane;
+        seg_idx[row0 + rank] = row0 + lane;
+      }
+      if (lane == 0) {
+        s_cnt = __popcll(b);
+        seg_count[seg] = __popcll(b);
+      }
+    }
+    __syncthreads();
+    const int cnt = uniform(s_cnt);
+    for (int o = threadIdx.x; o < cnt * T; o += kBlock) {
+      const int tok = o / cnt, e = o - tok * cnt;
+      seg_act[(size_t)tok * slots + row0 + e] = s_act[s_list[e]][tok];
+    }
+
+    // W_up dots of the union rows: tiles of 16 entries
+    const int nut = (cnt + 15) / 16;
 #pragma unroll
-  for (int rt = 0; rt < kTiles; ++rt)
+    for (int rt = 0; rt < kTiles; ++rt)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) s_red[wave][rt][nt][lane] = acc[rt][nt];
-  __syncthreads();
-  {
-    // lane holds h of rows 16 wave + 4g + i (i < 4) for tokens 16 nt + m
-    f32x4_t h[NT];
+      for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (nut > 0) {
+      int roff[kTiles * KUU];
+      stage_rows<kTiles, KUU>(roff, Cu, [&](int e) { return e < cnt ? row0 + s_list[e] : -1; });
+      int ks0, ks1;
+      kpart(Cu, wave, kParts, &ks0, &ks1);
+      stream_rows<kTiles, NT, KUU, 1>(ub, Cu, roff, nut, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+    }
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      h[nt] = ((s_red[0][wave][nt][lane] + s_red[1][wave][nt][lane]) + s_red[2][wave][nt][lane]) +
-              s_red[3][wave][nt][lane];
-    uint32_t mask = 0;
+    for (int rt = 0; rt < kTiles; ++rt)
+      if (rt < nut)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int rl = 16 * wave + 4 * g + i;
-      bool any = false;
+        for (int nt = 0; nt < NT; ++nt) s_red[wave][rt][nt][lane] = acc[rt][nt];
+    __syncthreads();
+
+    // wave w: union entries 16 w .. 16 w + 15 = half (w & 1) of fragment group w >> 1
+    const int gi = wave >> 1, half = wave & 1;
+    if (32 * gi < cnt) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const int tok = 16 * nt + m;
-        const float hv = h[nt][i];
-        const bool on = tok < T && hv > t;
-        if (tok < T && rl < nrows) s_act[rl][tok] = on ? hv - t : 0.f;
-        any |= on;
-      }
-      const uint64_t b = __ballot(any && rl < nrows);
+        f32x4_t v = {0.f, 0.f, 0.f, 0.f};
+        if (wave < nut)
+          v = ((s_red[0][wave][nt][lane] + s_red[1][wave][nt][lane]) + s_red[2][wave][nt][lane]) +
+              s_red[3][wave][nt][lane];
+        if (tok < T) {
+          uint32_t hw[2] = {0u, 0u}, lw[2] = {0u, 0u};
 #pragma unroll
-      for (int gg = 0; gg < 4; ++gg)
-        if ((b >> (16 * gg)) & 0xffffull) mask |= 1u << (4 * gg + i);
-    }
-    if (lane == 0) s_mask[wave] = mask;
-  }
-  __syncthreads();
-  if (wave == 0) {
-    const uint64_t on = (uint64_t)s_mask[0] | ((uint64_t)s_mask[1] << 16) | ((uint64_t)s_mask[2] << 32) |
-                        ((uint64_t)s_mask[3] << 48);
-    const bool sel = lane < nrows && (DENSE || ((on >> lane) & 1ull));
-    const uint64_t b = __ballot(sel);
-    const int rank = rank_in_mask(b);
-    if (sel) {
-      s_list[rank] = lane;
-      seg_idx[row0 + rank] = row0 + lane;
-    }
-    if (lane == 0) {
-      s_cnt = __popcll(b);
-      seg_count[seg] = __popcll(b);
-    }
-  }
-  __syncthreads();
-  const int cnt = uniform(s_cnt);
-  for (int o = threadIdx.x; o < cnt * T; o += kBlock) {
-    const int tok = o / cnt, e = o - tok * cnt;
-    seg_act[(size_t)tok * slots + row0 + e] = s_act[s_list[e]][tok];
-  }
-
-  // W_up dots of the union rows: tiles of 16 entries
-  const int nut = (cnt + 15) / 16;
-#pragma unroll
-  for (int rt = 0; rt < kTiles; ++rt)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (nut > 0) {
-    int roff[kTiles];
-#pragma unroll
-    for (int rt = 0; rt < kTiles; ++rt) {
-      const int e = 16 * rt + m;
-      roff[rt] = e < cnt ? (row0 + s_list[e]) * Cu : -1;
-    }
-    int ks0, ks1;
-    kpart(Cu, wave, kParts, &ks0, &ks1);
-    stream_rows<kTiles, NT, (NT == 1 ? 4 : 2), 1>(ub, Cu, roff, nut, xb, 0u, T, ks0, ks1, acc);
-  }
-#pragma unroll
-  for (int rt = 0; rt < kTiles; ++rt)
-    if (rt < nut)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) s_red[wave][rt][nt][lane] = acc[rt][nt];
-  __syncthreads();
-
-  // wave w: union entries 16 w .. 16 w + 15 = half (w & 1) of fragment group w >> 1
-  const int gi = wave >> 1, half = wave & 1;
-  if (32 * gi < cnt) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int tok = 16 * nt + m;
-      f32x4_t v = {0.f, 0.f, 0.f, 0.f};
-      if (wave < nut)
-        v = ((s_red[0][wave][nt][lane] + s_red[1][wave][nt][lane]) + s_red[2][wave][nt][lane]) +
-            s_red[3][wave][nt][lane];
-      if (tok < T) {
-        uint32_t hw[2] = {0u, 0u}, lw[2] = {0u, 0u};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = 16 * wave + 4 * g + i;
-          const float zz = e < cnt ? s_act[s_list[e]][tok] * v[i] : 0.f;
-          const __bf16 hb = (__bf16)zz;
-          const __bf16 lb = (__bf16)(zz - (float)hb);
-          hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
-          lw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, lb) << (16 * (i & 1));
+          for (int i = 0; i < 4; ++i) {
+            const int e = 16 * wave + 4 * g + i;
+            const float zz = e < cnt ? s_act[s_list[e]][tok] * v[i] : 0.f;
+            const __bf16 hb = (__bf16)zz;
+            const __bf16 lb = (__bf16)(zz - (float)hb);
+            hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
+            lw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, lb) << (16 * (i & 1));
+          }
+          uint2* frag = reinterpret_cast<uint2*>(zf + 2 * ((((size_t)seg * 2 + gi) * tc + tok) * 4 + g));
+          frag[half] = make_uint2(hw[0], hw[1]);
+          frag[2 + half] = make_uint2(lw[0], lw[1]);
         }
-        uint2* frag = reinterpret_cast<uint2*>(zf + 2 * ((((size_t)seg * 2 + gi) * tc + tok) * 4 + g));
-        frag[half] = make_uint2(hw[0], hw[1]);
-        frag[2 + half] = make_uint2(lw[0], lw[1]);
       }
     }
   }
@@ -575,7 +607,8 @@ template <bool LOPA, bool DENSE, int NT>
 hipError_t gate_mfma(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
                      float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
-  return launch_gate_kernel(k_gate_up_mfma<LOPA, DENSE, NT>, ws.nseg, s, x, (const float*)ws.z,
+  return launch_gate_kernel(k_gate_up_mfma<LOPA, DENSE, NT>, ws.nseg < kSegGrid ? ws.nseg : kSegGrid, s, x,
+                            (const float*)ws.z,
                             static_cast<const uint4*>(gate_w), Cg, static_cast<const uint4*>(w_up), Cu, sh.T, sh.d,
                             sh.d_ff, ws.nseg, t, ws.slots, ws.tc, ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act,
                             ws.zf, y);
@@ -628,7 +661,12 @@ bool batched_ok(const Shape& sh, Gate g) {
   return true;
 }
 
-int batched_segments(int d_ff) { return (d_ff + kSegRowsB - 1) / kSegRowsB; }
+// Row-balanced segments of at most 64 rows; beyond 128 of them the count is a multiple
+// of kSegGrid so that a grid of kSegGrid workgroups gives every workgroup the same number.
+int batched_segments(int d_ff) {
+  const int n = (d_ff + kSegRowsB - 1) / kSegRowsB;
+  return n > kSegGrid / 2 ? (n + kSegGrid - 1) / kSegGrid * kSegGrid : n;
+}
 
 hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
                           const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,

@@ -79,6 +79,24 @@ __device__ __forceinline__ float group_sum(float v, int width) {
 }
 __device__ __forceinline__ float wave_sum(float v) { return group_sum(v, kWave); }
 
+// Raw buffer loads.  A buffer resource covers [p, p + bytes), bytes < 2^31; a load at an
+// offset of kOOB or above returns zero without touching memory, so a lane with nothing to
+// load still issues the instruction and every lane of a wave issues the same loads.
+struct Buf {
+  __amdgpu_buffer_rsrc_t r;
+};
+__device__ __forceinline__ Buf make_buf(const void* p, uint32_t bytes) {
+  return Buf{__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000)};
+}
+constexpr uint32_t kOOB = 0x80000000u;
+__device__ __forceinline__ uint4 ldb(const Buf& b, uint32_t off) {  // through the caches
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b.r, off, 0, 0));
+}
+__device__ __forceinline__ uint4 ldb_nt(const Buf& b, uint32_t off) {  // streamed past them
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b.r, off, 0, 2));
+}
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 __device__ __forceinline__ int rank_in_mask(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }
@@ -127,18 +145,23 @@ __device__ void block_exclusive_scan(int* s, int n) {
   __syncthreads();
 }
 
-// Launch a gate kernel; if the benchmark hook armed a pair of events, the launch
-// records them at the kernel's start and end and disarms the hook.
+// Launch a gate kernel (the first, dominant kernel of a call); if the benchmark hook
+// armed a pair of events, the launch records them at the kernel's start and end and
+// disarms the hook.
 template <class K, class... Args>
-hipError_t launch_gate_kernel(K kernel, int grid, hipStream_t s, Args... args) {
+hipError_t launch_gate_kernel_n(K kernel, int grid, int block, hipStream_t s, Args... args) {
   GateTiming ev = g_gate_timing;
   if (ev.start) {
     g_gate_timing = GateTiming{};
-    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, s, ev.start, ev.stop, 0, args...);
+    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, s, ev.start, ev.stop, 0, args...);
   } else {
-    kernel<<<grid, kBlock, 0, s>>>(args...);
+    kernel<<<grid, block, 0, s>>>(args...);
   }
   return hipGetLastError();
+}
+template <class K, class... Args>
+hipError_t launch_gate_kernel(K kernel, int grid, hipStream_t s, Args... args) {
+  return launch_gate_kernel_n(kernel, grid, kBlock, s, args...);
 }
 
 }  // namespace

@@ -33,7 +33,7 @@ struct Workspace {
   float* seg_zval;     // [tc][slots]      act * <w_up[i], x_tau>
   float* z;            // [tc][r]          LoPA intermediate A x (LoPA only); for tc >= 2
                        //                  two partial copies [2][tc][r]
-  uint4* zf;           // [2 ceil(d_ff / 64)][tc][4][2]  zval fragments of the down product
+  uint4* zf;           // [2 batched_segments(d_ff)][tc][4][2]  zval fragments of the down product
                        //                  (matrix-core path, tc >= 2; empty for tc = 1)
 };
 
@@ -66,6 +66,7 @@ hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const 
 // Matrix-core path for batches of 2..64 tokens with bf16 weights (ffn_batched.hip):
 // the whole call (LoPA z, gate + union + W_up, down), clearing y first.
 bool batched_ok(const Shape& sh, Gate g);
+int batched_segments(int d_ff);
 hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
                           const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
                           float* y, hipStream_t s);

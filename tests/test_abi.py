@@ -36,6 +36,7 @@ def test_workspace_bytes():
     c = ffn.workspace_bytes(8, 4096, 14336, 512)
     assert 0 < a <= b < c
     assert a % 256 == 0
+    assert ffn.workspace_bytes(2, 4096, 14336, 512) < c < ffn.workspace_bytes(9, 4096, 14336, 512)
     # per-token state grows linearly with tokens up to the 64-token pass size, then stops
     assert ffn.workspace_bytes(64, 64, 100, 0) == ffn.workspace_bytes(500, 64, 100, 0)
     for bad in [(0, 8, 8, 0), (1, 0, 8, 0), (1, 8, 0, 0), (1, 8, 8, -1), (1, 1 << 20, 1 << 12, 0)]:

@@ -42,6 +42,8 @@ SMALL = [
     ("lopa_bf16_T20", 20, 264, 1000, 40, BF16, 1.3),        # two token tiles
     ("std_bf16_T40", 40, 136, 300, 0, BF16, 1.5),           # four token tiles, short rows
     ("std_bf16_T64", 64, 264, 1000, 0, BF16, 1.6),
+    ("std_bf16_d4096", 1, 4096, 2056, 0, BF16, 1.2816),    # full-width rows, short d_ff
+    ("std_bf16_d4096_odd", 1, 4096, 2052, 0, BF16, 1.2816),
     ("very_small", 1, 8, 3, 0, BF16, 0.0),
     ("d_is_1", 1, 1, 5, 0, F32, 0.0),
     ("lopa_r_is_1", 2, 16, 40, 1, F32, 0.1),
@@ -94,8 +96,9 @@ def test_full_size_dense(gu, r):
 
 # ---------------------------------------------------------------- edge cases
 EDGE_SHAPES = [(1, 264, 1000, 0, BF16), (1, 100, 77, 0, BF16), (1, 264, 1000, 40, BF16), (4, 64, 200, 0, F32),
-               (4, 264, 1000, 0, BF16), (16, 264, 1000, 40, BF16), (64, 136, 300, 0, BF16)]  # matrix-core batches
-POISON_SHAPES = EDGE_SHAPES[:3] + [(2, 264, 1000, 0, BF16), (2, 264, 1000, 40, BF16)]
+               (4, 264, 1000, 0, BF16), (16, 264, 1000, 40, BF16), (64, 136, 300, 0, BF16),  # matrix-core batches
+               (1, 4096, 1000, 0, BF16)]  # full-width rows, few segments
+POISON_SHAPES = EDGE_SHAPES[:3] + [(2, 264, 1000, 0, BF16), (2, 264, 1000, 40, BF16), (1, 4096, 1000, 0, BF16)]
 
 
 @pytest.mark.parametrize("shape", EDGE_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
