@@ -286,24 +286,28 @@ def cpu_baseline(inp, seed, pool, r, t, seconds):
                 host_cores_visible=len(os.sched_getaffinity(0)))
 
 
-def parity_sample(shape: Shape, r, t):
-    """Set 0, token 0: relative error of the library output against the oracle."""
+def parity_sample(shape: Shape, r, T, t):
+    """Step 0 of the timed workload (weight set 0, its first T tokens, the same call and
+    launch configuration): relative error of every token's output against the oracle,
+    and the active union against the union of the oracle's per-token active sets (a
+    neuron within 1e-3 of t for some token may go either way)."""
     import torch
     from oracle import ffn_oracle
     from paper_2609_31975_amd import ffn
     inp = shape.host0[r]
-    run = Runner(shape, r, 1, t, dense=False)
+    run = Runner(shape, r, T, t, dense=False)
     run(0)
     torch.cuda.synchronize()
-    y = run.y.cpu().numpy()[0].astype(np.float64)
-    x = shape.x[0][:1].cpu().numpy()
+    y = run.y.cpu().numpy().astype(np.float64)
+    x = run.args(0)[1].cpu().numpy()
     kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
     res = ffn_oracle.ffn(x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=inp.wdt, **kw)
-    idx, _ = ffn.ffn_active_set(run.ws, 1, shape.d, shape.d_ff, r, with_act=False)
-    ref = np.flatnonzero(res.active[0])
-    band = np.abs(res.h[0] - np.float32(t)) < 1e-3
+    idx, _ = ffn.ffn_active_set(run.ws, T, shape.d, shape.d_ff, r, with_act=False)
+    ref = np.flatnonzero(res.active.any(0))
+    band = (np.abs(res.h - np.float32(t)) < 1e-3).any(0)
     mism = np.setxor1d(idx, ref)
-    return dict(rel_err=float(np.linalg.norm(y - res.y[0]) / np.linalg.norm(res.y[0])),
+    err = [float(np.linalg.norm(y[k] - res.y[k]) / max(np.linalg.norm(res.y[k]), 1e-300)) for k in range(T)]
+    return dict(tokens=T, rel_err=max(err),
                 active_set_mismatches_outside_band=int((~band[mism]).sum()) if len(mism) else 0)
 
 
@@ -391,7 +395,7 @@ def main():
     rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True)
     gate_mean, gate_med = time_gate_kernel(run, K)
     gbytes = np.mean([gate_kernel_bytes(head.d, head.d_ff, r0, T0, k, False) for k in nlist])
-    par = parity_sample(sh, r0, head.t)
+    par = parity_sample(sh, r0, T0, head.t)
     traffic, traffic_src = recorded_traffic(head.name)
     log(f"[bench] headline {rec['us_per_call']} us/call, dense {dense_us:.2f}, gate kernel {gate_mean:.2f} us, "
         f"parity {par}")
