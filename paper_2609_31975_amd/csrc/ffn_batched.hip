@@ -421,20 +421,31 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict
 
 // ------------------------------------------------------------------ down projection
 // Workgroup b: column group b % S, row chunk b / S (segments [c nseg/R, (c+1) nseg/R)).
-// A column group is CW slots of 64 columns (two 32-column tiles), CW = 4 / NT; wave w
-// takes slot w % CW and every (4 / CW)-th used fragment group of the chunk (32 union
-// entries of one segment), the loads of its next group in flight while the current one
-// is multiplied.  The chunk's counts and slot indices are staged in LDS once.  The
-// waves' sums meet in LDS, then go to y with one fp32 atomic per token and column (y
-// was cleared by the gate kernel).
-constexpr int kDnTiles = 2;             // 32-column tiles per wave
-constexpr int kDnCols = 32 * kDnTiles;  // columns of a wave
-constexpr int kDnSlots = 8192;          // most slot indices of one row chunk
+// A wave owns DT 32-column tiles (DT = 4 for one token tile, else 2); a column group
+// is CW of them, and wave w takes column slot w % CW and every (4 / CW)-th used
+// fragment group of the chunk (32 union entries of one segment), the loads of its next
+// group in flight while the current one is multiplied.  A group's 32 W_down rows are
+// read (64 / 4 DT) rows x 64 DT bytes per instruction, streamed past the caches, and
+// reshaped through a wave-private LDS tile like the gate kernel's weights.  The chunk's
+// counts and slot indices are staged in LDS once.  The waves' sums meet in LDS, then go
+// to y with one fp32 atomic per token and column (y was cleared by the gate kernel).
+constexpr int kDnSlots = 4096;  // most slot indices of one row chunk
+
+template <int NT>
+struct DnCfg {
+  static constexpr int DT = NT == 1 ? 4 : 2;  // 32-column tiles per wave
+  static constexpr int CW = NT == 4 ? 1 : 2;  // column slots per workgroup
+  static constexpr int WCOLS = 32 * DT * CW;  // columns per workgroup
+  static constexpr int LPR = 4 * DT;          // lanes per row of a load instruction
+  static constexpr int RPI = kWave / LPR;     // rows per load instruction
+  static constexpr int NI = 32 / RPI;         // load instructions per group
+  static constexpr int PITCH = LPR + 1;       // chunks per LDS row (one pad chunk)
+};
 
 template <int NT>
 struct DnFrags {
-  uint4 t[kDnTiles][2];  // W_down rows of entries m and 16 + m, 8 columns each
-  uint4 zh[NT], zl[NT];  // zval fragments (hi, lo) of the token tiles
+  uint4 t[DnCfg<NT>::NI];  // W_down chunks as loaded: entry RPI i + lane / LPR, chunk lane % LPR
+  uint4 zh[NT], zl[NT];    // zval fragments (hi, lo) of the token tiles
 };
 
 struct DnChunk {
@@ -448,20 +459,18 @@ struct DnChunk {
 template <int NT>
 __device__ __forceinline__ void dn_load(DnFrags<NT>& f, int j, int ngrp, const DnChunk& ck, const Buf& db,
                                         const Buf& zb, int C, int cg0, int T, int tc) {
+  using K = DnCfg<NT>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
   const bool jv = j < ngrp;  // past the last group: out-of-range loads, nothing read
   const int sg = uniform(jv ? ck.grp[j] : 0), sl = sg >> 1, gi = sg & 1;
   const int cnt = uniform(ck.cnt[sl]), srow = uniform(ck.srow[sl]);
+  const int ch = cg0 + lane % K::LPR;
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int e = 32 * gi + 16 * hh + m;
-    const bool ok = jv && e < cnt;
+  for (int i = 0; i < K::NI; ++i) {
+    const int e = 32 * gi + K::RPI * i + lane / K::LPR;
+    const bool ok = jv && e < cnt && ch < C;
     const int idx = ok ? ck.idx[srow + e] : 0;
-#pragma unroll
-    for (int ct = 0; ct < kDnTiles; ++ct) {
-      const int ch = cg0 + 4 * ct + g;
-      f.t[ct][hh] = ldb(db, (ok && ch < C) ? 16u * (uint32_t)(idx * C + ch) : kOOB);
-    }
+    f.t[i] = ldb_nt(db, ok ? 16u * (uint32_t)(idx * C + ch) : kOOB);
   }
   const uint32_t zg = (uint32_t)((ck.seg_lo + sl) * 2 + gi) * (uint32_t)tc;
 #pragma unroll
@@ -473,12 +482,19 @@ __device__ __forceinline__ void dn_load(DnFrags<NT>& f, int j, int ngrp, const D
   }
 }
 
+// tile: this wave's LDS tile (32 PITCH uint4)
 template <int NT>
-__device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, const bf16x8_t (&sel)[2],
-                                       f32x4_t (&acc)[kDnTiles][2][NT]) {
+__device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, const bf16x8_t (&sel)[2], uint4* tile,
+                                       f32x4_t (&acc)[DnCfg<NT>::DT][2][NT]) {
+  using K = DnCfg<NT>;
+  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
 #pragma unroll
-  for (int ct = 0; ct < kDnTiles; ++ct) {
-    const bf16x8_t t0 = bf8(f.t[ct][0]), t1 = bf8(f.t[ct][1]);
+  for (int i = 0; i < K::NI; ++i) tile[(K::RPI * i + lane / K::LPR) * K::PITCH + lane % K::LPR] = f.t[i];
+  __builtin_amdgcn_wave_barrier();  // LDS operations of a wave complete in order
+#pragma unroll
+  for (int ct = 0; ct < K::DT; ++ct) {
+    // entries m and 16 + m, 8 columns (chunk g of the tile) each
+    const bf16x8_t t0 = bf8(tile[m * K::PITCH + 4 * ct + g]), t1 = bf8(tile[(16 + m) * K::PITCH + 4 * ct + g]);
     bf16x8_t bfrag[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -486,9 +502,9 @@ __device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, const bf16x8_t (&se
       const f32x4_t c0 = mfma16(t0, sel[h], zero);  // entries 4g..4g+3 of column 16h + m
       const f32x4_t c1 = mfma16(t1, sel[h], zero);  // entries 16+4g..16+4g+3
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        bfrag[h][j] = (__bf16)c0[j];
-        bfrag[h][4 + j] = (__bf16)c1[j];
+      for (int q = 0; q < 4; ++q) {
+        bfrag[h][q] = (__bf16)c0[q];
+        bfrag[h][4 + q] = (__bf16)c1[q];
       }
     }
 #pragma unroll
@@ -499,6 +515,7 @@ __device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, const bf16x8_t (&se
         acc[ct][h][nt] = mfma16(bf8(f.zl[nt]), bfrag[h], acc[ct][h][nt]);
       }
   }
+  __builtin_amdgcn_wave_barrier();
 }
 
 template <int NT>
@@ -507,7 +524,8 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
                                                       const uint4* __restrict__ zf, int nseg, int d_ff, int R, int tc,
                                                       const uint4* __restrict__ w_down_t, int C, int d, int T,
                                                       float* __restrict__ y) {
-  constexpr int CW = 4 / NT, GS = kParts / CW, WCOLS = kDnCols * CW;
+  using K = DnCfg<NT>;
+  constexpr int CW = K::CW, GS = kParts / CW, WCOLS = K::WCOLS;
   const Buf db = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
   const Buf zb = make_buf(zf, 256u * (uint32_t)nseg * (uint32_t)tc);
   __shared__ int s_cnt[kBlock];
@@ -516,6 +534,7 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   __shared__ int s_grp[2 * kBlock];
   __shared__ int s_idx[kDnSlots];
   __shared__ float s_y[16 * NT * WCOLS];
+  __shared__ uint4 s_stage[kParts][32 * K::PITCH];
 
   const int S = (C * 8 + WCOLS - 1) / WCOLS;
   const int chunk = blockIdx.x / S, cgrp = blockIdx.x % S;
@@ -550,34 +569,34 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
 #pragma unroll
     for (int j = 0; j < 8; ++j) sel[h][j] = (__bf16)((8 * g + j == 16 * h + m) ? 1.f : 0.f);
 
-  f32x4_t acc[kDnTiles][2][NT];
+  f32x4_t acc[K::DT][2][NT];
 #pragma unroll
-  for (int ct = 0; ct < kDnTiles; ++ct)
+  for (int ct = 0; ct < K::DT; ++ct)
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[ct][h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const DnChunk ck{s_grp, s_cnt, s_srow, s_idx, seg_lo};
-  const int cg0 = (cgrp * WCOLS + slot_w * kDnCols) / 8;  // first chunk of this wave's columns
+  const int cg0 = (cgrp * WCOLS + slot_w * 32 * K::DT) / 8;  // first chunk of this wave's columns
   if (phase < ngrp) {
     // two register sets alternate; loads past the last group read nothing
     DnFrags<NT> f0, f1;
     dn_load(f0, phase, ngrp, ck, db, zb, C, cg0, T, tc);
     for (int j = phase;;) {
       dn_load(f1, j + GS, ngrp, ck, db, zb, C, cg0, T, tc);
-      dn_mma(f0, sel, acc);
+      dn_mma(f0, sel, s_stage[wave], acc);
       j += GS;
       if (j >= ngrp) break;
       dn_load(f0, j + GS, ngrp, ck, db, zb, C, cg0, T, tc);
-      dn_mma(f1, sel, acc);
+      dn_mma(f1, sel, s_stage[wave], acc);
       j += GS;
       if (j >= ngrp) break;
     }
   }
   // lane holds tokens 16 nt + 4g + i of column 32 ct + 16 h + m of its slot
 #pragma unroll
-  for (int ct = 0; ct < kDnTiles; ++ct)
+  for (int ct = 0; ct < K::DT; ++ct)
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -585,7 +604,7 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int tok = 16 * nt + 4 * g + i;
-          if (tok < T) atomicAdd(&s_y[tok * WCOLS + slot_w * kDnCols + 32 * ct + 16 * h + m], acc[ct][h][nt][i]);
+          if (tok < T) atomicAdd(&s_y[tok * WCOLS + slot_w * 32 * K::DT + 32 * ct + 16 * h + m], acc[ct][h][nt][i]);
         }
   __syncthreads();
   for (int o = tid; o < T * WCOLS; o += kBlock) {
@@ -623,18 +642,18 @@ hipError_t gate_nt(const Shape& sh, const float* x, const void* gate_w, const vo
 }
 
 // Down grid: S column groups x R row chunks, about kDnWgTarget workgroups, at most
-// kDnAtomicsMax fp32 atomics into y (half that for 64-token tiles, whose workgroups
-// carry four times the zval traffic), every chunk within the LDS slot and segment limits.
+// kDnAtomicsMax fp32 atomics into y (fewer, longer row chunks measured faster than more
+// parallel short ones), every chunk within the LDS slot and segment limits.
 constexpr int kDnWgTarget = 512;
-constexpr int64_t kDnAtomicsMax = 2 << 20;
+constexpr int64_t kDnAtomicsMax = 1 << 20;
 
 template <int NT>
 hipError_t down_mfma(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
   const int C = sh.d / 8;
-  const int64_t wcols = kDnCols * (4 / NT);
+  const int64_t wcols = DnCfg<NT>::WCOLS;
   const int64_t S = ((int64_t)sh.d + wcols - 1) / wcols;
   int64_t R = (kDnWgTarget + S - 1) / S;
-  const int64_t amax = (NT == 4 ? kDnAtomicsMax / 2 : kDnAtomicsMax) / ((int64_t)sh.T * sh.d);
+  const int64_t amax = kDnAtomicsMax / ((int64_t)sh.T * sh.d);
   if (R > amax) R = amax;
   const int64_t rmin = (ws.nseg + kBlock - 1) / kBlock;
   if (R < rmin) R = rmin;
