@@ -51,16 +51,6 @@ __device__ __forceinline__ void load_vec(const float* __restrict__ v, int C, int
   }
 }
 
-template <int CPL>
-__device__ __forceinline__ void load_row(const uint4* __restrict__ row, bool valid, int C, int q, int lpr,
-                                         uint4 (&b)[CPL]) {
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const int ch = q + c * lpr;
-    b[c] = (valid && ch < C) ? ld_weights(row + ch) : make_uint4(0u, 0u, 0u, 0u);
-  }
-}
-
 template <class W, int CPL>
 __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const float (&v)[CPL][W::EPC]) {
   float acc0 = 0.f, acc1 = 0.f;
@@ -77,50 +67,68 @@ __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const float (&v
   return acc0 + acc1;
 }
 
-// Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n): each wave takes
-// passes of 64/lpr rows (passes wave, wave + 4, ...); with kPipeline the loads of its
-// next pass are issued before the current pass is reduced.  `sink(k, value)` runs on
-// lane q == 0.
-#ifndef FFN_GATE_PIPE
-#define FFN_GATE_PIPE 0
-#endif
-constexpr bool kPipeline = FFN_GATE_PIPE != 0;
+// Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n), of a matrix of
+// `bytes` bytes (< 2^31): each wave takes passes of 64/lpr rows (passes wave, wave + 4,
+// ...).  For rows of at most 8 chunks per lane and more than one pass per wave, two
+// register sets alternate, the loads of the next pass issued before the current pass is
+// reduced; the loads are raw buffer
+// loads (out-of-range offsets past the last pass), so every pass issues the same loads
+// and the load-counter waits are exact.  `sink(k, value)` runs on lane q == 0.
+template <class W, int CPL>
+__device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, bool ok, int row, uint4 (&b)[CPL]) {
+  const uint32_t base = ok ? 16u * (uint32_t)row * (uint32_t)C : kOOB;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = q + c * lpr;
+    b[c] = ldb_nt(mb, (ok && ch < C) ? base + 16u * (uint32_t)ch : kOOB);
+  }
+}
 
 template <class W, int CPL, class RowOf, class Sink>
-__device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, int C, int lpr, int lpr_log2, int n,
-                                         const float (&v)[CPL][W::EPC], RowOf row_of, Sink sink) {
+__device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
+                                         int n, const float (&v)[CPL][W::EPC], RowOf row_of, Sink sink) {
   constexpr int kWaves = kBlock / kWave;
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const Buf mb = make_buf(mat, bytes);
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int q = lane & (lpr - 1), p = lane >> lpr_log2;
   const int rpp = kWave >> lpr_log2;
   const int npass = (n + rpp - 1) / rpp;
-  int pass = wave;
-  if (pass >= npass) return;
-  int k = pass * rpp + p;
-  bool ok = k < n;
-  uint4 cur[CPL];
-  load_row<CPL>(mat + (size_t)row_of(ok ? k : 0) * C, ok, C, q, lpr, cur);
-  while (true) {
-    const int pass_n = pass + kWaves;
-    const int k_n = pass_n * rpp + p;
-    const bool more = pass_n < npass;
-    const bool ok_n = more && k_n < n;
-    uint4 nxt[CPL];
-    float sum;
-    if constexpr (kPipeline) {
-      if (more) load_row<CPL>(mat + (size_t)row_of(ok_n ? k_n : 0) * C, ok_n, C, q, lpr, nxt);
-      sum = group_sum(lane_dot<W, CPL>(cur, v), lpr);
-    } else {
-      sum = group_sum(lane_dot<W, CPL>(cur, v), lpr);
-      if (more) load_row<CPL>(mat + (size_t)row_of(ok_n ? k_n : 0) * C, ok_n, C, q, lpr, nxt);
+  if (wave >= npass) return;
+  auto load = [&](uint4 (&b)[CPL], int pass) {
+    const int k = pass * rpp + p;
+    const bool ok = pass < npass && k < n;
+    load_pass<W, CPL>(mb, C, q, lpr, ok, ok ? row_of(k) : 0, b);
+  };
+  auto finish = [&](const uint4 (&b)[CPL], int pass) {
+    const int k = pass * rpp + p;
+    const float sum = group_sum(lane_dot<W, CPL>(b, v), lpr);
+    if (q == 0 && k < n) sink(k, sum);
+  };
+  uint4 b0[CPL];
+  load(b0, wave);
+  if (wave + kWaves >= npass) {  // a single pass: nothing to overlap
+    finish(b0, wave);
+    return;
+  }
+  if constexpr (CPL <= 8) {
+    uint4 b1[CPL];
+    for (int pass = wave;;) {
+      load(b1, pass + kWaves);
+      finish(b0, pass);
+      pass += kWaves;
+      if (pass >= npass) break;
+      load(b0, pass + kWaves);
+      finish(b1, pass);
+      pass += kWaves;
+      if (pass >= npass) break;
     }
-    if (q == 0 && ok) sink(k, sum);
-    if (!more) break;
-    pass = pass_n;
-    k = k_n;
-    ok = ok_n;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) cur[c] = nxt[c];
+  } else {
+    for (int pass = wave;;) {
+      finish(b0, pass);
+      pass += kWaves;
+      if (pass >= npass) break;
+      load(b0, pass);
+    }
   }
 }
 
@@ -163,7 +171,7 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ 
   const int rows_per_block = (kBlock / kWave) * (kWave >> lpr_log2);
   const int k0 = blockIdx.x * rows_per_block;
   const int n = min(rows_per_block, r - k0);
-  dot_rows<W, CPL>(A, C, lpr, lpr_log2, n, xr, [&](int k) { return k0 + k; },
+  dot_rows<W, CPL>(A, 16u * (uint32_t)r * (uint32_t)C, C, lpr, lpr_log2, n, xr, [&](int k) { return k0 + k; },
                    [&](int k, float s) { z[k0 + k] = s; });
 }
 
@@ -196,23 +204,25 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
     {
       float zr[CPLG][W::EPC];
       load_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
-      dot_rows<W, CPLG>(gate_w, Cg, lprg, lprg_log2, nrows, zr, gate_row, gate_sink);
+      dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
+                        gate_sink);
     }
     __syncthreads();
     compact_segment(s_h, nrows, row0, seg, t, DENSE, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
     float xr[CPLU][W::EPC];
     load_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
-    dot_rows<W, CPLU>(w_up, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
+    dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   } else {
     static_assert(CPLG == CPLU, "standard gating shares the x registers");
     float xr[CPLU][W::EPC];
     load_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
-    dot_rows<W, CPLU>(gate_w, Cg, lprg, lprg_log2, nrows, xr, gate_row, gate_sink);
+    dot_rows<W, CPLU>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, xr, gate_row,
+                      gate_sink);
     __syncthreads();
     compact_segment(s_h, nrows, row0, seg, t, DENSE, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
-    dot_rows<W, CPLU>(w_up, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
+    dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   }
 }
 
@@ -510,10 +520,15 @@ int resident_segments(K kernel, int* per_cu, int d_ff) {
   return g;
 }
 
+// The fast single-token kernels address a matrix with 32-bit byte offsets below 2^31.
 bool fast_ok(const Shape& sh, Gate g) {
   const int epc_ = sh.wdt == 1 ? WBf16::EPC : WF32::EPC;
+  const int64_t wb = sh.wdt == 1 ? 2 : 4, lim = int64_t(1) << 31;
   if (sh.T != 1 || sh.d % epc_ != 0 || cpl_for(sh.d / epc_) == 0) return false;
-  if (g == Gate::LoPA && (sh.r % epc_ != 0 || cpl_for(sh.r / epc_) == 0)) return false;
+  if (wb * sh.d_ff * sh.d >= lim) return false;
+  if (g == Gate::LoPA && (sh.r % epc_ != 0 || cpl_for(sh.r / epc_) == 0 || wb * sh.r * sh.d >= lim ||
+                          wb * sh.d_ff * sh.r >= lim))
+    return false;
   return true;
 }
 
