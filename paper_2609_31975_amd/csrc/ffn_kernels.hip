@@ -499,13 +499,10 @@ int cu_count() {
   return cus[slot];
 }
 
-// Segments for the T = 1 gate kernel: kSegWaves row-balanced segments per workgroup
-// slot the GPU holds at once (so every CU gets the same number of rows), never more
-// than kSegMax rows per segment.  `per_cu` caches the kernel's occupancy.
-#ifndef FFN_SEG_WAVES
-#define FFN_SEG_WAVES 1
-#endif
-constexpr int kSegWaves = FFN_SEG_WAVES;
+// Segments for the T = 1 gate kernel: one row-balanced segment per workgroup slot the
+// GPU holds at once (so every CU gets the same number of rows; more segments than
+// resident slots measured slower), never more than kSegMax rows per segment.  `per_cu`
+// caches the kernel's occupancy.
 template <class K>
 int resident_segments(K kernel, int* per_cu, int d_ff) {
   if (*per_cu == 0) {
@@ -513,7 +510,7 @@ int resident_segments(K kernel, int* per_cu, int d_ff) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kBlock, 0) != hipSuccess || n <= 0) n = 1;
     *per_cu = n;
   }
-  int g = cu_count() * *per_cu * kSegWaves;
+  int g = cu_count() * *per_cu;
   const int lo = (d_ff + kSegMax - 1) / kSegMax;
   if (g < lo) g = lo;
   if (g > d_ff) g = d_ff;
@@ -590,10 +587,7 @@ hipError_t lopa_z(const Shape& sh, const float* x, const void* A, const Workspac
 
 // Down-projection grid for T = 1: S column slices x R row chunks, about
 // kDownWgPerCu workgroups per CU, at most 64 segments per chunk.
-#ifndef FFN_DOWN_WG_PER_CU
-#define FFN_DOWN_WG_PER_CU 2
-#endif
-constexpr int kDownWgPerCu = FFN_DOWN_WG_PER_CU;
+constexpr int kDownWgPerCu = 2;
 
 void down_grid(int C, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
   *S = (C + kWave - 1) / kWave;
