@@ -46,7 +46,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kTiles = 4;                // 16-row tiles of a gate segment
 constexpr int kSegRowsB = 16 * kTiles;   // rows per gate segment (one 64-lane ballot)
 constexpr int kParts = kBlock / kWave;   // k parts of a workgroup, one per wave
-constexpr int kSegGrid = 256;            // most workgroups of the gate kernel (one per CU)
+constexpr int kSegGrid = 256;            // most workgroups of the gate kernel, one per CU
+constexpr int kSegGrid2 = 512;           // the same at two workgroups per CU
 
 __device__ __forceinline__ f32x4_t mfma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -264,16 +265,14 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 // vectors holding entries 4g .. 4g + 3 then 16 + 4g .. 16 + 4g + 3 of the group; a used
 // group is written whole (zero past the union), an unused one is never read.
 // LOPA: the gate rows are B [d_ff][r] against z = zp[0] + zp[1]; otherwise W_gate x.
-template <bool LOPA, bool DENSE, int NT>
-__global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict__ x, const float* __restrict__ zp,
-                                                         const uint4* __restrict__ gate_w, int Cg,
-                                                         const uint4* __restrict__ w_up, int Cu, int T, int d,
-                                                         int d_ff, int nseg, float t, int slots, int tc,
-                                                         int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
-                                                         int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
-                                                         uint4* __restrict__ zf, float* __restrict__ y) {
-  constexpr int KU = (NT == 1 && !LOPA) ? 4 : 2;  // gate rows
-  constexpr int KUU = NT == 1 ? 4 : 2;               // W_up rows
+// KU / KUU: k steps per load group of the gate rows / the W_up rows.
+template <bool LOPA, bool DENSE, int NT, int KU, int KUU>
+__device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const float* __restrict__ zp,
+                                             const uint4* __restrict__ gate_w, int Cg, const uint4* __restrict__ w_up,
+                                             int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,
+                                             int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
+                                             int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
+                                             uint4* __restrict__ zf, float* __restrict__ y) {
   constexpr int STAGE = WStage<kTiles, (KU > KUU ? KU : KUU)>::WORDS;
   __shared__ uint4 s_stage[kParts][STAGE];
   __shared__ f32x4_t s_red[kParts][kTiles][NT][kWave];
@@ -418,6 +417,31 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(const float* __restrict
     }
   }
 }
+
+#define FFN_GATE_UP_PARAMS                                                                                         \
+  const float *__restrict__ x, const float *__restrict__ zp, const uint4 *__restrict__ gate_w, int Cg,             \
+      const uint4 *__restrict__ w_up, int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,       \
+      int32_t *__restrict__ meta, int32_t *__restrict__ seg_count, int32_t *__restrict__ seg_idx,                  \
+      float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y
+#define FFN_GATE_UP_ARGS x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y
+
+// One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
+// gate rows and for wider token tiles).
+template <bool LOPA, bool DENSE, int NT>
+__global__ __launch_bounds__(kBlock) void k_gate_up_mfma(FFN_GATE_UP_PARAMS) {
+  gate_up_body<LOPA, DENSE, NT, (NT == 1 && !LOPA) ? 4 : 2, NT == 1 ? 4 : 2>(FFN_GATE_UP_ARGS);
+}
+
+// Standard gating, one token tile: two k steps a group, so that two workgroups fit a CU
+// (at most 256 registers a lane); one workgroup's phase changes (LDS reductions, union)
+// then overlap the other's streaming.
+template <bool DENSE>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) void k_gate_up_mfma2(
+    FFN_GATE_UP_PARAMS) {
+  gate_up_body<false, DENSE, 1, 2, 2>(FFN_GATE_UP_ARGS);
+}
+#undef FFN_GATE_UP_PARAMS
+#undef FFN_GATE_UP_ARGS
 
 // ------------------------------------------------------------------ down projection
 // Workgroup b: column group b % S, row chunk b / S (segments [c nseg/R, (c+1) nseg/R)).
@@ -622,15 +646,30 @@ hipError_t z_mfma(const Shape& sh, const float* x, const void* lopa_a, const Wor
   return hipGetLastError();
 }
 
+// Row-balanced segments of at most 64 rows; beyond 128 of them the count is a multiple
+// of the gate kernel's grid so that every workgroup gets the same number.
+int segments_for(int d_ff, int grid) {
+  const int n = (d_ff + kSegRowsB - 1) / kSegRowsB;
+  return n > 128 ? (n + grid - 1) / grid * grid : n;
+}
+
 template <bool LOPA, bool DENSE, int NT>
 hipError_t gate_mfma(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
                      float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
-  return launch_gate_kernel(k_gate_up_mfma<LOPA, DENSE, NT>, ws.nseg < kSegGrid ? ws.nseg : kSegGrid, s, x,
-                            (const float*)ws.z,
-                            static_cast<const uint4*>(gate_w), Cg, static_cast<const uint4*>(w_up), Cu, sh.T, sh.d,
-                            sh.d_ff, ws.nseg, t, ws.slots, ws.tc, ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act,
-                            ws.zf, y);
+  constexpr bool two = !LOPA && NT == 1;
+  const int grid = two ? kSegGrid2 : kSegGrid;
+  ws.nseg = segments_for(sh.d_ff, grid);
+  const int g = ws.nseg < grid ? ws.nseg : grid;
+  auto kernel = [&] {
+    if constexpr (two)
+      return k_gate_up_mfma2<DENSE>;
+    else
+      return k_gate_up_mfma<LOPA, DENSE, NT>;
+  }();
+  return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
+                            static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y);
 }
 
 template <bool LOPA, bool DENSE>
@@ -674,18 +713,14 @@ bool batched_ok(const Shape& sh, Gate g) {
   if (sh.wdt != 1 || sh.T < 2 || sh.T > kTokChunk || sh.d % 8 != 0) return false;
   const int64_t lim = int64_t(1) << 31;
   if (2 * (int64_t)sh.d_ff * sh.d >= lim || 4 * (int64_t)kTokChunk * sh.d >= lim) return false;
-  if ((int64_t)((sh.d_ff + kSegRowsB - 1) / kSegRowsB) * 256 * kTokChunk >= lim) return false;
+  if ((int64_t)segments_for(sh.d_ff, kSegGrid2) * 256 * kTokChunk >= lim) return false;
   if (g == Gate::LoPA && (sh.r % 8 != 0 || 2 * (int64_t)sh.d_ff * sh.r >= lim || 2 * (int64_t)sh.r * sh.d >= lim))
     return false;
   return true;
 }
 
-// Row-balanced segments of at most 64 rows; beyond 128 of them the count is a multiple
-// of kSegGrid so that a grid of kSegGrid workgroups gives every workgroup the same number.
-int batched_segments(int d_ff) {
-  const int n = (d_ff + kSegRowsB - 1) / kSegRowsB;
-  return n > kSegGrid / 2 ? (n + kSegGrid - 1) / kSegGrid * kSegGrid : n;
-}
+// the most segments any gate kernel of this path uses (workspace sizing)
+int batched_segments(int d_ff) { return segments_for(d_ff, kSegGrid2); }
 
 hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
                           const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
@@ -697,7 +732,6 @@ hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, c
                    : sh.T <= 32 ? z_mfma<2>(sh, x, lopa_a, ws, s) : z_mfma<4>(sh, x, lopa_a, ws, s);
     if (e != hipSuccess) return e;
   }
-  ws.nseg = batched_segments(sh.d_ff);
   if (lopa)
     e = dense ? gate_nt<true, true>(sh, x, gate_w, w_up, t, ws, y, s)
               : gate_nt<true, false>(sh, x, gate_w, w_up, t, ws, y, s);
