@@ -44,6 +44,8 @@ SMALL = [
     ("std_bf16_T64", 64, 264, 1000, 0, BF16, 1.6),
     ("std_bf16_d4096", 1, 4096, 2056, 0, BF16, 1.2816),    # full-width rows, short d_ff
     ("std_bf16_d4096_odd", 1, 4096, 2052, 0, BF16, 1.2816),
+    ("std_bf16_T4_odd_d", 4, 100, 77, 0, BF16, 0.5),       # batch with d not a multiple of 8: element-wise
+    ("lopa_bf16_T3_odd_r", 3, 264, 1000, 36, BF16, 1.0),    # batch with r not a multiple of 8: element-wise
     ("very_small", 1, 8, 3, 0, BF16, 0.0),
     ("d_is_1", 1, 1, 5, 0, F32, 0.0),
     ("lopa_r_is_1", 2, 16, 40, 1, F32, 0.1),
