@@ -6,17 +6,18 @@
 // projection.  Token-side operands (x, z, zval) enter as bf16 hi + lo pairs (v - hi
 // rounded again): two MFMAs per step whose products are exact in fp32, so the split
 // leaves a relative error of about 2^-16 per element, far inside the 1e-3 band of the
-// active-set decision.  A 16-row weight tile is the A operand, streamed from HBM
-// straight into registers: lane l holds 8 consecutive bf16 of row l mod 16 and the
-// four lane groups l / 16 take four consecutive 16-byte chunks, so one instruction
-// reads 64 contiguous bytes of each of 16 rows.  Which k positions a lane group holds
-// does not matter for a full reduction as long as both operands use the same ones.
+// active-set decision.  A 16-row weight tile is the A operand: lane l holds 8
+// consecutive bf16 of row l mod 16 and the four lane groups l / 16 hold four
+// consecutive 16-byte chunks.  Which k positions a lane group holds does not matter for
+// a full reduction as long as both operands use the same ones.  Weights are read row by
+// row (up to 256 contiguous bytes of a row per instruction) and reshaped into that
+// layout through a wave-private LDS tile (see the streaming core).
 //
 // One call is three kernels (two for standard gating):
 //   k_lopa_z_mfma  z = A x as two partial sums over halves of the d range;
-//   k_gate_up_mfma per 64-row segment: gate, union of the tokens' active rows (ascending),
-//                  W_up dots of the union rows; zval = act * v is left in the A-operand
-//                  fragment order of the down product;
+//   k_gate_up_mfma per segment of at most 64 rows: gate, union of the tokens' active rows,
+//                  ascending, W_up dots of the union rows; zval = act * v is left in
+//                  the A-operand fragment order of the down product;
 //   k_down_mfma    Y[tokens][cols] += Z[tokens][entries] D[entries][cols] over the
 //                  union rows, segment by segment.
 // A wave of the gate kernel multiplies four row tiles over a quarter of the k range, so
@@ -256,11 +257,11 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 
 // ------------------------------------------------------------------ gate + union + W_up
 // Segments of at most 64 neurons, each workgroup taking every gridDim.x-th one.  Wave w
-// multiplies the segment's
-// four row tiles over k part w; the parts are added in LDS, wave w owning tile w.  A
-// neuron joins the union if any token activates it (h > t; NaN compares false); one
-// ballot orders the union ascending.  The W_up dots of the union rows use the same
-// split, and zval = act * v goes to the fragment buffer of the down kernel:
+// multiplies the segment's four row tiles over k part w; the parts are added in LDS,
+// wave w owning tile w.  A neuron joins the union if any token activates it (h > t;
+// NaN compares false); one ballot orders the union ascending.  The W_up dots of the
+// union rows use the same split, and zval = act * v goes to the fragment buffer of the
+// down kernel:
 // group (segment, entries 32 gi .. 32 gi + 31), token, lane group g, 16-byte hi and lo
 // vectors holding entries 4g .. 4g + 3 then 16 + 4g .. 16 + 4g + 3 of the group; a used
 // group is written whole (zero past the union), an unused one is never read.
