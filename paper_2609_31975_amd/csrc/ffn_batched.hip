@@ -424,7 +424,8 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       const uint4 *__restrict__ w_up, int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,       \
       int32_t *__restrict__ meta, int32_t *__restrict__ seg_count, int32_t *__restrict__ seg_idx,                  \
       float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y
-#define FFN_GATE_UP_ARGS x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y
+#define FFN_GATE_UP_ARGS \
+  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y
 
 // One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
 // gate rows and for wider token tiles).

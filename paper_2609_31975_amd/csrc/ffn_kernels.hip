@@ -653,7 +653,8 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, c
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s) {
-  if (sh.wdt == 1) return dense ? down<WBf16, true>(sh, w_down_t, ws, y, s) : down<WBf16, false>(sh, w_down_t, ws, y, s);
+  if (sh.wdt == 1)
+    return dense ? down<WBf16, true>(sh, w_down_t, ws, y, s) : down<WBf16, false>(sh, w_down_t, ws, y, s);
   return dense ? down<WF32, true>(sh, w_down_t, ws, y, s) : down<WF32, false>(sh, w_down_t, ws, y, s);
 }
 
