@@ -168,3 +168,32 @@ def test_repeatable(gu, r):
     y2, i2, a2, _ = gu.run_gpu(dev, 1.2816)
     assert np.array_equal(i1, i2) and np.array_equal(a1.view(np.uint32), a2.view(np.uint32))
     assert gu.rel_err(y2, y1) < 1e-6
+
+
+# ---------------------------------------------------------------- random shapes
+def _random_cases(n=12, seed=2026):
+    """Seeded shapes across every dispatch path: token counts 1..70, d and r multiples
+    of 8 (fast and matrix-core kernels) or not (element-wise), short and ragged d_ff."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        T = int(rng.choice([1, 1, 2, 3, 5, 8, 13, 16, 17, 33, 64, 70]))
+        d = int(rng.choice([8, 64, 136, 264, 520, 1032, 100, 250]))
+        d_ff = int(rng.integers(3, 1500))
+        r = int(rng.choice([0, 0, 8, 16, 40, 24, 36]))
+        wdt = BF16 if rng.random() < 0.75 else F32
+        t = float(rng.choice([0.0, 0.8416, 1.2816, 1.6449]))
+        cases.append((f"rand{i}_T{T}_d{d}_dff{d_ff}_r{r}_{'bf16' if wdt == BF16 else 'f32'}", T, d, d_ff, r, wdt, t))
+    return cases
+
+
+RANDOM = _random_cases()
+
+
+@pytest.mark.parametrize("case", RANDOM, ids=[c[0] for c in RANDOM])
+def test_random_shapes(gu, case):
+    name, T, d, d_ff, r, wdt, t = case
+    inp = wl.make_inputs(106, T, d, d_ff, r=r, wdt=wdt)
+    dev = gu.DevInputs(inp)
+    y, idx, act, _ = gu.run_gpu(dev, t)
+    gu.check_parity(gu.run_oracle(inp, t), y, idx, act, t, wdt, what=name)
