@@ -181,6 +181,26 @@ def test_lopa_signed_permutation(wdt):
     np.testing.assert_allclose(lop.y, std.y, rtol=1e-12, atol=1e-14)
 
 
+def test_lopa_general_factorization():
+    """r = d with A a random orthogonal matrix Q and B = W_gate Q^T (fp32): B (A x) is W_gate x
+    up to the fp32 rounding of the factors, so the gate, the active set outside a
+    1e-4 band and the output match standard gating."""
+    d, d_ff, t = 32, 90, 0.5
+    inp = wl.make_inputs(16, 3, d, d_ff, wdt=wl.F32)
+    Q, _ = np.linalg.qr(np.random.default_rng(6).standard_normal((d, d)))
+    A = Q.astype(np.float32)
+    B = (inp.w_gate.astype(np.float64) @ A.astype(np.float64).T).astype(np.float32)
+    common = dict(w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wl.F32)
+    std = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, **common)
+    lop = ffn_oracle.ffn(inp.x, lopa_a=A, lopa_b=B, **common)
+    np.testing.assert_allclose(lop.z, inp.x.astype(np.float64) @ A.astype(np.float64).T, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(lop.h, std.h, atol=1e-5)
+    far = np.abs(std.h - t) > 1e-4
+    assert np.array_equal(lop.active[far], std.active[far])
+    if np.array_equal(lop.active, std.active):
+        np.testing.assert_allclose(lop.y, std.y, rtol=1e-4, atol=1e-7)
+
+
 @pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
 def test_tokens_are_independent(wdt):
     inp = wl.make_inputs(15, 4, 24, 64, r=6, wdt=wdt)
