@@ -34,9 +34,9 @@
  * that share a workspace must be ordered (same stream); distinct workspaces may run
  * concurrently.  y must not overlap x, the weights or the workspace.
  *
- * Determinism: the active set and the activations are bit-reproducible.  For one
- * token the output is summed over row chunks with fp32 atomic adds, so its last bits
- * may differ between runs (the order of the additions is not fixed).
+ * Determinism: the active set and the activations are bit-reproducible.  The output
+ * is summed over row chunks with fp32 atomic adds, so its last bits may differ between
+ * runs (the order of the additions is not fixed).
  *
  * Errors: arguments are checked on the host before anything is enqueued; on a
  * negative return nothing was enqueued.  A launch failure returns FFN_ERR_HIP.
@@ -45,6 +45,10 @@
  * Semantics of special values: a NaN gate value is inactive (h > t is false).
  * Inf/NaN in the w_up / w_down_t rows of a neuron that is active for any token of
  * the batch propagate into every token's output (the row is read for the union).
+ * For batches of 2..64 tokens with bf16 weights and d a multiple of 8 (the
+ * matrix-core path) such a value in a w_down_t row also reaches the other columns of
+ * its 16-column block: the rows are transposed by a product with a 0/1 matrix, and
+ * 0 x Inf is NaN.  Rows of neurons inactive for every token are never read.
  */
 #ifndef FFN_SPARSE_H
 #define FFN_SPARSE_H
