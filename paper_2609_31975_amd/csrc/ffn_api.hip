@@ -165,8 +165,9 @@ int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_uni
       return FFN_ERR_HIP;
   }
   int n = 0;
+  const ffn::Split segs(d_ff, nseg);
   for (int s = 0; s < nseg; ++s) {
-    const int row0 = (int)(((int64_t)s * d_ff) / nseg), row1 = (int)(((int64_t)(s + 1) * d_ff) / nseg);
+    const int row0 = segs.start(s), row1 = segs.start(s + 1);
     if (cnt[s] < 0 || cnt[s] > row1 - row0) return FFN_ERR_HIP;  // workspace does not hold a finished call
     for (int e = 0; e < cnt[s]; ++e) {
       const int slot = row0 + e;

@@ -289,10 +289,11 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
   const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu);
 
   // segments blockIdx.x, blockIdx.x + gridDim.x, ... (the host makes the counts equal)
+  const Split segs(d_ff, nseg);
   for (int seg = blockIdx.x; seg < nseg; seg += gridDim.x) {
     if (seg != (int)blockIdx.x) __syncthreads();  // the previous segment's LDS reads are done
-    const int row0 = seg_row(seg, d_ff, nseg);
-    const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;  // <= kSegRowsB, guaranteed by the host
+    const int row0 = segs.start(seg);
+    const int nrows = segs.start(seg + 1) - row0;  // <= kSegRowsB, guaranteed by the host
 
     f32x4_t acc[kTiles][NT];
 #pragma unroll
@@ -556,7 +557,7 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   const Buf zb = make_buf(zf, 256u * (uint32_t)nseg * (uint32_t)tc);
   __shared__ int s_cnt[kBlock];
   __shared__ int s_srow[kBlock];
-  __shared__ int s_goff[kBlock + 1];
+  __shared__ int s_wgrp[kBlock / kWave];
   __shared__ int s_grp[2 * kBlock];
   __shared__ int s_idx[kDnSlots];
   __shared__ float s_y[16 * NT * WCOLS];
@@ -564,29 +565,39 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
 
   const int S = (C * 8 + WCOLS - 1) / WCOLS;
   const int chunk = blockIdx.x / S, cgrp = blockIdx.x % S;
-  const int seg_lo = (int)(((int64_t)chunk * nseg) / R), seg_hi = (int)(((int64_t)(chunk + 1) * nseg) / R);
+  const Split chunks(nseg, R), segs(d_ff, nseg);
+  const int seg_lo = chunks.start(chunk), seg_hi = chunks.start(chunk + 1);
   const int nsc = seg_hi - seg_lo;  // <= kBlock, guaranteed by the host
-  const int row_lo = seg_row(seg_lo, d_ff, nseg);
-  const int nslot = seg_row(seg_hi, d_ff, nseg) - row_lo;  // <= kDnSlots, guaranteed by the host
+  const int row_lo = segs.start(seg_lo);
+  const int nslot = segs.start(seg_hi) - row_lo;  // <= kDnSlots, guaranteed by the host
   const int tid = threadIdx.x, lane = lane_id(), wave = uniform(tid / kWave);
   const int m = lane & 15, g = lane >> 4;
   const int slot_w = wave % CW, phase = wave / CW;
 
+  // segment tid of the chunk has (c > 0) + (c > 32) fragment groups; their places in
+  // the group list come from two ballots and the per-wave totals
   const int c = tid < nsc ? seg_count[seg_lo + tid] : 0;
   s_cnt[tid] = c;
-  s_srow[tid] = tid < nsc ? seg_row(seg_lo + tid, d_ff, nseg) - row_lo : 0;
-  s_goff[tid] = (c > 0) + (c > 32);
+  s_srow[tid] = tid < nsc ? segs.start(seg_lo + tid) - row_lo : 0;
   for (int o = tid; o < nslot; o += kBlock) s_idx[o] = seg_idx[row_lo + o];
   for (int o = tid; o < T * WCOLS; o += kBlock) s_y[o] = 0.f;
+  const uint64_t has1 = __ballot(c > 0), has2 = __ballot(c > 32);
+  if (lane == 0) s_wgrp[wave] = __popcll(has1) + __popcll(has2);
   __syncthreads();
-  block_exclusive_scan(s_goff, kBlock);
+  int gbase = 0, ngrp = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / kWave; ++w) {
+    const int v = s_wgrp[w];
+    gbase += w < wave ? v : 0;
+    ngrp += v;
+  }
+  ngrp = uniform(ngrp);
   if (tid < nsc) {
-    const int b = s_goff[tid];
+    const int b = gbase + rank_in_mask(has1) + rank_in_mask(has2);
     if (c > 0) s_grp[b] = tid << 1;
     if (c > 32) s_grp[b + 1] = (tid << 1) | 1;
   }
   __syncthreads();
-  const int ngrp = uniform(s_goff[kBlock]);
 
   // 0/1 selectors: column 16 h + m of the 32-column tile
   bf16x8_t sel[2];

@@ -101,15 +101,17 @@ __device__ __forceinline__ int rank_in_mask(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }
 
-// ------------------------------------------------------------------ segments
-// The d_ff neurons are split into nseg row-balanced segments; segment w covers rows
-// [seg_row(w), seg_row(w + 1)) (at most kSegMax of them).  Its active neurons occupy
-// slots seg_row(w) .. seg_row(w) + seg_count[w] - 1, in ascending neuron order.
-__device__ __forceinline__ int seg_row(int w, int d_ff, int nseg) { return (int)(((int64_t)w * d_ff) / nseg); }
-
-// the segment that contains `row`: the largest w with seg_row(w) <= row
-__device__ __forceinline__ int seg_of_row(int row, int d_ff, int nseg) {
-  return (int)((((int64_t)row + 1) * nseg + d_ff - 1) / d_ff) - 1;
+// Inclusive prefix sum over the 64 lanes: shifts within each row of 16 lanes (DPP),
+// then the totals of the lower rows, read from lanes 15, 31 and 47.
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+            r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane_id() >> 4;
+  return v + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
 }
 
 // The gate kernels clear y (the down kernel accumulates into it) and record the

@@ -15,12 +15,31 @@ constexpr int kBlock = 256;       // threads per workgroup for every kernel
 constexpr int kTokChunk = 64;     // tokens per pass; a larger batch runs as several passes
 constexpr int kListWindow = 1024; // active entries staged in LDS at a time by the down kernel
 
+// Balanced split of n items into `parts` ranges; range w is [start(w), start(w + 1)).
+// The first n % parts ranges hold n / parts + 1 items, the others n / parts.  32-bit
+// arithmetic only (0 <= n < 2^31, parts >= 1): the one division happens when the split
+// is built, so a kernel pays it once and every range bound is a multiply and a min.
+struct Split {
+  uint32_t q, rem;
+  __host__ __device__ Split(int n, int parts)
+      : q((uint32_t)n / (uint32_t)parts), rem((uint32_t)n - (uint32_t)n / (uint32_t)parts * (uint32_t)parts) {}
+  __host__ __device__ int start(int w) const {
+    const uint32_t u = (uint32_t)w;
+    return (int)(u * q + (u < rem ? u : rem));
+  }
+  // the range that holds item i, 0 <= i < n
+  __host__ __device__ int of(int i) const {
+    const uint32_t u = (uint32_t)i, big = rem * (q + 1);
+    return (int)(u < big ? u / (q + 1) : rem + (u - big) / q);
+  }
+};
+
 // Workspace carve-up for one pass of up to `tc` tokens.  Every region starts on a
 // 256-byte boundary.  The neurons are split into nseg row-balanced segments (chosen
-// per call by the gate launcher and recorded in meta[0]); segment w covers rows
-// [w d_ff / nseg, (w+1) d_ff / nseg), and its active neurons occupy the slots from
-// its first row on: slot w d_ff / nseg + e holds its e-th active neuron (ascending),
-// for e < seg_count[w].  slots = d_ff.
+// per call by the gate launcher and recorded in meta[0]): segment w covers rows
+// [Split(d_ff, nseg).start(w), ....start(w + 1)), and its active neurons occupy the
+// slots from its first row on: slot start(w) + e holds its e-th active neuron
+// (ascending), for e < seg_count[w].  slots = d_ff.
 struct Workspace {
   int nseg;
   int slots;

@@ -192,8 +192,9 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
   __shared__ int s_cnt;
 
   const int seg = blockIdx.x;
-  const int row0 = seg_row(seg, d_ff, nseg);
-  const int nrows = seg_row(seg + 1, d_ff, nseg) - row0;
+  const Split segs(d_ff, nseg);
+  const int row0 = segs.start(seg);
+  const int nrows = segs.start(seg + 1) - row0;
   clear_output(y, d, meta, nseg);
   auto gate_sink = [&](int k, float s) { s_h[k] = s; };
   auto gate_row = [&](int k) { return row0 + k; };
@@ -246,8 +247,9 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
 
   const int S = (C + kWave - 1) / kWave;
   const int chunk = blockIdx.x / S, slice = blockIdx.x % S;
-  const int seg_lo = (int)(((int64_t)chunk * nseg) / R), seg_hi = (int)(((int64_t)(chunk + 1) * nseg) / R);
-  const int row_lo = seg_row(seg_lo, d_ff, nseg), row_hi = seg_row(seg_hi, d_ff, nseg);
+  const Split chunks(nseg, R), segs(d_ff, nseg);
+  const int seg_lo = chunks.start(chunk), seg_hi = chunks.start(chunk + 1);
+  const int row_lo = segs.start(seg_lo), row_hi = segs.start(seg_hi);
   const int raw_n = row_hi - row_lo;
   const int lane = lane_id(), wave = threadIdx.x / kWave;
 
@@ -267,11 +269,7 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
     if (wave == 0) {
       const int nsc = seg_hi - seg_lo;  // <= 64, guaranteed by the host
       const int c = lane < nsc ? seg_count[seg_lo + lane] : 0;
-      int v = c;
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int u = __shfl_up(v, o);
-        if (lane >= o) v += u;
-      }
+      const int v = wave_inclusive_scan(c);
       s_cnt[lane] = c;
       s_off[lane] = v - c;
       if (lane == kWave - 1) s_off[kWave] = v;
@@ -280,8 +278,8 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
     n = s_off[kWave];
     for (int p = threadIdx.x; p < raw_n; p += kBlock) {
       const int row = row_lo + p;
-      const int w = seg_of_row(row, d_ff, nseg) - seg_lo;
-      const int e = row - seg_row(seg_lo + w, d_ff, nseg);
+      const int w = segs.of(row) - seg_lo;
+      const int e = row - segs.start(seg_lo + w);
       if (e < s_cnt[w]) {
         l_idx[s_off[w] + e] = raw_idx[p];
         l_z[s_off[w] + e] = raw_z[p];
@@ -363,7 +361,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   __shared__ int s_list[kSegMax];
   __shared__ int s_cnt;
   const int seg = blockIdx.x;
-  const int row0 = seg_row(seg, d_ff, nseg), nrows = seg_row(seg + 1, d_ff, nseg) - row0;
+  const Split segs(d_ff, nseg);
+  const int row0 = segs.start(seg), nrows = segs.start(seg + 1) - row0;
   const int lane = lane_id(), wave = threadIdx.x / kWave;
   constexpr int kWaves = kBlock / kWave;
   const int len = LOPA ? r : d;
@@ -445,10 +444,11 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
     for (int base = 0; base < n; base += kListWindow) {
       const int wn = min(kListWindow, n - base);
       if (!DENSE) {
+        const Split segs(d_ff, nseg);
         for (int s = threadIdx.x; s < nseg; s += kBlock) {
           const int k0 = s_pre[s], k1 = s_pre[s + 1];
           const int lo = max(k0, base), hi = min(k1, base + wn);
-          const int slot0 = seg_row(s, d_ff, nseg);
+          const int slot0 = segs.start(s);
           for (int k = lo; k < hi; ++k) s_slot[k - base] = slot0 + (k - k0);
         }
         __syncthreads();
