@@ -45,10 +45,7 @@
  * Semantics of special values: a NaN gate value is inactive (h > t is false).
  * Inf/NaN in the w_up / w_down_t rows of a neuron that is active for any token of
  * the batch propagate into every token's output (the row is read for the union).
- * For batches of 2..64 tokens with bf16 weights and d a multiple of 8 (the
- * matrix-core path) such a value in a w_down_t row also reaches the other columns of
- * its 16-column block: the rows are transposed by a product with a 0/1 matrix, and
- * 0 x Inf is NaN.  Rows of neurons inactive for every token are never read.
+ * Rows of neurons inactive for every token are never read.
  */
 #ifndef FFN_SPARSE_H
 #define FFN_SPARSE_H

@@ -29,12 +29,10 @@
 // the same order and the load counter waits stay exact.
 //
 // The down product needs, per lane, 8 entries of one column as the B operand, while a
-// row gather gives a lane 8 columns of one entry.  An MFMA against a 0/1 selector
-// matrix transposes each 16 x 16 block exactly (every output is one weight times 1),
-// and its output layout (lane = column, lane group = entries 4g..4g+3) is already the
-// B-operand layout of the product.  A consequence: a non-finite weight in an active
-// row spreads over the 16-column block it sits in (0 x Inf is NaN), where the
-// definition would confine it to its own column.
+// row gather gives a lane 8 columns of one entry.  The gathered rows go to LDS as they
+// are and come back through gfx950's transposing LDS read (ds_read_b64_tr_b16), which
+// exchanges 16-bit elements between the lanes of a 16-lane group: one pair of such
+// reads hands every lane its 8 entries of one column.
 #include "ffn_device.h"
 #include "ffn_internal.h"
 
@@ -447,15 +445,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) voi
 #undef FFN_GATE_UP_ARGS
 
 // ------------------------------------------------------------------ down projection
-// Workgroup b: column group b % S, row chunk b / S (segments [c nseg/R, (c+1) nseg/R)).
+// Workgroup b: column group b % S, row chunk b / S (a balanced share of the segments).
 // A wave owns DT 32-column tiles (DT = 4 for one token tile, else 2); a column group
 // is CW of them, and wave w takes column slot w % CW and every (4 / CW)-th used
-// fragment group of the chunk (32 union entries of one segment), the loads of its next
-// group in flight while the current one is multiplied.  A group's 32 W_down rows are
-// read (64 / 4 DT) rows x 64 DT bytes per instruction, streamed past the caches, and
-// reshaped through a wave-private LDS tile like the gate kernel's weights.  The chunk's
-// counts and slot indices are staged in LDS once.  The waves' sums meet in LDS, then go
-// to y with one fp32 atomic per token and column (y was cleared by the gate kernel).
+// fragment group of the chunk (32 union entries of one segment).  A group's 32 W_down
+// rows are read (64 / 4 DT) rows x 64 DT bytes per instruction, streamed past the
+// caches, and written to a wave-private LDS tile; transposing LDS reads
+// (ds_read_b64_tr_b16) then hand every lane the 8 entries of one column that the
+// matrix-core B operand takes.  The chunk's slot indices and a table of its groups are
+// staged in LDS once; the loop reads a group's table entry two groups ahead and its slot
+// indices one group ahead, so the weight loads of the next group issue without waiting
+// on LDS.  The waves' sums meet in LDS, then go to y with one fp32 atomic per token and
+// column (y was cleared by the gate kernel).
 constexpr int kDnSlots = 4096;  // most slot indices of one row chunk
 
 template <int NT>
@@ -466,7 +467,9 @@ struct DnCfg {
   static constexpr int LPR = 4 * DT;          // lanes per row of a load instruction
   static constexpr int RPI = kWave / LPR;     // rows per load instruction
   static constexpr int NI = 32 / RPI;         // load instructions per group
-  static constexpr int PITCH = LPR + 1;       // chunks per LDS row (one pad chunk)
+  // chunks per LDS row: two pad chunks put the 8 rows that a half-wave's transposing
+  // reads touch on distinct banks
+  static constexpr int PITCH = LPR + 2;
 };
 
 template <int NT>
@@ -475,73 +478,85 @@ struct DnFrags {
   uint4 zh[NT], zl[NT];    // zval fragments (hi, lo) of the token tiles
 };
 
-struct DnChunk {
-  const int* grp;   // used groups: segment (relative) << 1 | group
-  const int* cnt;   // union size per segment
-  const int* srow;  // first slot per segment, relative to the chunk's first slot
-  const int* idx;   // slot -> neuron
-  int seg_lo;
+// A group's table entry: x = first slot (relative to the chunk's first row) | entries
+// << 16, y = the group's index in the zval fragment buffer.  The kDnPad table entries
+// past the last group are empty, so every load of such a group reads nothing.
+constexpr int kDnPad = 4 * kParts;
+
+template <int NT>
+struct DnRows {
+  int row[DnCfg<NT>::NI];  // neuron of the entry this lane loads, -1 for none
+  int2 info;
 };
 
 template <int NT>
-__device__ __forceinline__ void dn_load(DnFrags<NT>& f, int j, int ngrp, const DnChunk& ck, const Buf& db,
-                                        const Buf& zb, int C, int cg0, int T, int tc) {
+__device__ __forceinline__ DnRows<NT> dn_rows(int2 info, const int* s_idx, int C, int ch) {
   using K = DnCfg<NT>;
-  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
-  const bool jv = j < ngrp;  // past the last group: out-of-range loads, nothing read
-  const int sg = uniform(jv ? ck.grp[j] : 0), sl = sg >> 1, gi = sg & 1;
-  const int cnt = uniform(ck.cnt[sl]), srow = uniform(ck.srow[sl]);
-  const int ch = cg0 + lane % K::LPR;
+  const int lane = lane_id(), base = info.x & 0xFFFF, cnt = info.x >> 16;
+  DnRows<NT> a;
+  a.info = info;
 #pragma unroll
   for (int i = 0; i < K::NI; ++i) {
-    const int e = 32 * gi + K::RPI * i + lane / K::LPR;
-    const bool ok = jv && e < cnt && ch < C;
-    const int idx = ok ? ck.idx[srow + e] : 0;
-    f.t[i] = ldb_nt(db, ok ? 16u * (uint32_t)(idx * C + ch) : kOOB);
+    const int e = K::RPI * i + lane / K::LPR;
+    const bool ok = e < cnt && ch < C;
+    const int v = s_idx[ok ? base + e : 0];
+    a.row[i] = ok ? v : -1;
   }
-  const uint32_t zg = (uint32_t)((ck.seg_lo + sl) * 2 + gi) * (uint32_t)tc;
+  return a;
+}
+
+template <int NT>
+__device__ __forceinline__ void dn_issue(DnFrags<NT>& f, const DnRows<NT>& a, const Buf& db, const Buf& zb, int C,
+                                         int ch, int T, int tc) {
+  using K = DnCfg<NT>;
+  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < K::NI; ++i) f.t[i] = ldb_nt(db, a.row[i] >= 0 ? 16u * (uint32_t)(a.row[i] * C + ch) : kOOB);
+  const bool has = a.info.x >> 16 > 0;
+  const uint32_t zg = (uint32_t)a.info.y * (uint32_t)tc;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int tok = 16 * nt + m;
-    const uint32_t off = (jv && tok < T) ? 32u * ((zg + tok) * 4 + g) : kOOB;
+    const uint32_t off = (has && tok < T) ? 32u * ((zg + tok) * 4 + g) : kOOB;
     f.zh[nt] = ldb(zb, off);
     f.zl[nt] = ldb(zb, off + 16);
   }
 }
 
-// tile: this wave's LDS tile (32 PITCH uint4)
+typedef short short4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr16(const char* p) {
+  const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// tile: this wave's LDS tile (32 PITCH uint4).  Within each 16-lane group q of the
+// transposing read, lane 4a + b addresses 8 bytes (4 columns) of one tile row and lane
+// 4b + c receives element c of the chunks of lanes b, 4 + b, 8 + b, 12 + b.  With lane
+// 4a + b pointing at entry 4q + a (then 16 + 4q + a), columns 4b .. 4b + 3 of a 16-column
+// block, lane n of the group ends with entries 4q .. 4q + 3 (then 16 + 4q ..) of column
+// n: the B operand in the entry order of the zval fragments.
 template <int NT>
-__device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, const bf16x8_t (&sel)[2], uint4* tile,
-                                       f32x4_t (&acc)[DnCfg<NT>::DT][2][NT]) {
+__device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, uint4* tile, f32x4_t (&acc)[DnCfg<NT>::DT][2][NT]) {
   using K = DnCfg<NT>;
-  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+  constexpr int ROWB = 16 * K::PITCH;  // bytes per tile row
+  const int lane = lane_id();
 #pragma unroll
   for (int i = 0; i < K::NI; ++i) tile[(K::RPI * i + lane / K::LPR) * K::PITCH + lane % K::LPR] = f.t[i];
   __builtin_amdgcn_wave_barrier();  // LDS operations of a wave complete in order
+  const char* src = reinterpret_cast<const char*>(tile) + (4 * (lane >> 4) + ((lane >> 2) & 3)) * ROWB + 8 * (lane & 3);
 #pragma unroll
-  for (int ct = 0; ct < K::DT; ++ct) {
-    // entries m and 16 + m, 8 columns (chunk g of the tile) each
-    const bf16x8_t t0 = bf8(tile[m * K::PITCH + 4 * ct + g]), t1 = bf8(tile[(16 + m) * K::PITCH + 4 * ct + g]);
-    bf16x8_t bfrag[2];
+  for (int ct = 0; ct < K::DT; ++ct)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
-      const f32x4_t c0 = mfma16(t0, sel[h], zero);  // entries 4g..4g+3 of column 16h + m
-      const f32x4_t c1 = mfma16(t1, sel[h], zero);  // entries 16+4g..16+4g+3
+      const uint2 lo = lds_read_tr16(src + 64 * ct + 32 * h);
+      const uint2 hi = lds_read_tr16(src + 16 * ROWB + 64 * ct + 32 * h);
+      const bf16x8_t b = bf8(make_uint4(lo.x, lo.y, hi.x, hi.y));
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        bfrag[h][q] = (__bf16)c0[q];
-        bfrag[h][4 + q] = (__bf16)c1[q];
+      for (int nt = 0; nt < NT; ++nt) {
+        acc[ct][h][nt] = mfma16(bf8(f.zh[nt]), b, acc[ct][h][nt]);
+        acc[ct][h][nt] = mfma16(bf8(f.zl[nt]), b, acc[ct][h][nt]);
       }
     }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        acc[ct][h][nt] = mfma16(bf8(f.zh[nt]), bfrag[h], acc[ct][h][nt]);
-        acc[ct][h][nt] = mfma16(bf8(f.zl[nt]), bfrag[h], acc[ct][h][nt]);
-      }
-  }
   __builtin_amdgcn_wave_barrier();
 }
 
@@ -555,10 +570,8 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   constexpr int CW = K::CW, GS = kParts / CW, WCOLS = K::WCOLS;
   const Buf db = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
   const Buf zb = make_buf(zf, 256u * (uint32_t)nseg * (uint32_t)tc);
-  __shared__ int s_cnt[kBlock];
-  __shared__ int s_srow[kBlock];
   __shared__ int s_wgrp[kBlock / kWave];
-  __shared__ int s_grp[2 * kBlock];
+  __shared__ int2 s_ginfo[2 * kBlock + kDnPad];
   __shared__ int s_idx[kDnSlots];
   __shared__ float s_y[16 * NT * WCOLS];
   __shared__ uint4 s_stage[kParts][32 * K::PITCH];
@@ -575,10 +588,9 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   const int slot_w = wave % CW, phase = wave / CW;
 
   // segment tid of the chunk has (c > 0) + (c > 32) fragment groups; their places in
-  // the group list come from two ballots and the per-wave totals
+  // the group table come from two ballots and the per-wave totals
   const int c = tid < nsc ? seg_count[seg_lo + tid] : 0;
-  s_cnt[tid] = c;
-  s_srow[tid] = tid < nsc ? segs.start(seg_lo + tid) - row_lo : 0;
+  const int srow = tid < nsc ? segs.start(seg_lo + tid) - row_lo : 0;
   for (int o = tid; o < nslot; o += kBlock) s_idx[o] = seg_idx[row_lo + o];
   for (int o = tid; o < T * WCOLS; o += kBlock) s_y[o] = 0.f;
   const uint64_t has1 = __ballot(c > 0), has2 = __ballot(c > 32);
@@ -594,17 +606,12 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   ngrp = uniform(ngrp);
   if (tid < nsc) {
     const int b = gbase + rank_in_mask(has1) + rank_in_mask(has2);
-    if (c > 0) s_grp[b] = tid << 1;
-    if (c > 32) s_grp[b + 1] = (tid << 1) | 1;
+    const int zg = 2 * (seg_lo + tid);
+    if (c > 0) s_ginfo[b] = make_int2(srow | (min(c, 32) << 16), zg);
+    if (c > 32) s_ginfo[b + 1] = make_int2((srow + 32) | ((c - 32) << 16), zg + 1);
   }
+  if (tid < kDnPad) s_ginfo[ngrp + tid] = make_int2(0, 0);
   __syncthreads();
-
-  // 0/1 selectors: column 16 h + m of the 32-column tile
-  bf16x8_t sel[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) sel[h][j] = (__bf16)((8 * g + j == 16 * h + m) ? 1.f : 0.f);
 
   f32x4_t acc[K::DT][2][NT];
 #pragma unroll
@@ -614,21 +621,28 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[ct][h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const DnChunk ck{s_grp, s_cnt, s_srow, s_idx, seg_lo};
-  const int cg0 = (cgrp * WCOLS + slot_w * 32 * K::DT) / 8;  // first chunk of this wave's columns
+  // this lane's 16-byte chunk of the wave's columns
+  const int ch = (cgrp * WCOLS + slot_w * 32 * K::DT) / 8 + lane % K::LPR;
   if (phase < ngrp) {
-    // two register sets alternate; loads past the last group read nothing
+    // two register sets alternate, one group each per half-iteration; the table entry of
+    // group j + 3 GS and the slot indices of group j + 2 GS are read while group j is
+    // multiplied.  A pair always multiplies both halves (a group past the last one loads
+    // nothing and adds zeros), so no load sits on a conditional path.
     DnFrags<NT> f0, f1;
-    dn_load(f0, phase, ngrp, ck, db, zb, C, cg0, T, tc);
-    for (int j = phase;;) {
-      dn_load(f1, j + GS, ngrp, ck, db, zb, C, cg0, T, tc);
-      dn_mma(f0, sel, s_stage[wave], acc);
-      j += GS;
-      if (j >= ngrp) break;
-      dn_load(f0, j + GS, ngrp, ck, db, zb, C, cg0, T, tc);
-      dn_mma(f1, sel, s_stage[wave], acc);
-      j += GS;
-      if (j >= ngrp) break;
+    DnRows<NT> a = dn_rows<NT>(s_ginfo[phase], s_idx, C, ch);
+    dn_issue(f0, a, db, zb, C, ch, T, tc);
+    a = dn_rows<NT>(s_ginfo[phase + GS], s_idx, C, ch);
+    int2 info = s_ginfo[phase + 2 * GS];
+    for (int j = phase;; j += 2 * GS) {
+      dn_issue(f1, a, db, zb, C, ch, T, tc);
+      a = dn_rows<NT>(info, s_idx, C, ch);
+      info = s_ginfo[j + 3 * GS];
+      dn_mma(f0, s_stage[wave], acc);
+      dn_issue(f0, a, db, zb, C, ch, T, tc);
+      a = dn_rows<NT>(info, s_idx, C, ch);
+      info = s_ginfo[j + 4 * GS];
+      dn_mma(f1, s_stage[wave], acc);
+      if (j + 2 * GS >= ngrp) break;
     }
   }
   // lane holds tokens 16 nt + 4g + i of column 32 ct + 16 h + m of its slot
