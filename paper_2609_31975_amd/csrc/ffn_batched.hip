@@ -141,10 +141,11 @@ __device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& 
   }
 }
 
-// tile: this wave's LDS tile (Stage::WORDS uint4); ntile (uniform): row tiles in use
+// tile: this wave's LDS tile (Stage::WORDS uint4).  Every row tile is multiplied: one
+// past the rows in use was loaded as zeros and only adds zeros to an accumulator that
+// is never read.
 template <int RT, int NT, int KU, int NP>
-__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, int ntile, uint4* tile,
-                                          f32x4_t (&acc)[RT][NT]) {
+__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4* tile, f32x4_t (&acc)[RT][NT]) {
   using S = WStage<RT, KU>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
 #pragma unroll
@@ -176,35 +177,45 @@ __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, int nt
       bf16x8_t hi, lo;
       split8(v, hi, lo);
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        if (rt < ntile) {
-          const bf16x8_t a = bf8(tile[(16 * rt + m) * S::PITCH + 4 * u + g]);
-          acc[rt][nt] = mfma16(a, hi, acc[rt][nt]);
-          acc[rt][nt] = mfma16(a, lo, acc[rt][nt]);
-        }
+      for (int rt = 0; rt < RT; ++rt) {
+        const bf16x8_t a = bf8(tile[(16 * rt + m) * S::PITCH + 4 * u + g]);
+        acc[rt][nt] = mfma16(a, hi, acc[rt][nt]);
+        acc[rt][nt] = mfma16(a, lo, acc[rt][nt]);
+      }
     }
   __builtin_amdgcn_wave_barrier();
 }
 
+// Nothing is scheduled across it.  Placed after a group's loads: otherwise the
+// scheduler pulls work on the previous group (whose first use waits on its loads)
+// in among them, and that wait holds back the rest of the issue.
+__device__ __forceinline__ void issue_barrier() { __builtin_amdgcn_sched_barrier(0); }
+
 // acc[rt][nt] += weight tile rt . token tile nt over the k steps [ks0, ks1) (uniform).
 // Two register sets alternate: the loads of the next KU steps are issued before the
-// current ones are multiplied; loads past ks1 are out of range and read nothing.
+// current ones are multiplied; loads past ks1 are out of range and read nothing.  A
+// pair always multiplies both halves (a group past ks1 adds zeros) and the exit test
+// closes the pair, so no load sits on a conditional path: with an exit test between
+// the halves the compiler moved the loads next to their use and waited on them there.
 template <int RT, int NT, int KU, int NP>
-__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT * KU], int ntile,
-                                            uint4* tile, const Buf& tb, uint32_t part_bytes, int T, int ks0, int ks1,
+__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT * KU], uint4* tile,
+                                            const Buf& tb, uint32_t part_bytes, int T, int ks0, int ks1,
                                             f32x4_t (&acc)[RT][NT]) {
   if (ks0 >= ks1) return;
   Frags<RT, NT, KU, NP> f0, f1;
   load_frags(f0, wb, C, roff, tb, part_bytes, T, ks0, ks1);
-  for (int ks = ks0;;) {
+  if (ks0 + KU >= ks1) {  // a single group
+    mma_frags(f0, tile, acc);
+    return;
+  }
+  for (int ks = ks0;; ks += 2 * KU) {
     load_frags(f1, wb, C, roff, tb, part_bytes, T, ks + KU, ks1);
-    mma_frags(f0, ntile, tile, acc);
-    ks += KU;
-    if (ks >= ks1) break;
-    load_frags(f0, wb, C, roff, tb, part_bytes, T, ks + KU, ks1);
-    mma_frags(f1, ntile, tile, acc);
-    ks += KU;
-    if (ks >= ks1) break;
+    issue_barrier();
+    mma_frags(f0, tile, acc);
+    load_frags(f0, wb, C, roff, tb, part_bytes, T, ks + 2 * KU, ks1);
+    issue_barrier();
+    mma_frags(f1, tile, acc);
+    if (ks + 2 * KU >= ks1) break;
   }
 }
 
@@ -234,7 +245,7 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
   for (int nt = 0; nt < NT; ++nt) acc[0][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   int ks0, ks1;
   kpart(C, part * kZWaves + wave, kZParts * kZWaves, &ks0, &ks1);
-  stream_rows<1, NT, KU, 1>(ab, C, roff, 1, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+  stream_rows<1, NT, KU, 1>(ab, C, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[0][nt];
   __syncthreads();
@@ -303,14 +314,12 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       stage_rows<kTiles, KU>(roff, Cg, [&](int br) { return br < nrows ? row0 + br : -1; });
       int ks0, ks1;
       kpart(Cg, wave, kParts, &ks0, &ks1);
-      const int ntile = (nrows + 15) / 16;
       const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg);
       if constexpr (LOPA) {
         const uint32_t part = 32u * (uint32_t)tc * (uint32_t)Cg;
-        stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, ntile, s_stage[wave], make_buf(zp, 2 * part), part, T, ks0, ks1,
-                                       acc);
+        stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, s_stage[wave], make_buf(zp, 2 * part), part, T, ks0, ks1, acc);
       } else {
-        stream_rows<kTiles, NT, KU, 1>(gb, Cg, roff, ntile, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+        stream_rows<kTiles, NT, KU, 1>(gb, Cg, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
       }
     }
 #pragma unroll
@@ -379,7 +388,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       stage_rows<kTiles, KUU>(roff, Cu, [&](int e) { return e < cnt ? row0 + s_list[e] : -1; });
       int ks0, ks1;
       kpart(Cu, wave, kParts, &ks0, &ks1);
-      stream_rows<kTiles, NT, KUU, 1>(ub, Cu, roff, nut, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+      stream_rows<kTiles, NT, KUU, 1>(ub, Cu, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
     }
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt)
@@ -427,10 +436,12 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
   x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y
 
 // One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
-// gate rows and for wider token tiles).
+// gate rows and for wider token tiles; one for LoPA's gate rows with four token tiles,
+// whose fragments carry both partial copies of z).
 template <bool LOPA, bool DENSE, int NT>
 __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(FFN_GATE_UP_PARAMS) {
-  gate_up_body<LOPA, DENSE, NT, (NT == 1 && !LOPA) ? 4 : 2, NT == 1 ? 4 : 2>(FFN_GATE_UP_ARGS);
+  constexpr int KU = NT == 1 ? (LOPA ? 2 : 4) : (LOPA && NT == 4 ? 1 : 2);
+  gate_up_body<LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2>(FFN_GATE_UP_ARGS);
 }
 
 // Standard gating, one token tile: two k steps a group, so that two workgroups fit a CU
@@ -635,10 +646,12 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
     int2 info = s_ginfo[phase + 2 * GS];
     for (int j = phase;; j += 2 * GS) {
       dn_issue(f1, a, db, zb, C, ch, T, tc);
+      issue_barrier();
       a = dn_rows<NT>(info, s_idx, C, ch);
       info = s_ginfo[j + 3 * GS];
       dn_mma(f0, s_stage[wave], acc);
       dn_issue(f0, a, db, zb, C, ch, T, tc);
+      issue_barrier();
       a = dn_rows<NT>(info, s_idx, C, ch);
       info = s_ginfo[j + 4 * GS];
       dn_mma(f1, s_stage[wave], acc);
