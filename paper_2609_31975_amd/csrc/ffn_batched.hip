@@ -186,11 +186,6 @@ __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4*
   __builtin_amdgcn_wave_barrier();
 }
 
-// Nothing is scheduled across it.  Placed after a group's loads: otherwise the
-// scheduler pulls work on the previous group (whose first use waits on its loads)
-// in among them, and that wait holds back the rest of the issue.
-__device__ __forceinline__ void issue_barrier() { __builtin_amdgcn_sched_barrier(0); }
-
 // acc[rt][nt] += weight tile rt . token tile nt over the k steps [ks0, ks1) (uniform).
 // Two register sets alternate: the loads of the next KU steps are issued before the
 // current ones are multiplied; loads past ks1 are out of range and read nothing.  A

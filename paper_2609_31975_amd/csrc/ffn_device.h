@@ -97,6 +97,11 @@ __device__ __forceinline__ uint4 ldb_nt(const Buf& b, uint32_t off) {  // stream
 }
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Nothing is scheduled across it.  Placed after a group's loads in a double-buffered
+// loop: otherwise the scheduler pulls work on the previous group (whose first use waits
+// on its loads) in among them, and that wait holds back the rest of the issue.
+__device__ __forceinline__ void issue_barrier() { __builtin_amdgcn_sched_barrier(0); }
+
 __device__ __forceinline__ int rank_in_mask(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }

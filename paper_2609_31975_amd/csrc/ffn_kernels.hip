@@ -71,9 +71,11 @@ __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const float (&v
 // `bytes` bytes (< 2^31): each wave takes passes of 64/lpr rows (passes wave, wave + 4,
 // ...).  For rows of at most 8 chunks per lane and more than one pass per wave, two
 // register sets alternate, the loads of the next pass issued before the current pass is
-// reduced; the loads are raw buffer
-// loads (out-of-range offsets past the last pass), so every pass issues the same loads
-// and the load-counter waits are exact.  `sink(k, value)` runs on lane q == 0.
+// reduced; the loads are raw buffer loads (out-of-range offsets past the last pass), so
+// every pass issues the same loads and the load-counter waits are exact.  A pair of
+// passes always runs both halves (a pass past the last one loads nothing and sinks
+// nothing) and the exit test closes the pair, so no load sits on a conditional path.
+// `sink(k, value)` runs on lane q == 0.
 template <class W, int CPL>
 __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, bool ok, int row, uint4 (&b)[CPL]) {
   const uint32_t base = ok ? 16u * (uint32_t)row * (uint32_t)C : kOOB;
@@ -112,15 +114,14 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   }
   if constexpr (CPL <= 8) {
     uint4 b1[CPL];
-    for (int pass = wave;;) {
+    for (int pass = wave;; pass += 2 * kWaves) {
       load(b1, pass + kWaves);
+      issue_barrier();
       finish(b0, pass);
-      pass += kWaves;
-      if (pass >= npass) break;
-      load(b0, pass + kWaves);
-      finish(b1, pass);
-      pass += kWaves;
-      if (pass >= npass) break;
+      load(b0, pass + 2 * kWaves);
+      issue_barrier();
+      finish(b1, pass + kWaves);
+      if (pass + 2 * kWaves >= npass) break;
     }
   } else {
     for (int pass = wave;;) {
