@@ -576,11 +576,17 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   constexpr int CW = K::CW, GS = kParts / CW, WCOLS = K::WCOLS;
   const Buf db = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
   const Buf zb = make_buf(zf, 256u * (uint32_t)nseg * (uint32_t)tc);
+  // LDS: the waves' tiles and the chunk's slot indices during the loop; afterwards the
+  // same space holds every wave's sums, [wave][ct][h][nt][lane] as f32x4
+  constexpr int STAGE_U4 = kParts * 32 * K::PITCH, IDX_U4 = kDnSlots / 4;
+  constexpr int PART_U4 = kParts * K::DT * 2 * NT * kWave;
+  constexpr int BIG_U4 = STAGE_U4 + IDX_U4 > PART_U4 ? STAGE_U4 + IDX_U4 : PART_U4;
+  __shared__ uint4 s_big[BIG_U4];
   __shared__ int s_wgrp[kBlock / kWave];
   __shared__ int2 s_ginfo[2 * kBlock + kDnPad];
-  __shared__ int s_idx[kDnSlots];
-  __shared__ float s_y[16 * NT * WCOLS];
-  __shared__ uint4 s_stage[kParts][32 * K::PITCH];
+  uint4* const s_stage = s_big;
+  int* const s_idx = reinterpret_cast<int*>(s_big + STAGE_U4);
+  f32x4_t* const s_part = reinterpret_cast<f32x4_t*>(s_big);
 
   const int S = (C * 8 + WCOLS - 1) / WCOLS;
   const int chunk = blockIdx.x / S, cgrp = blockIdx.x % S;
@@ -590,15 +596,29 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   const int row_lo = segs.start(seg_lo);
   const int nslot = segs.start(seg_hi) - row_lo;  // <= kDnSlots, guaranteed by the host
   const int tid = threadIdx.x, lane = lane_id(), wave = uniform(tid / kWave);
-  const int m = lane & 15, g = lane >> 4;
   const int slot_w = wave % CW, phase = wave / CW;
 
   // segment tid of the chunk has (c > 0) + (c > 32) fragment groups; their places in
   // the group table come from two ballots and the per-wave totals
   const int c = tid < nsc ? seg_count[seg_lo + tid] : 0;
   const int srow = tid < nsc ? segs.start(seg_lo + tid) - row_lo : 0;
-  for (int o = tid; o < nslot; o += kBlock) s_idx[o] = seg_idx[row_lo + o];
-  for (int o = tid; o < T * WCOLS; o += kBlock) s_y[o] = 0.f;
+  {
+    // eight loads in flight per thread before their LDS stores
+    const Buf ib = make_buf(seg_idx + row_lo, 4u * (uint32_t)nslot);
+    for (int o0 = 0; o0 < nslot; o0 += 8 * kBlock) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int o = o0 + u * kBlock + tid;
+        v[u] = ldb32(ib, o < nslot ? 4u * (uint32_t)o : kOOB);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int o = o0 + u * kBlock + tid;
+        if (o < nslot) s_idx[o] = v[u];
+      }
+    }
+  }
   const uint64_t has1 = __ballot(c > 0), has2 = __ballot(c > 32);
   if (lane == 0) s_wgrp[wave] = __popcll(has1) + __popcll(has2);
   __syncthreads();
@@ -644,31 +664,39 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
       issue_barrier();
       a = dn_rows<NT>(info, s_idx, C, ch);
       info = s_ginfo[j + 3 * GS];
-      dn_mma(f0, s_stage[wave], acc);
+      dn_mma(f0, s_stage + wave * 32 * K::PITCH, acc);
       dn_issue(f0, a, db, zb, C, ch, T, tc);
       issue_barrier();
       a = dn_rows<NT>(info, s_idx, C, ch);
       info = s_ginfo[j + 4 * GS];
-      dn_mma(f1, s_stage[wave], acc);
+      dn_mma(f1, s_stage + wave * 32 * K::PITCH, acc);
       if (j + 2 * GS >= ngrp) break;
     }
   }
-  // lane holds tokens 16 nt + 4g + i of column 32 ct + 16 h + m of its slot
+  // lane m + 16 g of wave w holds tokens 16 nt + 4g .. + 3 of column 32 ct + 16 h + m
+  // of slot w % CW; the GS waves of a slot are added in a fixed order, then one fp32
+  // atomic per token and column goes to y
+  __syncthreads();  // every wave is done with its tile and the slot indices
 #pragma unroll
   for (int ct = 0; ct < K::DT; ++ct)
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int tok = 16 * nt + 4 * g + i;
-          if (tok < T) atomicAdd(&s_y[tok * WCOLS + slot_w * 32 * K::DT + 32 * ct + 16 * h + m], acc[ct][h][nt][i]);
-        }
+      for (int nt = 0; nt < NT; ++nt) s_part[(((wave * K::DT + ct) * 2 + h) * NT + nt) * kWave + lane] = acc[ct][h][nt];
   __syncthreads();
-  for (int o = tid; o < T * WCOLS; o += kBlock) {
-    const int tok = o / WCOLS, col = cgrp * WCOLS + (o - tok * WCOLS);
-    if (col < d) unsafeAtomicAdd(y + (size_t)tok * d + col, s_y[o]);
+  constexpr int NE = CW * K::DT * 2 * NT * kWave;
+  for (int o = tid; o < NE; o += kBlock) {
+    const int l = o % kWave, r = o / kWave;  // r = ((slot DT + ct) 2 + h) NT + nt
+    const int nt = r % NT, h = (r / NT) % 2, ct = (r / (2 * NT)) % K::DT, slot = r / (2 * NT * K::DT);
+    const int tok0 = 16 * nt + 4 * (l >> 4);
+    const int col = cgrp * WCOLS + slot * 32 * K::DT + 32 * ct + 16 * h + (l & 15);
+    if (tok0 >= T || col >= d) continue;
+    f32x4_t v = s_part[(((slot * K::DT + ct) * 2 + h) * NT + nt) * kWave + l];
+#pragma unroll
+    for (int p = 1; p < GS; ++p) v += s_part[((((slot + CW * p) * K::DT + ct) * 2 + h) * NT + nt) * kWave + l];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (tok0 + i < T) unsafeAtomicAdd(y + (size_t)(tok0 + i) * d + col, v[i]);
   }
 }
 

@@ -95,6 +95,9 @@ __device__ __forceinline__ uint4 ldb(const Buf& b, uint32_t off) {  // through t
 __device__ __forceinline__ uint4 ldb_nt(const Buf& b, uint32_t off) {  // streamed past them
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(b.r, off, 0, 2));
 }
+__device__ __forceinline__ int ldb32(const Buf& b, uint32_t off) {
+  return (int)__builtin_amdgcn_raw_buffer_load_b32(b.r, off, 0, 0);
+}
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Nothing is scheduled across it.  Placed after a group's loads in a double-buffered
