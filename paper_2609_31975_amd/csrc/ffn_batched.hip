@@ -278,7 +278,11 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
                                              int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                              int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                              uint4* __restrict__ zf, float* __restrict__ y) {
-  constexpr int STAGE = WStage<kTiles, (KU > KUU ? KU : KUU)>::WORDS;
+  // the W_up rows of a union of at most two row tiles go as two tiles with twice the k
+  // steps a group (one token tile only: the register budget of wider ones is spent)
+  constexpr bool NARROW = NT == 1;
+  constexpr int STAGE_A = WStage<kTiles, (KU > KUU ? KU : KUU)>::WORDS, STAGE_B = WStage<2, 2 * KUU>::WORDS;
+  constexpr int STAGE = NARROW && STAGE_B > STAGE_A ? STAGE_B : STAGE_A;
   __shared__ uint4 s_stage[kParts][STAGE];
   __shared__ f32x4_t s_red[kParts][kTiles][NT][kWave];
   __shared__ float s_act[kSegRowsB][16 * NT];
@@ -379,11 +383,19 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     if (nut > 0) {
-      int roff[kTiles * KUU];
-      stage_rows<kTiles, KUU>(roff, Cu, [&](int e) { return e < cnt ? row0 + s_list[e] : -1; });
       int ks0, ks1;
       kpart(Cu, wave, kParts, &ks0, &ks1);
-      stream_rows<kTiles, NT, KUU, 1>(ub, Cu, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+      auto up_row = [&](int e) { return e < cnt ? row0 + s_list[e] : -1; };
+      if (NARROW && nut <= 2) {
+        int roff[2 * 2 * KUU];
+        stage_rows<2, 2 * KUU>(roff, Cu, up_row);
+        stream_rows<2, NT, 2 * KUU, 1>(ub, Cu, roff, s_stage[wave], xb, 0u, T, ks0, ks1,
+                                        reinterpret_cast<f32x4_t(&)[2][NT]>(acc));
+      } else {
+        int roff[kTiles * KUU];
+        stage_rows<kTiles, KUU>(roff, Cu, up_row);
+        stream_rows<kTiles, NT, KUU, 1>(ub, Cu, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+      }
     }
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt)
