@@ -21,7 +21,6 @@ size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 }  // namespace
 
 size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out) {
-  (void)d;
   Workspace w{};
   w.nseg = 0;
   w.slots = d_ff;
@@ -42,6 +41,8 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
   const size_t bt = w.tc >= 2 ? (size_t)w.tc : 0;  // matrix-core path only
   w.z = reinterpret_cast<float*>(take(sizeof(float) * (bt ? 2 : 1) * (size_t)w.tc * (r > 0 ? r : 1)));
   w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * 4 * bt * 2 * (size_t)batched_segments(d_ff)));
+  const size_t xs_frags = bt >= (size_t)kPreSplitMin ? (size_t)((d + 31) / 32) * ((bt + 15) / 16) * kWave : 0;
+  w.xs = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * xs_frags));
   if (out) *out = w;
   return off;
 }

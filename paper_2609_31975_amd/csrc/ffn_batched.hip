@@ -102,19 +102,23 @@ __device__ __forceinline__ void stage_rows(int (&roff)[RT * KU], int C, RowOf ro
 }
 
 // Operands of one group: the weight chunks as loaded and, per k step and token tile, the
-// token fragment: the 8 fp32 of the chunk (two 16-byte halves) from each of NP partial
-// copies of the token matrix, summed and split into hi / lo when multiplied.  A token
-// matrix is [T][8 C] fp32; partial copy p starts part_bytes * p into its buffer.
+// token fragment.  Two forms of the token side:
+//  - fp32 rows: the 8 fp32 of the chunk (two 16-byte halves) from each of NP partial
+//    copies of the token matrix, summed and split into hi / lo when multiplied.  A token
+//    matrix is [T][8 C] fp32; partial copy p starts part_bytes * p into its buffer; tn = T.
+//  - PRE (pre-split, NP = 1): b[u][nt][0] = the hi and lo fragments of the lane, read from
+//    planes [k step][token tile][lane] of uint4 (k_split_tokens); the lo plane starts
+//    part_bytes after the hi plane; tn = the planes' token-tile count.
 template <int RT, int NT, int KU, int NP>
 struct Frags {
   uint4 a[RT * KU];
   uint4 b[KU][NT][NP][2];
 };
 
-template <int RT, int NT, int KU, int NP>
+template <int RT, int NT, int KU, int NP, bool PRE = false>
 __device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& wb, int C,
                                            const int (&roff)[RT * KU], const Buf& tb, uint32_t part_bytes,
-                                           int T, int ks, int ks1) {
+                                           int tn, int ks, int ks1) {
   using S = WStage<RT, KU>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
   {
@@ -124,6 +128,19 @@ __device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& 
     for (int i = 0; i < S::NI; ++i)
       f.a[i] = ldb_nt(wb, (cv && roff[i] >= 0) ? 16u * (uint32_t)(roff[i] + c) : kOOB);
   }
+  if constexpr (PRE) {
+    static_assert(NP == 1, "pre-split tokens have one copy");
+#pragma unroll
+    for (int u = 0; u < KU; ++u)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const uint32_t off = ks + u < ks1 ? 16u * ((uint32_t)((ks + u) * tn + nt) * kWave + lane) : kOOB;
+        f.b[u][nt][0][0] = ldb(tb, off);
+        f.b[u][nt][0][1] = ldb(tb, off + part_bytes);
+      }
+    return;
+  }
+  const int T = tn;
 #pragma unroll
   for (int u = 0; u < KU; ++u) {
     const int c = 4 * (ks + u) + g;
@@ -144,7 +161,33 @@ __device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& 
 // tile: this wave's LDS tile (Stage::WORDS uint4).  Every row tile is multiplied: one
 // past the rows in use was loaded as zeros and only adds zeros to an accumulator that
 // is never read.
-template <int RT, int NT, int KU, int NP>
+// The token fragment of one k step and token tile from fp32 rows: the NP copies of the
+// lane's 8 values summed, then split into hi / lo.
+template <int NP>
+__device__ __forceinline__ void sum_split(const uint4 (&b)[NP][2], bf16x8_t& hi, bf16x8_t& lo) {
+  float v[8];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint4 q = b[0][h];
+    v[4 * h] = __uint_as_float(q.x);
+    v[4 * h + 1] = __uint_as_float(q.y);
+    v[4 * h + 2] = __uint_as_float(q.z);
+    v[4 * h + 3] = __uint_as_float(q.w);
+  }
+#pragma unroll
+  for (int p = 1; p < NP; ++p)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint4 q = b[p][h];
+      v[4 * h] += __uint_as_float(q.x);
+      v[4 * h + 1] += __uint_as_float(q.y);
+      v[4 * h + 2] += __uint_as_float(q.z);
+      v[4 * h + 3] += __uint_as_float(q.w);
+    }
+  split8(v, hi, lo);
+}
+
+template <int RT, int NT, int KU, int NP, bool PRE = false>
 __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4* tile, f32x4_t (&acc)[RT][NT]) {
   using S = WStage<RT, KU>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
@@ -155,27 +198,13 @@ __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4*
   for (int u = 0; u < KU; ++u)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      float v[8];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint4 q = f.b[u][nt][0][h];
-        v[4 * h] = __uint_as_float(q.x);
-        v[4 * h + 1] = __uint_as_float(q.y);
-        v[4 * h + 2] = __uint_as_float(q.z);
-        v[4 * h + 3] = __uint_as_float(q.w);
-      }
-#pragma unroll
-      for (int p = 1; p < NP; ++p)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const uint4 q = f.b[u][nt][p][h];
-          v[4 * h] += __uint_as_float(q.x);
-          v[4 * h + 1] += __uint_as_float(q.y);
-          v[4 * h + 2] += __uint_as_float(q.z);
-          v[4 * h + 3] += __uint_as_float(q.w);
-        }
       bf16x8_t hi, lo;
-      split8(v, hi, lo);
+      if constexpr (PRE) {
+        hi = bf8(f.b[u][nt][0][0]);
+        lo = bf8(f.b[u][nt][0][1]);
+      } else {
+        sum_split<NP>(f.b[u][nt], hi, lo);
+      }
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         const bf16x8_t a = bf8(tile[(16 * rt + m) * S::PITCH + 4 * u + g]);
@@ -192,26 +221,67 @@ __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4*
 // pair always multiplies both halves (a group past ks1 adds zeros) and the exit test
 // closes the pair, so no load sits on a conditional path: with an exit test between
 // the halves the compiler moved the loads next to their use and waited on them there.
-template <int RT, int NT, int KU, int NP>
+template <int RT, int NT, int KU, int NP, bool PRE = false>
 __device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT * KU], uint4* tile,
-                                            const Buf& tb, uint32_t part_bytes, int T, int ks0, int ks1,
+                                            const Buf& tb, uint32_t part_bytes, int tn, int ks0, int ks1,
                                             f32x4_t (&acc)[RT][NT]) {
   if (ks0 >= ks1) return;
   Frags<RT, NT, KU, NP> f0, f1;
-  load_frags(f0, wb, C, roff, tb, part_bytes, T, ks0, ks1);
+  load_frags<RT, NT, KU, NP, PRE>(f0, wb, C, roff, tb, part_bytes, tn, ks0, ks1);
   if (ks0 + KU >= ks1) {  // a single group
-    mma_frags(f0, tile, acc);
+    mma_frags<RT, NT, KU, NP, PRE>(f0, tile, acc);
     return;
   }
   for (int ks = ks0;; ks += 2 * KU) {
-    load_frags(f1, wb, C, roff, tb, part_bytes, T, ks + KU, ks1);
+    load_frags<RT, NT, KU, NP, PRE>(f1, wb, C, roff, tb, part_bytes, tn, ks + KU, ks1);
     issue_barrier();
-    mma_frags(f0, tile, acc);
-    load_frags(f0, wb, C, roff, tb, part_bytes, T, ks + 2 * KU, ks1);
+    mma_frags<RT, NT, KU, NP, PRE>(f0, tile, acc);
+    load_frags<RT, NT, KU, NP, PRE>(f0, wb, C, roff, tb, part_bytes, tn, ks + 2 * KU, ks1);
     issue_barrier();
-    mma_frags(f1, tile, acc);
+    mma_frags<RT, NT, KU, NP, PRE>(f1, tile, acc);
     if (ks + 2 * KU >= ks1) break;
   }
+}
+
+// The token side of a product with rows of C chunks: fp32 rows of x, or (pre) the
+// planes written by k_split_tokens for ntt token tiles.
+struct TokSrc {
+  Buf b;
+  uint32_t part;
+  int tn;
+};
+__device__ __forceinline__ TokSrc token_source(bool pre, const float* x, const uint4* xs, int C, int T, int ntt) {
+  if (pre) {
+    const uint32_t plane = 16u * (uint32_t)((C + 3) / 4) * (uint32_t)ntt * (uint32_t)kWave;
+    return TokSrc{make_buf(xs, 2 * plane), plane, ntt};
+  }
+  return TokSrc{make_buf(x, 32u * (uint32_t)T * (uint32_t)C), 0u, T};
+}
+
+// ------------------------------------------------------------------ token pre-split
+// For batches of more than one token tile every gate workgroup multiplies all tokens
+// against its rows.  Read as fp32 rows, a token load instruction touches 16 rows (one per
+// token of the tile) and half of each cache line it uses, and every workgroup splits
+// every value again.  This kernel writes the split once, in fragment order: entry
+// ((ks ntt + nt) 64 + lane) of the hi plane holds the bf16 hi parts of tokens
+// 16 nt + (lane & 15), elements 32 ks + 8 (lane >> 4) .. + 7, the lo plane (nks ntt 64
+// entries later) their lo parts; zero past the batch and past d.
+__global__ __launch_bounds__(kBlock) void k_split_tokens(const float* __restrict__ x, int C, int T, int nks, int ntt,
+                                                         uint4* __restrict__ xs) {
+  const int n = nks * ntt * kWave, i = blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n) return;
+  const int lane = i % kWave, fr = i / kWave, nt = fr % ntt, ks = fr / ntt;
+  const int tok = 16 * nt + (lane & 15), c = 4 * ks + (lane >> 4);
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (tok < T && c < C) {
+    const float4* p = reinterpret_cast<const float4*>(x + 8 * ((size_t)tok * C + c));
+    const float4 a = p[0], b = p[1];
+    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+  }
+  bf16x8_t hi, lo;
+  split8(v, hi, lo);
+  xs[i] = __builtin_bit_cast(uint4, hi);
+  xs[n + i] = __builtin_bit_cast(uint4, lo);
 }
 
 // ------------------------------------------------------------------ LoPA z = A x
@@ -224,8 +294,10 @@ constexpr int kZParts = 2;
 
 template <int NT>
 __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __restrict__ x,
+                                                                 const uint4* __restrict__ xs, int ntt,
                                                                  const uint4* __restrict__ A, int C, int T, int r,
                                                                  int tc, float* __restrict__ zp) {
+  constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   __shared__ f32x4_t s_part[kZWaves][NT][kWave];
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int tile = blockIdx.x / kZParts, part = blockIdx.x % kZParts;
@@ -234,13 +306,13 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
   int roff[KU];
   stage_rows<1, KU>(roff, C, [&](int br) { return tile * 16 + br < r ? tile * 16 + br : -1; });
   const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)C);
-  const Buf xb = make_buf(x, 32u * (uint32_t)T * (uint32_t)C);
+  const TokSrc tok = token_source(PRE, x, xs, C, T, ntt);
   f32x4_t acc[1][NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[0][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   int ks0, ks1;
   kpart(C, part * kZWaves + wave, kZParts * kZWaves, &ks0, &ks1);
-  stream_rows<1, NT, KU, 1>(ab, C, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+  stream_rows<1, NT, KU, 1, PRE>(ab, C, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[0][nt];
   __syncthreads();
@@ -277,7 +349,9 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
                                              int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,
                                              int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                              int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
-                                             uint4* __restrict__ zf, float* __restrict__ y) {
+                                             uint4* __restrict__ zf, float* __restrict__ y,
+                                             const uint4* __restrict__ xs, int ntt) {
+  constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   // the W_up rows of a union of at most two row tiles go as two tiles with twice the k
   // steps a group (one token tile only: the register budget of wider ones is spent)
   constexpr bool NARROW = NT == 1;
@@ -293,7 +367,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int m = lane & 15, g = lane >> 4;
   clear_output(y, T * d, meta, nseg);
-  const Buf xb = make_buf(x, 32u * (uint32_t)T * (uint32_t)Cu);
+  const TokSrc tok = token_source(PRE, x, xs, Cu, T, ntt);
   const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu);
 
   // segments blockIdx.x, blockIdx.x + gridDim.x, ... (the host makes the counts equal)
@@ -318,7 +392,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
         const uint32_t part = 32u * (uint32_t)tc * (uint32_t)Cg;
         stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, s_stage[wave], make_buf(zp, 2 * part), part, T, ks0, ks1, acc);
       } else {
-        stream_rows<kTiles, NT, KU, 1>(gb, Cg, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+        stream_rows<kTiles, NT, KU, 1, PRE>(gb, Cg, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
       }
     }
 #pragma unroll
@@ -386,15 +460,22 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       int ks0, ks1;
       kpart(Cu, wave, kParts, &ks0, &ks1);
       auto up_row = [&](int e) { return e < cnt ? row0 + s_list[e] : -1; };
-      if (NARROW && nut <= 2) {
-        int roff[2 * 2 * KUU];
-        stage_rows<2, 2 * KUU>(roff, Cu, up_row);
-        stream_rows<2, NT, 2 * KUU, 1>(ub, Cu, roff, s_stage[wave], xb, 0u, T, ks0, ks1,
-                                        reinterpret_cast<f32x4_t(&)[2][NT]>(acc));
-      } else {
+      auto full = [&] {
         int roff[kTiles * KUU];
         stage_rows<kTiles, KUU>(roff, Cu, up_row);
-        stream_rows<kTiles, NT, KUU, 1>(ub, Cu, roff, s_stage[wave], xb, 0u, T, ks0, ks1, acc);
+        stream_rows<kTiles, NT, KUU, 1, PRE>(ub, Cu, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
+      };
+      if constexpr (NARROW) {
+        if (nut <= 2) {
+          int roff[2 * 2 * KUU];
+          stage_rows<2, 2 * KUU>(roff, Cu, up_row);
+          stream_rows<2, NT, 2 * KUU, 1>(ub, Cu, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1,
+                                          reinterpret_cast<f32x4_t(&)[2][NT]>(acc));
+        } else {
+          full();
+        }
+      } else {
+        full();
       }
     }
 #pragma unroll
@@ -438,9 +519,10 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
   const float *__restrict__ x, const float *__restrict__ zp, const uint4 *__restrict__ gate_w, int Cg,             \
       const uint4 *__restrict__ w_up, int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,       \
       int32_t *__restrict__ meta, int32_t *__restrict__ seg_count, int32_t *__restrict__ seg_idx,                  \
-      float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y
+      float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y, const uint4 *__restrict__ xs,  \
+      int ntt
 #define FFN_GATE_UP_ARGS \
-  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y
+  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt
 
 // One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
 // gate rows and for wider token tiles; one for LoPA's gate rows with four token tiles,
@@ -713,11 +795,19 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
 }
 
 // ------------------------------------------------------------------ host side
+int token_tiles(const Workspace& ws) { return (ws.tc + 15) / 16; }
+
+hipError_t split_tokens(const Shape& sh, const float* x, const Workspace& ws, hipStream_t s) {
+  const int C = sh.d / 8, nks = (C + 3) / 4, ntt = token_tiles(ws);
+  const int n = nks * ntt * kWave;
+  k_split_tokens<<<(n + kBlock - 1) / kBlock, kBlock, 0, s>>>(x, C, sh.T, nks, ntt, ws.xs);
+  return hipGetLastError();
+}
 template <int NT>
 hipError_t z_mfma(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
   const int C = sh.d / 8, grid = ((sh.r + 15) / 16) * kZParts;
-  k_lopa_z_mfma<NT><<<grid, kZWaves * kWave, 0, s>>>(x, static_cast<const uint4*>(lopa_a), C, sh.T, sh.r, ws.tc,
-                                                      ws.z);
+  k_lopa_z_mfma<NT><<<grid, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a),
+                                                      C, sh.T, sh.r, ws.tc, ws.z);
   return hipGetLastError();
 }
 
@@ -744,7 +834,7 @@ hipError_t gate_mfma(const Shape& sh, const float* x, const void* gate_w, const 
   }();
   return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                             static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
-                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y);
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws));
 }
 
 template <bool LOPA, bool DENSE>
@@ -802,6 +892,8 @@ hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, c
                           float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
   hipError_t e = hipSuccess;
+  // more than one token tile: the kernels read the tokens pre-split
+  if (sh.T > 16 && (e = split_tokens(sh, x, ws, s)) != hipSuccess) return e;
   if (lopa) {
     e = sh.T <= 16 ? z_mfma<1>(sh, x, lopa_a, ws, s)
                    : sh.T <= 32 ? z_mfma<2>(sh, x, lopa_a, ws, s) : z_mfma<4>(sh, x, lopa_a, ws, s);

@@ -14,6 +14,7 @@ constexpr int kSegGeneric = 32;   // rows per segment of the element-wise kernel
 constexpr int kBlock = 256;       // threads per workgroup for every kernel
 constexpr int kTokChunk = 64;     // tokens per pass; a larger batch runs as several passes
 constexpr int kListWindow = 1024; // active entries staged in LDS at a time by the down kernel
+constexpr int kPreSplitMin = 17;  // batches of more than one 16-token tile get their tokens pre-split
 
 // Balanced split of n items into `parts` ranges; range w is [start(w), start(w + 1)).
 // The first n % parts ranges hold n / parts + 1 items, the others n / parts.  32-bit
@@ -54,6 +55,8 @@ struct Workspace {
                        //                  two partial copies [2][tc][r]
   uint4* zf;           // [2 batched_segments(d_ff)][tc][4][2]  zval fragments of the down product
                        //                  (matrix-core path, tc >= 2; empty for tc = 1)
+  uint4* xs;           // [2][ceil(d / 32)][ceil(tc / 16)][64]  tokens split into bf16 hi / lo
+                       //                  matrix-core fragments (tc >= kPreSplitMin, else empty)
 };
 
 size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out);
