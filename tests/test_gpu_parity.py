@@ -42,6 +42,8 @@ SMALL = [
     ("lopa_bf16_T20", 20, 264, 1000, 40, BF16, 1.3),        # two token tiles
     ("std_bf16_T40", 40, 136, 300, 0, BF16, 1.5),           # four token tiles, short rows
     ("std_bf16_T64", 64, 264, 1000, 0, BF16, 1.6),
+    ("std_bf16_T17", 17, 136, 300, 0, BF16, 1.2),           # pre-split tokens, second tile nearly empty
+    ("lopa_bf16_T70", 70, 264, 1000, 40, BF16, 1.3),        # a pre-split 64-token pass, then 6 tokens
     ("std_bf16_d4096", 1, 4096, 2056, 0, BF16, 1.2816),    # full-width rows, short d_ff
     ("std_bf16_d4096_odd", 1, 4096, 2052, 0, BF16, 1.2816),
     ("std_bf16_T4_odd_d", 4, 100, 77, 0, BF16, 0.5),       # batch with d not a multiple of 8: element-wise
