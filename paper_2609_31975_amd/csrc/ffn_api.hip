@@ -40,7 +40,7 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
   w.seg_zval = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
   const size_t bt = w.tc >= 2 ? (size_t)w.tc : 0;  // matrix-core path only
   w.z = reinterpret_cast<float*>(take(sizeof(float) * (bt ? 2 : 1) * (size_t)w.tc * (r > 0 ? r : 1)));
-  w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * 4 * bt * 2 * (size_t)batched_segments(d_ff)));
+  w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * ((bt + 15) / 16) * 2 * kWave * (size_t)batched_segments(d_ff)));
   const size_t xs_frags = bt >= (size_t)kPreSplitMin ? (size_t)((d + 31) / 32) * ((bt + 15) / 16) * kWave : 0;
   w.xs = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * xs_frags));
   if (out) *out = w;

@@ -337,10 +337,11 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 // wave w owning tile w.  A neuron joins the union if any token activates it (h > t;
 // NaN compares false); one ballot orders the union ascending.  The W_up dots of the
 // union rows use the same split, and zval = act * v goes to the fragment buffer of the
-// down kernel:
-// group (segment, entries 32 gi .. 32 gi + 31), token, lane group g, 16-byte hi and lo
-// vectors holding entries 4g .. 4g + 3 then 16 + 4g .. 16 + 4g + 3 of the group; a used
-// group is written whole (zero past the union), an unused one is never read.
+// down kernel: per fragment group (segment, entries 32 gi .. 32 gi + 31) and token tile
+// a plane of 64 hi entries, then one of 64 lo entries; entry m + 16 g holds, for token
+// 16 nt + m, the bf16 parts of entries 4g .. 4g + 3 then 16 + 4g .. 16 + 4g + 3 of the
+// group.  A used group is written whole (zero past the union), an unused one is never
+// read.
 // LOPA: the gate rows are B [d_ff][r] against z = zp[0] + zp[1]; otherwise W_gate x.
 // KU / KUU: k steps per load group of the gate rows / the W_up rows.
 template <bool LOPA, bool DENSE, int NT, int KU, int KUU>
@@ -506,9 +507,10 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
             hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
             lw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, lb) << (16 * (i & 1));
           }
-          uint2* frag = reinterpret_cast<uint2*>(zf + 2 * ((((size_t)seg * 2 + gi) * tc + tok) * 4 + g));
-          frag[half] = make_uint2(hw[0], hw[1]);
-          frag[2 + half] = make_uint2(lw[0], lw[1]);
+          // hi plane entry of lane m + 16 g, then the lo plane 64 entries on
+          uint4* frag = zf + ((((size_t)seg * 2 + gi) * ntt + nt) * 2) * kWave + m + 16 * g;
+          reinterpret_cast<uint2*>(frag)[half] = make_uint2(hw[0], hw[1]);
+          reinterpret_cast<uint2*>(frag + kWave)[half] = make_uint2(lw[0], lw[1]);
         }
       }
     }
@@ -607,19 +609,19 @@ __device__ __forceinline__ DnRows<NT> dn_rows(int2 info, const int* s_idx, int C
 
 template <int NT>
 __device__ __forceinline__ void dn_issue(DnFrags<NT>& f, const DnRows<NT>& a, const Buf& db, const Buf& zb, int C,
-                                         int ch, int T, int tc) {
+                                         int ch, int T, int ntt) {
   using K = DnCfg<NT>;
-  const int lane = lane_id(), m = lane & 15, g = lane >> 4;
+  const int lane = lane_id(), m = lane & 15;
 #pragma unroll
   for (int i = 0; i < K::NI; ++i) f.t[i] = ldb_nt(db, a.row[i] >= 0 ? 16u * (uint32_t)(a.row[i] * C + ch) : kOOB);
   const bool has = a.info.x >> 16 > 0;
-  const uint32_t zg = (uint32_t)a.info.y * (uint32_t)tc;
+  const uint32_t zg = (uint32_t)a.info.y * (uint32_t)ntt;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int tok = 16 * nt + m;
-    const uint32_t off = (has && tok < T) ? 32u * ((zg + tok) * 4 + g) : kOOB;
+    const uint32_t off = (has && tok < T) ? 16u * (((zg + nt) * 2) * kWave + lane) : kOOB;
     f.zh[nt] = ldb(zb, off);
-    f.zl[nt] = ldb(zb, off + 16);
+    f.zl[nt] = ldb(zb, off + 16 * kWave);
   }
 }
 
@@ -669,7 +671,8 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   using K = DnCfg<NT>;
   constexpr int CW = K::CW, GS = kParts / CW, WCOLS = K::WCOLS;
   const Buf db = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
-  const Buf zb = make_buf(zf, 256u * (uint32_t)nseg * (uint32_t)tc);
+  const int ntt = (tc + 15) / 16;
+  const Buf zb = make_buf(zf, 4096u * (uint32_t)nseg * (uint32_t)ntt);
   // LDS: the waves' tiles and the chunk's slot indices during the loop; afterwards the
   // same space holds every wave's sums, [wave][ct][h][nt][lane] as f32x4
   constexpr int STAGE_U4 = kParts * 32 * K::PITCH, IDX_U4 = kDnSlots / 4;
@@ -750,16 +753,16 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
     // nothing and adds zeros), so no load sits on a conditional path.
     DnFrags<NT> f0, f1;
     DnRows<NT> a = dn_rows<NT>(s_ginfo[phase], s_idx, C, ch);
-    dn_issue(f0, a, db, zb, C, ch, T, tc);
+    dn_issue(f0, a, db, zb, C, ch, T, ntt);
     a = dn_rows<NT>(s_ginfo[phase + GS], s_idx, C, ch);
     int2 info = s_ginfo[phase + 2 * GS];
     for (int j = phase;; j += 2 * GS) {
-      dn_issue(f1, a, db, zb, C, ch, T, tc);
+      dn_issue(f1, a, db, zb, C, ch, T, ntt);
       issue_barrier();
       a = dn_rows<NT>(info, s_idx, C, ch);
       info = s_ginfo[j + 3 * GS];
       dn_mma(f0, s_stage + wave * 32 * K::PITCH, acc);
-      dn_issue(f0, a, db, zb, C, ch, T, tc);
+      dn_issue(f0, a, db, zb, C, ch, T, ntt);
       issue_barrier();
       a = dn_rows<NT>(info, s_idx, C, ch);
       info = s_ginfo[j + 4 * GS];

@@ -53,8 +53,9 @@ struct Workspace {
   float* seg_zval;     // [tc][slots]      act * <w_up[i], x_tau>
   float* z;            // [tc][r]          LoPA intermediate A x (LoPA only); for tc >= 2
                        //                  two partial copies [2][tc][r]
-  uint4* zf;           // [2 batched_segments(d_ff)][tc][4][2]  zval fragments of the down product
-                       //                  (matrix-core path, tc >= 2; empty for tc = 1)
+  uint4* zf;           // [2 batched_segments(d_ff)][ceil(tc / 16)][2][64]  zval fragments of the
+                       //                  down product, hi and lo planes of 64 lanes per fragment
+                       //                  group and token tile (matrix-core path, tc >= 2)
   uint4* xs;           // [2][ceil(d / 32)][ceil(tc / 16)][64]  tokens split into bf16 hi / lo
                        //                  matrix-core fragments (tc >= kPreSplitMin, else empty)
 };
