@@ -172,6 +172,50 @@ def test_repeatable(gu, r):
     assert gu.rel_err(y2, y1) < 1e-6
 
 
+GRAPH_SHAPES = [(1, 4096, 2056, 0), (4, 264, 1000, 40), (20, 264, 1000, 40), (64, 264, 1000, 0)]
+
+
+@pytest.mark.parametrize("shape", GRAPH_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}")
+def test_graph_replay(gu, shape):
+    """A call captured in a HIP graph gives the eager result on every replay, with y
+    filled with NaN and other eager work in between (y is fully overwritten each time)."""
+    import torch
+    from paper_2609_31975_amd import ffn
+    T, d, d_ff, r = shape
+    t = 1.2816
+    inp = wl.make_inputs(107, T, d, d_ff, r=r, wdt=BF16)
+    dev = gu.DevInputs(inp)
+    ws = ffn.alloc_workspace(T, d, d_ff, r)
+    y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+
+    def call():
+        if r:
+            ffn.ffn_lopa_sparse_forward(dev.x, dev.lopa_a, dev.lopa_b, dev.w_up, dev.w_down_t, t, y, ws)
+        else:
+            ffn.ffn_sparse_forward(dev.x, dev.w_gate, dev.w_up, dev.w_down_t, t, y, ws)
+
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        call()
+    torch.cuda.synchronize()
+    y_eager = y.cpu().numpy()
+    gu.check_parity(gu.run_oracle(inp, t), y_eager, None, None, t, BF16, what="eager")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        call()
+    other = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):
+        y.fill_(float("nan"))
+        other.mul_(1.0001)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        y_rep = y.cpu().numpy()
+        assert np.isfinite(y_rep).all(), f"replay {rep} left entries unwritten"
+        assert gu.rel_err(y_rep, y_eager) < 1e-6, f"replay {rep}"
+    del graph
+
+
 # ---------------------------------------------------------------- random shapes
 def _random_cases(n=12, seed=2026):
     """Seeded shapes across every dispatch path: token counts 1..70, d and r multiples
