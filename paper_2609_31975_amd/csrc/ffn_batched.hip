@@ -13,7 +13,9 @@
 // row (up to 256 contiguous bytes of a row per instruction) and reshaped into that
 // layout through a wave-private LDS tile (see the streaming core).
 //
-// One call is three kernels (two for standard gating):
+// One call is three kernels (two for standard gating), one more above 16 tokens:
+//   k_split_tokens (more than 16 tokens) the tokens split once into bf16 hi / lo planes
+//                  in fragment order, read by the next two kernels;
 //   k_lopa_z_mfma  z = A x as two partial sums over halves of the d range;
 //   k_gate_up_mfma per segment of at most 64 rows: gate, union of the tokens' active rows,
 //                  ascending, W_up dots of the union rows; zval = act * v is left in
@@ -21,8 +23,8 @@
 //   k_down_mfma    Y[tokens][cols] += Z[tokens][entries] D[entries][cols] over the
 //                  union rows, segment by segment.
 // A wave of the gate kernel multiplies four row tiles over a quarter of the k range, so
-// each token fragment it loads and splits feeds four tiles; the loads of the next k
-// steps are in flight while the current ones are multiplied.  All operand loads are
+// each token fragment it loads (and splits, when it reads fp32 rows) feeds four tiles;
+// the loads of the next k steps are in flight while the current ones are multiplied.  All operand loads are
 // raw buffer loads: a lane with nothing to load (a row past the segment or the union,
 // a token past the batch, a k step past the row) uses an offset beyond the buffer,
 // which returns zero without a memory access, so every wave issues the same loads in
