@@ -18,17 +18,30 @@
  *     before W3 is applied, so the sparse method skips row i of W3 and column i
  *     of W2 for every inactive i, while W1 x is always computed in full.
  *   LoPA gating, Section 3.3, Eq. (lopaapprox): W1 = G + U V with U (H x r),
- *     V (r x D).  This oracle implements the low-rank product only, h = U (V x),
- *     with V = lopa_a [r][d] and U = lopa_b [d_ff][r]; the fixed term G is zero.
+ *     V (r x D), V = lopa_a [r][d] and U = lopa_b [d_ff][r]: h = G x + U (V x).
+ *     G has a single nonzero per row, +1 or -1 (Section 3.3 and the ablation of
+ *     the fixed matrix): row i holds g_sign[i] in column g_idx[i], so
+ *     (G x)_i = g_sign[i] * x[g_idx[i]].  Without g_idx / g_sign, G = 0.
+ *     Optionally (Section 3.3, "LoPA in practice") an RMSNorm sits between the
+ *     two factors: h = G x + U RMSNorm(V x), RMSNorm(z)_k = gain_k z_k /
+ *     sqrt(mean_k z_k^2 + eps) over the r components.
+ *   Activation variants (Section 3.1 "R-S+ activation"; Section 3.3 "Double
+ *     activation"): act = 1 replaces the shifted ReLU by the shifted R-S+,
+ *     A(h) = (h - t) sigma(h - t) for h > t and 0 otherwise (sigma the logistic
+ *     function): the same active set, another value.  silu_up = 1 applies SiLU,
+ *     v sigma(v), to the W3 output of each active neuron.
  *   FLOP accounting, Section 3.1 Eq. (flops_ratio) and Section 3.3: the oracle
- *     counts every multiply-add it executes, so that the count can be compared
- *     with the paper's cost model: standard d*d_ff + 2|S|d, LoPA r(d + d_ff) + 2|S|d,
- *     dense 3 d d_ff (LoPA dense: r(d + d_ff) + 2 d d_ff).
+ *     counts every multiply-add of the three matrix products it executes, so that
+ *     the count can be compared with the paper's cost model: standard
+ *     d*d_ff + 2|S|d, LoPA r(d + d_ff) + 2|S|d, dense 3 d d_ff (LoPA dense:
+ *     r(d + d_ff) + 2 d d_ff).  Like the paper's model it leaves out G's gather
+ *     and the norm.
  *
  * Inputs are exactly the bit patterns the GPU receives: x is fp32, weights are
  * fp32 (wdt = 0) or bfloat16 bit patterns (wdt = 1); both widen to double
  * exactly.  t is the same fp32 value, widened.
  */
+#include <math.h>
 #include <stdint.h>
 #include <stddef.h>
 #include <stdlib.h>
@@ -51,8 +64,11 @@ static double row_dot(const void* w, int wdt, size_t i, int len, const double* v
   return s;
 }
 
+/* the logistic function 1 / (1 + e^-u) */
+static double logistic(double u) { return 1.0 / (1.0 + exp(-u)); }
+
 /*
- * oracle_ffn -- one FFN forward pass per token, tokens independent.
+ * oracle_ffn_ex -- one FFN forward pass per token, tokens independent.
  *
  *   gating        0: standard, h = W_gate x          (w_gate [d_ff][d])
  *                 1: LoPA,     h = B (A x)           (lopa_a [r][d], lopa_b [d_ff][r])
@@ -61,7 +77,14 @@ static double row_dot(const void* w, int wdt, size_t i, int len, const double* v
  *                 0: the dense FFN (every neuron evaluated, inactive ones weigh 0)
  *   wdt           weight storage: 0 = fp32, 1 = bf16 bit patterns
  *   x             [T][d] fp32
- *   t             activation threshold (shift of the ReLU)
+ *   t             activation threshold (shift of the activation)
+ *   act           0: shifted ReLU, 1: shifted R-S+
+ *   silu_up       1: SiLU on the W3 output (double activation)
+ *   g_idx, g_sign LoPA only: G's column (in [0, d)) and value (+1 / -1) per row,
+ *                 both NULL for G = 0
+ *   rms_norm      LoPA only: 1 for h = G x + U RMSNorm(V x)
+ *   rms_gain      [r] fp32 gain of the norm, NULL for all ones
+ *   rms_eps       added to the mean square (> 0 when rms_norm)
  * Outputs (any may be NULL):
  *   h_out         [T][d_ff] gate pre-activations, fp64
  *   z_out         [T][r] LoPA intermediate V x, fp64 (LoPA only)
@@ -70,14 +93,23 @@ static double row_dot(const void* w, int wdt, size_t i, int len, const double* v
  *   macs_out      [T] multiply-adds executed for that token
  * Returns 0, or -1 on a bad argument.
  */
-int oracle_ffn(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
-               const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
-               const void* w_up, const void* w_down_t, float t,
-               double* h_out, double* z_out, uint8_t* active_out, double* y_out, int64_t* macs_out) {
+int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
+                  const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
+                  const void* w_up, const void* w_down_t, float t, int act, int silu_up,
+                  const int32_t* g_idx, const int8_t* g_sign, int rms_norm, const float* rms_gain,
+                  float rms_eps, double* h_out, double* z_out, uint8_t* active_out, double* y_out,
+                  int64_t* macs_out) {
   if (T < 1 || d < 1 || d_ff < 1 || (wdt != 0 && wdt != 1) || !x || !w_up || !w_down_t) return -1;
   if (gating == 0 && !w_gate) return -1;
   if (gating == 1 && (r < 1 || !lopa_a || !lopa_b)) return -1;
   if (gating != 0 && gating != 1) return -1;
+  if ((act != 0 && act != 1) || (silu_up != 0 && silu_up != 1) || (rms_norm != 0 && rms_norm != 1)) return -1;
+  if ((g_idx == NULL) != (g_sign == NULL)) return -1;
+  if (gating == 0 && (g_idx || rms_norm)) return -1; /* G and the norm belong to LoPA */
+  if (rms_norm && !(rms_eps > 0.0f)) return -1;
+  if (g_idx)
+    for (int i = 0; i < d_ff; ++i)
+      if (g_idx[i] < 0 || g_idx[i] >= d || (g_sign[i] != 1 && g_sign[i] != -1)) return -1;
 
   const double tt = (double)t;
   int zlen = gating == 1 ? r : 1;
@@ -95,11 +127,17 @@ int oracle_ffn(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, i
     int64_t macs = 0;
     for (int j = 0; j < d; ++j) xv[j] = (double)x[(size_t)tok * d + j];
 
-    /* LoPA: the low-rank intermediate z = V x = A x */
+    /* LoPA: the low-rank intermediate z = V x = A x, then the optional RMSNorm */
     if (gating == 1) {
       for (int k = 0; k < r; ++k) zv[k] = row_dot(lopa_a, wdt, (size_t)k, d, xv, &macs);
       if (z_out)
         for (int k = 0; k < r; ++k) z_out[(size_t)tok * r + k] = zv[k];
+      if (rms_norm) {
+        double ss = 0.0;
+        for (int k = 0; k < r; ++k) ss += zv[k] * zv[k];
+        const double inv = 1.0 / sqrt(ss / (double)r + (double)rms_eps);
+        for (int k = 0; k < r; ++k) zv[k] = zv[k] * inv * (rms_gain ? (double)rms_gain[k] : 1.0);
+      }
     }
 
     double* y = y_out ? y_out + (size_t)tok * d : NULL;
@@ -110,13 +148,16 @@ int oracle_ffn(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, i
       /* gate pre-activation, computed for every neuron */
       double h = gating == 0 ? row_dot(w_gate, wdt, (size_t)i, d, xv, &macs)
                              : row_dot(lopa_b, wdt, (size_t)i, r, zv, &macs);
-      int active = h > tt; /* strict: A(h) = max(h - t, 0) is 0 at h == t; NaN is inactive */
+      if (g_idx) h += (double)g_sign[i] * xv[g_idx[i]]; /* (G x)_i */
+      int active = h > tt; /* strict: A(h) is 0 at h == t for both activations; NaN is inactive */
       if (h_out) h_out[(size_t)tok * d_ff + i] = h;
       if (active_out) active_out[(size_t)tok * d_ff + i] = (uint8_t)active;
       if (skip_inactive && !active) continue;
 
-      double a = active ? h - tt : 0.0;                  /* A(W1 x)_i */
+      double u = active ? h - tt : 0.0;
+      double a = act == 1 ? u * logistic(u) : u;              /* A(W1 x)_i */
       double v = row_dot(w_up, wdt, (size_t)i, d, xv, &macs); /* (W3 x)_i */
+      if (silu_up) v = v * logistic(v);
       double zi = a * v;
       /* y += zi * (column i of W2) = zi * w_down_t[i][:] */
       for (int j = 0; j < d; ++j) {
@@ -130,4 +171,13 @@ int oracle_ffn(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, i
   free(xv);
   free(zv);
   return 0;
+}
+
+/* oracle_ffn_ex with the default form: shifted ReLU, no activation on W3, G = 0, no norm */
+int oracle_ffn(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
+               const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
+               const void* w_up, const void* w_down_t, float t,
+               double* h_out, double* z_out, uint8_t* active_out, double* y_out, int64_t* macs_out) {
+  return oracle_ffn_ex(gating, skip_inactive, wdt, T, d, d_ff, r, x, w_gate, lopa_a, lopa_b, w_up, w_down_t, t,
+                       0, 0, NULL, NULL, 0, NULL, 0.0f, h_out, z_out, active_out, y_out, macs_out);
 }

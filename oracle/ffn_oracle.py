@@ -5,9 +5,11 @@ Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``oracle/_build/`` and calls it through ctypes.  Nothing here is shared with the
 GPU library: no headers, no helpers, no constants.
 
-The computation (gated FFN of Section 3.1, Eq. (ffn); shifted-ReLU activation;
-skipping of inactive neurons per Section 3.1 "FFN FLOP-ratio"; LoPA gate
-h = U (V x) of Section 3.3, Eq. (lopaapprox)) is documented in ``ffn_oracle.c``.
+The computation (gated FFN of Section 3.1, Eq. (ffn); shifted-ReLU or shifted R-S+
+activation; skipping of inactive neurons per Section 3.1 "FFN FLOP-ratio"; LoPA gate
+h = G x + U (V x), optionally with RMSNorm between the factors, Section 3.3,
+Eq. (lopaapprox); the double activation of Section 3.3) is documented in
+``ffn_oracle.c``.
 """
 from __future__ import annotations
 
@@ -32,7 +34,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
         tmp = _LIB_PATH + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math",
-                               "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC])
+                               "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -44,10 +46,10 @@ def _load():
             build(force=True)
         lib = ctypes.CDLL(_LIB_PATH)
         vp = ctypes.c_void_p
-        lib.oracle_ffn.restype = ctypes.c_int
-        lib.oracle_ffn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                                   ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, vp, ctypes.c_float,
-                                   vp, vp, vp, vp, vp]
+        i, f = ctypes.c_int, ctypes.c_float
+        lib.oracle_ffn_ex.restype = i
+        lib.oracle_ffn_ex.argtypes = [i, i, i, i, i, i, i, vp, vp, vp, vp, vp, vp, f, i, i, vp, vp, i, vp, f,
+                                      vp, vp, vp, vp, vp]
         _lib = lib
     return _lib
 
@@ -76,13 +78,18 @@ def _weights(w, wdt):
 
 
 def ffn(x, *, w_up, w_down_t, t, wdt, w_gate=None, lopa_a=None, lopa_b=None,
-        skip_inactive=True) -> OracleResult:
+        skip_inactive=True, act=0, silu_up=False, g_idx=None, g_sign=None, rms_norm=False,
+        rms_gain=None, rms_eps=1e-6) -> OracleResult:
     """Run the oracle on every token of ``x`` ([T, d] float32).
 
     Weights: float32 arrays (wdt=0) or uint16 arrays holding bfloat16 bit patterns
     (wdt=1), row-major: w_gate/w_up/w_down_t [d_ff, d], lopa_a [r, d], lopa_b [d_ff, r].
     Exactly one of ``w_gate`` (standard gating) or ``lopa_a``+``lopa_b`` (LoPA) is given.
     ``skip_inactive`` selects the sparse method (True) or the dense FFN (False).
+    ``act``: 0 shifted ReLU, 1 shifted R-S+; ``silu_up``: SiLU on the W3 output.
+    LoPA only: ``g_idx`` (int32 [d_ff]) and ``g_sign`` (int8 [d_ff], +1/-1) give the
+    fixed term G; ``rms_norm`` puts RMSNorm (gain ``rms_gain`` [r] or ones, ``rms_eps``)
+    between A and B.
     """
     lib = _load()
     x = np.ascontiguousarray(x, dtype=np.float32)
@@ -107,13 +114,22 @@ def ffn(x, *, w_up, w_down_t, t, wdt, w_gate=None, lopa_a=None, lopa_b=None,
         raise ValueError("lopa_a must be [r, d] and lopa_b [d_ff, r]")
 
     h = np.empty((T, d_ff), np.float64)
-    act = np.empty((T, d_ff), np.uint8)
+    active = np.empty((T, d_ff), np.uint8)
     y = np.empty((T, d), np.float64)
     macs = np.empty((T,), np.int64)
     z = np.empty((T, r), np.float64) if lopa else None
-    rc = lib.oracle_ffn(1 if lopa else 0, 1 if skip_inactive else 0, wdt, T, d, d_ff, r,
-                        _ptr(x), _ptr(w_gate), _ptr(lopa_a), _ptr(lopa_b), _ptr(w_up), _ptr(w_down_t),
-                        ctypes.c_float(np.float32(t)), _ptr(h), _ptr(z), _ptr(act), _ptr(y), _ptr(macs))
+    gi = None if g_idx is None else np.ascontiguousarray(g_idx, dtype=np.int32)
+    gs = None if g_sign is None else np.ascontiguousarray(g_sign, dtype=np.int8)
+    gain = None if rms_gain is None else np.ascontiguousarray(rms_gain, dtype=np.float32)
+    if (gi is not None and gi.shape != (d_ff,)) or (gs is not None and gs.shape != (d_ff,)):
+        raise ValueError("g_idx and g_sign must be [d_ff]")
+    if gain is not None and gain.shape != (r,):
+        raise ValueError("rms_gain must be [r]")
+    rc = lib.oracle_ffn_ex(1 if lopa else 0, 1 if skip_inactive else 0, wdt, T, d, d_ff, r,
+                           _ptr(x), _ptr(w_gate), _ptr(lopa_a), _ptr(lopa_b), _ptr(w_up), _ptr(w_down_t),
+                           ctypes.c_float(np.float32(t)), int(act), 1 if silu_up else 0, _ptr(gi), _ptr(gs),
+                           1 if rms_norm else 0, _ptr(gain), ctypes.c_float(np.float32(rms_eps)),
+                           _ptr(h), _ptr(z), _ptr(active), _ptr(y), _ptr(macs))
     if rc != 0:
-        raise ValueError(f"oracle_ffn rejected its arguments (rc={rc})")
-    return OracleResult(h=h, active=act.astype(bool), y=y, macs=macs, z=z)
+        raise ValueError(f"oracle_ffn_ex rejected its arguments (rc={rc})")
+    return OracleResult(h=h, active=active.astype(bool), y=y, macs=macs, z=z)

@@ -324,3 +324,144 @@ def test_threshold_gives_target_sparsity(r):
     p = 0.5 * math.erfc(t / sigma / math.sqrt(2))
     n = int(res.active.sum())
     assert abs(n - p * d_ff) < 4 * math.sqrt(d_ff * p * (1 - p)), (n, p * d_ff)
+
+
+# ---------------------------------------------------------------- the paper's full form
+# Shifted R-S+ (Section 3.1) and SiLU on the W3 output (Section 3.3, double activation)
+# at points where the logistic function has a closed form: sigma(ln 3) = 3/4 and
+# sigma(-ln 3) = 1/4 (e^-ln3 = 1/3), and at 0, where SiLU is exactly 0.
+LN3 = math.log(3.0)
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_rsplus_at_ln3(wdt):
+    """One active neuron with h - t = ln 3: R-S+ gives 3/4 of the shifted ReLU's output,
+    on the same active set, and inactive rows (NaN) are still never read."""
+    x, g, up, dn = _worked_standard()
+    t = float(np.float32(6.0 - LN3))   # only neuron 5 (h = 6) is active, u = 6 - t ~ ln 3
+    kw = dict(w_gate=_enc(g, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt), t=t, wdt=wdt)
+    relu = ffn_oracle.ffn(x, **kw)
+    rsp = ffn_oracle.ffn(x, act=1, **kw)
+    assert np.flatnonzero(relu.active[0]).tolist() == [5]
+    assert np.array_equal(rsp.active, relu.active)
+    assert relu.y[0, 3] != 0 and np.isfinite(rsp.y).all()
+    assert np.allclose(rsp.y, 0.75 * relu.y, rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_silu_on_up_output(wdt):
+    """W3 outputs +ln 3, -ln 3 and 0 on the three active neurons: SiLU scales them by
+    3/4 and 1/4 and zeroes the third, which then adds nothing to y."""
+    x, g, up, dn = _worked_standard()   # x = (1, -2, 3, 0.5), active {1, 2, 5} at t = 1
+    up = up.copy()
+    up[1] = [LN3, 0, 0, 0]
+    up[2] = [-LN3, 0, 0, 0]
+    up[5] = [0, 0, 0, 0]
+    kw = dict(w_gate=_enc(g, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt), t=1.0, wdt=wdt)
+    plain = ffn_oracle.ffn(x, **kw)
+    dbl = ffn_oracle.ffn(x, silu_up=True, **kw)
+    v = float(_widen(_enc([LN3], wdt), wdt)[0])   # the stored ln 3
+    # y = a1 v1 dn1 + a2 v2 dn2 (+ a5 * 0 * dn5), a = (1, 2, 5), dn1 = e0, dn2 = e1 + e2
+    assert plain.y.tolist() == [[v, -2 * v, -2 * v, 0.0]]
+    # bf16 stores ln 3 as 1.1015625: sigma moves by at most sigma' * 0.003 = 3/16 * 0.003,
+    # 0.1% of 3/4 and 0.25% of 1/4
+    rtol = 1e-6 if wdt == wl.F32 else 3e-3
+    assert np.allclose(dbl.y, [[0.75 * v, -0.5 * v, -0.5 * v, 0.0]], rtol=rtol, atol=0)
+    assert np.array_equal(dbl.active, plain.active)
+
+
+# LoPA with the fixed term G only (B = 0): h = G x.  G's rows: +e0, -e1, +e2, +e3, -e0, +e2
+#   x = (1, -2, 3, 0.5) -> h = (1, 2, 3, 0.5, -1, 3); t = 1: active {1, 2, 5}, a = (1, 2, 2)
+#   up/down rows of the standard example: v = (0.5, -1, 6), a*v = (0.5, -2, 12)
+#   y = 0.5 e0 - 2 (e1 + e2) + 12 * 0.5 e3 = (0.5, -2, -2, 6)
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_fixed_term_only(wdt):
+    x, _, up, dn = _worked_standard()
+    r = 2
+    A = np.ones((r, 4))
+    B = np.zeros((6, r))
+    g_idx = np.array([0, 1, 2, 3, 0, 2], np.int32)
+    g_sign = np.array([1, -1, 1, 1, -1, 1], np.int8)
+    res = ffn_oracle.ffn(x, lopa_a=_enc(A, wdt), lopa_b=_enc(B, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt),
+                         t=1.0, wdt=wdt, g_idx=g_idx, g_sign=g_sign)
+    assert res.h.tolist() == [[1, 2, 3, 0.5, -1, 3]]
+    assert np.flatnonzero(res.active[0]).tolist() == [1, 2, 5]
+    assert res.y.tolist() == [[0.5, -2, -2, 6]]
+    assert res.macs.tolist() == [r * (4 + 6) + 2 * 3 * 4]   # G's gather is not a multiply-add
+
+
+def test_fixed_term_is_the_matrix_G_plus_BA():
+    """h = G x + B (A x) equals standard gating with the dense matrix W_gate = G + B A
+    (Eq. (lopaapprox)), built with numpy and run through the standard path."""
+    d, d_ff, r, T, t = 24, 70, 6, 3, 0.4
+    inp = wl.make_inputs(21, T, d, d_ff, r=r, wdt=wl.F32)
+    rng = np.random.default_rng(22)
+    g_idx = rng.integers(0, d, d_ff).astype(np.int32)
+    g_sign = rng.choice([-1, 1], d_ff).astype(np.int8)
+    G = np.zeros((d_ff, d))
+    G[np.arange(d_ff), g_idx] = g_sign
+    W = (G + inp.lopa_b.astype(np.float64) @ inp.lopa_a.astype(np.float64)).astype(np.float32)
+    lopa = ffn_oracle.ffn(inp.x, lopa_a=inp.lopa_a, lopa_b=inp.lopa_b, w_up=inp.w_up, w_down_t=inp.w_down_t,
+                          t=t, wdt=wl.F32, g_idx=g_idx, g_sign=g_sign)
+    std = ffn_oracle.ffn(inp.x, w_gate=W, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wl.F32)
+    assert np.allclose(lopa.h, std.h, rtol=0, atol=1e-5)
+    band = np.abs(std.h - t) < 1e-4
+    assert np.array_equal(lopa.active[~band], std.active[~band])
+    assert not band.any()   # the seeded draw keeps every h away from t, so the outputs match too
+    assert np.allclose(lopa.y, std.y, rtol=1e-5, atol=1e-6)
+    no_sign = ffn_oracle.ffn(inp.x, lopa_a=inp.lopa_a, lopa_b=inp.lopa_b, w_up=inp.w_up, w_down_t=inp.w_down_t,
+                             t=t, wdt=wl.F32, g_idx=g_idx, g_sign=np.ones(d_ff, np.int8))
+    assert not np.allclose(no_sign.h, std.h, rtol=0, atol=1e-5)   # the sign is part of G
+
+
+# RMSNorm between the factors (Section 3.3): A picks z = (x2, 8 x3) = (3, 4) from
+#   x = (1, -2, 3, 0.5); mean(z^2) = 12.5, so RMSNorm(z) = (3, 4) / sqrt(12.5)
+#   = (3 sqrt2 / 5, 4 sqrt2 / 5).  B rows (1,0), (0,1), (1,1), (-1,0), (0,0), (2,-1).
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_rms_norm_worked(wdt):
+    x, _, up, dn = _worked_standard()
+    up = np.nan_to_num(up, nan=0.0)
+    dn = np.nan_to_num(dn, nan=0.0)
+    A = np.array([[0, 0, 1, 0], [0, 0, 0, 8]])
+    B = np.array([[1, 0], [0, 1], [1, 1], [-1, 0], [0, 0], [2, -1]])
+    kw = dict(lopa_a=_enc(A, wdt), lopa_b=_enc(B, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt), t=0.5,
+              wdt=wdt, rms_norm=True, rms_eps=1e-30)
+    res = ffn_oracle.ffn(x, **kw)
+    s2 = math.sqrt(2.0)
+    z0, z1 = 3 * s2 / 5, 4 * s2 / 5
+    assert np.allclose(res.h[0], [z0, z1, z0 + z1, -z0, 0, 2 * z0 - z1], rtol=1e-14, atol=1e-15)
+    gain = np.array([2.0, 0.25], np.float32)
+    res_g = ffn_oracle.ffn(x, rms_gain=gain, **kw)
+    assert np.allclose(res_g.h[0], [2 * z0, z1 / 4, 2 * z0 + z1 / 4, -2 * z0, 0, 4 * z0 - z1 / 4], rtol=1e-14,
+                       atol=1e-15)
+
+
+def test_rms_norm_is_scale_invariant():
+    """RMSNorm(c z) = RMSNorm(z) for c > 0: scaling A by 4 (exact in bf16) leaves the gate,
+    the active set and the output unchanged; without the norm the gate scales by 4."""
+    d, d_ff, r, T, t = 40, 90, 8, 3, 0.3
+    inp = wl.make_inputs(23, T, d, d_ff, r=r, wdt=wl.BF16)
+    A4 = wl.f32_to_bf16_bits(4 * wl.bf16_bits_to_f32(inp.lopa_a))
+    kw = dict(lopa_b=inp.lopa_b, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wl.BF16, rms_eps=1e-30)
+    r1 = ffn_oracle.ffn(inp.x, lopa_a=inp.lopa_a, rms_norm=True, **kw)
+    r4 = ffn_oracle.ffn(inp.x, lopa_a=A4, rms_norm=True, **kw)
+    assert np.allclose(r4.h, r1.h, rtol=1e-13, atol=1e-14)
+    assert np.array_equal(r4.active, r1.active)
+    assert np.allclose(r4.y, r1.y, rtol=1e-12, atol=1e-14)
+    p1 = ffn_oracle.ffn(inp.x, lopa_a=inp.lopa_a, **kw)
+    p4 = ffn_oracle.ffn(inp.x, lopa_a=A4, **kw)
+    assert np.allclose(p4.h, 4 * p1.h, rtol=1e-13, atol=1e-14)
+
+
+def test_full_form_rejects_bad_options():
+    x, g, up, dn = _worked_standard()
+    kw = dict(w_up=_enc(up, wl.F32), w_down_t=_enc(dn, wl.F32), t=1.0, wdt=wl.F32)
+    lkw = dict(lopa_a=_enc(np.ones((2, 4)), wl.F32), lopa_b=_enc(np.zeros((6, 2)), wl.F32), **kw)
+    with pytest.raises(ValueError):   # G belongs to LoPA
+        ffn_oracle.ffn(x, w_gate=_enc(g, wl.F32), g_idx=np.zeros(6, np.int32), g_sign=np.ones(6, np.int8), **kw)
+    with pytest.raises(ValueError):   # a sign other than +1 / -1
+        ffn_oracle.ffn(x, g_idx=np.zeros(6, np.int32), g_sign=np.full(6, 2, np.int8), **lkw)
+    with pytest.raises(ValueError):   # a column outside [0, d)
+        ffn_oracle.ffn(x, g_idx=np.full(6, 4, np.int32), g_sign=np.ones(6, np.int8), **lkw)
+    with pytest.raises(ValueError):   # the norm needs eps > 0
+        ffn_oracle.ffn(x, rms_norm=True, rms_eps=0.0, **lkw)
