@@ -67,7 +67,8 @@ enum {
   FFN_ERR_DTYPE = -3,     /* weight dtype is not FFN_F32 / FFN_BF16 */
   FFN_ERR_ALIGN = -4,     /* a pointer is not 16-byte aligned */
   FFN_ERR_WORKSPACE = -5, /* ws_bytes < ffn_workspace_bytes(...) */
-  FFN_ERR_HIP = -6        /* a HIP launch failed */
+  FFN_ERR_HIP = -6,       /* a HIP launch failed */
+  FFN_ERR_OPTION = -7     /* an ffn_options_t field is invalid (see ffn_options_t) */
 };
 
 /* Bytes of workspace the forward calls need for this shape (r = 0 for standard gating).
@@ -98,13 +99,67 @@ int ffn_lopa_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const
                            const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
                            hipStream_t stream);
 
+/* The paper's full FFN form (optional; the four calls above use the default form).
+ *   act        the gate activation, shifted by t (Section 3.1): FFN_ACT_RELU gives
+ *              max(h - t, 0); FFN_ACT_RSPLUS gives the R-S+ activation of h - t,
+ *              (h - t) sigma(h - t) where h > t and 0 elsewhere (sigma the logistic
+ *              function).  Both keep neuron i active iff h_i > t, so the sparse method
+ *              skips the same rows; only the activation value differs.
+ *   silu_up    1: SiLU, v sigma(v), on each neuron's W_up output v (the double activation
+ *              of Section 3.3); 0: v as is.
+ *   g_idx, g_sign  LoPA only (Section 3.3, Eq. (lopaapprox), W1 = G + U V): device arrays
+ *              of d_ff entries holding G's single nonzero per row, in column g_idx[i] with
+ *              value g_sign[i] (+1 or -1), so that h_i gains g_sign[i] x[g_idx[i]].  Both
+ *              NULL: G = 0.  Their contents are not checked on the host: a column outside
+ *              [0, d) reads 0 (never out of bounds), a value other than +-1 is used as is.
+ *   rms_norm   LoPA only: 1 for h = G x + B RMSNorm(A x) (Section 3.3), where
+ *              RMSNorm(z)_k = rms_gain[k] z_k / sqrt(mean_k z_k^2 + rms_eps) over the r
+ *              components of z.
+ *   rms_gain   device array of r gains, or NULL for ones (NULL without rms_norm).
+ *   rms_eps    added to the mean square inside the root; finite and > 0 with rms_norm.
+ * A NULL options pointer, or a zero-filled struct, gives the default form.  g_idx and
+ * rms_gain must be 4-byte aligned (else FFN_ERR_ALIGN).  FFN_ERR_OPTION: act not one of
+ * the two values; silu_up or rms_norm not 0 or 1; exactly one of g_idx, g_sign NULL; G or
+ * the norm with standard gating; rms_norm with an invalid rms_eps; rms_gain without
+ * rms_norm. */
+typedef enum { FFN_ACT_RELU = 0, FFN_ACT_RSPLUS = 1 } ffn_act_t;
+
+typedef struct {
+  ffn_act_t act;
+  int silu_up;
+  const int32_t* g_idx;
+  const int8_t* g_sign;
+  int rms_norm;
+  const float* rms_gain;
+  float rms_eps;
+} ffn_options_t;
+
+/* The four forward calls with options: same arguments, plus `opt`, a host pointer to the
+ * options (NULL for the default form), read during the call only; the device arrays it
+ * names must stay valid until the call's work on `stream` has finished. */
+int ffn_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                         const void* w_up, const void* w_down_t, float t, const ffn_options_t* opt, float* y,
+                         void* ws, size_t ws_bytes, hipStream_t stream);
+int ffn_sparse_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                          const void* w_up, const void* w_down_t, float t, const ffn_options_t* opt, float* y,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+int ffn_lopa_sparse_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                               const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                               float t, const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+int ffn_lopa_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                              const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                              float t, const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
 /* Inspection hook for tests and the benchmark (not on the hot path).  Synchronizes
  * `stream`, then copies the active set of the last forward call made with this
  * workspace and the same (T, d, d_ff, r) to host memory:
  *   *n_union        number of neurons active for at least one token
  *   idx_host        [d_ff] int32: those neurons, ascending (first *n_union entries)
- *   act_host        [T][d_ff] fp32 (may be NULL): act_host[tau][k] = h - t of neuron
- *                   idx_host[k] for token tau, or 0 where that token is inactive
+ *   act_host        [T][d_ff] fp32 (may be NULL): act_host[tau][k] = the activation value
+ *                   (h - t for the default form) of neuron idx_host[k] for token tau, or 0
+ *                   where that token is inactive
  * For a dense call every neuron is listed.  Returns FFN_OK or an error code. */
 int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
                    float* act_host, hipStream_t stream);

@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/ffn_sparse.h: argument checks,
 // workspace carve-up and kernel sequencing.  No allocation, no synchronization on the
 // forward path.
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -70,11 +71,39 @@ struct Call {
   const void* w_up;
   const void* w_down_t;
   float t;
+  const ffn_options_t* opt;  // NULL: the default form
   float* y;
   void* ws;
   size_t ws_bytes;
   hipStream_t stream;
 };
+
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+// Checks ffn_options_t (see the header) and splits it into the gate kernels' Form and the
+// norm's gain and eps (eps 0: no norm).
+int check_options(const ffn_options_t* o, bool lopa, Form* form, const float** gain, float* eps) {
+  *form = Form{};
+  *gain = nullptr;
+  *eps = 0.f;
+  if (!o) return FFN_OK;
+  if ((o->act != FFN_ACT_RELU && o->act != FFN_ACT_RSPLUS) || (o->silu_up != 0 && o->silu_up != 1) ||
+      (o->rms_norm != 0 && o->rms_norm != 1))
+    return FFN_ERR_OPTION;
+  if ((o->g_idx == nullptr) != (o->g_sign == nullptr)) return FFN_ERR_OPTION;
+  if (!lopa && (o->g_idx || o->rms_norm || o->rms_gain)) return FFN_ERR_OPTION;
+  if (o->rms_norm ? !(isfinite(o->rms_eps) && o->rms_eps > 0.f) : o->rms_gain != nullptr) return FFN_ERR_OPTION;
+  if (!aligned4(o->g_idx) || !aligned4(o->rms_gain)) return FFN_ERR_ALIGN;
+  form->act = o->act;
+  form->silu_up = o->silu_up;
+  form->g_idx = o->g_idx;
+  form->g_sign = o->g_sign;
+  if (o->rms_norm) {
+    *gain = o->rms_gain;
+    *eps = o->rms_eps;
+  }
+  return FFN_OK;
+}
 
 int run(const Call& c) {
   const bool lopa = c.r > 0;
@@ -85,6 +114,11 @@ int run(const Call& c) {
   if (!aligned(c.x) || !aligned(c.gate) || !aligned(c.w_up) || !aligned(c.w_down_t) || !aligned(c.y) ||
       !aligned(c.ws) || (lopa && !aligned(c.lopa_a)))
     return FFN_ERR_ALIGN;
+  Form form;
+  const float* gain;
+  float eps;
+  const int so = check_options(c.opt, lopa, &form, &gain, &eps);
+  if (so != FFN_OK) return so;
   Workspace ws;
   if (c.ws_bytes < workspace_layout(c.T, c.d, c.d_ff, c.r, c.ws, &ws)) return FFN_ERR_WORKSPACE;
 
@@ -96,10 +130,12 @@ int run(const Call& c) {
     const Gate g = lopa ? Gate::LoPA : Gate::Standard;
     hipError_t e = hipSuccess;
     if (batched_ok(sh, g)) {
-      e = launch_batched(sh, g, c.dense, x, c.lopa_a, c.gate, c.w_up, c.w_down_t, c.t, ws, y, c.stream);
+      e = launch_batched(sh, g, c.dense, form, gain, eps, x, c.lopa_a, c.gate, c.w_up, c.w_down_t, c.t, ws, y,
+                         c.stream);
     } else {
       if (lopa) e = launch_lopa_z(sh, x, c.lopa_a, ws, c.stream);
-      if (e == hipSuccess) e = launch_gate_up(sh, g, c.dense, x, c.gate, c.w_up, c.t, ws, y, c.stream);
+      if (e == hipSuccess && eps > 0.f) e = launch_rms_norm(ws.z, 1, ws.tc, sh.T, sh.r, gain, eps, c.stream);
+      if (e == hipSuccess) e = launch_gate_up(sh, g, c.dense, form, x, c.gate, c.w_up, c.t, ws, y, c.stream);
       if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
     }
     if (e != hipSuccess) return FFN_ERR_HIP;
@@ -122,27 +158,60 @@ size_t ffn_workspace_bytes(int T, int d, int d_ff, int r) {
 int ffn_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
                       const void* w_up, const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
                       hipStream_t stream) {
-  return ffn::run(Call{wdt, T, d, d_ff, 0, true, x, w_gate, nullptr, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+  return ffn::run(
+      Call{wdt, T, d, d_ff, 0, true, x, w_gate, nullptr, w_up, w_down_t, t, nullptr, y, ws, ws_bytes, stream});
 }
 
 int ffn_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
                        const void* w_up, const void* w_down_t, float t, float* y, void* ws, size_t ws_bytes,
                        hipStream_t stream) {
-  return ffn::run(Call{wdt, T, d, d_ff, 0, false, x, w_gate, nullptr, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+  return ffn::run(
+      Call{wdt, T, d, d_ff, 0, false, x, w_gate, nullptr, w_up, w_down_t, t, nullptr, y, ws, ws_bytes, stream});
 }
 
 int ffn_lopa_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x, const void* lopa_a,
                             const void* lopa_b, const void* w_up, const void* w_down_t, float t, float* y, void* ws,
                             size_t ws_bytes, hipStream_t stream) {
   if (r < 1) return FFN_ERR_SHAPE;
-  return ffn::run(Call{wdt, T, d, d_ff, r, false, x, lopa_b, lopa_a, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+  return ffn::run(
+      Call{wdt, T, d, d_ff, r, false, x, lopa_b, lopa_a, w_up, w_down_t, t, nullptr, y, ws, ws_bytes, stream});
 }
 
 int ffn_lopa_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x, const void* lopa_a,
                            const void* lopa_b, const void* w_up, const void* w_down_t, float t, float* y, void* ws,
                            size_t ws_bytes, hipStream_t stream) {
   if (r < 1) return FFN_ERR_SHAPE;
-  return ffn::run(Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, y, ws, ws_bytes, stream});
+  return ffn::run(
+      Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, nullptr, y, ws, ws_bytes, stream});
+}
+
+int ffn_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                         const void* w_up, const void* w_down_t, float t, const ffn_options_t* opt, float* y,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  return ffn::run(Call{wdt, T, d, d_ff, 0, true, x, w_gate, nullptr, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream});
+}
+
+int ffn_sparse_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                          const void* w_up, const void* w_down_t, float t, const ffn_options_t* opt, float* y,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  return ffn::run(
+      Call{wdt, T, d, d_ff, 0, false, x, w_gate, nullptr, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream});
+}
+
+int ffn_lopa_sparse_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                               const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                               float t, const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  if (r < 1) return FFN_ERR_SHAPE;
+  return ffn::run(Call{wdt, T, d, d_ff, r, false, x, lopa_b, lopa_a, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream});
+}
+
+int ffn_lopa_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                              const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                              float t, const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  if (r < 1) return FFN_ERR_SHAPE;
+  return ffn::run(Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream});
 }
 
 int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
@@ -193,9 +262,10 @@ const char* ffn_status_string(int status) {
     case FFN_ERR_NULL: return "null pointer argument";
     case FFN_ERR_SHAPE: return "invalid shape";
     case FFN_ERR_DTYPE: return "invalid weight dtype";
-    case FFN_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case FFN_ERR_ALIGN: return "pointer not aligned (16 bytes; g_idx and rms_gain 4 bytes)";
     case FFN_ERR_WORKSPACE: return "workspace too small";
     case FFN_ERR_HIP: return "HIP launch or copy failed";
+    case FFN_ERR_OPTION: return "invalid ffn_options_t field";
     default: return "unknown status";
   }
 }

@@ -346,14 +346,16 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 // read.
 // LOPA: the gate rows are B [d_ff][r] against z = zp[0] + zp[1]; otherwise W_gate x.
 // KU / KUU: k steps per load group of the gate rows / the W_up rows.
-template <bool LOPA, bool DENSE, int NT, int KU, int KUU>
+// FULL: the paper's full form (`form`): the activation value, SiLU on the W_up output and,
+// for LoPA, the fixed term G added to the gate before the union.
+template <bool LOPA, bool DENSE, int NT, int KU, int KUU, bool FULL>
 __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const float* __restrict__ zp,
                                              const uint4* __restrict__ gate_w, int Cg, const uint4* __restrict__ w_up,
                                              int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,
                                              int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                              int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                              uint4* __restrict__ zf, float* __restrict__ y,
-                                             const uint4* __restrict__ xs, int ntt) {
+                                             const uint4* __restrict__ xs, int ntt, Form form) {
   constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   // the W_up rows of a union of at most two row tiles go as two tiles with twice the k
   // steps a group (one token tile only: the register budget of wider ones is spent)
@@ -418,9 +420,12 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
           const int tok = 16 * nt + m;
-          const float hv = h[nt][i];
+          float hv = h[nt][i];
+          if constexpr (FULL) {  // LoPA's fixed term: h += G x
+            if (form.g_idx && tok < T && rl < nrows) hv += g_term(form, x + (size_t)tok * d, d, row0 + rl);
+          }
           const bool on = tok < T && hv > t;
-          if (tok < T && rl < nrows) s_act[rl][tok] = on ? hv - t : 0.f;
+          if (tok < T && rl < nrows) s_act[rl][tok] = on ? (FULL ? gate_value(form.act, hv - t) : hv - t) : 0.f;
           any |= on;
         }
         const uint64_t b = __ballot(any && rl < nrows);
@@ -503,7 +508,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int e = 16 * wave + 4 * g + i;
-            const float zz = e < cnt ? s_act[s_list[e]][tok] * v[i] : 0.f;
+            const float zz = e < cnt ? s_act[s_list[e]][tok] * (FULL ? up_value(form.silu_up, v[i]) : v[i]) : 0.f;
             const __bf16 hb = (__bf16)zz;
             const __bf16 lb = (__bf16)(zz - (float)hb);
             hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
@@ -524,26 +529,26 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       const uint4 *__restrict__ w_up, int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,       \
       int32_t *__restrict__ meta, int32_t *__restrict__ seg_count, int32_t *__restrict__ seg_idx,                  \
       float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y, const uint4 *__restrict__ xs,  \
-      int ntt
+      int ntt, Form form
 #define FFN_GATE_UP_ARGS \
-  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt
+  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt, form
 
 // One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
 // gate rows and for wider token tiles; one for LoPA's gate rows with four token tiles,
 // whose fragments carry both partial copies of z).
-template <bool LOPA, bool DENSE, int NT>
+template <bool LOPA, bool DENSE, int NT, bool FULL>
 __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(FFN_GATE_UP_PARAMS) {
   constexpr int KU = NT == 1 ? (LOPA ? 2 : 4) : (LOPA && NT == 4 ? 1 : 2);
-  gate_up_body<LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2>(FFN_GATE_UP_ARGS);
+  gate_up_body<LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2, FULL>(FFN_GATE_UP_ARGS);
 }
 
 // Standard gating, one token tile: two k steps a group, so that two workgroups fit a CU
 // (at most 256 registers a lane); one workgroup's phase changes (LDS reductions, union)
 // then overlap the other's streaming.
-template <bool DENSE>
+template <bool DENSE, bool FULL>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) void k_gate_up_mfma2(
     FFN_GATE_UP_PARAMS) {
-  gate_up_body<false, DENSE, 1, 2, 2>(FFN_GATE_UP_ARGS);
+  gate_up_body<false, DENSE, 1, 2, 2, FULL>(FFN_GATE_UP_ARGS);
 }
 #undef FFN_GATE_UP_PARAMS
 #undef FFN_GATE_UP_ARGS
@@ -823,9 +828,9 @@ int segments_for(int d_ff, int grid) {
   return n > 128 ? (n + grid - 1) / grid * grid : n;
 }
 
-template <bool LOPA, bool DENSE, int NT>
-hipError_t gate_mfma(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
-                     float* y, hipStream_t s) {
+template <bool LOPA, bool DENSE, int NT, bool FULL>
+hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up, float t,
+                     Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
   constexpr bool two = !LOPA && NT == 1;
   const int grid = two ? kSegGrid2 : kSegGrid;
@@ -833,21 +838,28 @@ hipError_t gate_mfma(const Shape& sh, const float* x, const void* gate_w, const 
   const int g = ws.nseg < grid ? ws.nseg : grid;
   auto kernel = [&] {
     if constexpr (two)
-      return k_gate_up_mfma2<DENSE>;
+      return k_gate_up_mfma2<DENSE, FULL>;
     else
-      return k_gate_up_mfma<LOPA, DENSE, NT>;
+      return k_gate_up_mfma<LOPA, DENSE, NT, FULL>;
   }();
   return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                             static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
-                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws));
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form);
+}
+
+template <bool LOPA, bool DENSE, bool FULL>
+hipError_t gate_nt(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
+                   Workspace& ws, float* y, hipStream_t s) {
+  if (sh.T <= 16) return gate_mfma<LOPA, DENSE, 1, FULL>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  if (sh.T <= 32) return gate_mfma<LOPA, DENSE, 2, FULL>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  return gate_mfma<LOPA, DENSE, 4, FULL>(sh, f, x, gate_w, w_up, t, ws, y, s);
 }
 
 template <bool LOPA, bool DENSE>
-hipError_t gate_nt(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
-                   float* y, hipStream_t s) {
-  if (sh.T <= 16) return gate_mfma<LOPA, DENSE, 1>(sh, x, gate_w, w_up, t, ws, y, s);
-  if (sh.T <= 32) return gate_mfma<LOPA, DENSE, 2>(sh, x, gate_w, w_up, t, ws, y, s);
-  return gate_mfma<LOPA, DENSE, 4>(sh, x, gate_w, w_up, t, ws, y, s);
+hipError_t gate_form(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
+                     Workspace& ws, float* y, hipStream_t s) {
+  return f.full() ? gate_nt<LOPA, DENSE, true>(sh, f, x, gate_w, w_up, t, ws, y, s)
+                  : gate_nt<LOPA, DENSE, false>(sh, f, x, gate_w, w_up, t, ws, y, s);
 }
 
 // Down grid: S column groups x R row chunks, about kDnWgTarget workgroups, at most
@@ -892,9 +904,9 @@ bool batched_ok(const Shape& sh, Gate g) {
 // the most segments any gate kernel of this path uses (workspace sizing)
 int batched_segments(int d_ff) { return segments_for(d_ff, kSegGrid2); }
 
-hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
-                          const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
-                          float* y, hipStream_t s) {
+hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* norm_gain,
+                          float norm_eps, const float* x, const void* lopa_a, const void* gate_w, const void* w_up,
+                          const void* w_down_t, float t, Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
   hipError_t e = hipSuccess;
   // more than one token tile: the kernels read the tokens pre-split
@@ -903,13 +915,16 @@ hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, c
     e = sh.T <= 16 ? z_mfma<1>(sh, x, lopa_a, ws, s)
                    : sh.T <= 32 ? z_mfma<2>(sh, x, lopa_a, ws, s) : z_mfma<4>(sh, x, lopa_a, ws, s);
     if (e != hipSuccess) return e;
+    // RMSNorm between A and B: the two partial copies of z become one normalised copy
+    if (norm_eps > 0.f && (e = launch_rms_norm(ws.z, 2, ws.tc, sh.T, sh.r, norm_gain, norm_eps, s)) != hipSuccess)
+      return e;
   }
   if (lopa)
-    e = dense ? gate_nt<true, true>(sh, x, gate_w, w_up, t, ws, y, s)
-              : gate_nt<true, false>(sh, x, gate_w, w_up, t, ws, y, s);
+    e = dense ? gate_form<true, true>(sh, form, x, gate_w, w_up, t, ws, y, s)
+              : gate_form<true, false>(sh, form, x, gate_w, w_up, t, ws, y, s);
   else
-    e = dense ? gate_nt<false, true>(sh, x, gate_w, w_up, t, ws, y, s)
-              : gate_nt<false, false>(sh, x, gate_w, w_up, t, ws, y, s);
+    e = dense ? gate_form<false, true>(sh, form, x, gate_w, w_up, t, ws, y, s)
+              : gate_form<false, false>(sh, form, x, gate_w, w_up, t, ws, y, s);
   if (e != hipSuccess) return e;
   if (sh.T <= 16) return down_mfma<1>(sh, w_down_t, ws, y, s);
   if (sh.T <= 32) return down_mfma<2>(sh, w_down_t, ws, y, s);

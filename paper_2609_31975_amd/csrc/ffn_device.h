@@ -122,6 +122,23 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
   return v + (row > 0 ? r0 : 0) + (row > 1 ? r1 : 0) + (row > 2 ? r2 : 0);
 }
 
+// ------------------------------------------------------------------ full form
+// Activation values of the paper's full form: the shifted R-S+ of u = h - t > 0
+// (Section 3.1), u sigma(u), or u itself; SiLU on the W_up output v (Section 3.3,
+// double activation), v sigma(v), or v itself.
+__device__ __forceinline__ float gate_value(int act, float u) { return act ? u / (1.f + expf(-u)) : u; }
+__device__ __forceinline__ float up_value(int silu, float v) { return silu ? v / (1.f + expf(-v)) : v; }
+
+// LoPA's fixed term for row `row` and the token whose fp32 row is `xt` (d values):
+// g_sign[row] x[g_idx[row]], read through a buffer of d floats so that a column
+// outside [0, d) reads 0.
+__device__ __forceinline__ float g_term(const Form& f, const float* xt, int d, int row) {
+  const Buf xb = make_buf(xt, 4u * (uint32_t)d);
+  const int c = f.g_idx[row];
+  const float v = __builtin_bit_cast(float, ldb32(xb, (uint32_t)c < (uint32_t)d ? 4u * (uint32_t)c : kOOB));
+  return (float)f.g_sign[row] * v;
+}
+
 // The gate kernels clear y (the down kernel accumulates into it) and record the
 // segment count for the inspection hook.
 __device__ __forceinline__ void clear_output(float* __restrict__ y, int n, int32_t* meta, int nseg) {

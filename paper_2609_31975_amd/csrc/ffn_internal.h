@@ -70,6 +70,17 @@ struct Shape {
 
 enum class Gate { Standard, LoPA };
 
+// The paper's full FFN form as the gate kernels see it (from ffn_options_t, checked on
+// the host): the activation, SiLU on the W_up output and LoPA's fixed term G.  The
+// norm on z is not here: it runs as a kernel of its own between z and the gate.
+struct Form {
+  int act = 0;                     // 0 shifted ReLU, 1 shifted R-S+
+  int silu_up = 0;                 // 1: SiLU on the W_up output
+  const int32_t* g_idx = nullptr;  // G's column per row (null: G = 0, and g_sign null)
+  const int8_t* g_sign = nullptr;  // G's value per row
+  bool full() const { return act != 0 || silu_up != 0 || g_idx != nullptr; }
+};
+
 // Events for the next gate-kernel launch on this host thread (benchmark hook).
 struct GateTiming {
   hipEvent_t start = nullptr;
@@ -80,9 +91,14 @@ extern thread_local GateTiming g_gate_timing;
 // Launchers (return hipSuccess or the launch error).  Every launcher enqueues on `s`.
 hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
                          hipStream_t s);
+// RMSNorm on z in place (Section 3.3): the `parts` partial copies [parts][tc][r] of each
+// token's z are summed into copy 0, scaled by gain / sqrt(mean z^2 + eps), and the other
+// copies are zeroed, so the gate kernels read the normalized z unchanged.
+hipError_t launch_rms_norm(float* z, int parts, int tc, int T, int r, const float* gain, float eps,
+                           hipStream_t s);
 // Also clears y[0 .. T*d) and sets ws.nseg / meta[0] for the down kernel.
-hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w,
-                          const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
+hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x,
+                          const void* gate_w, const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s);
 
@@ -90,8 +106,9 @@ hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const 
 // the whole call (LoPA z, gate + union + W_up, down), clearing y first.
 bool batched_ok(const Shape& sh, Gate g);
 int batched_segments(int d_ff);
-hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const float* x, const void* lopa_a,
-                          const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
-                          float* y, hipStream_t s);
+// With norm_gain / norm_eps: RMSNorm on z (norm_eps > 0 turns it on).
+hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* norm_gain,
+                          float norm_eps, const float* x, const void* lopa_a, const void* gate_w, const void* w_up,
+                          const void* w_down_t, float t, Workspace& ws, float* y, hipStream_t s);
 
 }  // namespace ffn

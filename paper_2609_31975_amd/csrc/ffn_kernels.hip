@@ -134,10 +134,11 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
 }
 
 // Ballot compaction of one segment (run by the first wave): neurons whose gate value
-// exceeds t (all neurons if `all`) get ascending ranks; their activation h - t is
-// kept in LDS for the W_up phase and published with the neuron index.
+// exceeds t (all neurons if `all`) get ascending ranks; their activation value (h - t,
+// or its R-S+ with act = 1) is kept in LDS for the W_up phase and published with the
+// neuron index.
 __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int row0, int seg, float t, bool all,
-                                                int* s_list, float* s_act, int* s_cnt, int32_t* seg_count,
+                                                int act, int* s_list, float* s_act, int* s_cnt, int32_t* seg_count,
                                                 int32_t* seg_idx, float* seg_act) {
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
@@ -148,7 +149,7 @@ __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int
     const uint64_t m = __ballot(sel);
     const int rank = rank_in_mask(m);
     if (sel) {
-      const float a = on ? h - t : 0.f;
+      const float a = on ? gate_value(act, h - t) : 0.f;
       s_list[rank] = lane;
       s_act[rank] = a;
       seg_idx[row0 + rank] = row0 + lane;
@@ -179,14 +180,17 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ 
 // One segment: gate values, compaction, W_up dots of the selected neurons.
 // LOPA: the gate rows are B [d_ff][r] against z; otherwise W_gate [d_ff][d] against x.
 // DENSE: every neuron of the segment is selected (act = max(h - t, 0)).
-template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU>
+// FULL: the paper's full form (`form`): the activation value, SiLU on the W_up output and,
+// for LoPA, the fixed term G added to the gate before the compaction.
+template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU, bool FULL>
 __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__ x, const float* __restrict__ z,
                                                        const uint4* __restrict__ gate_w, int Cg, int lprg,
                                                        int lprg_log2, const uint4* __restrict__ w_up, int Cu,
                                                        int lpru, int lpru_log2, int d_ff, int nseg, float t,
                                                        int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                                        int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
-                                                       float* __restrict__ seg_zval, float* __restrict__ y, int d) {
+                                                       float* __restrict__ seg_zval, float* __restrict__ y, int d,
+                                                       Form form) {
   __shared__ float s_h[kSegMax];
   __shared__ int s_list[kSegMax];
   __shared__ float s_act[kSegMax];
@@ -200,7 +204,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
   auto gate_sink = [&](int k, float s) { s_h[k] = s; };
   auto gate_row = [&](int k) { return row0 + k; };
   auto up_row = [&](int e) { return row0 + s_list[e]; };
-  auto up_sink = [&](int e, float v) { seg_zval[row0 + e] = s_act[e] * v; };
+  auto up_sink = [&](int e, float v) { seg_zval[row0 + e] = s_act[e] * (FULL ? up_value(form.silu_up, v) : v); };
+  const int act = FULL ? form.act : 0;
 
   if constexpr (LOPA) {
     {
@@ -210,7 +215,13 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
                         gate_sink);
     }
     __syncthreads();
-    compact_segment(s_h, nrows, row0, seg, t, DENSE, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
+    if constexpr (FULL) {
+      if (form.g_idx) {  // LoPA's fixed term: h += G x
+        if ((int)threadIdx.x < nrows) s_h[threadIdx.x] += g_term(form, x, d, row0 + threadIdx.x);
+        __syncthreads();
+      }
+    }
+    compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
     float xr[CPLU][W::EPC];
     load_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
@@ -222,7 +233,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
     dot_rows<W, CPLU>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, xr, gate_row,
                       gate_sink);
     __syncthreads();
-    compact_segment(s_h, nrows, row0, seg, t, DENSE, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
+    compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
     dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   }
@@ -348,7 +359,7 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_generic(const float* __restri
   }
 }
 
-template <class W, bool LOPA, bool DENSE>
+template <class W, bool LOPA, bool DENSE, bool FULL>
 __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restrict__ x, const float* __restrict__ z,
                                                             const void* __restrict__ gate_w,
                                                             const void* __restrict__ w_up, int T, int d, int d_ff,
@@ -357,7 +368,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
                                                             int32_t* __restrict__ seg_count,
                                                             int32_t* __restrict__ seg_idx,
                                                             float* __restrict__ seg_act,
-                                                            float* __restrict__ seg_zval, float* __restrict__ y) {
+                                                            float* __restrict__ seg_zval, float* __restrict__ y,
+                                                            Form form) {
   __shared__ float s_h[kSegMax][kTokChunk];
   __shared__ int s_list[kSegMax];
   __shared__ int s_cnt;
@@ -380,6 +392,15 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
     }
   }
   __syncthreads();
+  if constexpr (FULL) {
+    if (form.g_idx) {  // LoPA's fixed term: h += G x
+      for (int o = threadIdx.x; o < nrows * T; o += kBlock) {
+        const int k = o / T, tau = o - k * T;
+        s_h[k][tau] += g_term(form, x + (size_t)tau * d, d, row0 + k);
+      }
+      __syncthreads();
+    }
+  }
 
   if (threadIdx.x < kWave) {
     const bool valid = lane < nrows;
@@ -394,7 +415,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
       seg_idx[row0 + rank] = row0 + lane;
       for (int tau = 0; tau < T; ++tau) {
         const float h = s_h[lane][tau];
-        const float a = h > t ? h - t : 0.f;
+        const float a = h > t ? (FULL ? gate_value(form.act, h - t) : h - t) : 0.f;
         s_h[lane][tau] = a;  // this lane owns row `lane`: overwrite h with the activation
         seg_act[(size_t)tau * slots + row0 + rank] = a;
       }
@@ -414,7 +435,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
       float s = 0.f;
       for (int j = lane; j < d; j += kWave) s = fmaf(welem(W{}, w_up, rowoff + j), x[(size_t)tau * d + j], s);
       s = wave_sum(s);
-      if (lane == 0) seg_zval[(size_t)tau * slots + row0 + e] = s_h[kr][tau] * s;
+      if (lane == 0) seg_zval[(size_t)tau * slots + row0 + e] = s_h[kr][tau] * (FULL ? up_value(form.silu_up, s) : s);
     }
   }
 }
@@ -530,42 +551,74 @@ bool fast_ok(const Shape& sh, Gate g) {
   return true;
 }
 
-template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU>
-hipError_t go_gate_up_t1(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
-                         float* y, hipStream_t s) {
+template <class W, bool LOPA, bool DENSE, bool FULL, int CPLG, int CPLU>
+hipError_t go_gate_up_t1(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up,
+                         float t, Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / W::EPC, Cg = LOPA ? sh.r / W::EPC : Cu;
   const int lpru = lanes_per_row(Cu, CPLU), lprg = lanes_per_row(Cg, CPLG);
-  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU>;
+  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU, FULL>;
   static int per_cu = 0;  // one cache per instantiation
   ws.nseg = resident_segments(kernel, &per_cu, sh.d_ff);
   return launch_gate_kernel(kernel, ws.nseg, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg, lprg,
                             ilog2(lprg), static_cast<const uint4*>(w_up), Cu, lpru, ilog2(lpru), sh.d_ff, ws.nseg, t,
-                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d);
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d, form);
 }
 
-template <class W, bool LOPA, bool DENSE>
-hipError_t gate_up_fast(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t, Workspace& ws,
-                        float* y, hipStream_t s) {
+template <class W, bool LOPA, bool DENSE, bool FULL>
+hipError_t gate_up_fast(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
+                        Workspace& ws, float* y, hipStream_t s) {
   const int cplu = cpl_for(sh.d / W::EPC);
   if constexpr (LOPA) {
     const int cplg = cpl_for(sh.r / W::EPC);
-    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, 8, 8>(sh, x, gate_w, w_up, t, ws, y, s);
-    if (cplg == 8 && cplu == 16) return go_gate_up_t1<W, true, DENSE, 8, 16>(sh, x, gate_w, w_up, t, ws, y, s);
-    if (cplg == 16 && cplu == 8) return go_gate_up_t1<W, true, DENSE, 16, 8>(sh, x, gate_w, w_up, t, ws, y, s);
-    return go_gate_up_t1<W, true, DENSE, 16, 16>(sh, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, FULL, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == 8 && cplu == 16)
+      return go_gate_up_t1<W, true, DENSE, FULL, 8, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == 16 && cplu == 8)
+      return go_gate_up_t1<W, true, DENSE, FULL, 16, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, true, DENSE, FULL, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
   } else {
-    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, 8, 8>(sh, x, gate_w, w_up, t, ws, y, s);
-    return go_gate_up_t1<W, false, DENSE, 16, 16>(sh, x, gate_w, w_up, t, ws, y, s);
+    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, FULL, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, false, DENSE, FULL, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
   }
 }
 
-template <class W, bool LOPA, bool DENSE>
-hipError_t gate_up_generic(const Shape& sh, const float* x, const void* gate_w, const void* w_up, float t,
-                           Workspace& ws, float* y, hipStream_t s) {
+template <class W, bool LOPA, bool DENSE, bool FULL>
+hipError_t gate_up_generic(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up,
+                           float t, Workspace& ws, float* y, hipStream_t s) {
   ws.nseg = (sh.d_ff + kSegGeneric - 1) / kSegGeneric;
-  return launch_gate_kernel(k_gate_up_generic<W, LOPA, DENSE>, ws.nseg, s, x, (const float*)ws.z, gate_w, w_up, sh.T,
-                            sh.d, sh.d_ff, sh.r, ws.nseg, t, ws.slots, ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act,
-                            ws.seg_zval, y);
+  return launch_gate_kernel(k_gate_up_generic<W, LOPA, DENSE, FULL>, ws.nseg, s, x, (const float*)ws.z, gate_w, w_up,
+                            sh.T, sh.d, sh.d_ff, sh.r, ws.nseg, t, ws.slots, ws.meta, ws.seg_count, ws.seg_idx,
+                            ws.seg_act, ws.seg_zval, y, f);
+}
+
+// RMSNorm on z (Section 3.3), one workgroup per token: the partial copies summed into
+// copy 0 and scaled by gain / sqrt(mean z^2 + eps); the other copies zeroed.
+__global__ __launch_bounds__(kBlock) void k_rms_norm(float* __restrict__ z, int parts, int tc, int r,
+                                                     const float* __restrict__ gain, float eps) {
+  __shared__ float s_part[kBlock / kWave];
+  const int tok = blockIdx.x;
+  auto zsum = [&](int k) {
+    float v = 0.f;
+    for (int p = 0; p < parts; ++p) v += z[((size_t)p * tc + tok) * r + k];
+    return v;
+  };
+  float ss = 0.f;
+  for (int k = threadIdx.x; k < r; k += kBlock) {
+    const float v = zsum(k);
+    ss = fmaf(v, v, ss);
+  }
+  ss = wave_sum(ss);
+  if (lane_id() == 0) s_part[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kBlock / kWave; ++w) tot += s_part[w];
+  const float inv = 1.f / sqrtf(tot / (float)r + eps);
+  for (int k = threadIdx.x; k < r; k += kBlock) {
+    const float v = zsum(k);
+    z[(size_t)tok * r + k] = v * inv * (gain ? gain[k] : 1.f);
+    for (int p = 1; p < parts; ++p) z[((size_t)p * tc + tok) * r + k] = 0.f;
+  }
 }
 
 template <class W>
@@ -624,17 +677,25 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
+hipError_t launch_rms_norm(float* z, int parts, int tc, int T, int r, const float* gain, float eps, hipStream_t s) {
+  k_rms_norm<<<T, kBlock, 0, s>>>(z, parts, tc, r, gain, eps);
+  return hipGetLastError();
+}
+
 hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
   return sh.wdt == 1 ? lopa_z<WBf16>(sh, x, lopa_a, ws, s) : lopa_z<WF32>(sh, x, lopa_a, ws, s);
 }
 
-hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, const void* gate_w, const void* w_up,
-                          float t, Workspace& ws, float* y, hipStream_t s) {
+hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x, const void* gate_w,
+                          const void* w_up, float t, Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
   const bool fast = fast_ok(sh, g);
-#define FFN_GU(W, L, D)                                                                     \
-  return fast ? gate_up_fast<W, L, D>(sh, x, gate_w, w_up, t, ws, y, s)                    \
-              : gate_up_generic<W, L, D>(sh, x, gate_w, w_up, t, ws, y, s)
+#define FFN_GU2(W, L, D, F)                                                                     \
+  return fast ? gate_up_fast<W, L, D, F>(sh, form, x, gate_w, w_up, t, ws, y, s)               \
+              : gate_up_generic<W, L, D, F>(sh, form, x, gate_w, w_up, t, ws, y, s)
+#define FFN_GU(W, L, D)                                                    \
+  return form.full() ? [&] { FFN_GU2(W, L, D, true); }()                  \
+                     : [&] { FFN_GU2(W, L, D, false); }()
   if (sh.wdt == 1) {
     if (lopa) {
       if (dense) FFN_GU(WBf16, true, true);
@@ -650,6 +711,7 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const float* x, c
   if (dense) FFN_GU(WF32, false, true);
   FFN_GU(WF32, false, false);
 #undef FFN_GU
+#undef FFN_GU2
 }
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,

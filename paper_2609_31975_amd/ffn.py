@@ -20,7 +20,17 @@ FFN_F32 = 0
 FFN_BF16 = 1
 
 STATUS = {0: "FFN_OK", -1: "FFN_ERR_NULL", -2: "FFN_ERR_SHAPE", -3: "FFN_ERR_DTYPE", -4: "FFN_ERR_ALIGN",
-          -5: "FFN_ERR_WORKSPACE", -6: "FFN_ERR_HIP"}
+          -5: "FFN_ERR_WORKSPACE", -6: "FFN_ERR_HIP", -7: "FFN_ERR_OPTION"}
+
+FFN_ACT_RELU = 0
+FFN_ACT_RSPLUS = 1
+
+
+class Options(ctypes.Structure):
+    """``ffn_options_t``: the paper's full FFN form (activation, SiLU on W_up, G, RMSNorm)."""
+    _fields_ = [("act", ctypes.c_int), ("silu_up", ctypes.c_int), ("g_idx", ctypes.c_void_p),
+                ("g_sign", ctypes.c_void_p), ("rms_norm", ctypes.c_int), ("rms_gain", ctypes.c_void_p),
+                ("rms_eps", ctypes.c_float)]
 
 
 class FFNError(RuntimeError):
@@ -44,8 +54,13 @@ def lib() -> ctypes.CDLL:
         L.ffn_workspace_bytes.argtypes = [i, i, i, i]
         std = [i, i, i, i, vp, vp, vp, vp, f, vp, vp, sz, vp]
         lop = [i, i, i, i, i, vp, vp, vp, vp, vp, f, vp, vp, sz, vp]
+        op = ctypes.POINTER(Options)
+        std_ex = std[:9] + [op] + std[9:]
+        lop_ex = lop[:11] + [op] + lop[11:]
         for name, args in (("ffn_dense_forward", std), ("ffn_sparse_forward", std),
-                           ("ffn_lopa_sparse_forward", lop), ("ffn_lopa_dense_forward", lop)):
+                           ("ffn_lopa_sparse_forward", lop), ("ffn_lopa_dense_forward", lop),
+                           ("ffn_dense_forward_ex", std_ex), ("ffn_sparse_forward_ex", std_ex),
+                           ("ffn_lopa_sparse_forward_ex", lop_ex), ("ffn_lopa_dense_forward_ex", lop_ex)):
             getattr(L, name).restype = i
             getattr(L, name).argtypes = args
         L.ffn_active_set.restype = i
@@ -110,23 +125,35 @@ def alloc_workspace(T: int, d: int, d_ff: int, r: int = 0, device="cuda"):
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def _std_call(name, x, w_gate, w_up, w_down_t, t, y, ws, stream):
+def options(act=FFN_ACT_RELU, silu_up=False, g_idx=None, g_sign=None, rms_norm=False, rms_gain=None,
+            rms_eps=0.0) -> Options:
+    """Build an ``ffn_options_t``; g_idx (int32), g_sign (int8) and rms_gain (float32) are
+    device tensors or None.  The tensors must outlive the call's work on its stream."""
+    return Options(int(act), 1 if silu_up else 0, _dev(g_idx, "g_idx"), _dev(g_sign, "g_sign"),
+                   1 if rms_norm else 0, _dev(rms_gain, "rms_gain"), float(rms_eps))
+
+
+def _opt(opt):
+    return None if opt is None else ctypes.byref(opt)
+
+
+def _std_call(name, x, w_gate, w_up, w_down_t, t, y, ws, stream, opt=()):
     T, d = x.shape
     d_ff = w_up.shape[0]
     rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, _dev(x, "x"), _dev(w_gate, "w_gate"),
-                              _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t), _dev(y, "y"),
-                              _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+                              _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t), *opt,
+                              _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
     _check(name, rc)
     return y
 
 
-def _lopa_call(name, x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream):
+def _lopa_call(name, x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream, opt=()):
     T, d = x.shape
     d_ff, r = lopa_b.shape
     rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, r, _dev(x, "x"), _dev(lopa_a, "lopa_a"),
                               _dev(lopa_b, "lopa_b"), _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"),
-                              ctypes.c_float(t), _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(),
-                              _stream(stream))
+                              ctypes.c_float(t), *opt, _dev(y, "y"), _dev(ws, "ws"),
+                              ws.numel() * ws.element_size(), _stream(stream))
     _check(name, rc)
     return y
 
@@ -146,6 +173,24 @@ def ffn_lopa_sparse_forward(x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream=
 
 def ffn_lopa_dense_forward(x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream=None):
     return _lopa_call("ffn_lopa_dense_forward", x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream)
+
+
+def ffn_dense_forward_ex(x, w_gate, w_up, w_down_t, t, opt, y, ws, stream=None):
+    return _std_call("ffn_dense_forward_ex", x, w_gate, w_up, w_down_t, t, y, ws, stream, (_opt(opt),))
+
+
+def ffn_sparse_forward_ex(x, w_gate, w_up, w_down_t, t, opt, y, ws, stream=None):
+    return _std_call("ffn_sparse_forward_ex", x, w_gate, w_up, w_down_t, t, y, ws, stream, (_opt(opt),))
+
+
+def ffn_lopa_sparse_forward_ex(x, lopa_a, lopa_b, w_up, w_down_t, t, opt, y, ws, stream=None):
+    return _lopa_call("ffn_lopa_sparse_forward_ex", x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream,
+                      (_opt(opt),))
+
+
+def ffn_lopa_dense_forward_ex(x, lopa_a, lopa_b, w_up, w_down_t, t, opt, y, ws, stream=None):
+    return _lopa_call("ffn_lopa_dense_forward_ex", x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream,
+                      (_opt(opt),))
 
 
 def ffn_active_set(ws, T, d, d_ff, r=0, stream=None, with_act=True):

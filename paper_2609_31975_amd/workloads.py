@@ -17,6 +17,11 @@ Recipe (per weight set, ``seed``):
     W_down^T [d_ff, d]   N(0, 1/d_ff)    (row i = output vector of neuron i)
 With these scales every gate pre-activation is close to N(0, 1), so the threshold
 t = Phi^-1(s) gives sparsity s: 0, 0.8416, 1.2816, 1.6449 for 50/80/90/95%.
+The full FFN form (LoPA's fixed term G, RMSNorm between the factors) takes its extra
+inputs from ``make_form``: G's column per row uniform over [0, d), its sign +1 or -1
+with equal odds, and RMSNorm gains N(1, 0.25^2).  With G the gate pre-activation is
+close to N(0, 2) (B z and x[g_idx[i]] each contribute variance 1; after RMSNorm z has
+unit mean square), so the thresholds above scale by sqrt(2).
 The paper timed trained checkpoints, which are not available; these Gaussian
 weights reproduce the sparsity level but not the correlation of real masks, so
 the batched union here is the iid worst case.
@@ -100,6 +105,22 @@ def make_inputs(seed: int, T: int, d: int, d_ff: int, *, r: int = 0, wdt: int = 
     w_down_t = _encode(_normal(s_d, (d_ff, d), d_ff ** -0.5), wdt)
     return FFNInputs(x=x, w_up=w_up, w_down_t=w_down_t, w_gate=w_gate, lopa_a=lopa_a, lopa_b=lopa_b,
                      wdt=wdt, meta=dict(seed=seed))
+
+
+@dataclass
+class FormInputs:
+    g_idx: np.ndarray      # [d_ff] int32, G's column per row, in [0, d)
+    g_sign: np.ndarray     # [d_ff] int8, G's value per row, +1 or -1
+    rms_gain: np.ndarray   # [r] float32 RMSNorm gains
+
+
+def make_form(seed: int, d: int, d_ff: int, r: int) -> FormInputs:
+    """The extra inputs of the full form, from a stream of their own."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0xF0F1])))
+    g_idx = rng.integers(0, d, size=d_ff, dtype=np.int32)
+    g_sign = np.where(rng.random(d_ff) < 0.5, -1, 1).astype(np.int8)
+    rms_gain = (np.float32(1.0) + _normal(rng, (max(r, 0),), 0.25)).astype(np.float32)
+    return FormInputs(g_idx=g_idx, g_sign=g_sign, rms_gain=rms_gain)
 
 
 def make_tokens(seed: int, T: int, d: int) -> np.ndarray:

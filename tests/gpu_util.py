@@ -65,9 +65,59 @@ def run_gpu(dev: DevInputs, t: float, dense: bool = False, x=None):
     return y.cpu().numpy(), idx, act, ws
 
 
-def run_oracle(inp: wl.FFNInputs, t: float, dense: bool = False, x=None):
+class Form:
+    """A full-form option set: numpy inputs for the oracle, device tensors for the library."""
+
+    def __init__(self, act=0, silu_up=False, form: wl.FormInputs | None = None, use_g=False, rms_norm=False,
+                 use_gain=False, rms_eps=1e-6):
+        self.act, self.silu_up, self.rms_norm, self.rms_eps = act, silu_up, rms_norm, rms_eps
+        self.g_idx = form.g_idx if use_g else None
+        self.g_sign = form.g_sign if use_g else None
+        self.rms_gain = form.rms_gain if use_gain else None
+        self._dev = None
+
+    def oracle_kw(self):
+        return dict(act=self.act, silu_up=self.silu_up, g_idx=self.g_idx, g_sign=self.g_sign,
+                    rms_norm=self.rms_norm, rms_gain=self.rms_gain, rms_eps=self.rms_eps)
+
+    def options(self):
+        if self._dev is None:
+            self._dev = [to_dev(self.g_idx), to_dev(self.g_sign), to_dev(self.rms_gain)]
+        g_idx, g_sign, gain = self._dev
+        return ffn.options(act=self.act, silu_up=self.silu_up, g_idx=g_idx, g_sign=g_sign,
+                           rms_norm=self.rms_norm, rms_gain=gain, rms_eps=self.rms_eps if self.rms_norm else 0.0)
+
+    def act_value(self, u):
+        """The activation value of an active neuron, u = h - t > 0, in fp64."""
+        return u / (1.0 + np.exp(-u)) if self.act == 1 else u
+
+
+def run_gpu_ex(dev: DevInputs, t: float, form: Form, dense: bool = False):
+    """Run the matching ``_ex`` entry point; returns (y, idx, act, ws) like ``run_gpu``."""
+    tch = torch()
+    inp = dev.inp
+    T, d = dev.x.shape
+    ws = ffn.alloc_workspace(T, d, inp.d_ff, inp.r)
+    y = tch.full((T, d), float("nan"), dtype=tch.float32, device="cuda")
+    opt = form.options()
+    if inp.r:
+        fn = ffn.ffn_lopa_dense_forward_ex if dense else ffn.ffn_lopa_sparse_forward_ex
+        fn(dev.x, dev.lopa_a, dev.lopa_b, dev.w_up, dev.w_down_t, t, opt, y, ws)
+    else:
+        fn = ffn.ffn_dense_forward_ex if dense else ffn.ffn_sparse_forward_ex
+        fn(dev.x, dev.w_gate, dev.w_up, dev.w_down_t, t, opt, y, ws)
+    tch.cuda.synchronize()
+    idx, act = (None, None)
+    if T <= 64:
+        idx, act = ffn.ffn_active_set(ws, T, d, inp.d_ff, inp.r)
+    return y.cpu().numpy(), idx, act, ws
+
+
+def run_oracle(inp: wl.FFNInputs, t: float, dense: bool = False, x=None, form: Form | None = None):
     x = inp.x if x is None else x
     kw = dict(w_gate=inp.w_gate) if inp.r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    if form is not None:
+        kw.update(form.oracle_kw())
     return ffn_oracle.ffn(x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=inp.wdt, skip_inactive=not dense, **kw)
 
 
@@ -79,7 +129,7 @@ def rel_err(y, y_ref):
     return float(np.linalg.norm(np.asarray(y, np.float64) - y_ref) / nrm)
 
 
-def check_parity(res, y, idx, act, t, wdt, dense=False, what=""):
+def check_parity(res, y, idx, act, t, wdt, dense=False, what="", act_value=None):
     """Assert the parity rule; returns a dict of figures for reporting."""
     T, d_ff = res.h.shape
     tol = TOL[wdt]
@@ -107,10 +157,12 @@ def check_parity(res, y, idx, act, t, wdt, dense=False, what=""):
         assert not bad.any(), f"{what}: token {tau} active-set mismatch outside the band at {np.flatnonzero(bad)[:10]}"
         out["band_flips"] += int((on != ref).sum())
         out["n_active"].append(int(on.sum()))
-        # the activation values themselves: h - t within fp32 gate accuracy
+        # the activation values themselves: h - t (or its activation) within fp32 gate accuracy
         ok = on & ref
         if ok.any():
             ref_act = h[tau][ok] - np.float64(np.float32(t))
+            if act_value is not None:
+                ref_act = act_value(ref_act)
             got = np.zeros(d_ff)
             got[idx] = act[tau]
             assert np.allclose(got[ok], ref_act, rtol=1e-4, atol=1e-4), f"{what}: activation values differ"

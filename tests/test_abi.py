@@ -85,6 +85,47 @@ def test_lopa_argument_errors(fn):
     assert _lopa(fn, ws_bytes=ffn.workspace_bytes(1, 64, 128, 8) - 256) == -5
 
 
+def _opt(**kw):
+    return ctypes.byref(ffn.Options(**kw))
+
+
+def _std_ex(opt, fn="ffn_sparse_forward_ex", ws_bytes=1 << 30):
+    return getattr(L, fn)(1, 1, 64, 128, A, A, A, A, ctypes.c_float(0.5), opt, A, A, ws_bytes, None)
+
+
+def _lopa_ex(opt, fn="ffn_lopa_sparse_forward_ex", ws_bytes=1 << 30):
+    return getattr(L, fn)(1, 1, 64, 128, 8, A, A, A, A, A, ctypes.c_float(0.5), opt, A, A, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kind", ["sparse", "dense"])
+def test_option_errors(kind):
+    std = "ffn_sparse_forward_ex" if kind == "sparse" else "ffn_dense_forward_ex"
+    lop = "ffn_lopa_sparse_forward_ex" if kind == "sparse" else "ffn_lopa_dense_forward_ex"
+    small = ffn.workspace_bytes(1, 64, 128, 8) - 256
+    # a valid option set reaches the workspace check (no launch: the workspace is short)
+    assert _lopa_ex(_opt(act=1, silu_up=1, g_idx=A, g_sign=A, rms_norm=1, rms_gain=A, rms_eps=1e-6), lop,
+                    small) == -5
+    assert _lopa_ex(None, lop, small) == -5
+    assert _std_ex(_opt(act=1, silu_up=1), std, ffn.workspace_bytes(1, 64, 128, 0) - 1) == -5
+    # invalid option values
+    assert _std_ex(_opt(act=2), std) == -7
+    assert _std_ex(_opt(act=-1), std) == -7
+    assert _std_ex(_opt(silu_up=2), std) == -7
+    assert _lopa_ex(_opt(rms_norm=2, rms_eps=1e-6), lop) == -7
+    assert _lopa_ex(_opt(g_idx=A), lop) == -7                       # g_sign missing
+    assert _lopa_ex(_opt(g_sign=A), lop) == -7                      # g_idx missing
+    assert _std_ex(_opt(g_idx=A, g_sign=A), std) == -7              # G belongs to LoPA
+    assert _std_ex(_opt(rms_norm=1, rms_eps=1e-6), std) == -7       # so does the norm
+    assert _lopa_ex(_opt(rms_norm=1, rms_eps=0.0), lop) == -7
+    assert _lopa_ex(_opt(rms_norm=1, rms_eps=-1.0), lop) == -7
+    assert _lopa_ex(_opt(rms_norm=1, rms_eps=float("nan")), lop) == -7
+    assert _lopa_ex(_opt(rms_norm=1, rms_eps=float("inf")), lop) == -7
+    assert _lopa_ex(_opt(rms_gain=A), lop) == -7                    # gain without the norm
+    # alignment of the option arrays
+    assert _lopa_ex(_opt(g_idx=A + 2, g_sign=A + 1), lop) == -4
+    assert _lopa_ex(_opt(rms_norm=1, rms_gain=A + 1, rms_eps=1e-6), lop) == -4
+
+
 def test_active_set_argument_errors():
     n = ctypes.c_int32()
     assert L.ffn_active_set(None, 1, 64, 128, 0, ctypes.byref(n), A, None, None) == -1

@@ -1,0 +1,111 @@
+"""GPU parity of the paper's full FFN form (the ``_ex`` entry points) against the oracle:
+the R-S+ activation value, SiLU on the W_up output (the double activation of
+Section 3.3), LoPA's fixed term G and RMSNorm between the LoPA factors (Section 3.3,
+Eq. (lopaapprox)).  Every kernel family runs: the single-token kernels, the
+element-wise kernels (odd d or r), and the matrix-core batch path at one, two and
+four token tiles, with and without pre-split tokens.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2609_31975_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16 = wl.F32, wl.BF16
+S2 = math.sqrt(2.0)   # G adds a unit-variance term to the gate
+
+
+@pytest.fixture(scope="module")
+def gu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from tests import gpu_util
+    return gpu_util
+
+
+ACT = dict(act=1, silu_up=True)                                  # activations only
+ALL = dict(act=1, silu_up=True, use_g=True, rms_norm=True, use_gain=True)
+G_ONLY = dict(use_g=True)
+NORM_ONLY = dict(rms_norm=True)
+
+# name, T, d, d_ff, r, wdt, t, form flags
+CASES = [
+    ("t1_std_bf16_act", 1, 264, 1000, 0, BF16, 1.0, ACT),
+    ("t1_std_f32_rsplus", 1, 260, 999, 0, F32, 0.8, dict(act=1)),
+    ("t1_std_bf16_silu_d4096", 1, 4096, 2056, 0, BF16, 1.2816, dict(silu_up=True)),
+    ("t1_lopa_bf16_all", 1, 264, 1000, 40, BF16, 1.0 * S2, ALL),
+    ("t1_lopa_bf16_g", 1, 264, 1000, 40, BF16, 1.0 * S2, G_ONLY),
+    ("t1_lopa_bf16_norm", 1, 264, 1000, 40, BF16, 1.0, NORM_ONLY),
+    ("t1_lopa_f32_all", 1, 256, 1024, 32, F32, 1.2816 * S2, ALL),
+    ("gen_std_bf16_odd_d", 1, 100, 77, 0, BF16, 0.5, ACT),
+    ("gen_lopa_bf16_odd_r_T3", 3, 264, 1000, 36, BF16, 1.0 * S2, ALL),
+    ("gen_lopa_f32_r1_T2", 2, 16, 40, 1, F32, 0.1, ALL),
+    ("gen_std_f32_T70", 70, 64, 200, 0, F32, 1.0, ACT),
+    ("mc_std_bf16_T2", 2, 264, 1000, 0, BF16, 1.0, ACT),
+    ("mc_std_bf16_T12", 12, 264, 1000, 0, BF16, 1.2, ACT),
+    ("mc_lopa_bf16_T4_all", 4, 264, 1000, 40, BF16, 1.2 * S2, ALL),
+    ("mc_lopa_bf16_T8_norm", 8, 264, 1000, 40, BF16, 1.2, NORM_ONLY),
+    ("mc_lopa_bf16_T20_all", 20, 264, 1000, 40, BF16, 1.3 * S2, ALL),
+    ("mc_std_bf16_T40", 40, 136, 300, 0, BF16, 1.5, ACT),
+    ("mc_lopa_bf16_T64_all", 64, 264, 1000, 40, BF16, 1.6 * S2, ALL),
+    ("mc_lopa_bf16_T70_g", 70, 264, 1000, 40, BF16, 1.3 * S2, dict(act=1, use_g=True)),
+]
+
+
+def _form(gu, inp, flags):
+    return gu.Form(form=wl.make_form(7, inp.d, inp.d_ff, inp.r), **flags)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+@pytest.mark.parametrize("dense", [False, True], ids=["sparse", "dense"])
+def test_full_form_small(gu, case, dense):
+    name, T, d, d_ff, r, wdt, t, flags = case
+    inp = wl.make_inputs(201, T, d, d_ff, r=r, wdt=wdt)
+    form = _form(gu, inp, flags)
+    y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(inp), t, form, dense=dense)
+    res = gu.run_oracle(inp, t, dense=dense, form=form)
+    fig = gu.check_parity(res, y, idx, act, t, wdt, dense=dense, what=name, act_value=form.act_value)
+    if not dense and idx is not None:
+        assert 0 < fig["n_union"] < d_ff or T > 8, f"{name}: degenerate active set"
+
+
+def test_default_options_match_plain_calls(gu):
+    """A zero-filled option struct is the default form: same result as the plain call."""
+    for T, r in ((1, 0), (1, 40), (16, 40), (40, 0)):
+        inp = wl.make_inputs(202, T, 264, 1000, r=r, wdt=BF16)
+        dev = gu.DevInputs(inp)
+        y0, idx0, _, _ = gu.run_gpu(dev, 1.0)
+        y1, idx1, _, _ = gu.run_gpu_ex(dev, 1.0, gu.Form())
+        assert np.array_equal(idx0, idx1)
+        assert gu.rel_err(y1, y0) < 1e-6   # only the order of atomic additions differs
+
+
+def test_same_active_set_for_either_activation(gu):
+    """R-S+ and ReLU keep the same neurons (h > t); only their values differ."""
+    inp = wl.make_inputs(203, 4, 264, 1000, r=40, wdt=BF16)
+    dev = gu.DevInputs(inp)
+    fi = wl.make_form(7, inp.d, inp.d_ff, inp.r)
+    _, i0, a0, _ = gu.run_gpu_ex(dev, 1.3, gu.Form(form=fi, use_g=True))
+    _, i1, a1, _ = gu.run_gpu_ex(dev, 1.3, gu.Form(act=1, form=fi, use_g=True))
+    assert np.array_equal(i0, i1)
+    assert np.array_equal(a0 > 0, a1 > 0)
+    on = a0 > 0
+    np.testing.assert_allclose(a1[on], a0[on] / (1.0 + np.exp(-a0[on].astype(np.float64))), rtol=1e-5)
+
+
+# ---------------------------------------------------------------- full size: the 8B LoPA shape
+@pytest.mark.parametrize("T", [1, 16], ids=["T1", "T16"])
+def test_full_form_8b_lopa(gu, T):
+    d, d_ff, r = 4096, 14336, 512
+    inp = wl.make_inputs(1512, T, d, d_ff, r=r, wdt=BF16)
+    form = _form(gu, inp, ALL)
+    t = wl.THRESHOLD[0.90] * S2
+    y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(inp), t, form)
+    res = gu.run_oracle(inp, t, form=form)
+    fig = gu.check_parity(res, y, idx, act, t, BF16, what=f"8b lopa full T{T}", act_value=form.act_value)
+    frac = np.mean(fig["n_active"]) / d_ff
+    assert 0.05 < frac < 0.15, f"activation fraction {frac:.3f} far from the 10% the threshold targets"
+    print(f"8b lopa full form T{T}", fig["max_rel_err"], fig["n_union"], frac, flush=True)
