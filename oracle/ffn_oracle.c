@@ -25,6 +25,11 @@
  *     Optionally (Section 3.3, "LoPA in practice") an RMSNorm sits between the
  *     two factors: h = G x + U RMSNorm(V x), RMSNorm(z)_k = gain_k z_k /
  *     sqrt(mean_k z_k^2 + eps) over the r components.
+ *   Zeros of the gated intermediate (the s_gated site of Table ffn-sparsity-sites,
+ *     appendix on baseline details): a neuron whose value A(h) * v is exactly zero
+ *     adds nothing, so the sparse method skips its column of W2 as well.  With the
+ *     shifted ReLU or R-S+ on the gate and v or SiLU(v) on W3 this happens only
+ *     where v is exactly zero.
  *   Activation variants (Section 3.1 "R-S+ activation"; Section 3.3 "Double
  *     activation"): act = 1 replaces the shifted ReLU by the shifted R-S+,
  *     A(h) = (h - t) sigma(h - t) for h > t and 0 otherwise (sigma the logistic
@@ -159,6 +164,7 @@ int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff
       double v = row_dot(w_up, wdt, (size_t)i, d, xv, &macs); /* (W3 x)_i */
       if (silu_up) v = v * logistic(v);
       double zi = a * v;
+      if (skip_inactive && zi == 0.0) continue; /* s_gated: column i of W2 is not needed */
       /* y += zi * (column i of W2) = zi * w_down_t[i][:] */
       for (int j = 0; j < d; ++j) {
         double wd = weight_at(w_down_t, wdt, (size_t)i * d + (size_t)j);

@@ -147,6 +147,36 @@ def test_sparse_never_reads_inactive_rows(wdt):
 
 
 @pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("silu_up", [False, True])
+def test_zero_gated_value_skips_w2_row(wdt, silu_up):
+    """An active neuron whose W3 row is zero has gated value 0 (the s_gated site): its W2
+    column is not read (NaN there leaves y unchanged) and its d multiply-adds are not counted;
+    the dense baseline reads it."""
+    inp = wl.make_inputs(13, 1, 32, 96, wdt=wdt)
+    t = 0.5
+    clean = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=wdt,
+                           silu_up=silu_up)
+    on = np.flatnonzero(clean.active[0])
+    zero = on[::3]
+    assert len(zero) >= 3
+    up, dn = inp.w_up.copy(), inp.w_down_t.copy()
+    up[zero] = 0
+    ref = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=up, w_down_t=dn, t=t, wdt=wdt, silu_up=silu_up)
+    dn[zero] = np.float32(np.nan) if wdt == wl.F32 else np.uint16(0x7FC0)
+    pois = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=up, w_down_t=dn, t=t, wdt=wdt, silu_up=silu_up)
+    assert np.isfinite(pois.y).all() and np.array_equal(pois.y, ref.y)
+    assert pois.macs[0] == clean.macs[0] - 32 * len(zero)
+    # the same output as removing those neurons' W2 columns by hand (they carry zero weight)
+    dn0 = inp.w_down_t.copy()
+    dn0[zero] = 0
+    hand = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=dn0, t=t, wdt=wdt, silu_up=silu_up)
+    assert np.allclose(pois.y, hand.y, rtol=1e-12, atol=1e-12)
+    dense = ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=up, w_down_t=dn, t=t, wdt=wdt, silu_up=silu_up,
+                           skip_inactive=False)
+    assert np.isnan(dense.y).all()
+
+
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
 def test_lopa_with_identity_factor_is_standard_gating(wdt):
     """LoPA with r = d, A = I and B = W_gate is standard gating, bit for bit (Eq. lopaapprox with G = 0)."""
     inp = wl.make_inputs(13, 2, 48, 120, wdt=wdt)
