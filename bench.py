@@ -121,11 +121,14 @@ def gate_kernel_bytes(d, d_ff, r, T, n_union, dense):
 class Runner:
     """Enqueues step i of a workload: weight set i % n_sets, token batch (i // n_sets) % batches."""
 
-    def __init__(self, shape: Shape, r, T, t, dense):
+    def __init__(self, shape: Shape, r, T, t, dense, form=None):
         import torch
         from paper_2609_31975_amd import ffn
         self.ffn, self.torch = ffn, torch
         self.s, self.r, self.T, self.t, self.dense = shape, r, T, t, dense
+        # the full form: option arrays on the device, held for the runner's lifetime
+        self.form = form
+        self.opt = None if form is None else ffn.options(**form)
         self.batches = shape.pool // T
         self.ws = ffn.alloc_workspace(T, shape.d, shape.d_ff, r)
         self.y = torch.empty((T, shape.d), dtype=torch.float32, device="cuda")
@@ -139,7 +142,11 @@ class Runner:
     def __call__(self, i):
         s, f = self.s, self.ffn
         k, x = self.args(i)
-        if self.r:
+        if self.opt is not None:
+            a, b = s.lopa[self.r][k]
+            fn = f.ffn_lopa_dense_forward_ex if self.dense else f.ffn_lopa_sparse_forward_ex
+            fn(x, a, b, s.up[k], s.down[k], self.t, self.opt, self.y, self.ws)
+        elif self.r:
             a, b = s.lopa[self.r][k]
             fn = f.ffn_lopa_dense_forward if self.dense else f.ffn_lopa_sparse_forward
             fn(x, a, b, s.up[k], s.down[k], self.t, self.y, self.ws)
@@ -228,8 +235,8 @@ def steps_for(run: Runner, K: int, budget_s: float = 1.0) -> int:
     return int(max(10, min(K, budget_s / max(dt, 1e-7))))
 
 
-def measure(shape, r, T, t, K, W, dense_us=None, name="", exact=False):
-    sp = Runner(shape, r, T, t, dense=False)
+def measure(shape, r, T, t, K, W, dense_us=None, name="", exact=False, form=None):
+    sp = Runner(shape, r, T, t, dense=False, form=form)
     if not exact:
         K = steps_for(sp, K)
         W = min(W, K)
@@ -247,8 +254,18 @@ def measure(shape, r, T, t, K, W, dense_us=None, name="", exact=False):
     return rec, sp, n
 
 
-def dense_time(shape, r, T, K, W, exact=False):
-    de = Runner(shape, r, T, 1.2816, dense=True)
+def full_form(shape: Shape, r, seed):
+    """Device option arrays of the full form (R-S+, SiLU on W_up, G, RMSNorm) for rank r."""
+    import torch
+    from paper_2609_31975_amd import workloads as wl
+    fi = wl.make_form(seed, shape.d, shape.d_ff, r)
+    dev = lambda a: torch.from_numpy(a).to("cuda")  # noqa: E731
+    return dict(act=1, silu_up=True, g_idx=dev(fi.g_idx), g_sign=dev(fi.g_sign), rms_norm=True,
+                rms_gain=dev(fi.rms_gain), rms_eps=1e-6)
+
+
+def dense_time(shape, r, T, K, W, exact=False, form=None):
+    de = Runner(shape, r, T, 1.2816, dense=True, form=form)
     if not exact:
         K = steps_for(de, K)
         W = min(W, K)
@@ -286,7 +303,7 @@ def cpu_baseline(inp, seed, pool, r, t, seconds):
                 host_cores_visible=len(os.sched_getaffinity(0)))
 
 
-def parity_sample(shape: Shape, r, T, t):
+def parity_sample(shape: Shape, r, T, t, form=None, form_seed=None):
     """Step 0 of the timed workload (weight set 0, its first T tokens, the same call and
     launch configuration): relative error of every token's output against the oracle,
     and the active union against the union of the oracle's per-token active sets (a
@@ -294,13 +311,18 @@ def parity_sample(shape: Shape, r, T, t):
     import torch
     from oracle import ffn_oracle
     from paper_2609_31975_amd import ffn
+    from paper_2609_31975_amd import workloads as wl
     inp = shape.host0[r]
-    run = Runner(shape, r, T, t, dense=False)
+    run = Runner(shape, r, T, t, dense=False, form=form)
     run(0)
     torch.cuda.synchronize()
     y = run.y.cpu().numpy().astype(np.float64)
     x = run.args(0)[1].cpu().numpy()
     kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    if form is not None:
+        fi = wl.make_form(form_seed, shape.d, shape.d_ff, r)
+        kw.update(act=form["act"], silu_up=form["silu_up"], g_idx=fi.g_idx, g_sign=fi.g_sign,
+                  rms_norm=form["rms_norm"], rms_gain=fi.rms_gain, rms_eps=form["rms_eps"])
     res = ffn_oracle.ffn(x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=inp.wdt, **kw)
     idx, _ = ffn.ffn_active_set(run.ws, T, shape.d, shape.d_ff, r, with_act=False)
     ref = np.flatnonzero(res.active.any(0))
@@ -391,11 +413,12 @@ def main():
     sh = get_shape(head.d, head.d_ff, ranks, max(n_sets, lopa_sets if not args.no_sweep else n_sets), head.seed,
                    pool=max(64, 4 * 64))
     log(f"[bench] headline {head.name}: {sh.n_sets} sets, K={K}, W={W}")
+    hform = full_form(sh, r0, head.seed) if head.form == "full" else None
     dense_us, dense_rec = dense_time(sh, 0, T0, K, W, exact=True)
-    rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True)
+    rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True, form=hform)
     gate_mean, gate_med = time_gate_kernel(run, K)
     gbytes = np.mean([gate_kernel_bytes(head.d, head.d_ff, r0, T0, k, False) for k in nlist])
-    par = parity_sample(sh, r0, T0, head.t)
+    par = parity_sample(sh, r0, T0, head.t, form=hform, form_seed=head.seed)
     traffic, traffic_src = recorded_traffic(head.name)
     log(f"[bench] headline {rec['us_per_call']} us/call, dense {dense_us:.2f}, gate kernel {gate_mean:.2f} us, "
         f"parity {par}")
@@ -439,14 +462,20 @@ def main():
         for w in wl.workloads():
             if w.name == head.name or w.d != head.d or w.name.startswith("tiny"):
                 continue
-            rw = measure(sh, w.r, w.T, w.t, K, W, name=w.name)[0]
+            form = full_form(sh, w.r, w.seed) if w.form == "full" else None
+            rw = measure(sh, w.r, w.T, w.t, K, W, name=w.name, form=form)[0]
+            if form is not None:
+                rw["form"] = "full: R-S+ activation, SiLU on W_up, G term, RMSNorm between A and B"
+                base = [q for q in sweep if q.get("workload") == f"8b_lopa512_s90_T{w.T}"]
+                if base:
+                    rw["default_form_us_per_call"] = base[0]["us_per_call"]
             du = dense_us if w.T == T0 else None
             if w.T != T0:
                 du, _ = dense_time(sh, 0, w.T, K, W)
             rw["dense_us_per_call"] = round(du, 3)
             rw["speedup_vs_dense"] = round(du / rw["us_per_call"], 3)
             if w.r:
-                ldu, lrec = dense_time(sh, w.r, w.T, K, W)
+                ldu, lrec = dense_time(sh, w.r, w.T, K, W, form=form)
                 rw["lopa_dense_us_per_call"] = round(ldu, 3)
                 rw["speedup_vs_lopa_dense"] = round(ldu / rw["us_per_call"], 3)
             rw["path"] = "sparse"

@@ -41,6 +41,8 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
   w.seg_zval = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
   const size_t bt = w.tc >= 2 ? (size_t)w.tc : 0;  // matrix-core path only
   w.z = reinterpret_cast<float*>(take(sizeof(float) * (bt ? 2 : 1) * (size_t)w.tc * (r > 0 ? r : 1)));
+  w.zsq = reinterpret_cast<float*>(take(sizeof(float) * (size_t)(r > 0 ? r : 1)));
+  w.gx = reinterpret_cast<float*>(take(sizeof(float) * (r > 0 ? (size_t)w.tc * d_ff : 1)));
   w.zf = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * ((bt + 15) / 16) * 2 * kWave * (size_t)batched_segments(d_ff)));
   const size_t xs_frags = bt >= (size_t)kPreSplitMin ? (size_t)((d + 31) / 32) * ((bt + 15) / 16) * kWave : 0;
   w.xs = reinterpret_cast<uint4*>(take(sizeof(uint4) * 2 * xs_frags));
@@ -82,10 +84,8 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 
 // Checks ffn_options_t (see the header) and splits it into the gate kernels' Form and the
 // norm's gain and eps (eps 0: no norm).
-int check_options(const ffn_options_t* o, bool lopa, Form* form, const float** gain, float* eps) {
+int check_options(const ffn_options_t* o, bool lopa, Form* form) {
   *form = Form{};
-  *gain = nullptr;
-  *eps = 0.f;
   if (!o) return FFN_OK;
   if ((o->act != FFN_ACT_RELU && o->act != FFN_ACT_RSPLUS) || (o->silu_up != 0 && o->silu_up != 1) ||
       (o->rms_norm != 0 && o->rms_norm != 1))
@@ -99,8 +99,8 @@ int check_options(const ffn_options_t* o, bool lopa, Form* form, const float** g
   form->g_idx = o->g_idx;
   form->g_sign = o->g_sign;
   if (o->rms_norm) {
-    *gain = o->rms_gain;
-    *eps = o->rms_eps;
+    form->rms_gain = o->rms_gain;
+    form->rms_eps = o->rms_eps;
   }
   return FFN_OK;
 }
@@ -115,9 +115,7 @@ int run(const Call& c) {
       !aligned(c.ws) || (lopa && !aligned(c.lopa_a)))
     return FFN_ERR_ALIGN;
   Form form;
-  const float* gain;
-  float eps;
-  const int so = check_options(c.opt, lopa, &form, &gain, &eps);
+  const int so = check_options(c.opt, lopa, &form);
   if (so != FFN_OK) return so;
   Workspace ws;
   if (c.ws_bytes < workspace_layout(c.T, c.d, c.d_ff, c.r, c.ws, &ws)) return FFN_ERR_WORKSPACE;
@@ -130,11 +128,9 @@ int run(const Call& c) {
     const Gate g = lopa ? Gate::LoPA : Gate::Standard;
     hipError_t e = hipSuccess;
     if (batched_ok(sh, g)) {
-      e = launch_batched(sh, g, c.dense, form, gain, eps, x, c.lopa_a, c.gate, c.w_up, c.w_down_t, c.t, ws, y,
-                         c.stream);
+      e = launch_batched(sh, g, c.dense, form, x, c.lopa_a, c.gate, c.w_up, c.w_down_t, c.t, ws, y, c.stream);
     } else {
-      if (lopa) e = launch_lopa_z(sh, x, c.lopa_a, ws, c.stream);
-      if (e == hipSuccess && eps > 0.f) e = launch_rms_norm(ws.z, 1, ws.tc, sh.T, sh.r, gain, eps, c.stream);
+      if (lopa) e = launch_lopa_z(sh, form, x, c.lopa_a, ws, c.stream);
       if (e == hipSuccess) e = launch_gate_up(sh, g, c.dense, form, x, c.gate, c.w_up, c.t, ws, y, c.stream);
       if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
     }

@@ -298,7 +298,8 @@ template <int NT>
 __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __restrict__ x,
                                                                  const uint4* __restrict__ xs, int ntt,
                                                                  const uint4* __restrict__ A, int C, int T, int r,
-                                                                 int tc, float* __restrict__ zp) {
+                                                                 int tc, float* __restrict__ zp, GWork gw) {
+  if (g_precompute(gw)) return;
   constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   __shared__ f32x4_t s_part[kZWaves][NT][kWave];
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
@@ -346,16 +347,18 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 // read.
 // LOPA: the gate rows are B [d_ff][r] against z = zp[0] + zp[1]; otherwise W_gate x.
 // KU / KUU: k steps per load group of the gate rows / the W_up rows.
-// FULL: the paper's full form (`form`): the activation value, SiLU on the W_up output and,
-// for LoPA, the fixed term G added to the gate before the union.
-template <bool LOPA, bool DENSE, int NT, int KU, int KUU, bool FULL>
+// FORM (a FormKind): the paper's full form (`form`): the activation value, SiLU on the
+// W_up output and, with kFormLoPA, the fixed term G added to the gate before the union.
+template <bool LOPA, bool DENSE, int NT, int KU, int KUU, int FORM>
 __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const float* __restrict__ zp,
                                              const uint4* __restrict__ gate_w, int Cg, const uint4* __restrict__ w_up,
                                              int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,
                                              int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                              int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                              uint4* __restrict__ zf, float* __restrict__ y,
-                                             const uint4* __restrict__ xs, int ntt, Form form) {
+                                             const uint4* __restrict__ xs, int ntt, Form form,
+                                             const float* __restrict__ gx) {
+  constexpr bool FULL = FORM != kFormDefault, HAS_G = FORM == kFormLoPA;
   constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   // the W_up rows of a union of at most two row tiles go as two tiles with twice the k
   // steps a group (one token tile only: the register budget of wider ones is spent)
@@ -400,6 +403,21 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
         stream_rows<kTiles, NT, KU, 1, PRE>(gb, Cg, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
       }
     }
+    // LoPA's fixed term (G x) of the rows and tokens this lane thresholds, written by the z
+    // kernel's extra workgroups: loaded after the gate stream (no registers held across
+    // it), so that the wait falls after the LDS reduction
+    uint32_t gxb[HAS_G ? NT : 1][4] = {};
+    if constexpr (HAS_G) {
+      const Buf xb = make_buf(gx, 4u * (uint32_t)tc * (uint32_t)d_ff);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tok = 16 * nt + m, rl = 16 * wave + 4 * g + i;
+          gxb[nt][i] = ldb32(xb, tok < T && rl < nrows ? 4u * ((uint32_t)tok * (uint32_t)d_ff + (uint32_t)(row0 + rl))
+                                                        : kOOB);
+        }
+    }
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt)
 #pragma unroll
@@ -421,9 +439,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
         for (int nt = 0; nt < NT; ++nt) {
           const int tok = 16 * nt + m;
           float hv = h[nt][i];
-          if constexpr (FULL) {  // LoPA's fixed term: h += G x
-            if (form.g_idx && tok < T && rl < nrows) hv += g_term(form, x + (size_t)tok * d, d, row0 + rl);
-          }
+          if constexpr (HAS_G) hv += __builtin_bit_cast(float, gxb[nt][i]);  // h += G x
           const bool on = tok < T && hv > t;
           if (tok < T && rl < nrows) s_act[rl][tok] = on ? (FULL ? gate_value(form.act, hv - t) : hv - t) : 0.f;
           any |= on;
@@ -529,26 +545,26 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       const uint4 *__restrict__ w_up, int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,       \
       int32_t *__restrict__ meta, int32_t *__restrict__ seg_count, int32_t *__restrict__ seg_idx,                  \
       float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y, const uint4 *__restrict__ xs,  \
-      int ntt, Form form
+      int ntt, Form form, const float *__restrict__ gx
 #define FFN_GATE_UP_ARGS \
-  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt, form
+  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt, form, gx
 
 // One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
 // gate rows and for wider token tiles; one for LoPA's gate rows with four token tiles,
 // whose fragments carry both partial copies of z).
-template <bool LOPA, bool DENSE, int NT, bool FULL>
+template <bool LOPA, bool DENSE, int NT, int FORM>
 __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(FFN_GATE_UP_PARAMS) {
   constexpr int KU = NT == 1 ? (LOPA ? 2 : 4) : (LOPA && NT == 4 ? 1 : 2);
-  gate_up_body<LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2, FULL>(FFN_GATE_UP_ARGS);
+  gate_up_body<LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2, FORM>(FFN_GATE_UP_ARGS);
 }
 
 // Standard gating, one token tile: two k steps a group, so that two workgroups fit a CU
 // (at most 256 registers a lane); one workgroup's phase changes (LDS reductions, union)
 // then overlap the other's streaming.
-template <bool DENSE, bool FULL>
+template <bool DENSE, int FORM>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) void k_gate_up_mfma2(
     FFN_GATE_UP_PARAMS) {
-  gate_up_body<false, DENSE, 1, 2, 2, FULL>(FFN_GATE_UP_ARGS);
+  gate_up_body<false, DENSE, 1, 2, 2, FORM>(FFN_GATE_UP_ARGS);
 }
 #undef FFN_GATE_UP_PARAMS
 #undef FFN_GATE_UP_ARGS
@@ -814,10 +830,14 @@ hipError_t split_tokens(const Shape& sh, const float* x, const Workspace& ws, hi
   return hipGetLastError();
 }
 template <int NT>
-hipError_t z_mfma(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
+hipError_t z_mfma(const Shape& sh, const Form& form, const float* x, const void* lopa_a, const Workspace& ws,
+                  hipStream_t s) {
   const int C = sh.d / 8, grid = ((sh.r + 15) / 16) * kZParts;
-  k_lopa_z_mfma<NT><<<grid, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a),
-                                                      C, sh.T, sh.r, ws.tc, ws.z);
+  // with G, extra workgroups write G x for the gate kernel
+  const GWork gw{form, x, ws.gx, sh.T, sh.d, sh.d_ff, grid};
+  const int g = grid + (form.g_idx ? (g_items(sh.d_ff, sh.T) + kZWaves * kWave - 1) / (kZWaves * kWave) : 0);
+  k_lopa_z_mfma<NT><<<g, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a), C,
+                                                   sh.T, sh.r, ws.tc, ws.z, gw);
   return hipGetLastError();
 }
 
@@ -828,7 +848,7 @@ int segments_for(int d_ff, int grid) {
   return n > 128 ? (n + grid - 1) / grid * grid : n;
 }
 
-template <bool LOPA, bool DENSE, int NT, bool FULL>
+template <bool LOPA, bool DENSE, int NT, int FORM>
 hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up, float t,
                      Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
@@ -838,28 +858,32 @@ hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const vo
   const int g = ws.nseg < grid ? ws.nseg : grid;
   auto kernel = [&] {
     if constexpr (two)
-      return k_gate_up_mfma2<DENSE, FULL>;
+      return k_gate_up_mfma2<DENSE, FORM>;
     else
-      return k_gate_up_mfma<LOPA, DENSE, NT, FULL>;
+      return k_gate_up_mfma<LOPA, DENSE, NT, FORM>;
   }();
   return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                             static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
-                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form);
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form,
+                            (const float*)ws.gx);
 }
 
-template <bool LOPA, bool DENSE, bool FULL>
+template <bool LOPA, bool DENSE, int FORM>
 hipError_t gate_nt(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
                    Workspace& ws, float* y, hipStream_t s) {
-  if (sh.T <= 16) return gate_mfma<LOPA, DENSE, 1, FULL>(sh, f, x, gate_w, w_up, t, ws, y, s);
-  if (sh.T <= 32) return gate_mfma<LOPA, DENSE, 2, FULL>(sh, f, x, gate_w, w_up, t, ws, y, s);
-  return gate_mfma<LOPA, DENSE, 4, FULL>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  if (sh.T <= 16) return gate_mfma<LOPA, DENSE, 1, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  if (sh.T <= 32) return gate_mfma<LOPA, DENSE, 2, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  return gate_mfma<LOPA, DENSE, 4, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
 }
 
 template <bool LOPA, bool DENSE>
 hipError_t gate_form(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
                      Workspace& ws, float* y, hipStream_t s) {
-  return f.full() ? gate_nt<LOPA, DENSE, true>(sh, f, x, gate_w, w_up, t, ws, y, s)
-                  : gate_nt<LOPA, DENSE, false>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  // the norm runs before this kernel, so only G needs the LoPA form here
+  if constexpr (LOPA)
+    if (f.g_idx) return gate_nt<LOPA, DENSE, kFormLoPA>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  return f.full() ? gate_nt<LOPA, DENSE, kFormAct>(sh, f, x, gate_w, w_up, t, ws, y, s)
+                  : gate_nt<LOPA, DENSE, kFormDefault>(sh, f, x, gate_w, w_up, t, ws, y, s);
 }
 
 // Down grid: S column groups x R row chunks, about kDnWgTarget workgroups, at most
@@ -896,7 +920,8 @@ bool batched_ok(const Shape& sh, Gate g) {
   const int64_t lim = int64_t(1) << 31;
   if (2 * (int64_t)sh.d_ff * sh.d >= lim || 4 * (int64_t)kTokChunk * sh.d >= lim) return false;
   if ((int64_t)segments_for(sh.d_ff, kSegGrid2) * 256 * kTokChunk >= lim) return false;
-  if (g == Gate::LoPA && (sh.r % 8 != 0 || 2 * (int64_t)sh.d_ff * sh.r >= lim || 2 * (int64_t)sh.r * sh.d >= lim))
+  if (g == Gate::LoPA && (sh.r % 8 != 0 || 2 * (int64_t)sh.d_ff * sh.r >= lim || 2 * (int64_t)sh.r * sh.d >= lim ||
+                          4 * (int64_t)kTokChunk * sh.d_ff >= lim))  // G x, read through a buffer
     return false;
   return true;
 }
@@ -904,19 +929,20 @@ bool batched_ok(const Shape& sh, Gate g) {
 // the most segments any gate kernel of this path uses (workspace sizing)
 int batched_segments(int d_ff) { return segments_for(d_ff, kSegGrid2); }
 
-hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* norm_gain,
-                          float norm_eps, const float* x, const void* lopa_a, const void* gate_w, const void* w_up,
-                          const void* w_down_t, float t, Workspace& ws, float* y, hipStream_t s) {
+hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* x,
+                          const void* lopa_a, const void* gate_w, const void* w_up, const void* w_down_t, float t,
+                          Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
   hipError_t e = hipSuccess;
   // more than one token tile: the kernels read the tokens pre-split
   if (sh.T > 16 && (e = split_tokens(sh, x, ws, s)) != hipSuccess) return e;
   if (lopa) {
-    e = sh.T <= 16 ? z_mfma<1>(sh, x, lopa_a, ws, s)
-                   : sh.T <= 32 ? z_mfma<2>(sh, x, lopa_a, ws, s) : z_mfma<4>(sh, x, lopa_a, ws, s);
+    e = sh.T <= 16 ? z_mfma<1>(sh, form, x, lopa_a, ws, s)
+                   : sh.T <= 32 ? z_mfma<2>(sh, form, x, lopa_a, ws, s) : z_mfma<4>(sh, form, x, lopa_a, ws, s);
     if (e != hipSuccess) return e;
     // RMSNorm between A and B: the two partial copies of z become one normalised copy
-    if (norm_eps > 0.f && (e = launch_rms_norm(ws.z, 2, ws.tc, sh.T, sh.r, norm_gain, norm_eps, s)) != hipSuccess)
+    if (form.rms_eps > 0.f &&
+        (e = launch_rms_norm(ws.z, 2, ws.tc, sh.T, sh.r, form.rms_gain, form.rms_eps, s)) != hipSuccess)
       return e;
   }
   if (lopa)

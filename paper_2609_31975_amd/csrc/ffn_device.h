@@ -129,14 +129,66 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
 __device__ __forceinline__ float gate_value(int act, float u) { return act ? u / (1.f + expf(-u)) : u; }
 __device__ __forceinline__ float up_value(int silu, float v) { return silu ? v / (1.f + expf(-v)) : v; }
 
-// LoPA's fixed term for row `row` and the token whose fp32 row is `xt` (d values):
-// g_sign[row] x[g_idx[row]], read through a buffer of d floats so that a column
-// outside [0, d) reads 0.
-__device__ __forceinline__ float g_term(const Form& f, const float* xt, int d, int row) {
+// LoPA's fixed term g_sign[row] x[g_idx[row]] in two steps, so that the gather of x
+// (which needs the column) does not wait for the column in front of the gate stream:
+// g_fetch loads G's column and value of `row` (row < 0: column 0, value 0, and no
+// memory access, so that f.g_idx may be null then), g_gather reads x through a buffer of
+// d floats, so that a column outside [0, d) reads 0.  Both are branch-free, so that
+// their loads issue back to back.
+struct GEntry {
+  uint32_t col;
+  float sgn;
+};
+__device__ __forceinline__ GEntry g_fetch(const Form& f, int d_ff, int row) {
+  const Buf ib = make_buf(f.g_idx, 4u * (uint32_t)d_ff), sb = make_buf(f.g_sign, (uint32_t)d_ff);
+  const bool ok = row >= 0;
+  const uint32_t col = ldb32(ib, ok ? 4u * (uint32_t)row : kOOB);
+  const int8_t s = (int8_t)__builtin_amdgcn_raw_buffer_load_b8(sb.r, ok ? (uint32_t)row : kOOB, 0, 0);
+  return GEntry{col, (float)s};
+}
+__device__ __forceinline__ uint32_t g_gather_bits(const GEntry& e, const float* xt, int d, bool ok = true) {
   const Buf xb = make_buf(xt, 4u * (uint32_t)d);
-  const int c = f.g_idx[row];
-  const float v = __builtin_bit_cast(float, ldb32(xb, (uint32_t)c < (uint32_t)d ? 4u * (uint32_t)c : kOOB));
-  return (float)f.g_sign[row] * v;
+  return ldb32(xb, ok && e.col < (uint32_t)d ? 4u * e.col : kOOB);
+}
+__device__ __forceinline__ float g_value(const GEntry& e, uint32_t bits) {
+  return e.sgn * __builtin_bit_cast(float, bits);
+}
+__device__ __forceinline__ float g_gather(const GEntry& e, const float* xt, int d, bool ok = true) {
+  return g_value(e, g_gather_bits(e, xt, d, ok));
+}
+
+// G x of every row and token, gx[tok][row], computed by the workgroups [first, gridDim.x)
+// of a LoPA z kernel (which otherwise leave idle compute units), so that the gate kernel
+// reads it with one independent load instead of two dependent ones.  Returns true in
+// those workgroups (they do nothing else).
+struct GWork {
+  Form form;
+  const float* x;
+  float* gx;
+  int T, d, d_ff, first;
+};
+// Work item j: row j % d_ff for the group of kGTok tokens j / d_ff (G's entry, kGTok
+// gathers in flight, their stores).
+constexpr int kGTok = 8;
+__host__ __device__ inline int g_items(int d_ff, int T) { return d_ff * ((T + kGTok - 1) / kGTok); }
+__device__ __forceinline__ bool g_precompute(const GWork& w) {
+  if ((int)blockIdx.x < w.first) return false;
+  const int nb = (int)gridDim.x - w.first, b = (int)blockIdx.x - w.first;
+  const int n = g_items(w.d_ff, w.T);
+  for (int j = b * (int)blockDim.x + (int)threadIdx.x; j < n; j += nb * (int)blockDim.x) {
+    const int t0 = j / w.d_ff * kGTok, i = j - j / w.d_ff * w.d_ff;
+    const GEntry e = g_fetch(w.form, w.d_ff, i);
+    uint32_t v[kGTok];
+#pragma unroll
+    for (int u = 0; u < kGTok; ++u) {
+      const int tok = t0 + u;
+      v[u] = g_gather_bits(e, w.x + (size_t)(tok < w.T ? tok : 0) * w.d, w.d, tok < w.T);
+    }
+#pragma unroll
+    for (int u = 0; u < kGTok; ++u)
+      if (t0 + u < w.T) w.gx[(size_t)(t0 + u) * w.d_ff + i] = g_value(e, v[u]);
+  }
+  return true;
 }
 
 // The gate kernels clear y (the down kernel accumulates into it) and record the

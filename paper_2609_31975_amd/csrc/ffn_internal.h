@@ -53,6 +53,9 @@ struct Workspace {
   float* seg_zval;     // [tc][slots]      act * <w_up[i], x_tau>
   float* z;            // [tc][r]          LoPA intermediate A x (LoPA only); for tc >= 2
                        //                  two partial copies [2][tc][r]
+  float* zsq;          // [r]              squares of z (single-token LoPA path with RMSNorm)
+  float* gx;           // [tc][d_ff]       G x per token (LoPA with G, single-token and
+                       //                  matrix-core paths; written by the z kernel)
   uint4* zf;           // [2 batched_segments(d_ff)][ceil(tc / 16)][2][64]  zval fragments of the
                        //                  down product, hi and lo planes of 64 lanes per fragment
                        //                  group and token tile (matrix-core path, tc >= 2)
@@ -73,12 +76,19 @@ enum class Gate { Standard, LoPA };
 // The paper's full FFN form as the gate kernels see it (from ffn_options_t, checked on
 // the host): the activation, SiLU on the W_up output and LoPA's fixed term G.  The
 // norm on z is not here: it runs as a kernel of its own between z and the gate.
+// Compile-time form of a gate kernel: the default form, the full form's activations
+// only, or (LoPA) also G and RMSNorm.
+enum FormKind : int { kFormDefault = 0, kFormAct = 1, kFormLoPA = 2 };
+
 struct Form {
   int act = 0;                     // 0 shifted ReLU, 1 shifted R-S+
   int silu_up = 0;                 // 1: SiLU on the W_up output
   const int32_t* g_idx = nullptr;  // G's column per row (null: G = 0, and g_sign null)
   const int8_t* g_sign = nullptr;  // G's value per row
-  bool full() const { return act != 0 || silu_up != 0 || g_idx != nullptr; }
+  const float* rms_gain = nullptr;  // RMSNorm gains over z (null: ones)
+  float rms_eps = 0.f;              // > 0: RMSNorm between the LoPA factors
+  bool full() const { return act != 0 || silu_up != 0 || g_idx != nullptr || rms_eps > 0.f; }
+  int kind() const { return g_idx != nullptr || rms_eps > 0.f ? kFormLoPA : full() ? kFormAct : kFormDefault; }
 };
 
 // Events for the next gate-kernel launch on this host thread (benchmark hook).
@@ -89,14 +99,18 @@ struct GateTiming {
 extern thread_local GateTiming g_gate_timing;
 
 // Launchers (return hipSuccess or the launch error).  Every launcher enqueues on `s`.
-hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws,
+// With form.rms_eps > 0 on the single-token path, z is stored times the RMSNorm gains and
+// its squares go to ws.zsq; the gate kernel then scales each gate value by the norm.
+hipError_t launch_lopa_z(const Shape& sh, const Form& form, const float* x, const void* lopa_a, const Workspace& ws,
                          hipStream_t s);
 // RMSNorm on z in place (Section 3.3): the `parts` partial copies [parts][tc][r] of each
 // token's z are summed into copy 0, scaled by gain / sqrt(mean z^2 + eps), and the other
 // copies are zeroed, so the gate kernels read the normalized z unchanged.
 hipError_t launch_rms_norm(float* z, int parts, int tc, int T, int r, const float* gain, float eps,
                            hipStream_t s);
-// Also clears y[0 .. T*d) and sets ws.nseg / meta[0] for the down kernel.
+// Also clears y[0 .. T*d) and sets ws.nseg / meta[0] for the down kernel.  With
+// form.rms_eps > 0 (LoPA) z is normalised first: inside the single-token gate kernel,
+// else by launch_rms_norm.
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x,
                           const void* gate_w, const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
@@ -106,9 +120,9 @@ hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const 
 // the whole call (LoPA z, gate + union + W_up, down), clearing y first.
 bool batched_ok(const Shape& sh, Gate g);
 int batched_segments(int d_ff);
-// With norm_gain / norm_eps: RMSNorm on z (norm_eps > 0 turns it on).
-hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* norm_gain,
-                          float norm_eps, const float* x, const void* lopa_a, const void* gate_w, const void* w_up,
-                          const void* w_down_t, float t, Workspace& ws, float* y, hipStream_t s);
+// form.rms_eps > 0: RMSNorm on z between the LoPA factors.
+hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* x,
+                          const void* lopa_a, const void* gate_w, const void* w_up, const void* w_down_t, float t,
+                          Workspace& ws, float* y, hipStream_t s);
 
 }  // namespace ffn

@@ -163,26 +163,42 @@ __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int
   }
 }
 
+// components of z (or of its squares) a thread keeps in registers for RMSNorm
+constexpr int kNormRegs = 4;
+
 // ------------------------------------------------------------------ fast kernels, T = 1
 // z = A x for one token (rows of A: C chunks); one pass of 64/lpr rows per wave.
-template <class W, int CPL>
+// NORM (RMSNorm between the factors, Section 3.3): z_k is stored times gain_k and z_k^2
+// goes to zsq, from which the gate kernel takes the norm; the norm being one scalar per
+// token, it scales each gate value B (gain . z) after the dot product.
+template <class W, int CPL, bool NORM>
 __global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ x, const uint4* __restrict__ A,
-                                                      int C, int lpr, int lpr_log2, int r, float* __restrict__ z) {
+                                                      int C, int lpr, int lpr_log2, int r, float* __restrict__ z,
+                                                      const float* __restrict__ gain, float* __restrict__ zsq,
+                                                      GWork gw) {
+  if (g_precompute(gw)) return;
   float xr[CPL][W::EPC];
   load_vec<W, CPL>(x, C, lane_id() & (lpr - 1), lpr, xr);
   const int rows_per_block = (kBlock / kWave) * (kWave >> lpr_log2);
   const int k0 = blockIdx.x * rows_per_block;
   const int n = min(rows_per_block, r - k0);
   dot_rows<W, CPL>(A, 16u * (uint32_t)r * (uint32_t)C, C, lpr, lpr_log2, n, xr, [&](int k) { return k0 + k; },
-                   [&](int k, float s) { z[k0 + k] = s; });
+                   [&](int k, float s) {
+                     if constexpr (NORM) {
+                       z[k0 + k] = gain ? s * gain[k0 + k] : s;
+                       zsq[k0 + k] = s * s;
+                     } else {
+                       z[k0 + k] = s;
+                     }
+                   });
 }
 
 // One segment: gate values, compaction, W_up dots of the selected neurons.
 // LOPA: the gate rows are B [d_ff][r] against z; otherwise W_gate [d_ff][d] against x.
 // DENSE: every neuron of the segment is selected (act = max(h - t, 0)).
-// FULL: the paper's full form (`form`): the activation value, SiLU on the W_up output and,
-// for LoPA, the fixed term G added to the gate before the compaction.
-template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU, bool FULL>
+// FORM (a FormKind): the paper's full form (`form`): the activation value, SiLU on the
+// W_up output and, with kFormLoPA, the fixed term G and RMSNorm of z.
+template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU, int FORM>
 __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__ x, const float* __restrict__ z,
                                                        const uint4* __restrict__ gate_w, int Cg, int lprg,
                                                        int lprg_log2, const uint4* __restrict__ w_up, int Cu,
@@ -190,8 +206,11 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
                                                        int32_t* __restrict__ meta, int32_t* __restrict__ seg_count,
                                                        int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                                        float* __restrict__ seg_zval, float* __restrict__ y, int d,
-                                                       Form form) {
+                                                       Form form, const float* __restrict__ zsq,
+                                                       const float* __restrict__ gx) {
+  constexpr bool FULL = FORM != kFormDefault, EXTRA = LOPA && FORM == kFormLoPA;
   __shared__ float s_h[kSegMax];
+  __shared__ float s_ss[kBlock / kWave];
   __shared__ int s_list[kSegMax];
   __shared__ float s_act[kSegMax];
   __shared__ int s_cnt;
@@ -208,16 +227,52 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
   const int act = FULL ? form.act : 0;
 
   if constexpr (LOPA) {
+    // LoPA's fixed term (G x)_i of this thread's row (written by the z kernel's extra
+    // workgroups) and the squares of z for RMSNorm: loaded before the gate stream, used
+    // after it, branch-free so that nothing waits for them in front of the stream
+    const bool has_g = EXTRA && form.g_idx;
+    const uint32_t gbits =
+        EXTRA ? ldb32(make_buf(gx, 4u * (uint32_t)d_ff), has_g && (int)threadIdx.x < nrows
+                                                               ? 4u * (uint32_t)(row0 + (int)threadIdx.x)
+                                                               : kOOB)
+              : 0u;
+    const bool norm = EXTRA && form.rms_eps > 0.f;
+    const int r = Cg * W::EPC;
+    uint32_t sq[EXTRA ? kNormRegs : 1] = {};
+    if constexpr (EXTRA) {
+      const Buf qb = make_buf(zsq, 4u * (uint32_t)r);
+#pragma unroll
+      for (int j = 0; j < kNormRegs; ++j) {
+        const int k = (int)threadIdx.x + j * kBlock;
+        sq[j] = ldb32(qb, norm && k < r ? 4u * (uint32_t)k : kOOB);
+      }
+    }
     {
       float zr[CPLG][W::EPC];
-      load_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
+      const int q = lane_id() & (lprg - 1);
+      load_vec<W, CPLG>(z, Cg, q, lprg, zr);
       dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
                         gate_sink);
     }
+    const float gv = __builtin_bit_cast(float, gbits);
     __syncthreads();
-    if constexpr (FULL) {
-      if (form.g_idx) {  // LoPA's fixed term: h += G x
-        if ((int)threadIdx.x < nrows) s_h[threadIdx.x] += g_term(form, x, d, row0 + threadIdx.x);
+    if constexpr (EXTRA) {
+      float inv = 1.f;
+      if (norm) {  // 1 / sqrt(mean z^2 + eps)
+        float ss = 0.f;
+#pragma unroll
+        for (int j = 0; j < kNormRegs; ++j) ss += __builtin_bit_cast(float, sq[j]);
+        for (int k = threadIdx.x + kNormRegs * kBlock; k < r; k += kBlock) ss += zsq[k];
+        ss = wave_sum(ss);
+        if (lane_id() == 0) s_ss[threadIdx.x / kWave] = ss;
+        __syncthreads();
+        float tot = 0.f;
+#pragma unroll
+        for (int w = 0; w < kBlock / kWave; ++w) tot += s_ss[w];
+        inv = 1.f / sqrtf(tot / (float)r + form.rms_eps);
+      }
+      if (norm || form.g_idx) {  // h = inv * B (gain . z) + G x
+        if ((int)threadIdx.x < nrows) s_h[threadIdx.x] = s_h[threadIdx.x] * inv + gv;
         __syncthreads();
       }
     }
@@ -240,7 +295,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
 }
 
 // y += sum over the listed neurons of a row chunk of zval * w_down_t[neuron], for one
-// 64-chunk column slice (1 KB of every bf16 row, read by one wave instruction).
+// 64-chunk column slice (1 KB of every bf16 row, read by one wave instruction).  A
+// listed neuron with zval exactly 0 (the s_gated site) is skipped: its row is not read.
 // Workgroup b covers column slice b % S of the neurons in segments [c nseg/R,
 // (c+1) nseg/R), c = b / S.  Its four waves take the chunk's active rows in turn;
 // their partial sums are added in a fixed order and then into y with one atomic
@@ -320,7 +376,9 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
         row = ok ? l_idx[kk] : 0;
         zz[u] = ok ? l_z[kk] : 0.f;
       }
-      wv[u] = (ok && cvalid) ? ld_weights(w_down_t + (size_t)row * C + ch) : make_uint4(0u, 0u, 0u, 0u);
+      // a zero gated value (the s_gated site) needs no W_down row
+      const bool need = ok && cvalid && (DENSE || zz[u] != 0.f);
+      wv[u] = need ? ld_weights(w_down_t + (size_t)row * C + ch) : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -396,7 +454,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
     if (form.g_idx) {  // LoPA's fixed term: h += G x
       for (int o = threadIdx.x; o < nrows * T; o += kBlock) {
         const int k = o / T, tau = o - k * T;
-        s_h[k][tau] += g_term(form, x + (size_t)tau * d, d, row0 + k);
+        s_h[k][tau] += g_gather(g_fetch(form, d_ff, row0 + k), x + (size_t)tau * d, d);
       }
       __syncthreads();
     }
@@ -482,7 +540,10 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
           const float w = welem(W{}, w_down_t, (size_t)row * d + col);
 #pragma unroll
           for (int u = 0; u < 8; ++u)
-            if (u < tn) acc[u] = fmaf(seg_zval[(size_t)(tg + u) * slots + slot], w, acc[u]);
+            if (u < tn) {
+              const float zv = seg_zval[(size_t)(tg + u) * slots + slot];
+              if (DENSE || zv != 0.f) acc[u] = fmaf(zv, w, acc[u]);  // s_gated: zero adds nothing
+            }
         }
       }
       if (!DENSE) __syncthreads();
@@ -551,34 +612,35 @@ bool fast_ok(const Shape& sh, Gate g) {
   return true;
 }
 
-template <class W, bool LOPA, bool DENSE, bool FULL, int CPLG, int CPLU>
+template <class W, bool LOPA, bool DENSE, int FORM, int CPLG, int CPLU>
 hipError_t go_gate_up_t1(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up,
                          float t, Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / W::EPC, Cg = LOPA ? sh.r / W::EPC : Cu;
   const int lpru = lanes_per_row(Cu, CPLU), lprg = lanes_per_row(Cg, CPLG);
-  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU, FULL>;
+  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU, FORM>;
   static int per_cu = 0;  // one cache per instantiation
   ws.nseg = resident_segments(kernel, &per_cu, sh.d_ff);
   return launch_gate_kernel(kernel, ws.nseg, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg, lprg,
                             ilog2(lprg), static_cast<const uint4*>(w_up), Cu, lpru, ilog2(lpru), sh.d_ff, ws.nseg, t,
-                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d, form);
+                            ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d, form,
+                            (const float*)ws.zsq, (const float*)ws.gx);
 }
 
-template <class W, bool LOPA, bool DENSE, bool FULL>
+template <class W, bool LOPA, bool DENSE, int FORM>
 hipError_t gate_up_fast(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
                         Workspace& ws, float* y, hipStream_t s) {
   const int cplu = cpl_for(sh.d / W::EPC);
   if constexpr (LOPA) {
     const int cplg = cpl_for(sh.r / W::EPC);
-    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, FULL, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, FORM, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
     if (cplg == 8 && cplu == 16)
-      return go_gate_up_t1<W, true, DENSE, FULL, 8, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
+      return go_gate_up_t1<W, true, DENSE, FORM, 8, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
     if (cplg == 16 && cplu == 8)
-      return go_gate_up_t1<W, true, DENSE, FULL, 16, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
-    return go_gate_up_t1<W, true, DENSE, FULL, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
+      return go_gate_up_t1<W, true, DENSE, FORM, 16, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, true, DENSE, FORM, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
   } else {
-    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, FULL, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
-    return go_gate_up_t1<W, false, DENSE, FULL, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, FORM, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, false, DENSE, FORM, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
   }
 }
 
@@ -592,7 +654,8 @@ hipError_t gate_up_generic(const Shape& sh, const Form& f, const float* x, const
 }
 
 // RMSNorm on z (Section 3.3), one workgroup per token: the partial copies summed into
-// copy 0 and scaled by gain / sqrt(mean z^2 + eps); the other copies zeroed.
+// copy 0 and scaled by gain / sqrt(mean z^2 + eps); the other copies zeroed.  The first
+// kNormRegs * kBlock components stay in registers between the two passes.
 __global__ __launch_bounds__(kBlock) void k_rms_norm(float* __restrict__ z, int parts, int tc, int r,
                                                      const float* __restrict__ gain, float eps) {
   __shared__ float s_part[kBlock / kWave];
@@ -602,10 +665,17 @@ __global__ __launch_bounds__(kBlock) void k_rms_norm(float* __restrict__ z, int 
     for (int p = 0; p < parts; ++p) v += z[((size_t)p * tc + tok) * r + k];
     return v;
   };
+  float v[kNormRegs];
   float ss = 0.f;
-  for (int k = threadIdx.x; k < r; k += kBlock) {
-    const float v = zsum(k);
-    ss = fmaf(v, v, ss);
+#pragma unroll
+  for (int j = 0; j < kNormRegs; ++j) {
+    const int k = (int)threadIdx.x + j * kBlock;
+    v[j] = k < r ? zsum(k) : 0.f;
+    ss = fmaf(v[j], v[j], ss);
+  }
+  for (int k = threadIdx.x + kNormRegs * kBlock; k < r; k += kBlock) {
+    const float u = zsum(k);
+    ss = fmaf(u, u, ss);
   }
   ss = wave_sum(ss);
   if (lane_id() == 0) s_part[threadIdx.x / kWave] = ss;
@@ -614,24 +684,39 @@ __global__ __launch_bounds__(kBlock) void k_rms_norm(float* __restrict__ z, int 
 #pragma unroll
   for (int w = 0; w < kBlock / kWave; ++w) tot += s_part[w];
   const float inv = 1.f / sqrtf(tot / (float)r + eps);
-  for (int k = threadIdx.x; k < r; k += kBlock) {
-    const float v = zsum(k);
-    z[(size_t)tok * r + k] = v * inv * (gain ? gain[k] : 1.f);
+  auto put = [&](int k, float u) {
+    z[(size_t)tok * r + k] = u * inv * (gain ? gain[k] : 1.f);
     for (int p = 1; p < parts; ++p) z[((size_t)p * tc + tok) * r + k] = 0.f;
+  };
+  for (int k = threadIdx.x + kNormRegs * kBlock; k < r; k += kBlock) put(k, zsum(k));
+#pragma unroll
+  for (int j = 0; j < kNormRegs; ++j) {
+    const int k = (int)threadIdx.x + j * kBlock;
+    if (k < r) put(k, v[j]);
   }
 }
 
 template <class W>
-hipError_t lopa_z(const Shape& sh, const float* x, const void* A, const Workspace& ws, hipStream_t s) {
+hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void* A, const Workspace& ws,
+                  hipStream_t s) {
   if (fast_ok(sh, Gate::LoPA)) {
     const int C = sh.d / W::EPC;
     const int cpl = cpl_for(C), lpr = lanes_per_row(C, cpl), lg = ilog2(lpr);
     const int rows_per_block = (kBlock / kWave) * (kWave >> lg);
     const int grid = (sh.r + rows_per_block - 1) / rows_per_block;
-    if (cpl == 8)
-      k_lopa_z_t1<W, 8><<<grid, kBlock, 0, s>>>(x, static_cast<const uint4*>(A), C, lpr, lg, sh.r, ws.z);
+    const uint4* a = static_cast<const uint4*>(A);
+    const bool norm = form.rms_eps > 0.f;
+    // with G, extra workgroups write G x for the gate kernel
+    const GWork gw{form, x, ws.gx, 1, sh.d, sh.d_ff, grid};
+    const int g = grid + (form.g_idx ? (g_items(sh.d_ff, 1) + kBlock - 1) / kBlock : 0);
+    if (cpl == 8 && norm)
+      k_lopa_z_t1<W, 8, true><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, form.rms_gain, ws.zsq, gw);
+    else if (cpl == 8)
+      k_lopa_z_t1<W, 8, false><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, nullptr, nullptr, gw);
+    else if (norm)
+      k_lopa_z_t1<W, 16, true><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, form.rms_gain, ws.zsq, gw);
     else
-      k_lopa_z_t1<W, 16><<<grid, kBlock, 0, s>>>(x, static_cast<const uint4*>(A), C, lpr, lg, sh.r, ws.z);
+      k_lopa_z_t1<W, 16, false><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, nullptr, nullptr, gw);
   } else {
     const int grid = (sh.r + kBlock / kWave - 1) / (kBlock / kWave);
     k_lopa_z_generic<W><<<grid, kBlock, 0, s>>>(x, A, sh.T, sh.d, sh.r, ws.z);
@@ -674,6 +759,20 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
   return hipGetLastError();
 }
 
+// the kernels for the form: the compile-time kind of the single-token kernel, the full
+// flag of the element-wise one (G and the norm need LoPA; the options check enforces it)
+template <class W, bool LOPA, bool DENSE>
+hipError_t gate_up_form(const Shape& sh, bool fast, const Form& f, const float* x, const void* gate_w,
+                        const void* w_up, float t, Workspace& ws, float* y, hipStream_t s) {
+  if (!fast)
+    return f.full() ? gate_up_generic<W, LOPA, DENSE, true>(sh, f, x, gate_w, w_up, t, ws, y, s)
+                    : gate_up_generic<W, LOPA, DENSE, false>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  if constexpr (LOPA)
+    if (f.kind() == kFormLoPA) return gate_up_fast<W, LOPA, DENSE, kFormLoPA>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  return f.full() ? gate_up_fast<W, LOPA, DENSE, kFormAct>(sh, f, x, gate_w, w_up, t, ws, y, s)
+                  : gate_up_fast<W, LOPA, DENSE, kFormDefault>(sh, f, x, gate_w, w_up, t, ws, y, s);
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
@@ -682,36 +781,29 @@ hipError_t launch_rms_norm(float* z, int parts, int tc, int T, int r, const floa
   return hipGetLastError();
 }
 
-hipError_t launch_lopa_z(const Shape& sh, const float* x, const void* lopa_a, const Workspace& ws, hipStream_t s) {
-  return sh.wdt == 1 ? lopa_z<WBf16>(sh, x, lopa_a, ws, s) : lopa_z<WF32>(sh, x, lopa_a, ws, s);
+hipError_t launch_lopa_z(const Shape& sh, const Form& form, const float* x, const void* lopa_a, const Workspace& ws,
+                         hipStream_t s) {
+  return sh.wdt == 1 ? lopa_z<WBf16>(sh, form, x, lopa_a, ws, s) : lopa_z<WF32>(sh, form, x, lopa_a, ws, s);
 }
 
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x, const void* gate_w,
                           const void* w_up, float t, Workspace& ws, float* y, hipStream_t s) {
   const bool lopa = g == Gate::LoPA;
   const bool fast = fast_ok(sh, g);
-#define FFN_GU2(W, L, D, F)                                                                     \
-  return fast ? gate_up_fast<W, L, D, F>(sh, form, x, gate_w, w_up, t, ws, y, s)               \
-              : gate_up_generic<W, L, D, F>(sh, form, x, gate_w, w_up, t, ws, y, s)
-#define FFN_GU(W, L, D)                                                    \
-  return form.full() ? [&] { FFN_GU2(W, L, D, true); }()                  \
-                     : [&] { FFN_GU2(W, L, D, false); }()
+  if (lopa && !fast && form.rms_eps > 0.f) {  // the single-token kernel normalises z itself
+    const hipError_t e = launch_rms_norm(ws.z, 1, ws.tc, sh.T, sh.r, form.rms_gain, form.rms_eps, s);
+    if (e != hipSuccess) return e;
+  }
   if (sh.wdt == 1) {
-    if (lopa) {
-      if (dense) FFN_GU(WBf16, true, true);
-      FFN_GU(WBf16, true, false);
-    }
-    if (dense) FFN_GU(WBf16, false, true);
-    FFN_GU(WBf16, false, false);
+    if (lopa) return dense ? gate_up_form<WBf16, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
+                           : gate_up_form<WBf16, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
+    return dense ? gate_up_form<WBf16, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
+                 : gate_up_form<WBf16, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
   }
-  if (lopa) {
-    if (dense) FFN_GU(WF32, true, true);
-    FFN_GU(WF32, true, false);
-  }
-  if (dense) FFN_GU(WF32, false, true);
-  FFN_GU(WF32, false, false);
-#undef FFN_GU
-#undef FFN_GU2
+  if (lopa) return dense ? gate_up_form<WF32, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
+                         : gate_up_form<WF32, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
+  return dense ? gate_up_form<WF32, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
+               : gate_up_form<WF32, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
 }
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,

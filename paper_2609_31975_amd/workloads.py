@@ -140,6 +140,7 @@ class Workload:
     t: float
     seed: int
     n_sets: int
+    form: str = ""    # "" the default form; "full": R-S+, SiLU on W_up, G and RMSNorm (LoPA)
 
 
 # The five workload families; every (sparsity, T) point is its own entry.
@@ -151,6 +152,9 @@ def workloads() -> list[Workload]:
         out.append(Workload(f"8b_lopa512_s{int(s * 100)}", 4096, 14336, 512, 1, BF16, THRESHOLD[s], 2000, 4))
     for T in (1, 4, 16, 64):
         out.append(Workload(f"8b_lopa512_s90_T{T}", 4096, 14336, 512, T, BF16, THRESHOLD[0.90], 3000, 4))
+    for T in (1, 16):
+        out.append(Workload(f"8b_lopa512_full_s90_T{T}", 4096, 14336, 512, T, BF16,
+                            round(THRESHOLD[0.90] * 2 ** 0.5, 4), 3000, 4, "full"))
     for T in (1, 8):
         out.append(Workload(f"70b_std_s90_T{T}", 8192, 28672, 0, T, BF16, THRESHOLD[0.90], 4000, 2))
         out.append(Workload(f"70b_lopa1024_s90_T{T}", 8192, 28672, 1024, T, BF16, THRESHOLD[0.90], 5000, 2))

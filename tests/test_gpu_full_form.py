@@ -96,16 +96,47 @@ def test_same_active_set_for_either_activation(gu):
     np.testing.assert_allclose(a1[on], a0[on] / (1.0 + np.exp(-a0[on].astype(np.float64))), rtol=1e-5)
 
 
-# ---------------------------------------------------------------- full size: the 8B LoPA shape
-@pytest.mark.parametrize("T", [1, 16], ids=["T1", "T16"])
-def test_full_form_8b_lopa(gu, T):
-    d, d_ff, r = 4096, 14336, 512
-    inp = wl.make_inputs(1512, T, d, d_ff, r=r, wdt=BF16)
-    form = _form(gu, inp, ALL)
-    t = wl.THRESHOLD[0.90] * S2
+# ---------------------------------------------------------------- full size: the benchmarked full-form workloads
+FULL_FORM = [w for w in wl.workloads() if w.form == "full"]
+
+
+@pytest.mark.parametrize("w", FULL_FORM, ids=[w.name for w in FULL_FORM])
+def test_full_form_workloads(gu, w):
+    inp = wl.make_inputs(w.seed, w.T, w.d, w.d_ff, r=w.r, wdt=w.wdt)
+    form = gu.Form(form=wl.make_form(w.seed, w.d, w.d_ff, w.r), **ALL)
+    y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(inp), w.t, form)
+    res = gu.run_oracle(inp, w.t, form=form)
+    fig = gu.check_parity(res, y, idx, act, w.t, w.wdt, what=w.name, act_value=form.act_value)
+    frac = np.mean(fig["n_active"]) / w.d_ff
+    assert 0.05 < frac < 0.15, f"activation fraction {frac:.3f} far from the 10% the threshold targets"
+    print(w.name, fig["max_rel_err"], fig["n_union"], frac, flush=True)
+
+
+# ---------------------------------------------------------------- s_gated: zero gated values
+# (T, d, d_ff, r, wdt): the single-token kernels and the element-wise kernels (any T).  The
+# matrix-core batch path multiplies every union row by every token's gated value.
+SGATED = [(1, 264, 1000, 0, BF16), (1, 264, 1000, 40, BF16), (1, 260, 999, 0, F32), (1, 100, 77, 0, BF16),
+          (3, 100, 77, 0, BF16), (4, 64, 200, 0, F32), (2, 264, 1000, 40, F32)]
+
+
+@pytest.mark.parametrize("shape", SGATED, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
+@pytest.mark.parametrize("silu_up", [False, True], ids=["plain", "silu"])
+def test_zero_gated_value_rows_not_read(gu, shape, silu_up):
+    """Active neurons with a zero W_up row have gated value 0: NaN in their W_down rows
+    leaves the output equal to the oracle's (which skips those rows too)."""
+    T, d, d_ff, r, wdt = shape
+    inp = wl.make_inputs(205, T, d, d_ff, r=r, wdt=wdt)
+    t = 0.8
+    form = gu.Form(silu_up=silu_up)
+    on = np.flatnonzero(gu.run_oracle(inp, t, form=form).active.any(0))
+    zero = on[::3]
+    assert len(zero) >= 3
+    nan = np.uint16(0x7FC0) if wdt == BF16 else np.float32(np.nan)
+    inp.w_up = inp.w_up.copy()
+    inp.w_down_t = inp.w_down_t.copy()
+    inp.w_up[zero] = 0
+    inp.w_down_t[zero] = nan
     y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(inp), t, form)
     res = gu.run_oracle(inp, t, form=form)
-    fig = gu.check_parity(res, y, idx, act, t, BF16, what=f"8b lopa full T{T}", act_value=form.act_value)
-    frac = np.mean(fig["n_active"]) / d_ff
-    assert 0.05 < frac < 0.15, f"activation fraction {frac:.3f} far from the 10% the threshold targets"
-    print(f"8b lopa full form T{T}", fig["max_rel_err"], fig["n_union"], frac, flush=True)
+    assert np.isfinite(res.y).all()
+    gu.check_parity(res, y, idx, act, t, wdt, what=f"s_gated {shape}")
