@@ -45,6 +45,16 @@
  * Inputs are exactly the bit patterns the GPU receives: x is fp32, weights are
  * fp32 (wdt = 0) or bfloat16 bit patterns (wdt = 1); both widen to double
  * exactly.  t is the same fp32 value, widened.
+ *
+ * Weight-only quantization (wdt = 2: int8, wdt = 3: int4; the setting of the
+ * appendix on quantization-aware training, whose kernels read int8 or int4
+ * weights at inference): the paper fixes no scheme, so one is chosen here.  Every
+ * matrix row i carries a code row q_i and an fp32 scale s_i, and its weights are
+ * s_i * q_ij, formed exactly in double.  int8 codes are signed bytes; int4 codes
+ * are two's-complement nibbles, two per byte, element 2k in the low nibble of byte
+ * k of the row (rows of even length).  The matrix rows are those of the stored
+ * layout: W_gate, W3, V, U by output unit, W2 by hidden neuron (its transposed
+ * rows).
  */
 #include <math.h>
 #include <stdint.h>
@@ -52,9 +62,17 @@
 #include <stdlib.h>
 #include <string.h>
 
-/* element k of a weight matrix, widened exactly to double */
-static double weight_at(const void* w, int wdt, size_t k) {
+/* element k (in row `row`) of a weight matrix, widened exactly to double; for the
+   quantized formats the row's scale times its code */
+static double weight_at(const void* w, int wdt, const float* scale, size_t row, size_t k) {
   if (wdt == 0) return (double)((const float*)w)[k];
+  if (wdt == 2) return (double)scale[row] * (double)((const int8_t*)w)[k];
+  if (wdt == 3) {
+    int b = ((const uint8_t*)w)[k >> 1];
+    int q = (k & 1) ? (b >> 4) : (b & 15); /* element 2k in the low nibble */
+    if (q >= 8) q -= 16;                   /* two's complement */
+    return (double)scale[row] * (double)q;
+  }
   uint32_t bits = ((uint32_t)((const uint16_t*)w)[k]) << 16; /* bf16 = top half of an fp32 */
   float f;
   memcpy(&f, &bits, sizeof f);
@@ -62,9 +80,10 @@ static double weight_at(const void* w, int wdt, size_t k) {
 }
 
 /* <row i of an [n][len] matrix, v>, ascending j, counting multiply-adds */
-static double row_dot(const void* w, int wdt, size_t i, int len, const double* v, int64_t* macs) {
+static double row_dot(const void* w, int wdt, const float* scale, size_t i, int len, const double* v,
+                      int64_t* macs) {
   double s = 0.0;
-  for (int j = 0; j < len; ++j) s += weight_at(w, wdt, i * (size_t)len + (size_t)j) * v[j];
+  for (int j = 0; j < len; ++j) s += weight_at(w, wdt, scale, i, i * (size_t)len + (size_t)j) * v[j];
   *macs += len;
   return s;
 }
@@ -73,14 +92,17 @@ static double row_dot(const void* w, int wdt, size_t i, int len, const double* v
 static double logistic(double u) { return 1.0 / (1.0 + exp(-u)); }
 
 /*
- * oracle_ffn_ex -- one FFN forward pass per token, tokens independent.
+ * oracle_ffn_q -- one FFN forward pass per token, tokens independent.
  *
  *   gating        0: standard, h = W_gate x          (w_gate [d_ff][d])
  *                 1: LoPA,     h = B (A x)           (lopa_a [r][d], lopa_b [d_ff][r])
  *   skip_inactive 1: the sparse method (inactive neurons' W_up rows and W_down
  *                    columns are never read)
  *                 0: the dense FFN (every neuron evaluated, inactive ones weigh 0)
- *   wdt           weight storage: 0 = fp32, 1 = bf16 bit patterns
+ *   wdt           weight storage: 0 = fp32, 1 = bf16 bit patterns, 2 = int8 codes,
+ *                 3 = int4 codes (row lengths d and r even)
+ *   s_gate, s_a, s_b, s_up, s_down  int8 / int4 only: the fp32 row scales of
+ *                 W_gate [d_ff], A [r], B [d_ff], W_up [d_ff], W_down^T [d_ff]
  *   x             [T][d] fp32
  *   t             activation threshold (shift of the activation)
  *   act           0: shifted ReLU, 1: shifted R-S+
@@ -98,16 +120,21 @@ static double logistic(double u) { return 1.0 / (1.0 + exp(-u)); }
  *   macs_out      [T] multiply-adds executed for that token
  * Returns 0, or -1 on a bad argument.
  */
-int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
-                  const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
-                  const void* w_up, const void* w_down_t, float t, int act, int silu_up,
-                  const int32_t* g_idx, const int8_t* g_sign, int rms_norm, const float* rms_gain,
-                  float rms_eps, double* h_out, double* z_out, uint8_t* active_out, double* y_out,
-                  int64_t* macs_out) {
-  if (T < 1 || d < 1 || d_ff < 1 || (wdt != 0 && wdt != 1) || !x || !w_up || !w_down_t) return -1;
+int oracle_ffn_q(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
+                 const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
+                 const void* w_up, const void* w_down_t, const float* s_gate, const float* s_a,
+                 const float* s_b, const float* s_up, const float* s_down, float t, int act, int silu_up,
+                 const int32_t* g_idx, const int8_t* g_sign, int rms_norm, const float* rms_gain,
+                 float rms_eps, double* h_out, double* z_out, uint8_t* active_out, double* y_out,
+                 int64_t* macs_out) {
+  if (T < 1 || d < 1 || d_ff < 1 || wdt < 0 || wdt > 3 || !x || !w_up || !w_down_t) return -1;
   if (gating == 0 && !w_gate) return -1;
   if (gating == 1 && (r < 1 || !lopa_a || !lopa_b)) return -1;
   if (gating != 0 && gating != 1) return -1;
+  if (wdt >= 2) { /* quantized: every matrix in use has its scales */
+    if (!s_up || !s_down || (gating == 0 && !s_gate) || (gating == 1 && (!s_a || !s_b))) return -1;
+    if (wdt == 3 && (d % 2 != 0 || (gating == 1 && r % 2 != 0))) return -1;
+  }
   if ((act != 0 && act != 1) || (silu_up != 0 && silu_up != 1) || (rms_norm != 0 && rms_norm != 1)) return -1;
   if ((g_idx == NULL) != (g_sign == NULL)) return -1;
   if (gating == 0 && (g_idx || rms_norm)) return -1; /* G and the norm belong to LoPA */
@@ -134,7 +161,7 @@ int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff
 
     /* LoPA: the low-rank intermediate z = V x = A x, then the optional RMSNorm */
     if (gating == 1) {
-      for (int k = 0; k < r; ++k) zv[k] = row_dot(lopa_a, wdt, (size_t)k, d, xv, &macs);
+      for (int k = 0; k < r; ++k) zv[k] = row_dot(lopa_a, wdt, s_a, (size_t)k, d, xv, &macs);
       if (z_out)
         for (int k = 0; k < r; ++k) z_out[(size_t)tok * r + k] = zv[k];
       if (rms_norm) {
@@ -151,8 +178,8 @@ int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff
 
     for (int i = 0; i < d_ff; ++i) {
       /* gate pre-activation, computed for every neuron */
-      double h = gating == 0 ? row_dot(w_gate, wdt, (size_t)i, d, xv, &macs)
-                             : row_dot(lopa_b, wdt, (size_t)i, r, zv, &macs);
+      double h = gating == 0 ? row_dot(w_gate, wdt, s_gate, (size_t)i, d, xv, &macs)
+                             : row_dot(lopa_b, wdt, s_b, (size_t)i, r, zv, &macs);
       if (g_idx) h += (double)g_sign[i] * xv[g_idx[i]]; /* (G x)_i */
       int active = h > tt; /* strict: A(h) is 0 at h == t for both activations; NaN is inactive */
       if (h_out) h_out[(size_t)tok * d_ff + i] = h;
@@ -161,13 +188,13 @@ int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff
 
       double u = active ? h - tt : 0.0;
       double a = act == 1 ? u * logistic(u) : u;              /* A(W1 x)_i */
-      double v = row_dot(w_up, wdt, (size_t)i, d, xv, &macs); /* (W3 x)_i */
+      double v = row_dot(w_up, wdt, s_up, (size_t)i, d, xv, &macs); /* (W3 x)_i */
       if (silu_up) v = v * logistic(v);
       double zi = a * v;
       if (skip_inactive && zi == 0.0) continue; /* s_gated: column i of W2 is not needed */
       /* y += zi * (column i of W2) = zi * w_down_t[i][:] */
       for (int j = 0; j < d; ++j) {
-        double wd = weight_at(w_down_t, wdt, (size_t)i * d + (size_t)j);
+        double wd = weight_at(w_down_t, wdt, s_down, (size_t)i, (size_t)i * d + (size_t)j);
         if (y) y[j] += zi * wd;
       }
       macs += d;
@@ -177,6 +204,19 @@ int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff
   free(xv);
   free(zv);
   return 0;
+}
+
+/* oracle_ffn_q for fp32 / bf16 weights (no scales) */
+int oracle_ffn_ex(int gating, int skip_inactive, int wdt, int T, int d, int d_ff, int r,
+                  const float* x, const void* w_gate, const void* lopa_a, const void* lopa_b,
+                  const void* w_up, const void* w_down_t, float t, int act, int silu_up,
+                  const int32_t* g_idx, const int8_t* g_sign, int rms_norm, const float* rms_gain,
+                  float rms_eps, double* h_out, double* z_out, uint8_t* active_out, double* y_out,
+                  int64_t* macs_out) {
+  if (wdt != 0 && wdt != 1) return -1;
+  return oracle_ffn_q(gating, skip_inactive, wdt, T, d, d_ff, r, x, w_gate, lopa_a, lopa_b, w_up, w_down_t, NULL,
+                      NULL, NULL, NULL, NULL, t, act, silu_up, g_idx, g_sign, rms_norm, rms_gain, rms_eps, h_out,
+                      z_out, active_out, y_out, macs_out);
 }
 
 /* oracle_ffn_ex with the default form: shifted ReLU, no activation on W3, G = 0, no norm */

@@ -47,9 +47,9 @@ def _load():
         lib = ctypes.CDLL(_LIB_PATH)
         vp = ctypes.c_void_p
         i, f = ctypes.c_int, ctypes.c_float
-        lib.oracle_ffn_ex.restype = i
-        lib.oracle_ffn_ex.argtypes = [i, i, i, i, i, i, i, vp, vp, vp, vp, vp, vp, f, i, i, vp, vp, i, vp, f,
-                                      vp, vp, vp, vp, vp]
+        lib.oracle_ffn_q.restype = i
+        lib.oracle_ffn_q.argtypes = [i, i, i, i, i, i, i, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, f, i, i, vp, vp,
+                                     i, vp, f, vp, vp, vp, vp, vp]
         _lib = lib
     return _lib
 
@@ -67,23 +67,34 @@ def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
+_WDTYPE = {0: np.float32, 1: np.uint16, 2: np.int8, 3: np.uint8}
+
+
 def _weights(w, wdt):
     if w is None:
         return None
-    want = np.float32 if wdt == 0 else np.uint16
+    want = _WDTYPE[wdt]
     w = np.ascontiguousarray(w)
     if w.dtype != want:
         raise TypeError(f"weights must be {want.__name__} for wdt={wdt}, got {w.dtype}")
     return w
 
 
+def _cols(w, wdt):
+    """Logical row length of a stored matrix (int4 packs two codes a byte)."""
+    return w.shape[1] * (2 if wdt == 3 else 1)
+
+
 def ffn(x, *, w_up, w_down_t, t, wdt, w_gate=None, lopa_a=None, lopa_b=None,
         skip_inactive=True, act=0, silu_up=False, g_idx=None, g_sign=None, rms_norm=False,
-        rms_gain=None, rms_eps=1e-6) -> OracleResult:
+        rms_gain=None, rms_eps=1e-6, scales=None) -> OracleResult:
     """Run the oracle on every token of ``x`` ([T, d] float32).
 
-    Weights: float32 arrays (wdt=0) or uint16 arrays holding bfloat16 bit patterns
-    (wdt=1), row-major: w_gate/w_up/w_down_t [d_ff, d], lopa_a [r, d], lopa_b [d_ff, r].
+    Weights: float32 arrays (wdt=0), uint16 arrays holding bfloat16 bit patterns
+    (wdt=1), int8 codes (wdt=2) or uint8 arrays of two int4 codes a byte, element 2k in
+    the low nibble (wdt=3), row-major: w_gate/w_up/w_down_t [d_ff, d], lopa_a [r, d],
+    lopa_b [d_ff, r] (int4: half the columns).  Quantized weights take ``scales``, a dict
+    of float32 row scales: gate [d_ff] or a [r] and b [d_ff], up [d_ff], down [d_ff].
     Exactly one of ``w_gate`` (standard gating) or ``lopa_a``+``lopa_b`` (LoPA) is given.
     ``skip_inactive`` selects the sparse method (True) or the dense FFN (False).
     ``act``: 0 shifted ReLU, 1 shifted R-S+; ``silu_up``: SiLU on the W3 output.
@@ -106,12 +117,23 @@ def ffn(x, *, w_up, w_down_t, t, wdt, w_gate=None, lopa_a=None, lopa_b=None,
     lopa_a = _weights(lopa_a, wdt)
     lopa_b = _weights(lopa_b, wdt)
     r = lopa_a.shape[0] if lopa else 0
-    if w_up.shape != (d_ff, d) or w_down_t.shape != (d_ff, d):
+    if w_up.shape[0] != d_ff or _cols(w_up, wdt) != d or w_down_t.shape[0] != d_ff or _cols(w_down_t, wdt) != d:
         raise ValueError("w_up and w_down_t must be [d_ff, d]")
-    if not lopa and w_gate.shape != (d_ff, d):
+    if not lopa and (w_gate.shape[0] != d_ff or _cols(w_gate, wdt) != d):
         raise ValueError("w_gate must be [d_ff, d]")
-    if lopa and (lopa_a.shape != (r, d) or lopa_b.shape != (d_ff, r)):
+    if lopa and (lopa_a.shape[0] != r or _cols(lopa_a, wdt) != d or lopa_b.shape[0] != d_ff or
+                 _cols(lopa_b, wdt) != r):
         raise ValueError("lopa_a must be [r, d] and lopa_b [d_ff, r]")
+    sc = {}
+    if wdt >= 2:
+        if scales is None:
+            raise ValueError("quantized weights need row scales")
+        want = dict(up=d_ff, down=d_ff, **(dict(a=r, b=d_ff) if lopa else dict(gate=d_ff)))
+        for k, n in want.items():
+            v = np.ascontiguousarray(scales[k], dtype=np.float32)
+            if v.shape != (n,):
+                raise ValueError(f"scales[{k!r}] must be [{n}]")
+            sc[k] = v
 
     h = np.empty((T, d_ff), np.float64)
     active = np.empty((T, d_ff), np.uint8)
@@ -125,11 +147,12 @@ def ffn(x, *, w_up, w_down_t, t, wdt, w_gate=None, lopa_a=None, lopa_b=None,
         raise ValueError("g_idx and g_sign must be [d_ff]")
     if gain is not None and gain.shape != (r,):
         raise ValueError("rms_gain must be [r]")
-    rc = lib.oracle_ffn_ex(1 if lopa else 0, 1 if skip_inactive else 0, wdt, T, d, d_ff, r,
-                           _ptr(x), _ptr(w_gate), _ptr(lopa_a), _ptr(lopa_b), _ptr(w_up), _ptr(w_down_t),
-                           ctypes.c_float(np.float32(t)), int(act), 1 if silu_up else 0, _ptr(gi), _ptr(gs),
-                           1 if rms_norm else 0, _ptr(gain), ctypes.c_float(np.float32(rms_eps)),
-                           _ptr(h), _ptr(z), _ptr(active), _ptr(y), _ptr(macs))
+    rc = lib.oracle_ffn_q(1 if lopa else 0, 1 if skip_inactive else 0, wdt, T, d, d_ff, r,
+                          _ptr(x), _ptr(w_gate), _ptr(lopa_a), _ptr(lopa_b), _ptr(w_up), _ptr(w_down_t),
+                          _ptr(sc.get("gate")), _ptr(sc.get("a")), _ptr(sc.get("b")), _ptr(sc.get("up")),
+                          _ptr(sc.get("down")), ctypes.c_float(np.float32(t)), int(act), 1 if silu_up else 0,
+                          _ptr(gi), _ptr(gs), 1 if rms_norm else 0, _ptr(gain), ctypes.c_float(np.float32(rms_eps)),
+                          _ptr(h), _ptr(z), _ptr(active), _ptr(y), _ptr(macs))
     if rc != 0:
-        raise ValueError(f"oracle_ffn_ex rejected its arguments (rc={rc})")
+        raise ValueError(f"oracle_ffn_q rejected its arguments (rc={rc})")
     return OracleResult(h=h, active=active.astype(bool), y=y, macs=macs, z=z)

@@ -15,6 +15,9 @@ Recipe (per weight set, ``seed``):
     B        [d_ff, r]   N(0, 1/r)       LoPA U factor
     W_up     [d_ff, d]   N(0, 1/d)
     W_down^T [d_ff, d]   N(0, 1/d_ff)    (row i = output vector of neuron i)
+Quantized weight sets (int8 / int4) draw the codes directly: per matrix a PCG64 stream gives
+q = clip(rint(N(0, (qmax/3)^2)), -qmax, qmax) with qmax = 127 or 7, then one scale per row,
+s_i = std / (qmax/3) * U(0.8, 1.2), so that s_i q_ij has about the standard deviation above.
 With these scales every gate pre-activation is close to N(0, 1), so the threshold
 t = Phi^-1(s) gives sparsity s: 0, 0.8416, 1.2816, 1.6449 for 50/80/90/95%.
 The full FFN form (LoPA's fixed term G, RMSNorm between the factors) takes its extra
@@ -34,6 +37,9 @@ import numpy as np
 
 F32 = 0
 BF16 = 1
+I8 = 2     # int8 codes with an fp32 scale per row
+I4 = 3     # int4 codes, two a byte (element 2k in the low nibble), fp32 scale per row
+QMAX = {I8: 127, I4: 7}
 
 # activation thresholds for a target sparsity under N(0, 1) gate pre-activations
 THRESHOLD = {0.50: 0.0, 0.80: 0.8416, 0.90: 1.2816, 0.95: 1.6449}
@@ -61,6 +67,35 @@ def _encode(a: np.ndarray, wdt: int) -> np.ndarray:
     return a if wdt == F32 else f32_to_bf16_bits(a)
 
 
+def pack_int4(q: np.ndarray) -> np.ndarray:
+    """int8 codes in [-8, 7], [rows, cols] with cols even -> uint8 [rows, cols/2], element 2k in
+    the low nibble of byte k (two's-complement nibbles)."""
+    q = np.asarray(q, np.int8)
+    lo = q[:, 0::2].astype(np.uint8) & np.uint8(15)
+    hi = (q[:, 1::2].astype(np.uint8) & np.uint8(15)) << np.uint8(4)
+    return (lo | hi).astype(np.uint8)
+
+
+def unpack_int4(b: np.ndarray) -> np.ndarray:
+    """Inverse of pack_int4."""
+    b = np.asarray(b, np.uint8)
+    lo = (b & np.uint8(15)).astype(np.int16)
+    hi = (b >> np.uint8(4)).astype(np.int16)
+    q = np.empty((b.shape[0], 2 * b.shape[1]), np.int16)
+    q[:, 0::2], q[:, 1::2] = lo, hi
+    return np.where(q >= 8, q - 16, q).astype(np.int8)
+
+
+def _codes(rng: np.random.Generator, shape, std: float, wdt: int):
+    """Quantized matrix of about the given standard deviation: (codes, row scales)."""
+    qmax = QMAX[wdt]
+    sq = qmax / 3.0
+    q = np.clip(np.rint(rng.standard_normal(size=shape, dtype=np.float32) * np.float32(sq)), -qmax, qmax)
+    q = q.astype(np.int8)
+    s = (np.float32(std / sq) * rng.uniform(0.8, 1.2, size=shape[0]).astype(np.float32)).astype(np.float32)
+    return (q if wdt == I8 else pack_int4(q)), s
+
+
 @dataclass
 class FFNInputs:
     x: np.ndarray                  # [T, d] float32
@@ -71,6 +106,7 @@ class FFNInputs:
     lopa_b: np.ndarray | None = None   # [d_ff, r] (LoPA)
     wdt: int = BF16
     meta: dict = field(default_factory=dict)
+    scales: dict | None = None     # int8 / int4: row scales gate | a, b, up, down (float32)
 
     @property
     def T(self):
@@ -94,6 +130,19 @@ def make_inputs(seed: int, T: int, d: int, d_ff: int, *, r: int = 0, wdt: int = 
     s_x, s_g, s_b, s_u, s_d = (np.random.Generator(np.random.PCG64(s))
                                for s in np.random.SeedSequence(seed).spawn(5))
     x = _normal(s_x, (T, d), 1.0)
+    if wdt in QMAX:
+        sc = {}
+        if r > 0:
+            lopa_a, sc["a"] = _codes(s_g, (r, d), d ** -0.5, wdt)
+            lopa_b, sc["b"] = _codes(s_b, (d_ff, r), r ** -0.5, wdt)
+            w_gate = None
+        else:
+            w_gate, sc["gate"] = _codes(s_g, (d_ff, d), d ** -0.5, wdt)
+            lopa_a = lopa_b = None
+        w_up, sc["up"] = _codes(s_u, (d_ff, d), d ** -0.5, wdt)
+        w_down_t, sc["down"] = _codes(s_d, (d_ff, d), d_ff ** -0.5, wdt)
+        return FFNInputs(x=x, w_up=w_up, w_down_t=w_down_t, w_gate=w_gate, lopa_a=lopa_a, lopa_b=lopa_b,
+                         wdt=wdt, meta=dict(seed=seed), scales=sc)
     if r > 0:
         lopa_a = _encode(_normal(s_g, (r, d), d ** -0.5), wdt)
         lopa_b = _encode(_normal(s_b, (d_ff, r), r ** -0.5), wdt)

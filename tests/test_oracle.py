@@ -60,6 +60,91 @@ def test_worked_example_standard(wdt):
     assert res.macs.tolist() == [48]
 
 
+def _quantize_exact(w, wdt):
+    """Codes and row scales of a hand-built matrix whose rows are (scale x small integers):
+    the scale is the row's largest magnitude, NaN rows get NaN scales and zero codes."""
+    w = np.asarray(w, np.float64)
+    codes = np.zeros(w.shape, np.int8)
+    scales = np.full(w.shape[0], np.nan, np.float32)
+    for i, row in enumerate(w):
+        if np.isnan(row).any():
+            continue
+        m = np.abs(row).max()
+        scales[i] = m if m > 0 else 1.0
+        q = row / scales[i]
+        assert np.array_equal(q, np.rint(q)) and np.abs(q).max() <= wl.QMAX[wdt]
+        codes[i] = q.astype(np.int8)
+    return (codes if wdt == wl.I8 else wl.pack_int4(codes)), scales
+
+
+@pytest.mark.parametrize("wdt", [wl.I8, wl.I4])
+def test_worked_example_quantized(wdt):
+    """The worked example with int8 / int4 codes and one scale per row (row i of W is
+    s_i q_i): the same gate values, active set, output and multiply-adds.  Inactive rows
+    carry NaN scales, so the sparse method must not read them; unit-vector rows pin the
+    nibble order (element 2k in the low nibble)."""
+    x, g, up, dn = _worked_standard()
+    qg, sg = _quantize_exact(g, wdt)
+    qu, su = _quantize_exact(up, wdt)
+    qd, sd = _quantize_exact(dn, wdt)
+    res = ffn_oracle.ffn(x, w_gate=qg, w_up=qu, w_down_t=qd, t=1.0, wdt=wdt,
+                         scales=dict(gate=sg, up=su, down=sd))
+    assert res.h.tolist() == [[1, 2, 3, 0.5, -1, 6]]
+    assert np.flatnonzero(res.active[0]).tolist() == [1, 2, 5]
+    assert res.y.tolist() == [[0.5, -2, -2, 15]]
+    assert res.macs.tolist() == [48]
+
+
+@pytest.mark.parametrize("wdt", [wl.I8, wl.I4])
+@pytest.mark.parametrize("r", [0, 16])
+def test_quantized_equals_float_on_dequantized_weights(wdt, r):
+    """Codes times row scales, written out as fp32 weights (exact: scales k / 2^12 with small
+    k), give the fp32 oracle's results bit for bit; decoding the int4 bytes here uses the
+    generator's unpacker, not the oracle's."""
+    T, d, d_ff = 3, 64, 200
+    rng = np.random.default_rng(21)
+    qmax = wl.QMAX[wdt]
+
+    def mat(rows, cols):
+        q = rng.integers(-qmax - (1 if wdt == wl.I4 else 0), qmax + 1, size=(rows, cols)).astype(np.int8)
+        s = (rng.integers(1, 4096, size=rows) / 4096.0 * (cols ** -0.5) * 8).astype(np.float32)
+        stored = q if wdt == wl.I8 else wl.pack_int4(q)
+        back = q if wdt == wl.I8 else wl.unpack_int4(stored)
+        assert np.array_equal(back, q)
+        deq = (s[:, None].astype(np.float64) * back).astype(np.float32)
+        assert np.array_equal(deq.astype(np.float64), s[:, None].astype(np.float64) * back)  # exact in fp32
+        return stored, s, deq
+
+    x = rng.standard_normal((T, d)).astype(np.float32)
+    up, s_up, f_up = mat(d_ff, d)
+    dn, s_dn, f_dn = mat(d_ff, d)
+    if r:
+        a, s_a, f_a = mat(r, d)
+        b, s_b, f_b = mat(d_ff, r)
+        qkw, fkw, sc = dict(lopa_a=a, lopa_b=b), dict(lopa_a=f_a, lopa_b=f_b), dict(a=s_a, b=s_b)
+    else:
+        g, s_g, f_g = mat(d_ff, d)
+        qkw, fkw, sc = dict(w_gate=g), dict(w_gate=f_g), dict(gate=s_g)
+    sc.update(up=s_up, down=s_dn)
+    for skip in (True, False):
+        q = ffn_oracle.ffn(x, w_up=up, w_down_t=dn, t=0.5, wdt=wdt, scales=sc, skip_inactive=skip, **qkw)
+        f = ffn_oracle.ffn(x, w_up=f_up, w_down_t=f_dn, t=0.5, wdt=wl.F32, skip_inactive=skip, **fkw)
+        assert np.array_equal(q.h, f.h) and np.array_equal(q.y, f.y) and np.array_equal(q.macs, f.macs)
+        assert 0 < q.active.sum() < q.active.size
+
+
+def test_quantized_rejects_bad_arguments():
+    inp = wl.make_inputs(3, 1, 64, 100, wdt=wl.I8)
+    with pytest.raises(ValueError):   # scales missing
+        ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.0, wdt=wl.I8)
+    with pytest.raises(ValueError):   # a scale vector of the wrong length
+        sc = dict(inp.scales, up=inp.scales["up"][:-1])
+        ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.0, wdt=wl.I8, scales=sc)
+    with pytest.raises(TypeError):    # int8 codes given as int4
+        ffn_oracle.ffn(inp.x, w_gate=inp.w_gate, w_up=inp.w_up, w_down_t=inp.w_down_t, t=0.0, wdt=wl.I4,
+                       scales=inp.scales)
+
+
 # LoPA, d=4, d_ff=6, r=2:  A rows e0, e2 -> z = (1, 3)
 #   B rows (1,0), (0,1), (1,1), (-1,0), (.5,.5), (2,-1) -> h = (1, 3, 4, -1, 2, -1)
 #   t = 1.5: active = {1, 2, 4}, a = (1.5, 2.5, 0.5)
