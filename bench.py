@@ -63,58 +63,106 @@ class Shape:
     seeded numpy generator (the oracle's inputs); sets 1.. are drawn on the device with
     a seeded torch generator from the same distributions."""
 
-    def __init__(self, d, d_ff, ranks, n_sets, seed, pool):
+    def __init__(self, d, d_ff, ranks, n_sets, seed, pool, wdt=None):
         import torch
         from paper_2609_31975_amd import workloads as wl
-        self.d, self.d_ff, self.n_sets, self.seed = d, d_ff, n_sets, seed
-        self.host0 = {r: wl.make_inputs(seed, 1, d, d_ff, r=r, wdt=wl.BF16) for r in ranks}
+        wdt = wl.BF16 if wdt is None else wdt
+        self.d, self.d_ff, self.n_sets, self.seed, self.wdt = d, d_ff, n_sets, seed, wdt
+        self.host0 = {r: wl.make_inputs(seed, 1, d, d_ff, r=r, wdt=wdt) for r in ranks}
         h0 = self.host0[ranks[0]]
         self.pool = pool
         self.x = []
         self.up, self.down, self.gate, self.lopa = [], [], [], {r: [] for r in ranks if r}
+        # quantized sets: the row scales of each matrix, same indexing as the codes
+        self.s_up, self.s_down, self.s_gate, self.s_lopa = [], [], [], {r: [] for r in ranks if r}
         g = torch.Generator(device="cuda")
+        quant = wdt in wl.QMAX
 
         def bf16(a):
+            if a.dtype != np.uint16:  # int8 / packed int4 codes, float32 scales
+                return torch.from_numpy(a).to("cuda")
             return torch.from_numpy(a.view(np.int16)).to("cuda").view(torch.bfloat16)
 
         def randn(shape, std, k, tag):
             g.manual_seed(seed * 1000003 + k * 101 + tag)
-            return (torch.randn(shape, generator=g, device="cuda") * std).to(torch.bfloat16)
+            if not quant:
+                dt = torch.float32 if wdt == wl.F32 else torch.bfloat16
+                return (torch.randn(shape, generator=g, device="cuda") * std).to(dt)
+            # codes and row scales drawn as the seeded generator does, on the device
+            qmax = wl.QMAX[wdt]
+            sq = qmax / 3.0
+            q = torch.clamp(torch.round(torch.randn(shape, generator=g, device="cuda") * sq), -qmax, qmax)
+            q = q.to(torch.int8)
+            if wdt == wl.I4:
+                q = ((q[:, 0::2].to(torch.uint8) & 15) | ((q[:, 1::2].to(torch.uint8) & 15) << 4)).contiguous()
+            sc = (std / sq) * (0.8 + 0.4 * torch.rand(shape[0], generator=g, device="cuda"))
+            return q, sc.to(torch.float32)
+
+        def put(codes_list, scale_list, v):
+            if quant:
+                codes_list.append(v[0])
+                scale_list.append(v[1])
+            else:
+                codes_list.append(v)
 
         for k in range(n_sets):
             if k == 0:
                 self.x.append(torch.from_numpy(wl.make_tokens(seed, pool, d)).to("cuda"))
-                self.up.append(bf16(h0.w_up))
-                self.down.append(bf16(h0.w_down_t))
-                self.gate.append(bf16(self.host0[0].w_gate) if 0 in ranks else None)
+
+                def host(h, name, key):
+                    a = bf16(getattr(h, name))
+                    return (a, bf16(h.scales[key])) if quant else a
+                put(self.up, self.s_up, host(h0, "w_up", "up"))
+                put(self.down, self.s_down, host(h0, "w_down_t", "down"))
+                if 0 in ranks:
+                    put(self.gate, self.s_gate, host(self.host0[0], "w_gate", "gate"))
+                else:
+                    self.gate.append(None)
                 for r in self.lopa:
-                    self.lopa[r].append((bf16(self.host0[r].lopa_a), bf16(self.host0[r].lopa_b)))
+                    a, b = host(self.host0[r], "lopa_a", "a"), host(self.host0[r], "lopa_b", "b")
+                    if quant:
+                        self.lopa[r].append((a[0], b[0]))
+                        self.s_lopa[r].append((a[1], b[1]))
+                    else:
+                        self.lopa[r].append((a, b))
             else:
                 g.manual_seed(seed * 1000003 + k * 101)
                 self.x.append(torch.randn((pool, d), generator=g, device="cuda"))
-                self.up.append(randn((d_ff, d), d ** -0.5, k, 1))
-                self.down.append(randn((d_ff, d), d_ff ** -0.5, k, 2))
-                self.gate.append(randn((d_ff, d), d ** -0.5, k, 3) if 0 in ranks else None)
+                put(self.up, self.s_up, randn((d_ff, d), d ** -0.5, k, 1))
+                put(self.down, self.s_down, randn((d_ff, d), d_ff ** -0.5, k, 2))
+                if 0 in ranks:
+                    put(self.gate, self.s_gate, randn((d_ff, d), d ** -0.5, k, 3))
+                else:
+                    self.gate.append(None)
                 for r in self.lopa:
-                    self.lopa[r].append((randn((r, d), d ** -0.5, k, 4 + 2 * r), randn((d_ff, r), r ** -0.5, k, 5 + 2 * r)))
+                    a, b = randn((r, d), d ** -0.5, k, 4 + 2 * r), randn((d_ff, r), r ** -0.5, k, 5 + 2 * r)
+                    if quant:
+                        self.lopa[r].append((a[0], b[0]))
+                        self.s_lopa[r].append((a[1], b[1]))
+                    else:
+                        self.lopa[r].append((a, b))
         torch.cuda.synchronize()
 
 
-def algorithmic_bytes(d, d_ff, r, T, n_union, dense):
-    """Bytes the method must move per call (bf16 weights, fp32 x and y)."""
-    wb = 2
-    gate = wb * (r * d + d_ff * r) if r else wb * d * d_ff
+# bytes per weight of each format (fp32, bf16, int8, int4); quantized rows add a 4-byte scale
+WEIGHT_BYTES = {0: 4, 1: 2, 2: 1, 3: 0.5}
+
+
+def algorithmic_bytes(d, d_ff, r, T, n_union, dense, wdt=1):
+    """Bytes the method must move per call (weights in format wdt, fp32 x and y)."""
+    wb, sb = WEIGHT_BYTES[wdt], (4 if wdt >= 2 else 0)
+    gate = (wb * (r * d + d_ff * r) + sb * (r + d_ff)) if r else (wb * d * d_ff + sb * d_ff)
     rows = d_ff if dense else n_union
-    return gate + 2 * wb * rows * d + 8 * T * d
+    return gate + 2 * (wb * d + sb) * rows + 8 * T * d
 
 
-def gate_kernel_bytes(d, d_ff, r, T, n_union, dense):
+def gate_kernel_bytes(d, d_ff, r, T, n_union, dense, wdt=1):
     """Algorithmic bytes of the gate kernel: the gate matrix (B for LoPA), the W_up rows
     it reads, and the tokens."""
-    wb = 2
-    gate = wb * d_ff * r if r else wb * d * d_ff
+    wb, sb = WEIGHT_BYTES[wdt], (4 if wdt >= 2 else 0)
+    gate = (wb * d_ff * r if r else wb * d * d_ff) + sb * d_ff
     rows = d_ff if dense else n_union
-    return gate + wb * rows * d + 4 * T * d + (4 * T * r if r else 0)
+    return gate + (wb * d + sb) * rows + 4 * T * d + (4 * T * r if r else 0)
 
 
 # ---------------------------------------------------------------- timing
@@ -142,7 +190,18 @@ class Runner:
     def __call__(self, i):
         s, f = self.s, self.ffn
         k, x = self.args(i)
-        if self.opt is not None:
+        if s.wdt >= 2:  # quantized weights: the _q calls with the set's row scales
+            if self.r:
+                a, b = s.lopa[self.r][k]
+                sa, sb = s.s_lopa[self.r][k]
+                sc = f.scales(lopa_a=sa, lopa_b=sb, up=s.s_up[k], down=s.s_down[k])
+                fn = f.ffn_lopa_dense_forward_q if self.dense else f.ffn_lopa_sparse_forward_q
+                fn(x, a, b, s.up[k], s.down[k], sc, self.t, self.opt, self.y, self.ws)
+            else:
+                sc = f.scales(gate=s.s_gate[k], up=s.s_up[k], down=s.s_down[k])
+                fn = f.ffn_dense_forward_q if self.dense else f.ffn_sparse_forward_q
+                fn(x, s.gate[k], s.up[k], s.down[k], sc, self.t, self.opt, self.y, self.ws)
+        elif self.opt is not None:
             a, b = s.lopa[self.r][k]
             fn = f.ffn_lopa_dense_forward_ex if self.dense else f.ffn_lopa_sparse_forward_ex
             fn(x, a, b, s.up[k], s.down[k], self.t, self.opt, self.y, self.ws)
@@ -243,7 +302,7 @@ def measure(shape, r, T, t, K, W, dense_us=None, name="", exact=False, form=None
     n = sp.union_sizes(K)
     us_wall, us_ev = time_graph(sp, K, W)
     nbar = float(np.mean(n))
-    by = np.mean([algorithmic_bytes(shape.d, shape.d_ff, r, T, k, False) for k in n])
+    by = np.mean([algorithmic_bytes(shape.d, shape.d_ff, r, T, k, False, shape.wdt) for k in n])
     rec = dict(workload=name, gating="lopa" if r else "standard", r=r, T=T, t=t, d=shape.d, d_ff=shape.d_ff,
                weight_sets=shape.n_sets, steps=K, us_per_call=round(us_wall, 3), us_per_call_events=round(us_ev, 3),
                n_union=round(nbar, 1), realized_union_frac=round(nbar / shape.d_ff, 4),
@@ -270,7 +329,7 @@ def dense_time(shape, r, T, K, W, exact=False, form=None):
         K = steps_for(de, K)
         W = min(W, K)
     us, _ = time_graph(de, K, W)
-    by = algorithmic_bytes(shape.d, shape.d_ff, r, T, shape.d_ff, True)
+    by = algorithmic_bytes(shape.d, shape.d_ff, r, T, shape.d_ff, True, shape.wdt)
     return us, dict(path="lopa_dense" if r else "dense", r=r, T=T, d=shape.d, d_ff=shape.d_ff,
                     us_per_call=round(us, 3), bytes_per_call=int(by),
                     hbm_gbps_touched=round(by / us / 1e3, 1), hbm_frac_touched=round(by / us / 1e3 / PEAK_HBM_GBPS, 4))
@@ -319,6 +378,8 @@ def parity_sample(shape: Shape, r, T, t, form=None, form_seed=None):
     y = run.y.cpu().numpy().astype(np.float64)
     x = run.args(0)[1].cpu().numpy()
     kw = dict(w_gate=inp.w_gate) if r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
+    if inp.scales is not None:
+        kw["scales"] = inp.scales
     if form is not None:
         fi = wl.make_form(form_seed, shape.d, shape.d_ff, r)
         kw.update(act=form["act"], silu_up=form["silu_up"], g_idx=fi.g_idx, g_sign=fi.g_sign,
@@ -395,29 +456,29 @@ def main():
 
     shapes = {}
 
-    def get_shape(d, d_ff, ranks, n_sets, seed, pool=64):
-        key = (d, d_ff)
+    def get_shape(d, d_ff, ranks, n_sets, seed, pool=64, wdt=wl.BF16):
+        key = (d, d_ff, wdt)
         if key not in shapes:
             shapes.clear()
             torch.cuda.empty_cache()
-            log(f"[bench] generating {n_sets} weight sets d={d} d_ff={d_ff} ranks={ranks}")
-            shapes[key] = Shape(d, d_ff, ranks, n_sets, seed, pool)
+            log(f"[bench] generating {n_sets} weight sets d={d} d_ff={d_ff} ranks={ranks} format={wdt}")
+            shapes[key] = Shape(d, d_ff, ranks, n_sets, seed, pool, wdt=wdt)
         return shapes[key]
 
     # ---- headline
     r0, T0 = head.r, head.T
-    per_call = algorithmic_bytes(head.d, head.d_ff, r0, T0, 0.1 * head.d_ff, False)
+    per_call = algorithmic_bytes(head.d, head.d_ff, r0, T0, 0.1 * head.d_ff, False, head.wdt)
     n_sets = sets_for(per_call, head.n_sets)
     ranks = sorted({0, 512} if head.d == 4096 else {0, 1024}) if not args.no_sweep else sorted({0, r0})
     lopa_sets = sets_for(algorithmic_bytes(head.d, head.d_ff, 512, 1, 0.1 * head.d_ff, False), head.n_sets)
     sh = get_shape(head.d, head.d_ff, ranks, max(n_sets, lopa_sets if not args.no_sweep else n_sets), head.seed,
-                   pool=max(64, 4 * 64))
+                   pool=max(64, 4 * 64), wdt=head.wdt)
     log(f"[bench] headline {head.name}: {sh.n_sets} sets, K={K}, W={W}")
     hform = full_form(sh, r0, head.seed) if head.form == "full" else None
     dense_us, dense_rec = dense_time(sh, 0, T0, K, W, exact=True)
     rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True, form=hform)
     gate_mean, gate_med = time_gate_kernel(run, K)
-    gbytes = np.mean([gate_kernel_bytes(head.d, head.d_ff, r0, T0, k, False) for k in nlist])
+    gbytes = np.mean([gate_kernel_bytes(head.d, head.d_ff, r0, T0, k, False, head.wdt) for k in nlist])
     par = parity_sample(sh, r0, T0, head.t, form=hform, form_seed=head.seed)
     traffic, traffic_src = recorded_traffic(head.name)
     log(f"[bench] headline {rec['us_per_call']} us/call, dense {dense_us:.2f}, gate kernel {gate_mean:.2f} us, "
@@ -435,7 +496,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
-        "weight_dtype": "bf16",
+        "weight_dtype": {0: "f32", 1: "bf16", 2: "int8", 3: "int4"}[head.wdt],
         "data": "synthetic: seeded Gaussian weights (N(0,1/d), W_down N(0,1/d_ff)), iid N(0,1) tokens",
         "config": {"workload": head.name, "d": head.d, "d_ff": head.d_ff, "T": T0, "gating": "lopa" if r0 else
                    "standard", "r": r0, "t": head.t, "weight_sets": sh.n_sets, "timing": "HIP graph of K calls"},
@@ -460,7 +521,7 @@ def main():
     host_head = sh.host0[r0]
     if not args.no_sweep:
         for w in wl.workloads():
-            if w.name == head.name or w.d != head.d or w.name.startswith("tiny"):
+            if w.name == head.name or w.d != head.d or w.name.startswith("tiny") or w.wdt != wl.BF16:
                 continue
             form = full_form(sh, w.r, w.seed) if w.form == "full" else None
             rw = measure(sh, w.r, w.T, w.t, K, W, name=w.name, form=form)[0]
@@ -481,10 +542,42 @@ def main():
             rw["path"] = "sparse"
             sweep.append(rw)
             log(f"[bench] {w.name}: {rw['us_per_call']} us, x{rw['speedup_vs_dense']} vs dense")
-        # 70B shapes
         del run
         shapes.clear()
         torch.cuda.empty_cache()
+        # quantized weights (8B shape, T = 1): sparse and dense in the same format, against
+        # the bf16 dense call and an fp32 dense call (the paper's full-precision baseline)
+        qw = [w for w in wl.workloads() if w.wdt in wl.QMAX and w.d == head.d]
+        if qw:
+            f32 = Shape(head.d, head.d_ff, [0], sets_for(algorithmic_bytes(head.d, head.d_ff, 0, 1, head.d_ff, True,
+                                                                          wl.F32), 2), head.seed, 64, wdt=wl.F32)
+            f32_us, _ = dense_time(f32, 0, 1, K, W)
+            del f32
+            torch.cuda.empty_cache()
+            log(f"[bench] fp32 dense {f32_us:.2f} us")
+            for wdt in sorted({w.wdt for w in qw}):
+                ws_ = [w for w in qw if w.wdt == wdt]
+                per = algorithmic_bytes(head.d, head.d_ff, 0, 1, 0.1 * head.d_ff, False, wdt)
+                shq = Shape(head.d, head.d_ff, sorted({0} | {w.r for w in ws_}), sets_for(per, 4), ws_[0].seed, 64,
+                            wdt=wdt)
+                qdense = {}
+                for w in ws_:
+                    rw = measure(shq, w.r, w.T, w.t, K, W, name=w.name)[0]
+                    if w.r not in qdense:
+                        qdense[w.r] = dense_time(shq, w.r, w.T, K, W)[0]
+                    rw.update(weights={wl.I8: "int8", wl.I4: "int4"}[wdt], path="sparse",
+                              dense_same_format_us_per_call=round(qdense[w.r], 3),
+                              speedup_vs_dense_same_format=round(qdense[w.r] / rw["us_per_call"], 3),
+                              dense_us_per_call=round(dense_us, 3),
+                              speedup_vs_dense=round(dense_us / rw["us_per_call"], 3),
+                              fp32_dense_us_per_call=round(f32_us, 3),
+                              speedup_vs_fp32_dense=round(f32_us / rw["us_per_call"], 3))
+                    sweep.append(rw)
+                    log(f"[bench] {w.name}: {rw['us_per_call']} us, x{rw['speedup_vs_dense']} vs bf16 dense, "
+                        f"x{rw['speedup_vs_fp32_dense']} vs fp32 dense")
+                del shq
+                torch.cuda.empty_cache()
+        # 70B shapes
         w70 = [w for w in wl.workloads() if w.d == 8192]
         if w70:
             per = algorithmic_bytes(8192, 28672, 1024, 1, 0.1 * 28672, False)

@@ -58,13 +58,20 @@
 extern "C" {
 #endif
 
-typedef enum { FFN_F32 = 0, FFN_BF16 = 1 } ffn_dtype_t;
+/* Weight formats.  FFN_F32 / FFN_BF16: the values.  FFN_I8 / FFN_I4 (the *_q calls only):
+ * weight-only quantized codes with one fp32 scale per stored matrix row, the weight
+ * being scale[row] * code; int8 codes are signed bytes, int4 codes two's-complement
+ * nibbles, two per byte, element 2k of a row in the low nibble of the row's byte k
+ * (rows of even length, each starting on a byte).  The appendix on quantization-aware
+ * training reads int8 / int4 weights at inference without fixing a scheme; this is the
+ * one taken. */
+typedef enum { FFN_F32 = 0, FFN_BF16 = 1, FFN_I8 = 2, FFN_I4 = 3 } ffn_dtype_t;
 
 enum {
   FFN_OK = 0,
   FFN_ERR_NULL = -1,      /* a required pointer is NULL */
   FFN_ERR_SHAPE = -2,     /* T, d, d_ff < 1, or r < 1 for LoPA, or a size overflows int32 indexing */
-  FFN_ERR_DTYPE = -3,     /* weight dtype is not FFN_F32 / FFN_BF16 */
+  FFN_ERR_DTYPE = -3,     /* weight dtype not FFN_F32 / FFN_BF16 (FFN_I8 / FFN_I4 for the *_q calls) */
   FFN_ERR_ALIGN = -4,     /* a pointer is not 16-byte aligned */
   FFN_ERR_WORKSPACE = -5, /* ws_bytes < ffn_workspace_bytes(...) */
   FFN_ERR_HIP = -6,       /* a HIP launch failed */
@@ -151,6 +158,45 @@ int ffn_lopa_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, int r, co
                               const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
                               float t, const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes,
                               hipStream_t stream);
+
+/* Row scales of quantized weights: device arrays of fp32 (4-byte aligned), one per stored
+ * row: gate [d_ff] (W_gate), lopa_a [r] (A), lopa_b [d_ff] (B), up [d_ff] (W_up),
+ * down [d_ff] (W_down^T, i.e. one per hidden neuron).  The ones the call uses must be
+ * non-NULL; the others are ignored.  The struct itself is host memory, read during the
+ * call only. */
+typedef struct {
+  const float* gate;
+  const float* lopa_a;
+  const float* lopa_b;
+  const float* up;
+  const float* down;
+} ffn_scales_t;
+
+/* The four forward calls with weights in any ffn_dtype_t: the *_ex arguments plus
+ * `scales` (required, with the arrays above, for FFN_I8 / FFN_I4; NULL for FFN_F32 /
+ * FFN_BF16).  Codes are device arrays, 16-byte aligned, row-major: a row of n int8 codes
+ * is n bytes, of n int4 codes n/2 bytes.  FFN_I4 needs d even, and r even for LoPA
+ * (else FFN_ERR_SHAPE).  Errors as for the other calls; FFN_ERR_NULL for a missing
+ * scales struct or array, FFN_ERR_ALIGN for a misaligned scale array, FFN_ERR_OPTION for
+ * scales with fp32 / bf16 weights.  Quantized weights take the single-token kernels
+ * (T = 1, d a multiple of 16 (int8) or 32 (int4), up to 8192) or the element-wise kernels
+ * (any other shape or batch).  The single-token kernels form their dot products with
+ * the integer dot instructions against a 24-bit fixed-point copy of x (or z): relative
+ * to the vector's largest magnitude, each element is exact to 2^-24. */
+int ffn_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                        const void* w_up, const void* w_down_t, const ffn_scales_t* scales, float t,
+                        const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes, hipStream_t stream);
+int ffn_sparse_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                         const void* w_up, const void* w_down_t, const ffn_scales_t* scales, float t,
+                         const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes, hipStream_t stream);
+int ffn_lopa_sparse_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                              const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                              const ffn_scales_t* scales, float t, const ffn_options_t* opt, float* y, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+int ffn_lopa_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                             const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                             const ffn_scales_t* scales, float t, const ffn_options_t* opt, float* y, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
 
 /* Inspection hook for tests and the benchmark (not on the hot path).  Synchronizes
  * `stream`, then copies the active set of the last forward call made with this

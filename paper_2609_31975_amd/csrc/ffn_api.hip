@@ -78,6 +78,8 @@ struct Call {
   void* ws;
   size_t ws_bytes;
   hipStream_t stream;
+  bool quant_call = false;             // a *_q entry point (any ffn_dtype_t)
+  const ffn_scales_t* scales = nullptr;
 };
 
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
@@ -105,24 +107,44 @@ int check_options(const ffn_options_t* o, bool lopa, Form* form) {
   return FFN_OK;
 }
 
+// The row scales of a quantized call, checked: FFN_OK with `out` filled, or an error.
+int check_scales(const Call& c, bool lopa, Scales* out) {
+  *out = Scales{};
+  const bool quant = c.wdt == FFN_I8 || c.wdt == FFN_I4;
+  if (!quant) return c.scales ? FFN_ERR_OPTION : FFN_OK;
+  if (!c.scales) return FFN_ERR_NULL;
+  const ffn_scales_t& s = *c.scales;
+  if (!s.up || !s.down || (lopa ? (!s.lopa_a || !s.lopa_b) : !s.gate)) return FFN_ERR_NULL;
+  if (!aligned4(s.up) || !aligned4(s.down) ||
+      (lopa ? (!aligned4(s.lopa_a) || !aligned4(s.lopa_b)) : !aligned4(s.gate)))
+    return FFN_ERR_ALIGN;
+  *out = lopa ? Scales{nullptr, s.lopa_a, s.lopa_b, s.up, s.down} : Scales{s.gate, nullptr, nullptr, s.up, s.down};
+  return FFN_OK;
+}
+
 int run(const Call& c) {
   const bool lopa = c.r > 0;
   if (!c.x || !c.gate || !c.w_up || !c.w_down_t || !c.y || !c.ws || (lopa && !c.lopa_a)) return FFN_ERR_NULL;
-  if (c.wdt != FFN_F32 && c.wdt != FFN_BF16) return FFN_ERR_DTYPE;
+  const bool quant = c.wdt == FFN_I8 || c.wdt == FFN_I4;
+  if ((c.wdt != FFN_F32 && c.wdt != FFN_BF16 && !quant) || (quant && !c.quant_call)) return FFN_ERR_DTYPE;
   const int sc = check_shape(c.T, c.d, c.d_ff, c.r, lopa);
   if (sc != FFN_OK) return sc;
+  if (c.wdt == FFN_I4 && (c.d % 2 != 0 || (lopa && c.r % 2 != 0))) return FFN_ERR_SHAPE;
   if (!aligned(c.x) || !aligned(c.gate) || !aligned(c.w_up) || !aligned(c.w_down_t) || !aligned(c.y) ||
       !aligned(c.ws) || (lopa && !aligned(c.lopa_a)))
     return FFN_ERR_ALIGN;
   Form form;
   const int so = check_options(c.opt, lopa, &form);
   if (so != FFN_OK) return so;
+  Scales scales;
+  const int ss = check_scales(c, lopa, &scales);
+  if (ss != FFN_OK) return ss;
   Workspace ws;
   if (c.ws_bytes < workspace_layout(c.T, c.d, c.d_ff, c.r, c.ws, &ws)) return FFN_ERR_WORKSPACE;
 
   // tokens run in passes of up to kTokChunk; each pass is an independent FFN call
   for (int t0 = 0; t0 < c.T; t0 += kTokChunk) {
-    Shape sh{c.T - t0 < kTokChunk ? c.T - t0 : kTokChunk, c.d, c.d_ff, c.r, c.wdt == FFN_BF16 ? 1 : 0};
+    Shape sh{c.T - t0 < kTokChunk ? c.T - t0 : kTokChunk, c.d, c.d_ff, c.r, (int)c.wdt, scales};
     const float* x = c.x + (size_t)t0 * c.d;
     float* y = c.y + (size_t)t0 * c.d;
     const Gate g = lopa ? Gate::LoPA : Gate::Standard;
@@ -208,6 +230,38 @@ int ffn_lopa_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, int r, co
                               hipStream_t stream) {
   if (r < 1) return FFN_ERR_SHAPE;
   return ffn::run(Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream});
+}
+
+int ffn_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                        const void* w_up, const void* w_down_t, const ffn_scales_t* scales, float t,
+                        const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return ffn::run(Call{wdt, T, d, d_ff, 0, true, x, w_gate, nullptr, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream,
+                       true, scales});
+}
+
+int ffn_sparse_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                         const void* w_up, const void* w_down_t, const ffn_scales_t* scales, float t,
+                         const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return ffn::run(Call{wdt, T, d, d_ff, 0, false, x, w_gate, nullptr, w_up, w_down_t, t, opt, y, ws, ws_bytes,
+                       stream, true, scales});
+}
+
+int ffn_lopa_sparse_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                              const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                              const ffn_scales_t* scales, float t, const ffn_options_t* opt, float* y, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  if (r < 1) return FFN_ERR_SHAPE;
+  return ffn::run(Call{wdt, T, d, d_ff, r, false, x, lopa_b, lopa_a, w_up, w_down_t, t, opt, y, ws, ws_bytes,
+                       stream, true, scales});
+}
+
+int ffn_lopa_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
+                             const void* lopa_a, const void* lopa_b, const void* w_up, const void* w_down_t,
+                             const ffn_scales_t* scales, float t, const ffn_options_t* opt, float* y, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  if (r < 1) return FFN_ERR_SHAPE;
+  return ffn::run(Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, opt, y, ws, ws_bytes, stream,
+                       true, scales});
 }
 
 int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,

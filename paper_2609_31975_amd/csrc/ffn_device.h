@@ -18,6 +18,19 @@ struct WBf16 {
 struct WF32 {
   static constexpr int EPC = 4;
 };
+// Quantized weights: codes with one fp32 scale per row.  The dot products against a
+// vector run on the 4-way byte dot instructions (v_dot4_i32_i8, v_dot4_u32_u8) against
+// the three bytes of a 24-bit fixed-point copy of the vector.  LB: bits per code.
+struct WI8 {  // signed bytes
+  static constexpr int EPC = 16, LB = 8;
+};
+struct WI4 {  // two's-complement nibbles, element 2k in the low nibble of byte k
+  static constexpr int EPC = 32, LB = 4;
+};
+template <class W>
+constexpr bool is_quant() {
+  return W::EPC >= 16;
+}
 
 __device__ __forceinline__ void unpack(WBf16, const uint4& v, float (&f)[8]) {
   // a bf16 is the high half of an fp32: shift the low element up, mask the high one
@@ -37,11 +50,33 @@ __device__ __forceinline__ void unpack(WF32, const uint4& v, float (&f)[4]) {
   f[3] = __uint_as_float(v.w);
 }
 
+__device__ __forceinline__ void unpack(WI8, const uint4& v, float (&f)[16]) {
+  const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int b = 0; b < 4; ++b) f[4 * i + b] = (float)((int32_t)(d[i] << (24 - 8 * b)) >> 24);
+}
+__device__ __forceinline__ void unpack(WI4, const uint4& v, float (&f)[32]) {
+  const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int b = 0; b < 8; ++b) f[8 * i + b] = (float)((int32_t)(d[i] << (28 - 4 * b)) >> 28);
+}
+
 __device__ __forceinline__ float welem(WBf16, const void* w, size_t k) {
   return __uint_as_float((uint32_t)(static_cast<const uint16_t*>(w)[k]) << 16);
 }
 __device__ __forceinline__ float welem(WF32, const void* w, size_t k) {
   return static_cast<const float*>(w)[k];
+}
+__device__ __forceinline__ float welem(WI8, const void* w, size_t k) {
+  return (float)static_cast<const int8_t*>(w)[k];
+}
+__device__ __forceinline__ float welem(WI4, const void* w, size_t k) {  // rows of even length
+  const uint32_t b = static_cast<const uint8_t*>(w)[k >> 1];
+  return (float)((int32_t)(b << (28 - 4 * (int)(k & 1))) >> 28);
 }
 
 // Weights are read once per call: stream them past the caches.
@@ -78,6 +113,16 @@ __device__ __forceinline__ float group_sum(float v, int width) {
   return v;
 }
 __device__ __forceinline__ float wave_sum(float v) { return group_sum(v, kWave); }
+__device__ __forceinline__ float group_max(float v, int width) {
+  if (width >= 2) v = fmaxf(v, dpp_move<kDppXor1>(v));
+  if (width >= 4) v = fmaxf(v, dpp_move<kDppXor2>(v));
+  if (width >= 8) v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
+  if (width >= 16) v = fmaxf(v, dpp_move<kDppMirror>(v));
+  if (width >= 32) v = fmaxf(v, __shfl_xor(v, 16));
+  if (width >= 64) v = fmaxf(v, __shfl_xor(v, 32));
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) { return group_max(v, kWave); }
 
 // Raw buffer loads.  A buffer resource covers [p, p + bytes), bytes < 2^31; a load at an
 // offset of kOOB or above returns zero without touching memory, so a lane with nothing to

@@ -66,20 +66,30 @@ struct Workspace {
 size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* out);
 
 // Kernel launch parameters decided on the host.
+// Row scales of quantized weights (FFN_I8 / FFN_I4): one fp32 per stored matrix row; all
+// null for fp32 / bf16 weights.
+struct Scales {
+  const float* gate = nullptr;  // [d_ff]
+  const float* a = nullptr;     // [r]
+  const float* b = nullptr;     // [d_ff]
+  const float* up = nullptr;    // [d_ff]
+  const float* down = nullptr;  // [d_ff]
+};
+
 struct Shape {
   int T, d, d_ff, r;
-  int wdt;  // 0 fp32, 1 bf16
+  int wdt;    // 0 fp32, 1 bf16, 2 int8, 3 int4 (the ffn_dtype_t values)
+  Scales sc;  // row scales (int8 / int4)
 };
 
 enum class Gate { Standard, LoPA };
 
-// The paper's full FFN form as the gate kernels see it (from ffn_options_t, checked on
-// the host): the activation, SiLU on the W_up output and LoPA's fixed term G.  The
-// norm on z is not here: it runs as a kernel of its own between z and the gate.
 // Compile-time form of a gate kernel: the default form, the full form's activations
 // only, or (LoPA) also G and RMSNorm.
 enum FormKind : int { kFormDefault = 0, kFormAct = 1, kFormLoPA = 2 };
 
+// The paper's full FFN form (from ffn_options_t, checked on the host): the activation,
+// SiLU on the W_up output, LoPA's fixed term G and RMSNorm of z.
 struct Form {
   int act = 0;                     // 0 shifted ReLU, 1 shifted R-S+
   int silu_up = 0;                 // 1: SiLU on the W_up output

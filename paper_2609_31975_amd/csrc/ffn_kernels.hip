@@ -51,30 +51,201 @@ __device__ __forceinline__ void load_vec(const float* __restrict__ v, int C, int
   }
 }
 
+// The vector a lane multiplies its chunks of a row with.  fp32 / bf16 weights: the fp32
+// elements.  Quantized weights: X = rint(v * 127 * 2^16 / max |v|), a 24-bit fixed-point
+// copy, kept as its three bytes: the signed top byte s2 and the unsigned bytes u1, u0,
+// four elements a word, in the order the codes' words take them (int4: each code word
+// gives a word of its even and one of its odd elements).  The dot products then run on
+// v_dot4_i32_i8 (codes x s2) and v_dot4_u32_u8 (codes + 128, or int4 codes + 8, x u1 and
+// x u0), and the per-lane sums of the limbs correct the offsets exactly in 32-bit
+// integers; `scale` turns the sums back into the vector's units.  The workgroup converts
+// the vector once, each thread a share, into LDS (prepare_lane_vec, called by dot_rows
+// after its first weight loads); each lane then reads the words of its chunks.
+template <class W, int CPL, bool Q = is_quant<W>()>
+struct LaneVec {
+  float f[CPL][W::EPC];
+};
 template <class W, int CPL>
-__device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const float (&v)[CPL][W::EPC]) {
-  float acc0 = 0.f, acc1 = 0.f;
-#pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    float f[W::EPC];
-    unpack(W{}, b[c], f);
-#pragma unroll
-    for (int e = 0; e < W::EPC; e += 2) {
-      acc0 = fmaf(f[e], v[c][e], acc0);
-      acc1 = fmaf(f[e + 1], v[c][e + 1], acc1);
-    }
+struct LaneVec<W, CPL, true> {
+  static constexpr int WPC = W::EPC / 4;  // limb words per chunk
+  uint32_t s2[CPL][WPC], u1[CPL][WPC], u0[CPL][WPC];
+  int32_t ss2, su1, su0;  // sums over the lane's elements
+  float scale;
+  const float* src;  // the vector, C chunks, until converted
+  int C, q, lpr;
+  bool ready;
+};
+
+template <class W, int CPL>
+__device__ __forceinline__ void make_lane_vec(const float* __restrict__ v, int C, int q, int lpr,
+                                              LaneVec<W, CPL>& out) {
+  if constexpr (!is_quant<W>()) {
+    load_vec<W, CPL>(v, C, q, lpr, out.f);
+  } else {
+    out.src = v;
+    out.C = C;
+    out.q = q;
+    out.lpr = lpr;
+    out.ready = false;
   }
-  return acc0 + acc1;
+}
+
+// The quantized vector's limb words, [3][kLimbWords]: s2, u1, u0 (vectors up to 8192).
+constexpr int kLimbWords = 2048;
+
+// Called by every thread of the workgroup at the same point (it has barriers).
+template <class W, int CPL>
+__device__ __forceinline__ void prepare_lane_vec(LaneVec<W, CPL>& out) {
+  if constexpr (is_quant<W>()) {
+    if (out.ready) return;
+    out.ready = true;
+    __shared__ uint32_t s_limb[3][kLimbWords];
+    __shared__ float s_max[2][kBlock / kWave];
+    constexpr float kFull = 127.f * 65536.f;
+    constexpr int G = W::LB == 8 ? 4 : 8;     // elements a thread converts at a time
+    constexpr int GPT = 8192 / G / kBlock;  // groups a thread holds (vectors of 8192 elements at most)
+    const int len = out.C * W::EPC, ngroups = len / G;
+    // the thread's groups: g = threadIdx.x + i * kBlock
+    float4 vals[GPT][G / 4];
+    float m = 0.f, nan = 0.f;
+#pragma unroll
+    for (int i = 0; i < GPT; ++i) {
+      const int g = (int)threadIdx.x + i * kBlock;
+#pragma unroll
+      for (int h = 0; h < G / 4; ++h) {
+        vals[i][h] = g < ngroups ? reinterpret_cast<const float4*>(out.src)[g * (G / 4) + h]
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 f = vals[i][h];
+        m = fmaxf(fmaxf(fmaxf(m, fabsf(f.x)), fmaxf(fabsf(f.y), fabsf(f.z))), fabsf(f.w));
+        nan += ((f.x * 0.f + f.y * 0.f) + (f.z * 0.f + f.w * 0.f));  // NaN if any is NaN or infinite
+      }
+    }
+    m = wave_max(m);
+    const float bad = wave_max(nan == 0.f ? 0.f : 1.f);
+    const int wave = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+      s_max[0][wave] = m;
+      s_max[1][wave] = bad;
+    }
+    __syncthreads();
+    float mm = 0.f, bb = 0.f;
+#pragma unroll
+    for (int w = 0; w < kBlock / kWave; ++w) {
+      mm = fmaxf(mm, s_max[0][w]);
+      bb = fmaxf(bb, s_max[1][w]);
+    }
+    const float k = (bb == 0.f && mm > 0.f) ? kFull / mm : 0.f;
+    out.scale = bb != 0.f ? __builtin_nanf("") : mm / kFull;
+#pragma unroll
+    for (int i = 0; i < GPT; ++i) {
+      const int g = (int)threadIdx.x + i * kBlock;
+      if (g < ngroups) {
+        const float e[8] = {vals[i][0].x, vals[i][0].y, vals[i][0].z, vals[i][0].w,
+                            vals[i][G / 4 - 1].x, vals[i][G / 4 - 1].y, vals[i][G / 4 - 1].z, vals[i][G / 4 - 1].w};
+#pragma unroll
+        for (int wi = 0; wi < G / 4; ++wi) {
+          // int8: the group's 4 elements; int4: its even (wi = 0) or odd (wi = 1) elements
+          int X[4];
+#pragma unroll
+          for (int b = 0; b < 4; ++b)  // |e k| <= kFull (NaN: clamped, the scale is NaN then)
+            X[b] = (int)rintf(fminf(fmaxf(e[G == 4 ? b : 2 * b + wi] * k, -kFull), kFull));
+          // byte j of X0..X3 into one word per j (v_perm_b32: selector bytes 0-3 pick the
+          // second operand's bytes, 4-7 the first's, 12 gives zero)
+          const uint32_t lo = __builtin_amdgcn_perm((uint32_t)X[1], (uint32_t)X[0], 0x06020400u);  // X0.b0 X1.b0 X0.b2 X1.b2
+          const uint32_t hi = __builtin_amdgcn_perm((uint32_t)X[3], (uint32_t)X[2], 0x06020400u);  // X2.b0 X3.b0 X2.b2 X3.b2
+          const uint32_t mid = __builtin_amdgcn_perm((uint32_t)X[1], (uint32_t)X[0], 0x0c0c0501u);  // X0.b1 X1.b1 0 0
+          const uint32_t mid2 = __builtin_amdgcn_perm((uint32_t)X[3], (uint32_t)X[2], 0x0c0c0501u); // X2.b1 X3.b1 0 0
+          const int word = g * (G / 4) + wi;
+          s_limb[0][word] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);     // byte 2 of X0..X3
+          s_limb[1][word] = __builtin_amdgcn_perm(mid2, mid, 0x05040100u);  // byte 1
+          s_limb[2][word] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);     // byte 0
+        }
+      }
+    }
+    __syncthreads();
+    constexpr int WPC = W::EPC / 4;
+    int32_t ss2 = 0, su1 = 0, su0 = 0;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int ch = out.q + c * out.lpr;
+#pragma unroll
+      for (int wi = 0; wi < WPC; ++wi) {
+        const bool ok = ch < out.C;
+        const int word = ch * WPC + wi;
+        const uint32_t w2 = ok ? s_limb[0][word] : 0u, w1 = ok ? s_limb[1][word] : 0u, w0 = ok ? s_limb[2][word] : 0u;
+        out.s2[c][wi] = w2;
+        out.u1[c][wi] = w1;
+        out.u0[c][wi] = w0;
+        ss2 = __builtin_amdgcn_sdot4((int)w2, 0x01010101, ss2, false);
+        su1 = (int32_t)__builtin_amdgcn_udot4(w1, 0x01010101u, (uint32_t)su1, false);
+        su0 = (int32_t)__builtin_amdgcn_udot4(w0, 0x01010101u, (uint32_t)su0, false);
+      }
+    }
+    out.ss2 = ss2;
+    out.su1 = su1;
+    out.su0 = su0;
+    __syncthreads();  // the limb words are read before any later conversion overwrites them
+  }
+}
+
+template <class W, int CPL>
+__device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const LaneVec<W, CPL>& v) {
+  if constexpr (!is_quant<W>()) {
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      float f[W::EPC];
+      unpack(W{}, b[c], f);
+#pragma unroll
+      for (int e = 0; e < W::EPC; e += 2) {
+        acc0 = fmaf(f[e], v.f[c][e], acc0);
+        acc1 = fmaf(f[e + 1], v.f[c][e + 1], acc1);
+      }
+    }
+    return acc0 + acc1;
+  } else {
+    int32_t a2 = 0;
+    uint32_t a1 = 0u, a0 = 0u;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const uint32_t cw[4] = {b[c].x, b[c].y, b[c].z, b[c].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (W::LB == 8) {  // signed codes w; w ^ 0x80 per byte = w + 128
+          const uint32_t off = cw[i] ^ 0x80808080u;
+          a2 = __builtin_amdgcn_sdot4((int)cw[i], (int)v.s2[c][i], a2, false);
+          a1 = __builtin_amdgcn_udot4(off, v.u1[c][i], a1, false);
+          a0 = __builtin_amdgcn_udot4(off, v.u0[c][i], a0, false);
+        } else {  // nibble n -> byte n + 8 (two's complement nibble xor 8), even then odd
+          const uint32_t ev = (cw[i] & 0x0F0F0F0Fu) ^ 0x08080808u;
+          const uint32_t od = ((cw[i] >> 4) & 0x0F0F0F0Fu) ^ 0x08080808u;
+          a2 = __builtin_amdgcn_sdot4((int)ev, (int)v.s2[c][2 * i], a2, false);
+          a2 = __builtin_amdgcn_sdot4((int)od, (int)v.s2[c][2 * i + 1], a2, false);
+          a1 = __builtin_amdgcn_udot4(ev, v.u1[c][2 * i], a1, false);
+          a1 = __builtin_amdgcn_udot4(od, v.u1[c][2 * i + 1], a1, false);
+          a0 = __builtin_amdgcn_udot4(ev, v.u0[c][2 * i], a0, false);
+          a0 = __builtin_amdgcn_udot4(od, v.u0[c][2 * i + 1], a0, false);
+        }
+      }
+    }
+    // remove the code offsets: int8 sum (w + 128) u = sum w u + 128 sum u; int4 likewise
+    // with 8, also on the signed limb
+    constexpr int kOff = W::LB == 8 ? 128 : 8;
+    const int32_t e2 = W::LB == 8 ? a2 : a2 - kOff * v.ss2;
+    const int32_t e1 = (int32_t)a1 - kOff * v.su1, e0 = (int32_t)a0 - kOff * v.su0;
+    return fmaf((float)e2, 65536.f, fmaf((float)e1, 256.f, (float)e0)) * v.scale;
+  }
 }
 
 // Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n), of a matrix of
 // `bytes` bytes (< 2^31): each wave takes passes of 64/lpr rows (passes wave, wave + 4,
 // ...).  For rows of at most 8 chunks per lane and more than one pass per wave, two
-// register sets alternate, the loads of the next pass issued before the current pass is
-// reduced; the loads are raw buffer loads (out-of-range offsets past the last pass), so
-// every pass issues the same loads and the load-counter waits are exact.  A pair of
-// passes always runs both halves (a pass past the last one loads nothing and sinks
-// nothing) and the exit test closes the pair, so no load sits on a conditional path.
+// register sets alternate (four for at most 4 chunks a lane), the loads of the next
+// passes issued before the current pass is reduced; the loads are raw buffer loads
+// (out-of-range offsets past the last pass), so every pass issues the same loads and the
+// load-counter waits are exact.  A group of passes always runs whole (a pass past the
+// last one loads nothing and sinks nothing) and the exit test closes the group, so no
+// load sits on a conditional path.
 // `sink(k, value)` runs on lane q == 0.
 template <class W, int CPL>
 __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, bool ok, int row, uint4 (&b)[CPL]) {
@@ -88,14 +259,13 @@ __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, 
 
 template <class W, int CPL, class RowOf, class Sink>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
-                                         int n, const float (&v)[CPL][W::EPC], RowOf row_of, Sink sink) {
+                                         int n, LaneVec<W, CPL>& v, RowOf row_of, Sink sink) {
   constexpr int kWaves = kBlock / kWave;
   const Buf mb = make_buf(mat, bytes);
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int q = lane & (lpr - 1), p = lane >> lpr_log2;
   const int rpp = kWave >> lpr_log2;
   const int npass = (n + rpp - 1) / rpp;
-  if (wave >= npass) return;
   auto load = [&](uint4 (&b)[CPL], int pass) {
     const int k = pass * rpp + p;
     const bool ok = pass < npass && k < n;
@@ -106,14 +276,38 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
     const float sum = group_sum(lane_dot<W, CPL>(b, v), lpr);
     if (q == 0 && k < n) sink(k, sum);
   };
-  uint4 b0[CPL];
-  load(b0, wave);
+  constexpr bool DEEP = CPL <= 4;  // short lane rows (the quantized formats): four passes in
+                                   // flight, as many bytes outstanding as two bf16 passes
+  uint4 b0[CPL], b1[CPL], b2[CPL];
+  load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
+  if constexpr (DEEP) {
+    load(b1, wave + kWaves);
+    load(b2, wave + 2 * kWaves);
+  }
+  prepare_lane_vec<W, CPL>(v);  // quantized: the whole workgroup converts the vector
+  if (wave >= npass) return;
   if (wave + kWaves >= npass) {  // a single pass: nothing to overlap
     finish(b0, wave);
     return;
   }
-  if constexpr (CPL <= 8) {
-    uint4 b1[CPL];
+  if constexpr (DEEP) {
+    uint4 b3[CPL];
+    for (int pass = wave;; pass += 4 * kWaves) {
+      load(b3, pass + 3 * kWaves);
+      issue_barrier();
+      finish(b0, pass);
+      load(b0, pass + 4 * kWaves);
+      issue_barrier();
+      finish(b1, pass + kWaves);
+      load(b1, pass + 5 * kWaves);
+      issue_barrier();
+      finish(b2, pass + 2 * kWaves);
+      load(b2, pass + 6 * kWaves);
+      issue_barrier();
+      finish(b3, pass + 3 * kWaves);
+      if (pass + 4 * kWaves >= npass) break;
+    }
+  } else if constexpr (CPL <= 8) {
     for (int pass = wave;; pass += 2 * kWaves) {
       load(b1, pass + kWaves);
       issue_barrier();
@@ -175,22 +369,39 @@ template <class W, int CPL, bool NORM>
 __global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ x, const uint4* __restrict__ A,
                                                       int C, int lpr, int lpr_log2, int r, float* __restrict__ z,
                                                       const float* __restrict__ gain, float* __restrict__ zsq,
-                                                      GWork gw) {
+                                                      GWork gw, const float* __restrict__ s_a) {
   if (g_precompute(gw)) return;
-  float xr[CPL][W::EPC];
-  load_vec<W, CPL>(x, C, lane_id() & (lpr - 1), lpr, xr);
+  __shared__ float s_z[kBlock];  // quantized: the block's sums before their row scales
+  LaneVec<W, CPL> xr;
+  make_lane_vec<W, CPL>(x, C, lane_id() & (lpr - 1), lpr, xr);
   const int rows_per_block = (kBlock / kWave) * (kWave >> lpr_log2);
   const int k0 = blockIdx.x * rows_per_block;
   const int n = min(rows_per_block, r - k0);
+  auto put = [&](int k, float s) {
+    if constexpr (NORM) {
+      z[k0 + k] = gain ? s * gain[k0 + k] : s;
+      zsq[k0 + k] = s * s;
+    } else {
+      z[k0 + k] = s;
+    }
+  };
+  // quantized: thread i's row scale, loaded before the stream and applied after it
+  const float sa = is_quant<W>() ? __builtin_bit_cast(float, ldb32(make_buf(s_a, 4u * (uint32_t)r),
+                                                                   (int)threadIdx.x < n
+                                                                       ? 4u * (uint32_t)(k0 + (int)threadIdx.x)
+                                                                       : kOOB))
+                                 : 1.f;
   dot_rows<W, CPL>(A, 16u * (uint32_t)r * (uint32_t)C, C, lpr, lpr_log2, n, xr, [&](int k) { return k0 + k; },
                    [&](int k, float s) {
-                     if constexpr (NORM) {
-                       z[k0 + k] = gain ? s * gain[k0 + k] : s;
-                       zsq[k0 + k] = s * s;
-                     } else {
-                       z[k0 + k] = s;
-                     }
+                     if constexpr (is_quant<W>())
+                       s_z[k] = s;
+                     else
+                       put(k, s);
                    });
+  if constexpr (is_quant<W>()) {
+    __syncthreads();
+    if ((int)threadIdx.x < n) put(threadIdx.x, s_z[threadIdx.x] * sa);
+  }
 }
 
 // One segment: gate values, compaction, W_up dots of the selected neurons.
@@ -207,12 +418,14 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
                                                        int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                                        float* __restrict__ seg_zval, float* __restrict__ y, int d,
                                                        Form form, const float* __restrict__ zsq,
-                                                       const float* __restrict__ gx) {
+                                                       const float* __restrict__ gx, const float* __restrict__ s_g,
+                                                       const float* __restrict__ s_up) {
   constexpr bool FULL = FORM != kFormDefault, EXTRA = LOPA && FORM == kFormLoPA;
   __shared__ float s_h[kSegMax];
   __shared__ float s_ss[kBlock / kWave];
   __shared__ int s_list[kSegMax];
   __shared__ float s_act[kSegMax];
+  __shared__ float s_usc[kSegMax];  // quantized: the W_up row scales of the segment
   __shared__ int s_cnt;
 
   const int seg = blockIdx.x;
@@ -220,10 +433,29 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
   const int row0 = segs.start(seg);
   const int nrows = segs.start(seg + 1) - row0;
   clear_output(y, d, meta, nseg);
+  // quantized: thread i's row scales (gate, W_up), loaded branch-free before the streams and
+  // applied after the gate stream, so that no load waits inside a stream
+  const bool own = (int)threadIdx.x < nrows;
+  const uint32_t srow = own ? 4u * (uint32_t)(row0 + (int)threadIdx.x) : kOOB;
+  const float sg = is_quant<W>() ? __builtin_bit_cast(float, ldb32(make_buf(s_g, 4u * (uint32_t)d_ff), srow)) : 1.f;
+  const float su = is_quant<W>() ? __builtin_bit_cast(float, ldb32(make_buf(s_up, 4u * (uint32_t)d_ff), srow)) : 1.f;
   auto gate_sink = [&](int k, float s) { s_h[k] = s; };
   auto gate_row = [&](int k) { return row0 + k; };
   auto up_row = [&](int e) { return row0 + s_list[e]; };
-  auto up_sink = [&](int e, float v) { seg_zval[row0 + e] = s_act[e] * (FULL ? up_value(form.silu_up, v) : v); };
+  auto up_sink = [&](int e, float v) {
+    if constexpr (is_quant<W>()) v *= s_usc[s_list[e]];
+    seg_zval[row0 + e] = s_act[e] * (FULL ? up_value(form.silu_up, v) : v);
+  };
+  // after the gate stream: the gate's row scales, and the W_up ones to LDS
+  auto apply_scales = [&] {
+    if constexpr (is_quant<W>()) {
+      if (own) {
+        s_h[threadIdx.x] *= sg;
+        s_usc[threadIdx.x] = su;
+      }
+      __syncthreads();
+    }
+  };
   const int act = FULL ? form.act : 0;
 
   if constexpr (LOPA) {
@@ -248,14 +480,14 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
       }
     }
     {
-      float zr[CPLG][W::EPC];
-      const int q = lane_id() & (lprg - 1);
-      load_vec<W, CPLG>(z, Cg, q, lprg, zr);
+      LaneVec<W, CPLG> zr;
+      make_lane_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
       dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
                         gate_sink);
     }
     const float gv = __builtin_bit_cast(float, gbits);
     __syncthreads();
+    apply_scales();
     if constexpr (EXTRA) {
       float inv = 1.f;
       if (norm) {  // 1 / sqrt(mean z^2 + eps)
@@ -278,16 +510,17 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
     }
     compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
-    float xr[CPLU][W::EPC];
-    load_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
+    LaneVec<W, CPLU> xr;
+    make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
     dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   } else {
     static_assert(CPLG == CPLU, "standard gating shares the x registers");
-    float xr[CPLU][W::EPC];
-    load_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
+    LaneVec<W, CPLU> xr;
+    make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
     dot_rows<W, CPLU>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, xr, gate_row,
                       gate_sink);
     __syncthreads();
+    apply_scales();
     compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
     dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
@@ -306,7 +539,7 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
                                                     const int32_t* __restrict__ seg_idx,
                                                     const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
                                                     const uint4* __restrict__ w_down_t, int C, int d,
-                                                    float* __restrict__ y) {
+                                                    float* __restrict__ y, const float* __restrict__ s_down) {
   constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave;
   extern __shared__ int s_dyn[];  // raw slots, then the compacted list (sparse only)
   __shared__ int s_cnt[kWave];
@@ -379,6 +612,7 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
       // a zero gated value (the s_gated site) needs no W_down row
       const bool need = ok && cvalid && (DENSE || zz[u] != 0.f);
       wv[u] = need ? ld_weights(w_down_t + (size_t)row * C + ch) : make_uint4(0u, 0u, 0u, 0u);
+      if constexpr (is_quant<W>()) zz[u] *= ok ? s_down[row] : 0.f;  // the row's scale
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -405,7 +639,8 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
 // batches the specialised kernels do not cover.
 template <class W>
 __global__ __launch_bounds__(kBlock) void k_lopa_z_generic(const float* __restrict__ x, const void* __restrict__ A,
-                                                           int T, int d, int r, float* __restrict__ z) {
+                                                           int T, int d, int r, float* __restrict__ z,
+                                                           const float* __restrict__ s_a) {
   const int k = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
   if (k >= r) return;
   const int lane = lane_id();
@@ -413,6 +648,7 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_generic(const float* __restri
     float s = 0.f;
     for (int j = lane; j < d; j += kWave) s = fmaf(welem(W{}, A, (size_t)k * d + j), x[(size_t)tau * d + j], s);
     s = wave_sum(s);
+    if constexpr (is_quant<W>()) s *= s_a[k];
     if (lane == 0) z[(size_t)tau * r + k] = s;
   }
 }
@@ -427,7 +663,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
                                                             int32_t* __restrict__ seg_idx,
                                                             float* __restrict__ seg_act,
                                                             float* __restrict__ seg_zval, float* __restrict__ y,
-                                                            Form form) {
+                                                            Form form, const float* __restrict__ s_g,
+                                                            const float* __restrict__ s_up) {
   __shared__ float s_h[kSegMax][kTokChunk];
   __shared__ int s_list[kSegMax];
   __shared__ int s_cnt;
@@ -446,6 +683,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
       float s = 0.f;
       for (int j = lane; j < len; j += kWave) s = fmaf(welem(W{}, gate_w, rowoff + j), vec[(size_t)tau * len + j], s);
       s = wave_sum(s);
+      if constexpr (is_quant<W>()) s *= s_g[row0 + k];
       if (lane == 0) s_h[k][tau] = s;
     }
   }
@@ -493,6 +731,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
       float s = 0.f;
       for (int j = lane; j < d; j += kWave) s = fmaf(welem(W{}, w_up, rowoff + j), x[(size_t)tau * d + j], s);
       s = wave_sum(s);
+      if constexpr (is_quant<W>()) s *= s_up[row0 + kr];
       if (lane == 0) seg_zval[(size_t)tau * slots + row0 + e] = s_h[kr][tau] * (FULL ? up_value(form.silu_up, s) : s);
     }
   }
@@ -504,7 +743,7 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
                                                          const int32_t* __restrict__ seg_idx,
                                                          const float* __restrict__ seg_zval, int nseg, int d_ff,
                                                          int slots, const void* __restrict__ w_down_t, int T, int d,
-                                                         float* __restrict__ y) {
+                                                         float* __restrict__ y, const float* __restrict__ s_down) {
   extern __shared__ int s_pre[];  // [nseg + 1] list offsets (sparse only)
   __shared__ int s_slot[kListWindow];
   const int col = blockIdx.x * kBlock + threadIdx.x;
@@ -537,7 +776,8 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
         for (int k = 0; k < wn; ++k) {
           const int slot = DENSE ? base + k : s_slot[k];
           const int row = DENSE ? slot : seg_idx[slot];
-          const float w = welem(W{}, w_down_t, (size_t)row * d + col);
+          float w = welem(W{}, w_down_t, (size_t)row * d + col);
+          if constexpr (is_quant<W>()) w *= s_down[row];
 #pragma unroll
           for (int u = 0; u < 8; ++u)
             if (u < tn) {
@@ -567,7 +807,25 @@ int lanes_per_row(int C, int cpl) {
   return lpr;
 }
 
-int cpl_for(int C) { return C <= 8 * kWave ? 8 : (C <= 16 * kWave ? 16 : 0); }
+// chunks a lane holds of a vector of C chunks: `lo` if 64 lanes cover it so, else 2 lo,
+// else 0 (too long for the single-token kernels)
+int cpl_pick(int C, int lo) { return C <= lo * kWave ? lo : (C <= 2 * lo * kWave ? 2 * lo : 0); }
+// the smaller choice per format: 16-byte chunks hold 4 to 32 elements, and the quantized
+// formats keep their vector as limbs (3 or 6 words per 4 words of codes)
+template <class W>
+constexpr int cpl_lo() {
+  if constexpr (is_quant<W>())
+    return W::LB == 8 ? 4 : 2;
+  else
+    return 8;
+}
+int cpl_for(int C) { return cpl_pick(C, 8); }
+// bytes of a rows x cols matrix in format wdt
+int64_t mat_bytes(int wdt, int64_t rows, int64_t cols) {
+  return wdt == 0 ? 4 * rows * cols : wdt == 1 ? 2 * rows * cols : wdt == 2 ? rows * cols : rows * (cols / 2);
+}
+int epc_of(int wdt) { return wdt == 0 ? WF32::EPC : wdt == 1 ? WBf16::EPC : wdt == 2 ? WI8::EPC : WI4::EPC; }
+int cpl_lo_of(int wdt) { return wdt == 0 ? cpl_lo<WF32>() : wdt == 1 ? cpl_lo<WBf16>() : wdt == 2 ? cpl_lo<WI8>() : cpl_lo<WI4>(); }
 
 int cu_count() {
   static int cus[16] = {0};
@@ -602,12 +860,12 @@ int resident_segments(K kernel, int* per_cu, int d_ff) {
 
 // The fast single-token kernels address a matrix with 32-bit byte offsets below 2^31.
 bool fast_ok(const Shape& sh, Gate g) {
-  const int epc_ = sh.wdt == 1 ? WBf16::EPC : WF32::EPC;
-  const int64_t wb = sh.wdt == 1 ? 2 : 4, lim = int64_t(1) << 31;
-  if (sh.T != 1 || sh.d % epc_ != 0 || cpl_for(sh.d / epc_) == 0) return false;
-  if (wb * sh.d_ff * sh.d >= lim) return false;
-  if (g == Gate::LoPA && (sh.r % epc_ != 0 || cpl_for(sh.r / epc_) == 0 || wb * sh.r * sh.d >= lim ||
-                          wb * sh.d_ff * sh.r >= lim))
+  const int epc_ = epc_of(sh.wdt), lo = cpl_lo_of(sh.wdt);
+  const int64_t lim = int64_t(1) << 31;
+  if (sh.T != 1 || sh.d % epc_ != 0 || cpl_pick(sh.d / epc_, lo) == 0) return false;
+  if (mat_bytes(sh.wdt, sh.d_ff, sh.d) >= lim) return false;
+  if (g == Gate::LoPA && (sh.r % epc_ != 0 || cpl_pick(sh.r / epc_, lo) == 0 ||
+                          mat_bytes(sh.wdt, sh.r, sh.d) >= lim || mat_bytes(sh.wdt, sh.d_ff, sh.r) >= lim))
     return false;
   return true;
 }
@@ -623,24 +881,23 @@ hipError_t go_gate_up_t1(const Shape& sh, const Form& form, const float* x, cons
   return launch_gate_kernel(kernel, ws.nseg, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg, lprg,
                             ilog2(lprg), static_cast<const uint4*>(w_up), Cu, lpru, ilog2(lpru), sh.d_ff, ws.nseg, t,
                             ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d, form,
-                            (const float*)ws.zsq, (const float*)ws.gx);
+                            (const float*)ws.zsq, (const float*)ws.gx, LOPA ? sh.sc.b : sh.sc.gate, sh.sc.up);
 }
 
 template <class W, bool LOPA, bool DENSE, int FORM>
 hipError_t gate_up_fast(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
                         Workspace& ws, float* y, hipStream_t s) {
-  const int cplu = cpl_for(sh.d / W::EPC);
+  constexpr int L = cpl_lo<W>(), H = 2 * L;
+  const int cplu = cpl_pick(sh.d / W::EPC, L);
   if constexpr (LOPA) {
-    const int cplg = cpl_for(sh.r / W::EPC);
-    if (cplg == 8 && cplu == 8) return go_gate_up_t1<W, true, DENSE, FORM, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
-    if (cplg == 8 && cplu == 16)
-      return go_gate_up_t1<W, true, DENSE, FORM, 8, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
-    if (cplg == 16 && cplu == 8)
-      return go_gate_up_t1<W, true, DENSE, FORM, 16, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
-    return go_gate_up_t1<W, true, DENSE, FORM, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    const int cplg = cpl_pick(sh.r / W::EPC, L);
+    if (cplg == L && cplu == L) return go_gate_up_t1<W, true, DENSE, FORM, L, L>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == L && cplu == H) return go_gate_up_t1<W, true, DENSE, FORM, L, H>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplg == H && cplu == L) return go_gate_up_t1<W, true, DENSE, FORM, H, L>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, true, DENSE, FORM, H, H>(sh, f, x, gate_w, w_up, t, ws, y, s);
   } else {
-    if (cplu == 8) return go_gate_up_t1<W, false, DENSE, FORM, 8, 8>(sh, f, x, gate_w, w_up, t, ws, y, s);
-    return go_gate_up_t1<W, false, DENSE, FORM, 16, 16>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (cplu == L) return go_gate_up_t1<W, false, DENSE, FORM, L, L>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    return go_gate_up_t1<W, false, DENSE, FORM, H, H>(sh, f, x, gate_w, w_up, t, ws, y, s);
   }
 }
 
@@ -650,7 +907,7 @@ hipError_t gate_up_generic(const Shape& sh, const Form& f, const float* x, const
   ws.nseg = (sh.d_ff + kSegGeneric - 1) / kSegGeneric;
   return launch_gate_kernel(k_gate_up_generic<W, LOPA, DENSE, FULL>, ws.nseg, s, x, (const float*)ws.z, gate_w, w_up,
                             sh.T, sh.d, sh.d_ff, sh.r, ws.nseg, t, ws.slots, ws.meta, ws.seg_count, ws.seg_idx,
-                            ws.seg_act, ws.seg_zval, y, f);
+                            ws.seg_act, ws.seg_zval, y, f, LOPA ? sh.sc.b : sh.sc.gate, sh.sc.up);
 }
 
 // RMSNorm on z (Section 3.3), one workgroup per token: the partial copies summed into
@@ -700,8 +957,9 @@ template <class W>
 hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void* A, const Workspace& ws,
                   hipStream_t s) {
   if (fast_ok(sh, Gate::LoPA)) {
+    constexpr int L = cpl_lo<W>(), H = 2 * L;
     const int C = sh.d / W::EPC;
-    const int cpl = cpl_for(C), lpr = lanes_per_row(C, cpl), lg = ilog2(lpr);
+    const int cpl = cpl_pick(C, L), lpr = lanes_per_row(C, cpl), lg = ilog2(lpr);
     const int rows_per_block = (kBlock / kWave) * (kWave >> lg);
     const int grid = (sh.r + rows_per_block - 1) / rows_per_block;
     const uint4* a = static_cast<const uint4*>(A);
@@ -709,17 +967,19 @@ hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void*
     // with G, extra workgroups write G x for the gate kernel
     const GWork gw{form, x, ws.gx, 1, sh.d, sh.d_ff, grid};
     const int g = grid + (form.g_idx ? (g_items(sh.d_ff, 1) + kBlock - 1) / kBlock : 0);
-    if (cpl == 8 && norm)
-      k_lopa_z_t1<W, 8, true><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, form.rms_gain, ws.zsq, gw);
-    else if (cpl == 8)
-      k_lopa_z_t1<W, 8, false><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, nullptr, nullptr, gw);
+    const float* gain = norm ? form.rms_gain : nullptr;
+    float* zsq = norm ? ws.zsq : nullptr;
+    if (cpl == L && norm)
+      k_lopa_z_t1<W, L, true><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, gain, zsq, gw, sh.sc.a);
+    else if (cpl == L)
+      k_lopa_z_t1<W, L, false><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, gain, zsq, gw, sh.sc.a);
     else if (norm)
-      k_lopa_z_t1<W, 16, true><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, form.rms_gain, ws.zsq, gw);
+      k_lopa_z_t1<W, H, true><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, gain, zsq, gw, sh.sc.a);
     else
-      k_lopa_z_t1<W, 16, false><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, nullptr, nullptr, gw);
+      k_lopa_z_t1<W, H, false><<<g, kBlock, 0, s>>>(x, a, C, lpr, lg, sh.r, ws.z, gain, zsq, gw, sh.sc.a);
   } else {
     const int grid = (sh.r + kBlock / kWave - 1) / (kBlock / kWave);
-    k_lopa_z_generic<W><<<grid, kBlock, 0, s>>>(x, A, sh.T, sh.d, sh.r, ws.z);
+    k_lopa_z_generic<W><<<grid, kBlock, 0, s>>>(x, A, sh.T, sh.d, sh.r, ws.z, sh.sc.a);
   }
   return hipGetLastError();
 }
@@ -749,12 +1009,12 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
     const size_t shmem = DENSE ? 0 : 4 * sizeof(int) * rows;
     if (shmem > 96 * 1024) return hipErrorInvalidValue;
     k_down_t1<W, DENSE><<<S * R, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R,
-                                                      static_cast<const uint4*>(w_down_t), C, sh.d, y);
+                                                      static_cast<const uint4*>(w_down_t), C, sh.d, y, sh.sc.down);
   } else {
     const size_t shmem = DENSE ? 0 : sizeof(int) * (size_t)(ws.nseg + 1);
     const int grid = (sh.d + kBlock - 1) / kBlock;
     k_down_generic<W, DENSE><<<grid, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
-                                                        ws.slots, w_down_t, sh.T, sh.d, y);
+                                                        ws.slots, w_down_t, sh.T, sh.d, y, sh.sc.down);
   }
   return hipGetLastError();
 }
@@ -781,9 +1041,20 @@ hipError_t launch_rms_norm(float* z, int parts, int tc, int T, int r, const floa
   return hipGetLastError();
 }
 
+// calls f with a value of the weight-format type of wdt
+template <class F>
+hipError_t by_format(int wdt, F&& f) {
+  switch (wdt) {
+    case 0: return f(WF32{});
+    case 1: return f(WBf16{});
+    case 2: return f(WI8{});
+    default: return f(WI4{});
+  }
+}
+
 hipError_t launch_lopa_z(const Shape& sh, const Form& form, const float* x, const void* lopa_a, const Workspace& ws,
                          hipStream_t s) {
-  return sh.wdt == 1 ? lopa_z<WBf16>(sh, form, x, lopa_a, ws, s) : lopa_z<WF32>(sh, form, x, lopa_a, ws, s);
+  return by_format(sh.wdt, [&](auto w) { return lopa_z<decltype(w)>(sh, form, x, lopa_a, ws, s); });
 }
 
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x, const void* gate_w,
@@ -794,23 +1065,21 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form,
     const hipError_t e = launch_rms_norm(ws.z, 1, ws.tc, sh.T, sh.r, form.rms_gain, form.rms_eps, s);
     if (e != hipSuccess) return e;
   }
-  if (sh.wdt == 1) {
-    if (lopa) return dense ? gate_up_form<WBf16, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
-                           : gate_up_form<WBf16, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
-    return dense ? gate_up_form<WBf16, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
-                 : gate_up_form<WBf16, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
-  }
-  if (lopa) return dense ? gate_up_form<WF32, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
-                         : gate_up_form<WF32, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
-  return dense ? gate_up_form<WF32, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
-               : gate_up_form<WF32, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
+  return by_format(sh.wdt, [&](auto w) {
+    using W = decltype(w);
+    if (lopa) return dense ? gate_up_form<W, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
+                           : gate_up_form<W, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
+    return dense ? gate_up_form<W, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
+                 : gate_up_form<W, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
+  });
 }
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
                        hipStream_t s) {
-  if (sh.wdt == 1)
-    return dense ? down<WBf16, true>(sh, w_down_t, ws, y, s) : down<WBf16, false>(sh, w_down_t, ws, y, s);
-  return dense ? down<WF32, true>(sh, w_down_t, ws, y, s) : down<WF32, false>(sh, w_down_t, ws, y, s);
+  return by_format(sh.wdt, [&](auto w) {
+    using W = decltype(w);
+    return dense ? down<W, true>(sh, w_down_t, ws, y, s) : down<W, false>(sh, w_down_t, ws, y, s);
+  });
 }
 
 }  // namespace ffn

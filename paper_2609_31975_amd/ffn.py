@@ -18,12 +18,20 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "ffn_sparse.h")
 
 FFN_F32 = 0
 FFN_BF16 = 1
+FFN_I8 = 2
+FFN_I4 = 3
 
 STATUS = {0: "FFN_OK", -1: "FFN_ERR_NULL", -2: "FFN_ERR_SHAPE", -3: "FFN_ERR_DTYPE", -4: "FFN_ERR_ALIGN",
           -5: "FFN_ERR_WORKSPACE", -6: "FFN_ERR_HIP", -7: "FFN_ERR_OPTION"}
 
 FFN_ACT_RELU = 0
 FFN_ACT_RSPLUS = 1
+
+
+class Scales(ctypes.Structure):
+    """``ffn_scales_t``: fp32 row scales of quantized weights (device pointers)."""
+    _fields_ = [("gate", ctypes.c_void_p), ("lopa_a", ctypes.c_void_p), ("lopa_b", ctypes.c_void_p),
+                ("up", ctypes.c_void_p), ("down", ctypes.c_void_p)]
 
 
 class Options(ctypes.Structure):
@@ -55,12 +63,17 @@ def lib() -> ctypes.CDLL:
         std = [i, i, i, i, vp, vp, vp, vp, f, vp, vp, sz, vp]
         lop = [i, i, i, i, i, vp, vp, vp, vp, vp, f, vp, vp, sz, vp]
         op = ctypes.POINTER(Options)
+        sp = ctypes.POINTER(Scales)
         std_ex = std[:9] + [op] + std[9:]
         lop_ex = lop[:11] + [op] + lop[11:]
+        std_q = std[:8] + [sp] + std[8:9] + [op] + std[9:]
+        lop_q = lop[:10] + [sp] + lop[10:11] + [op] + lop[11:]
         for name, args in (("ffn_dense_forward", std), ("ffn_sparse_forward", std),
                            ("ffn_lopa_sparse_forward", lop), ("ffn_lopa_dense_forward", lop),
                            ("ffn_dense_forward_ex", std_ex), ("ffn_sparse_forward_ex", std_ex),
-                           ("ffn_lopa_sparse_forward_ex", lop_ex), ("ffn_lopa_dense_forward_ex", lop_ex)):
+                           ("ffn_lopa_sparse_forward_ex", lop_ex), ("ffn_lopa_dense_forward_ex", lop_ex),
+                           ("ffn_dense_forward_q", std_q), ("ffn_sparse_forward_q", std_q),
+                           ("ffn_lopa_sparse_forward_q", lop_q), ("ffn_lopa_dense_forward_q", lop_q)):
             getattr(L, name).restype = i
             getattr(L, name).argtypes = args
         L.ffn_active_set.restype = i
@@ -92,6 +105,22 @@ def weight_dtype(w) -> int:
     if w.dtype == torch.float32:
         return FFN_F32
     raise TypeError(f"weights must be bfloat16 or float32, got {w.dtype}")
+
+
+def quant_dtype(w, d: int) -> int:
+    """FFN_I8 for int8 codes of row length d, FFN_I4 for uint8 bytes holding d/2 code pairs."""
+    torch = _torch()
+    if w.dtype == torch.int8 and w.shape[-1] == d:
+        return FFN_I8
+    if w.dtype == torch.uint8 and 2 * w.shape[-1] == d:
+        return FFN_I4
+    raise TypeError(f"quantized weights must be int8 [.., d] or uint8 [.., d/2], got {w.dtype} {tuple(w.shape)}")
+
+
+def scales(gate=None, lopa_a=None, lopa_b=None, up=None, down=None) -> Scales:
+    """Build an ``ffn_scales_t`` from float32 device tensors (or None)."""
+    return Scales(*(_dev(t, n) for t, n in ((gate, "gate"), (lopa_a, "lopa_a"), (lopa_b, "lopa_b"), (up, "up"),
+                                             (down, "down"))))
 
 
 def _dev(t, what):
@@ -191,6 +220,38 @@ def ffn_lopa_sparse_forward_ex(x, lopa_a, lopa_b, w_up, w_down_t, t, opt, y, ws,
 def ffn_lopa_dense_forward_ex(x, lopa_a, lopa_b, w_up, w_down_t, t, opt, y, ws, stream=None):
     return _lopa_call("ffn_lopa_dense_forward_ex", x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream,
                       (_opt(opt),))
+
+
+def _q_call(name, x, gate, lopa_a, w_up, w_down_t, sc, t, opt, y, ws, stream, r):
+    T, d = x.shape
+    d_ff = w_up.shape[0]
+    wdt = quant_dtype(w_up, d) if w_up.dtype != _torch().float32 and w_up.dtype != _torch().bfloat16 \
+        else weight_dtype(w_up)
+    head = [wdt, T, d, d_ff] + ([r] if r else [])
+    ptrs = [_dev(x, "x")] + ([_dev(lopa_a, "lopa_a")] if r else []) + [_dev(gate, "gate"), _dev(w_up, "w_up"),
+                                                                       _dev(w_down_t, "w_down_t")]
+    rc = getattr(lib(), name)(*head, *ptrs, None if sc is None else ctypes.byref(sc), ctypes.c_float(t), _opt(opt),
+                              _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+    _check(name, rc)
+    return y
+
+
+def ffn_dense_forward_q(x, w_gate, w_up, w_down_t, sc, t, opt, y, ws, stream=None):
+    return _q_call("ffn_dense_forward_q", x, w_gate, None, w_up, w_down_t, sc, t, opt, y, ws, stream, 0)
+
+
+def ffn_sparse_forward_q(x, w_gate, w_up, w_down_t, sc, t, opt, y, ws, stream=None):
+    return _q_call("ffn_sparse_forward_q", x, w_gate, None, w_up, w_down_t, sc, t, opt, y, ws, stream, 0)
+
+
+def ffn_lopa_sparse_forward_q(x, lopa_a, lopa_b, w_up, w_down_t, sc, t, opt, y, ws, stream=None):
+    r = lopa_a.shape[0]
+    return _q_call("ffn_lopa_sparse_forward_q", x, lopa_b, lopa_a, w_up, w_down_t, sc, t, opt, y, ws, stream, r)
+
+
+def ffn_lopa_dense_forward_q(x, lopa_a, lopa_b, w_up, w_down_t, sc, t, opt, y, ws, stream=None):
+    r = lopa_a.shape[0]
+    return _q_call("ffn_lopa_dense_forward_q", x, lopa_b, lopa_a, w_up, w_down_t, sc, t, opt, y, ws, stream, r)
 
 
 def ffn_active_set(ws, T, d, d_ff, r=0, stream=None, with_act=True):

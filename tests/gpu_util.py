@@ -15,7 +15,9 @@ from paper_2609_31975_amd import ffn
 from paper_2609_31975_amd import workloads as wl
 
 BAND = 1e-3
-TOL = {wl.F32: 1e-5, wl.BF16: 2e-3}
+# int8 / int4: the oracle reads the same codes and scales; the GPU's 24-bit fixed-point copy
+# of x (or z) and its fp32 sums stay far below 2e-5
+TOL = {wl.F32: 1e-5, wl.BF16: 2e-3, wl.I8: 2e-5, wl.I4: 2e-5}
 
 
 def torch():
@@ -42,6 +44,11 @@ class DevInputs:
         self.lopa_b = to_dev(inp.lopa_b)
         self.w_up = to_dev(inp.w_up)
         self.w_down_t = to_dev(inp.w_down_t)
+        self.scales = None if inp.scales is None else {k: to_dev(v) for k, v in inp.scales.items()}
+
+    def scales_struct(self):
+        sc = self.scales
+        return ffn.scales(gate=sc.get("gate"), lopa_a=sc.get("a"), lopa_b=sc.get("b"), up=sc["up"], down=sc["down"])
 
 
 def run_gpu(dev: DevInputs, t: float, dense: bool = False, x=None):
@@ -92,6 +99,28 @@ class Form:
         return u / (1.0 + np.exp(-u)) if self.act == 1 else u
 
 
+def run_gpu_q(dev: DevInputs, t: float, dense: bool = False, form: Form | None = None):
+    """Run the matching ``_q`` entry point (quantized weights); returns (y, idx, act, ws)."""
+    tch = torch()
+    inp = dev.inp
+    T, d = dev.x.shape
+    ws = ffn.alloc_workspace(T, d, inp.d_ff, inp.r)
+    y = tch.full((T, d), float("nan"), dtype=tch.float32, device="cuda")
+    opt = None if form is None else form.options()
+    sc = dev.scales_struct()
+    if inp.r:
+        fn = ffn.ffn_lopa_dense_forward_q if dense else ffn.ffn_lopa_sparse_forward_q
+        fn(dev.x, dev.lopa_a, dev.lopa_b, dev.w_up, dev.w_down_t, sc, t, opt, y, ws)
+    else:
+        fn = ffn.ffn_dense_forward_q if dense else ffn.ffn_sparse_forward_q
+        fn(dev.x, dev.w_gate, dev.w_up, dev.w_down_t, sc, t, opt, y, ws)
+    tch.cuda.synchronize()
+    idx, act = (None, None)
+    if T <= 64:
+        idx, act = ffn.ffn_active_set(ws, T, d, inp.d_ff, inp.r)
+    return y.cpu().numpy(), idx, act, ws
+
+
 def run_gpu_ex(dev: DevInputs, t: float, form: Form, dense: bool = False):
     """Run the matching ``_ex`` entry point; returns (y, idx, act, ws) like ``run_gpu``."""
     tch = torch()
@@ -118,6 +147,8 @@ def run_oracle(inp: wl.FFNInputs, t: float, dense: bool = False, x=None, form: F
     kw = dict(w_gate=inp.w_gate) if inp.r == 0 else dict(lopa_a=inp.lopa_a, lopa_b=inp.lopa_b)
     if form is not None:
         kw.update(form.oracle_kw())
+    if inp.scales is not None:
+        kw["scales"] = inp.scales
     return ffn_oracle.ffn(x, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t, wdt=inp.wdt, skip_inactive=not dense, **kw)
 
 

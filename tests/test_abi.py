@@ -126,6 +126,41 @@ def test_option_errors(kind):
     assert _lopa_ex(_opt(rms_norm=1, rms_gain=A + 1, rms_eps=1e-6), lop) == -4
 
 
+def _q(fn, wdt, sc, d=64, r=0, ws_bytes=1 << 30, T=1):
+    if r:
+        return getattr(L, fn)(wdt, T, d, 128, r, A, A, A, A, A, sc, ctypes.c_float(0.5), None, A, A, ws_bytes, None)
+    return getattr(L, fn)(wdt, T, d, 128, A, A, A, A, sc, ctypes.c_float(0.5), None, A, A, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kind", ["sparse", "dense"])
+def test_quantized_argument_errors(kind):
+    std, lop = f"ffn_{kind}_forward_q", f"ffn_lopa_{kind}_forward_q"
+    full = ctypes.byref(ffn.Scales(A, A, A, A, A))
+    small = ffn.workspace_bytes(1, 64, 128, 0) - 1
+    # valid quantized calls reach the workspace check (no launch: the workspace is short)
+    for wdt in (ffn.FFN_I8, ffn.FFN_I4):
+        assert _q(std, wdt, full, ws_bytes=small) == -5
+        assert _q(lop, wdt, full, r=8, ws_bytes=ffn.workspace_bytes(1, 64, 128, 8) - 256) == -5
+    assert _q(std, ffn.FFN_BF16, None, ws_bytes=small) == -5      # float weights, no scales
+    # the plain and _ex calls take no quantized weights
+    assert _std(fn="ffn_sparse_forward", wdt=ffn.FFN_I8) == -3
+    assert _lopa(fn="ffn_lopa_sparse_forward", wdt=ffn.FFN_I4) == -3
+    assert _q(std, 4, full) == -3
+    # scales: required, complete, aligned; none for float weights
+    assert _q(std, ffn.FFN_I8, None) == -1
+    assert _q(std, ffn.FFN_I8, ctypes.byref(ffn.Scales(None, A, A, A, A))) == -1      # gate missing
+    assert _q(std, ffn.FFN_I8, ctypes.byref(ffn.Scales(A, None, None, None, A))) == -1  # up missing
+    assert _q(lop, ffn.FFN_I8, ctypes.byref(ffn.Scales(A, None, A, A, A)), r=8) == -1   # A's missing
+    assert _q(lop, ffn.FFN_I8, ctypes.byref(ffn.Scales(None, A, A, A, A)), r=8,
+              ws_bytes=ffn.workspace_bytes(1, 64, 128, 8) - 256) == -5                 # gate's unused
+    assert _q(std, ffn.FFN_I8, ctypes.byref(ffn.Scales(A, None, None, A + 2, A))) == -4
+    assert _q(std, ffn.FFN_F32, full) == -7
+    # int4 rows must hold whole bytes
+    assert _q(std, ffn.FFN_I4, full, d=65) == -2
+    assert _q(lop, ffn.FFN_I4, full, r=9) == -2
+    assert _q(lop, ffn.FFN_I8, full, r=9, ws_bytes=ffn.workspace_bytes(1, 64, 128, 9) - 256) == -5
+
+
 def test_active_set_argument_errors():
     n = ctypes.c_int32()
     assert L.ffn_active_set(None, 1, 64, 128, 0, ctypes.byref(n), A, None, None) == -1
