@@ -169,11 +169,21 @@ def gate_kernel_bytes(d, d_ff, r, T, n_union, dense, wdt=1):
 class Runner:
     """Enqueues step i of a workload: weight set i % n_sets, token batch (i // n_sets) % batches."""
 
-    def __init__(self, shape: Shape, r, T, t, dense, form=None):
+    def __init__(self, shape: Shape, r, T, t, dense, form=None, rho=0.0):
         import torch
         from paper_2609_31975_amd import ffn
         self.ffn, self.torch = ffn, torch
         self.s, self.r, self.T, self.t, self.dense = shape, r, T, t, dense
+        # correlated batches: each batch of T tokens shares a common N(0, 1) part
+        self.xc = None
+        if rho > 0:
+            g = torch.Generator(device="cuda").manual_seed(7919)
+            nb = shape.pool // T
+            self.xc = []
+            for xs in shape.x:
+                c = torch.randn((nb, 1, shape.d), generator=g, device="cuda")
+                mix = rho ** 0.5 * c + (1.0 - rho) ** 0.5 * xs[:nb * T].view(nb, T, shape.d)
+                self.xc.append(mix.reshape(nb * T, shape.d).contiguous())
         # the full form: option arrays on the device, held for the runner's lifetime
         self.form = form
         self.opt = None if form is None else ffn.options(**form)
@@ -185,7 +195,8 @@ class Runner:
         s = self.s
         k = i % s.n_sets
         b = (i // s.n_sets) % self.batches
-        return k, s.x[k][b * self.T:(b + 1) * self.T]
+        pool = s.x if self.xc is None else self.xc
+        return k, pool[k][b * self.T:(b + 1) * self.T]
 
     def __call__(self, i):
         s, f = self.s, self.ffn
@@ -294,8 +305,8 @@ def steps_for(run: Runner, K: int, budget_s: float = 1.0) -> int:
     return int(max(10, min(K, budget_s / max(dt, 1e-7))))
 
 
-def measure(shape, r, T, t, K, W, dense_us=None, name="", exact=False, form=None):
-    sp = Runner(shape, r, T, t, dense=False, form=form)
+def measure(shape, r, T, t, K, W, dense_us=None, name="", exact=False, form=None, rho=0.0):
+    sp = Runner(shape, r, T, t, dense=False, form=form, rho=rho)
     if not exact:
         K = steps_for(sp, K)
         W = min(W, K)
@@ -360,6 +371,39 @@ def cpu_baseline(inp, seed, pool, r, t, seconds):
                 sample=f"{n} calls of the headline workload (weight set 0, tokens 0..{min(n, len(xs)) - 1}), "
                        f"fp64 C oracle, single-threaded, {el:.1f} s",
                 host_cores_visible=len(os.sched_getaffinity(0)))
+
+
+def lopa_approx_record(D, H, r, cpu, log, max_iters=3):
+    """Time ffn_lopa_approx on a Gaussian H x D gate (std D^-1/2) at rank r; with `cpu`, the
+    oracle (numpy fp64 SVD) on the same matrix, one UV step."""
+    import torch
+    from paper_2609_31975_amd import ffn
+    g = torch.Generator(device="cuda").manual_seed(16)
+    w = (torch.randn((H, D), generator=g, device="cuda") * D ** -0.5).contiguous()
+    ffn.ffn_lopa_approx(w, r, 1)  # load rocBLAS / rocSOLVER kernels
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    _, _, _, _, it, obj = ffn.ffn_lopa_approx(w, r, max_iters)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    # fp64 work of one UV step: Gram matrix (SYRK, D^2 H), U and the residual (2 x 2 H D r)
+    flops = D * D * H + 4.0 * H * D * r
+    rec = dict(workload=f"lopa_approx_{H}x{D}_r{r}", path="lopa_approx", H=H, D=D, r=r, uv_steps=it,
+               objective=obj, seconds=round(dt, 4), seconds_per_uv_step=round(dt / max(it, 1), 4),
+               gemm_tflops_per_step=round(flops / 1e12, 3),
+               note="fp64: rocBLAS SYRK/GEMM, rocSOLVER dsyevd (the eigensolver dominates), M step kernel")
+    log(f"[bench] lopa approx {H}x{D} r={r}: {dt:.3f} s, {it} UV steps")
+    if cpu:
+        from oracle import lopa_approx as la
+        W = w.cpu().double().numpy()
+        t0 = time.perf_counter()
+        la.lopa_approx(W, r, max_iters=1)
+        rec["cpu_oracle_seconds_one_uv_step"] = round(time.perf_counter() - t0, 3)
+        rec["cpu_oracle_cores"] = len(os.sched_getaffinity(0))
+        log(f"[bench] lopa approx oracle: {rec['cpu_oracle_seconds_one_uv_step']} s")
+    del w
+    torch.cuda.empty_cache()
+    return rec
 
 
 def parity_sample(shape: Shape, r, T, t, form=None, form_seed=None):
@@ -476,7 +520,8 @@ def main():
     log(f"[bench] headline {head.name}: {sh.n_sets} sets, K={K}, W={W}")
     hform = full_form(sh, r0, head.seed) if head.form == "full" else None
     dense_us, dense_rec = dense_time(sh, 0, T0, K, W, exact=True)
-    rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True, form=hform)
+    rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True, form=hform,
+                              rho=head.rho)
     gate_mean, gate_med = time_gate_kernel(run, K)
     gbytes = np.mean([gate_kernel_bytes(head.d, head.d_ff, r0, T0, k, False, head.wdt) for k in nlist])
     par = parity_sample(sh, r0, T0, head.t, form=hform, form_seed=head.seed)
@@ -524,7 +569,13 @@ def main():
             if w.name == head.name or w.d != head.d or w.name.startswith("tiny") or w.wdt != wl.BF16:
                 continue
             form = full_form(sh, w.r, w.seed) if w.form == "full" else None
-            rw = measure(sh, w.r, w.T, w.t, K, W, name=w.name, form=form)[0]
+            rw = measure(sh, w.r, w.T, w.t, K, W, name=w.name, form=form, rho=w.rho)[0]
+            if w.rho:
+                rw["token_correlation"] = w.rho
+                base = [q for q in sweep if q.get("workload") == f"8b_lopa512_s90_T{w.T}"]
+                if base:
+                    rw["iid_us_per_call"] = base[0]["us_per_call"]
+                    rw["iid_union"] = base[0]["n_union"]
             if form is not None:
                 rw["form"] = "full: R-S+ activation, SiLU on W_up, G term, RMSNorm between A and B"
                 base = [q for q in sweep if q.get("workload") == f"8b_lopa512_s90_T{w.T}"]
@@ -577,6 +628,9 @@ def main():
                         f"x{rw['speedup_vs_fp32_dense']} vs fp32 dense")
                 del shq
                 torch.cuda.empty_cache()
+        # LoPA approximation of the 8B gate (Section 3.3): one conversion, timed end to end
+        out_approx = lopa_approx_record(head.d, head.d_ff, 512, cpu=not args.no_cpu, log=log)
+        sweep.append(out_approx)
         # 70B shapes
         w70 = [w for w in wl.workloads() if w.d == 8192]
         if w70:

@@ -12,9 +12,10 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("ffn_api.hip", "ffn_kernels.hip", "ffn_batched.hip")]
-HEADERS = [os.path.join(ROOT, "include", "ffn_sparse.h")] + [os.path.join(PKG, "csrc", f) for f in
-                                                             ("ffn_internal.h", "ffn_device.h")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("ffn_api.hip", "ffn_kernels.hip", "ffn_batched.hip",
+                                                  "ffn_lopa_approx.hip")]
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("ffn_sparse.h", "ffn_lopa_approx.h")] + \
+    [os.path.join(PKG, "csrc", f) for f in ("ffn_internal.h", "ffn_device.h")]
 LIB = os.path.join(PKG, "libffn_sparse.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -29,7 +30,9 @@ FLAGS = [
 def build(verbose: bool = False) -> str:
     """Compile the library (always recompiles) and return its path."""
     tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *SOURCES]
+    # rocBLAS / rocSOLVER: the LoPA approximation's Gram matrix, products and eigensolver
+    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *SOURCES, "-L/opt/rocm/lib", "-lrocblas",
+           "-lrocsolver", "-Wl,-rpath,/opt/rocm/lib"]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -15,6 +15,7 @@ import re
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libffn_sparse.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "ffn_sparse.h")
+HEADERS = [HEADER, os.path.join(os.path.dirname(PKG), "include", "ffn_lopa_approx.h")]
 
 FFN_F32 = 0
 FFN_BF16 = 1
@@ -80,6 +81,11 @@ def lib() -> ctypes.CDLL:
         L.ffn_active_set.argtypes = [vp, i, i, i, i, vp, vp, vp, vp]
         L.ffn_time_next_gate_kernel.restype = i
         L.ffn_time_next_gate_kernel.argtypes = [vp, vp]
+        L.ffn_lopa_approx_workspace_bytes.restype = sz
+        L.ffn_lopa_approx_workspace_bytes.argtypes = [i, i, i]
+        L.ffn_lopa_approx.restype = i
+        L.ffn_lopa_approx.argtypes = [i, i, i, vp, i, vp, vp, vp, vp, ctypes.POINTER(ctypes.c_int),
+                                      ctypes.POINTER(ctypes.c_double), vp, sz, vp]
         L.ffn_status_string.restype = ctypes.c_char_p
         L.ffn_status_string.argtypes = [i]
         _lib = L
@@ -87,8 +93,8 @@ def lib() -> ctypes.CDLL:
 
 
 def declared_functions() -> list[str]:
-    """Names of the functions the public header declares."""
-    text = open(HEADER).read()
+    """Names of the functions the public headers declare."""
+    text = "".join(open(h).read() for h in HEADERS)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+[\s*]+(ffn_\w+)\s*\(", text, re.M)))
 
 
@@ -271,6 +277,28 @@ def ffn_time_next_gate_kernel(start, stop):
     """Arm torch.cuda.Event pair (enable_timing=True) for the next call's gate kernel."""
     rc = lib().ffn_time_next_gate_kernel(ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event))
     _check("ffn_time_next_gate_kernel", rc)
+
+
+def ffn_lopa_approx(w, r: int, max_iters: int = 20, stream=None):
+    """LoPA approximation of a gate matrix w ([H, D] float32 device tensor): returns
+    (g_idx int32 [H], g_sign int8 [H], lopa_b = U [H, r] f32, lopa_a = V [r, D] f32,
+    iters, objective), the arrays as device tensors."""
+    torch = _torch()
+    H, D = w.shape
+    n = int(lib().ffn_lopa_approx_workspace_bytes(H, D, r))
+    if n == 0:
+        raise FFNError("ffn_lopa_approx_workspace_bytes", -2)
+    ws = torch.empty(n, dtype=torch.uint8, device=w.device)
+    g_idx = torch.empty(H, dtype=torch.int32, device=w.device)
+    g_sign = torch.empty(H, dtype=torch.int8, device=w.device)
+    U = torch.empty((H, r), dtype=torch.float32, device=w.device)
+    V = torch.empty((r, D), dtype=torch.float32, device=w.device)
+    it, obj = ctypes.c_int(0), ctypes.c_double(0.0)
+    rc = lib().ffn_lopa_approx(H, D, r, _dev(w, "w"), max_iters, _dev(g_idx, "g_idx"), _dev(g_sign, "g_sign"),
+                               _dev(U, "lopa_b"), _dev(V, "lopa_a"), ctypes.byref(it), ctypes.byref(obj),
+                               _dev(ws, "ws"), n, _stream(stream))
+    _check("ffn_lopa_approx", rc)
+    return g_idx, g_sign, U, V, it.value, obj.value
 
 
 def ffn_status_string(code: int) -> str:

@@ -15,6 +15,9 @@ Recipe (per weight set, ``seed``):
     B        [d_ff, r]   N(0, 1/r)       LoPA U factor
     W_up     [d_ff, d]   N(0, 1/d)
     W_down^T [d_ff, d]   N(0, 1/d_ff)    (row i = output vector of neuron i)
+Correlated batches (make_tokens_correlated): x_tau = sqrt(rho) c + sqrt(1 - rho) n_tau with
+one common N(0, 1) vector c per batch, so every token is still N(0, 1) (the thresholds
+hold) while the active sets of a batch overlap and their union shrinks.
 Quantized weight sets (int8 / int4) draw the codes directly: per matrix a PCG64 stream gives
 q = clip(rint(N(0, (qmax/3)^2)), -qmax, qmax) with qmax = 127 or 7, then one scale per row,
 s_i = std / (qmax/3) * U(0.8, 1.2), so that s_i q_ij has about the standard deviation above.
@@ -172,6 +175,15 @@ def make_form(seed: int, d: int, d_ff: int, r: int) -> FormInputs:
     return FormInputs(g_idx=g_idx, g_sign=g_sign, rms_gain=rms_gain)
 
 
+def make_tokens_correlated(seed: int, T: int, d: int, rho: float) -> np.ndarray:
+    """T tokens sharing a common part: x_tau = sqrt(rho) c + sqrt(1 - rho) n_tau, c and the
+    n_tau iid N(0, 1) (each token stays N(0, 1); two tokens correlate by rho)."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0xC0C0])))
+    c = _normal(rng, (1, d), 1.0)
+    n = _normal(rng, (T, d), 1.0)
+    return (np.float32(np.sqrt(rho)) * c + np.float32(np.sqrt(1.0 - rho)) * n).astype(np.float32)
+
+
 def make_tokens(seed: int, T: int, d: int) -> np.ndarray:
     """A separate pool of iid N(0, 1) tokens [T, d] (its own stream, independent of weights)."""
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0x70C3])))
@@ -190,6 +202,7 @@ class Workload:
     seed: int
     n_sets: int
     form: str = ""    # "" the default form; "full": R-S+, SiLU on W_up, G and RMSNorm (LoPA)
+    rho: float = 0.0  # token correlation of a batch (0: iid tokens)
 
 
 # The five workload families; every (sparsity, T) point is its own entry.
@@ -201,6 +214,10 @@ def workloads() -> list[Workload]:
         out.append(Workload(f"8b_lopa512_s{int(s * 100)}", 4096, 14336, 512, 1, BF16, THRESHOLD[s], 2000, 4))
     for T in (1, 4, 16, 64):
         out.append(Workload(f"8b_lopa512_s90_T{T}", 4096, 14336, 512, T, BF16, THRESHOLD[0.90], 3000, 4))
+    for rho in (0.5, 0.9):
+        for T in (16, 64):
+            out.append(Workload(f"8b_lopa512_s90_T{T}_rho{int(rho * 10)}", 4096, 14336, 512, T, BF16,
+                                THRESHOLD[0.90], 3000, 4, rho=rho))
     for wdt, tag in ((I8, "i8"), (I4, "i4")):
         out.append(Workload(f"8b_std_s90_{tag}", 4096, 14336, 0, 1, wdt, THRESHOLD[0.90], 6000, 4))
         out.append(Workload(f"8b_lopa512_s90_{tag}", 4096, 14336, 512, 1, wdt, THRESHOLD[0.90], 7000, 4))

@@ -161,6 +161,27 @@ def test_quantized_argument_errors(kind):
     assert _q(lop, ffn.FFN_I8, full, r=9, ws_bytes=ffn.workspace_bytes(1, 64, 128, 9) - 256) == -5
 
 
+def test_lopa_approx_argument_errors():
+    n = ffn.workspace_bytes  # noqa: F841 (the forward workspace is unrelated)
+    assert L.ffn_lopa_approx_workspace_bytes(0, 8, 1) == 0
+    assert L.ffn_lopa_approx_workspace_bytes(8, 8, 9) == 0
+    assert L.ffn_lopa_approx_workspace_bytes(1 << 16, 1 << 16, 4) == 0
+    ws = L.ffn_lopa_approx_workspace_bytes(64, 32, 4)
+    assert ws > 0
+    it, obj = ctypes.c_int(), ctypes.c_double()
+
+    def call(H=64, D=32, r=4, w=A, iters=3, ws_bytes=ws, gs=A, it_p=ctypes.byref(it)):
+        return L.ffn_lopa_approx(H, D, r, w, iters, A, gs, A, A, it_p, ctypes.byref(obj), A, ws_bytes, None)
+    assert call(w=None) == -1
+    assert call(it_p=None) == -1
+    assert call(r=0) == -2
+    assert call(r=33) == -2
+    assert call(iters=0) == -7
+    assert call(w=MIS) == -4
+    assert call(gs=A + 2) == -4
+    assert call(ws_bytes=ws - 1) == -5
+
+
 def test_active_set_argument_errors():
     n = ctypes.c_int32()
     assert L.ffn_active_set(None, 1, 64, 128, 0, ctypes.byref(n), A, None, None) == -1

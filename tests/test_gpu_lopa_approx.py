@@ -1,0 +1,95 @@
+"""GPU parity of the LoPA approximation (include/ffn_lopa_approx.h) against the oracle
+(Section 3.3, "LoPA approximation"): the same M, step count and error on small matrices,
+exact recovery of a planted M + rank-r product, an error that never rises with more steps,
+and, on the 8B gate shape (14336 x 4096, r = 512), the properties of the result.
+"""
+import numpy as np
+import pytest
+
+from oracle import lopa_approx as la
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2609_31975_amd import ffn
+    return torch, ffn
+
+
+def run(dev, W, r, max_iters=20):
+    torch, ffn = dev
+    w = torch.from_numpy(np.ascontiguousarray(W, np.float32)).to("cuda")
+    gi, gs, U, V, it, obj = ffn.ffn_lopa_approx(w, r, max_iters)
+    torch.cuda.synchronize()
+    return gi.cpu().numpy(), gs.cpu().numpy(), U.cpu().numpy().astype(np.float64), \
+        V.cpu().numpy().astype(np.float64), it, obj
+
+
+def planted(seed, H, D, r, small=0.05):
+    rng = np.random.default_rng(seed)
+    idx = rng.integers(0, D, size=H).astype(np.int32)
+    sgn = np.where(rng.random(H) < 0.5, -1, 1).astype(np.int8)
+    UV = (rng.standard_normal((H, r)) * small) @ (rng.standard_normal((r, D)) * small)
+    W = (la.dense_m(idx, sgn, D) + UV).astype(np.float32)
+    return W, idx, sgn, UV
+
+
+@pytest.mark.parametrize("H,D,r", [(300, 200, 8), (128, 256, 16)])
+def test_planted_recovery(dev, H, D, r):
+    W, idx, sgn, UV = planted(11, H, D, r)
+    gi, gs, U, V, it, obj = run(dev, W, r)
+    assert np.array_equal(gi, idx) and np.array_equal(gs, sgn)
+    assert 1 <= it <= 2
+    # W is fp32: the planted UV is recovered up to W's rounding
+    assert np.linalg.norm(U @ V - UV) / np.linalg.norm(UV) < 1e-5
+    assert obj < 1e-9 * H * D
+
+
+@pytest.mark.parametrize("seed,H,D,r", [(12, 256, 128, 16), (13, 200, 300, 24), (14, 64, 64, 1)])
+def test_matches_the_oracle(dev, seed, H, D, r):
+    rng = np.random.default_rng(seed)
+    W = rng.standard_normal((H, D)).astype(np.float32)
+    for cap in (1, 3, 50):
+        ref = la.lopa_approx(W.astype(np.float64), r, max_iters=cap)
+        gi, gs, U, V, it, obj = run(dev, W, r, cap)
+        assert it == ref.iters
+        assert np.array_equal(gi, ref.g_idx) and np.array_equal(gs, ref.g_sign)
+        assert obj == pytest.approx(ref.history[-1], rel=1e-9)
+        UVr = ref.U @ ref.V
+        assert np.linalg.norm(U @ V - UVr) / np.linalg.norm(UVr) < 2e-6   # fp32 outputs
+
+
+def test_error_never_rises_with_more_steps(dev):
+    rng = np.random.default_rng(15)
+    W = rng.standard_normal((192, 96)).astype(np.float32)
+    objs = [run(dev, W, 8, k)[5] for k in (1, 2, 3, 4, 6)]
+    assert all(b <= a * (1 + 1e-12) for a, b in zip(objs, objs[1:])), objs
+
+
+def test_full_size_gate_properties(dev):
+    """The 8B gate shape: the returned M is optimal for the returned U V, V has orthonormal
+    rows, U = (W - M) V^T, and the reported error is ||W - M - U V||^2 (all in fp64)."""
+    torch, ffn = dev
+    H, D, r = 14336, 4096, 512
+    g = torch.Generator(device="cuda").manual_seed(16)
+    w = (torch.randn((H, D), generator=g, device="cuda") * D ** -0.5).contiguous()
+    gi, gs, U, V, it, obj = ffn.ffn_lopa_approx(w, r, 2)
+    assert 1 <= it <= 2
+    W64, U64, V64 = w.double(), U.double(), V.double()
+    M = torch.zeros_like(W64)
+    M[torch.arange(H, device="cuda"), gi.long()] = gs.double()
+    R = W64 - U64 @ V64
+    err = float(((R - M) ** 2).sum())
+    assert err == pytest.approx(obj, rel=1e-5)
+    # M: the largest-magnitude entry of each residual row, with its sign
+    pick = R.gather(1, gi.long()[:, None])[:, 0]
+    assert bool(torch.all(pick.abs() >= R.abs().max(1).values - 1e-6))
+    assert bool(torch.all(torch.sign(pick) == gs.double()))
+    VVt = V64 @ V64.T
+    assert float((VVt - torch.eye(r, device="cuda", dtype=torch.float64)).abs().max()) < 1e-5
+    Uref = (W64 - M) @ V64.T
+    assert float((U64 - Uref).norm() / Uref.norm()) < 1e-5
+    print("8b gate approx:", it, obj, flush=True)

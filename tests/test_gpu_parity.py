@@ -77,7 +77,7 @@ def _inputs(key, T, d, d_ff, r, seed):
 
 
 # the full form and quantized weights have files of their own
-FULL = [w for w in wl.workloads() if w.name != "tiny_f32_std_s90" and not w.form and w.wdt == BF16]
+FULL = [w for w in wl.workloads() if w.name != "tiny_f32_std_s90" and not w.form and w.wdt == BF16 and not w.rho]
 
 
 @pytest.mark.parametrize("w", FULL, ids=[w.name for w in FULL])
@@ -244,3 +244,23 @@ def test_random_shapes(gu, case):
     dev = gu.DevInputs(inp)
     y, idx, act, _ = gu.run_gpu(dev, t)
     gu.check_parity(gu.run_oracle(inp, t), y, idx, act, t, wdt, what=name)
+
+
+# ---------------------------------------------------------------- correlated batches
+@pytest.mark.parametrize("rho", [0.5, 0.9, 1.0])
+@pytest.mark.parametrize("T,r", [(16, 512), (64, 512), (20, 0)])
+def test_correlated_batches(gu, rho, T, r):
+    """Tokens sharing a common part (the union shrinks as rho grows; rho = 1: T identical
+    tokens, one active set)."""
+    d, d_ff = 4096, 14336 if r else 3000
+    inp = _inputs((d, d_ff, r, T, 3000 + r), T, d, d_ff, r, 3000 + r)
+    x = wl.make_tokens_correlated(71, T, d, rho)
+    tch = __import__("torch")
+    y, idx, act, _ = gu.run_gpu(gu.DevInputs(inp), 1.2816, x=tch.from_numpy(x).to("cuda"))
+    res = gu.run_oracle(inp, 1.2816, x=x)
+    fig = gu.check_parity(res, y, idx, act, 1.2816, BF16, what=f"rho={rho} T={T} r={r}")
+    n1 = np.mean(fig["n_active"])
+    assert n1 <= fig["n_union"] <= T * n1
+    if rho == 1.0:
+        assert fig["n_union"] == round(n1)
+    print(f"rho={rho} T={T} r={r}: union {fig['n_union']} of {d_ff}, per token {n1:.0f}", flush=True)
