@@ -240,8 +240,9 @@ __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const LaneVec<W
 // Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n), of a matrix of
 // `bytes` bytes (< 2^31): each wave takes passes of 64/lpr rows (passes wave, wave + 4,
 // ...).  For rows of at most 8 chunks per lane and more than one pass per wave, two
-// register sets alternate (four for at most 4 chunks a lane), the loads of the next
-// passes issued before the current pass is reduced; the loads are raw buffer loads
+// register sets alternate, the loads of the next pass issued before the current pass is
+// reduced (measured: preloading both sets, or four sets, around the quantized vector's
+// conversion ran slower); the loads are raw buffer loads
 // (out-of-range offsets past the last pass), so every pass issues the same loads and the
 // load-counter waits are exact.  A group of passes always runs whole (a pass past the
 // last one loads nothing and sinks nothing) and the exit test closes the group, so no
@@ -276,38 +277,15 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
     const float sum = group_sum(lane_dot<W, CPL>(b, v), lpr);
     if (q == 0 && k < n) sink(k, sum);
   };
-  constexpr bool DEEP = CPL <= 4;  // short lane rows (the quantized formats): four passes in
-                                   // flight, as many bytes outstanding as two bf16 passes
-  uint4 b0[CPL], b1[CPL], b2[CPL];
+  uint4 b0[CPL], b1[CPL];
   load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
-  if constexpr (DEEP) {
-    load(b1, wave + kWaves);
-    load(b2, wave + 2 * kWaves);
-  }
   prepare_lane_vec<W, CPL>(v);  // quantized: the whole workgroup converts the vector
   if (wave >= npass) return;
   if (wave + kWaves >= npass) {  // a single pass: nothing to overlap
     finish(b0, wave);
     return;
   }
-  if constexpr (DEEP) {
-    uint4 b3[CPL];
-    for (int pass = wave;; pass += 4 * kWaves) {
-      load(b3, pass + 3 * kWaves);
-      issue_barrier();
-      finish(b0, pass);
-      load(b0, pass + 4 * kWaves);
-      issue_barrier();
-      finish(b1, pass + kWaves);
-      load(b1, pass + 5 * kWaves);
-      issue_barrier();
-      finish(b2, pass + 2 * kWaves);
-      load(b2, pass + 6 * kWaves);
-      issue_barrier();
-      finish(b3, pass + 3 * kWaves);
-      if (pass + 4 * kWaves >= npass) break;
-    }
-  } else if constexpr (CPL <= 8) {
+  if constexpr (CPL <= 8) {
     for (int pass = wave;; pass += 2 * kWaves) {
       load(b1, pass + kWaves);
       issue_barrier();
@@ -528,25 +506,28 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
 }
 
 // y += sum over the listed neurons of a row chunk of zval * w_down_t[neuron], for one
-// 64-chunk column slice (1 KB of every bf16 row, read by one wave instruction).  A
-// listed neuron with zval exactly 0 (the s_gated site) is skipped: its row is not read.
-// Workgroup b covers column slice b % S of the neurons in segments [c nseg/R,
-// (c+1) nseg/R), c = b / S.  Its four waves take the chunk's active rows in turn;
-// their partial sums are added in a fixed order and then into y with one atomic
-// per column (y was cleared by the gate kernel).
-template <class W, bool DENSE>
+// column slice of LG 16-byte chunks a row.  A listed neuron with zval exactly 0 (the
+// s_gated site) is skipped: its row is not read.  Workgroup b covers column slice b % S of
+// the neurons in segments [c nseg/R, (c+1) nseg/R), c = b / S.  A wave reads 64/LG rows an
+// instruction (LG lanes a row: 64 for fp32 / bf16, whose 64 chunks are 1 KB of a bf16 row;
+// 16 for the quantized formats, so that a slice stays 256 - 512 columns wide); the row
+// groups of a wave, then its four waves, add their partial sums in a fixed order, and one
+// atomic per column adds them into y (y was cleared by the gate kernel).
+template <class W, bool DENSE, int LG>
 __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ seg_count,
                                                     const int32_t* __restrict__ seg_idx,
                                                     const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
                                                     const uint4* __restrict__ w_down_t, int C, int d,
                                                     float* __restrict__ y, const float* __restrict__ s_down) {
-  constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave;
+  constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave, RG = kWave / LG;
   extern __shared__ int s_dyn[];  // raw slots, then the compacted list (sparse only)
   __shared__ int s_cnt[kWave];
   __shared__ int s_off[kWave + 1];
-  __shared__ float s_red[kWaves][kWave * EPC];
+  // [wave][e][q], rows padded to LG + 1: lanes (consecutive q) write, and threads
+  // (consecutive e) read, distinct banks
+  __shared__ float s_red[kWaves][EPC * (LG + 1)];
 
-  const int S = (C + kWave - 1) / kWave;
+  const int S = (C + LG - 1) / LG;
   const int chunk = blockIdx.x / S, slice = blockIdx.x % S;
   const Split chunks(nseg, R), segs(d_ff, nseg);
   const int seg_lo = chunks.start(chunk), seg_hi = chunks.start(chunk + 1);
@@ -589,17 +570,18 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
     __syncthreads();
   }
 
-  const int ch = slice * kWave + lane;
+  const int q = lane % LG, g = lane / LG;
+  const int ch = slice * LG + q;
   const bool cvalid = ch < C;
   float acc[EPC];
 #pragma unroll
   for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-  for (int k = wave; k < n; k += kWaves * U) {
+  for (int k = wave * RG + g; k < n; k += kWaves * RG * U) {
     uint4 wv[U];
     float zz[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kk = k + u * kWaves;
+      const int kk = k + u * kWaves * RG;
       const bool ok = kk < n;
       int row;
       if constexpr (DENSE) {
@@ -622,14 +604,22 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
       for (int e = 0; e < EPC; ++e) acc[e] = fmaf(zz[u], f[e], acc[e]);
     }
   }
+  // the row groups of the wave (lanes q, q + LG, ...), then the waves
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) s_red[wave][lane * EPC + e] = acc[e];
+  for (int e = 0; e < EPC; ++e) {
+    float a = acc[e];
+    if constexpr (RG >= 2) a += __shfl_xor(a, LG);
+    if constexpr (RG >= 4) a += __shfl_xor(a, 2 * LG);
+    if (g == 0) s_red[wave][e * (LG + 1) + q] = a;
+  }
   __syncthreads();
-  for (int o = threadIdx.x; o < kWave * EPC; o += kBlock) {
-    float s = s_red[0][o];
+  // consecutive threads, consecutive columns: each atomic instruction covers whole lines
+  for (int o = threadIdx.x; o < LG * EPC; o += kBlock) {
+    const int qq = o / EPC, e = o - qq * EPC;
+    float s = s_red[0][e * (LG + 1) + qq];
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) s += s_red[w][o];
-    const int col = slice * kWave * EPC + o;
+    for (int w = 1; w < kWaves; ++w) s += s_red[w][e * (LG + 1) + qq];
+    const int col = slice * LG * EPC + o;
     if (col < d) unsafeAtomicAdd(y + col, s);
   }
 }
@@ -988,8 +978,8 @@ hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void*
 // kDownWgPerCu workgroups per CU, at most 64 segments per chunk.
 constexpr int kDownWgPerCu = 2;
 
-void down_grid(int C, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
-  *S = (C + kWave - 1) / kWave;
+void down_grid(int C, int lg, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
+  *S = (C + lg - 1) / lg;
   int r = (kDownWgPerCu * cu_count() + *S - 1) / *S;
   const int rmin = (nseg + kWave - 1) / kWave;
   if (r < rmin) r = rmin;
@@ -1005,11 +995,13 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
     const int C = sh.d / W::EPC;
     int S, R;
     size_t rows;
-    down_grid(C, ws.nseg, sh.d_ff, &S, &R, &rows);
+    constexpr int LG = is_quant<W>() ? 16 : kWave;
+    down_grid(C, LG, ws.nseg, sh.d_ff, &S, &R, &rows);
     const size_t shmem = DENSE ? 0 : 4 * sizeof(int) * rows;
     if (shmem > 96 * 1024) return hipErrorInvalidValue;
-    k_down_t1<W, DENSE><<<S * R, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R,
-                                                      static_cast<const uint4*>(w_down_t), C, sh.d, y, sh.sc.down);
+    k_down_t1<W, DENSE, LG><<<S * R, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R,
+                                                          static_cast<const uint4*>(w_down_t), C, sh.d, y,
+                                                          sh.sc.down);
   } else {
     const size_t shmem = DENSE ? 0 : sizeof(int) * (size_t)(ws.nseg + 1);
     const int grid = (sh.d + kBlock - 1) / kBlock;
