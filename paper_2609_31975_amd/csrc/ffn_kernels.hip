@@ -598,6 +598,9 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
+      // past the wave's last row: nothing left to unpack (wave-uniform: the wave's first
+      // row of this u is k - g + u kWaves RG)
+      if (k - g + u * kWaves * RG >= n) break;
       float f[EPC];
       unpack(W{}, wv[u], f);
 #pragma unroll
