@@ -509,23 +509,30 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
 // column slice of LG 16-byte chunks a row.  A listed neuron with zval exactly 0 (the
 // s_gated site) is skipped: its row is not read.  Workgroup b covers column slice b % S of
 // the neurons in segments [c nseg/R, (c+1) nseg/R), c = b / S.  A wave reads 64/LG rows an
-// instruction (LG lanes a row: 64 for fp32 / bf16, whose 64 chunks are 1 KB of a bf16 row;
-// 16 for the quantized formats, so that a slice stays 256 - 512 columns wide); the row
-// groups of a wave, then its four waves, add their partial sums in a fixed order, and one
-// atomic per column adds them into y (y was cleared by the gate kernel).
+// instruction (LG lanes a row: 32 for fp32 / bf16, whose 32 chunks are 512 bytes of a bf16
+// row; 16 for the quantized formats, so that a slice stays 256 - 512 columns wide).  Each lane's
+// partial sums go to LDS; the row groups and waves are added there in a fixed order, and
+// one atomic per column adds them into y (y was cleared by the gate kernel).
+//
+// Every load is a raw buffer load (an unused slot gets an offset past the buffer), and
+// every LDS read of the list is unconditional, so that the loads of a round issue back to
+// back: with predicated loads each one sat behind its own branch and LDS wait.  The host
+// guarantees w_down_t < 2^31 bytes.
+constexpr int kDownSlotsPerThread = 4, kDownSlots = kDownSlotsPerThread * kBlock;
+
 template <class W, bool DENSE, int LG>
 __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ seg_count,
                                                     const int32_t* __restrict__ seg_idx,
                                                     const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
                                                     const uint4* __restrict__ w_down_t, int C, int d,
                                                     float* __restrict__ y, const float* __restrict__ s_down) {
-  constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave, RG = kWave / LG;
-  extern __shared__ int s_dyn[];  // raw slots, then the compacted list (sparse only)
+  constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave, RG = kWave / LG, PT = kDownSlotsPerThread;
+  extern __shared__ int s_dyn[];  // the compacted list (sparse only): indices, then values
   __shared__ int s_cnt[kWave];
   __shared__ int s_off[kWave + 1];
-  // [wave][e][q], rows padded to LG + 1: lanes (consecutive q) write, and threads
-  // (consecutive e) read, distinct banks
-  __shared__ float s_red[kWaves][EPC * (LG + 1)];
+  // [wave row group][e][q], rows padded to LG + 1: lanes (consecutive q) write, and
+  // threads (consecutive e) read, distinct banks
+  __shared__ float s_red[kWaves * RG][EPC * (LG + 1)];
 
   const int S = (C + LG - 1) / LG;
   const int chunk = blockIdx.x / S, slice = blockIdx.x % S;
@@ -533,97 +540,134 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
   const int seg_lo = chunks.start(chunk), seg_hi = chunks.start(chunk + 1);
   const int row_lo = segs.start(seg_lo), row_hi = segs.start(seg_hi);
   const int raw_n = row_hi - row_lo;
-  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
+  const Buf zb = make_buf(seg_zval, 4u * (uint32_t)d_ff);
 
   int n = raw_n;
-  int* l_idx = nullptr;
-  float* l_z = nullptr;
+  int* l_idx = s_dyn;
+  float* l_z = reinterpret_cast<float*>(s_dyn + raw_n);
   if constexpr (!DENSE) {
-    int* raw_idx = s_dyn;
-    float* raw_z = reinterpret_cast<float*>(s_dyn + raw_n);
-    l_idx = s_dyn + 2 * raw_n;
-    l_z = reinterpret_cast<float*>(s_dyn + 3 * raw_n);
-    // one round trip: every slot of the chunk plus the segment counts
-    for (int p = threadIdx.x; p < raw_n; p += kBlock) {
-      raw_idx[p] = seg_idx[row_lo + p];
-      raw_z[p] = seg_zval[row_lo + p];
-    }
-    if (wave == 0) {
-      const int nsc = seg_hi - seg_lo;  // <= 64, guaranteed by the host
-      const int c = lane < nsc ? seg_count[seg_lo + lane] : 0;
-      const int v = wave_inclusive_scan(c);
-      s_cnt[lane] = c;
-      s_off[lane] = v - c;
-      if (lane == kWave - 1) s_off[kWave] = v;
-    }
-    __syncthreads();
-    n = s_off[kWave];
-    for (int p = threadIdx.x; p < raw_n; p += kBlock) {
-      const int row = row_lo + p;
-      const int w = segs.of(row) - seg_lo;
-      const int e = row - segs.start(seg_lo + w);
-      if (e < s_cnt[w]) {
-        l_idx[s_off[w] + e] = raw_idx[p];
-        l_z[s_off[w] + e] = raw_z[p];
+    // one round trip: the chunk's slots into registers (kDownSlots a round), the segment
+    // counts into LDS; then each valid slot goes to its place in the compacted list
+    const Buf ib = make_buf(seg_idx, 4u * (uint32_t)d_ff);
+    for (int p0 = 0; p0 < raw_n; p0 += kDownSlots) {
+      int ri[PT];
+      float rz[PT];
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        const int p = p0 + threadIdx.x + u * kBlock;
+        const uint32_t off = p < raw_n ? 4u * (uint32_t)(row_lo + p) : kOOB;
+        ri[u] = ldb32(ib, off);
+        rz[u] = __int_as_float(ldb32(zb, off));
+      }
+      if (p0 == 0 && wave == 0) {
+        const int nsc = seg_hi - seg_lo;  // <= 64, guaranteed by the host
+        const Buf cb = make_buf(seg_count, 4u * (uint32_t)nseg);
+        const int c = ldb32(cb, lane < nsc ? 4u * (uint32_t)(seg_lo + lane) : kOOB);
+        const int v = wave_inclusive_scan(c);
+        s_cnt[lane] = c;
+        s_off[lane] = v - c;
+        if (lane == kWave - 1) s_off[kWave] = v;
+      }
+      __syncthreads();
+      // segment and rank of each slot, their counts and offsets read back to back; a
+      // group of slots wholly past the chunk is skipped (a workgroup-uniform test)
+      int rw[PT], re[PT], rc[PT], ro[PT];
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        if (p0 + u * kBlock >= raw_n) break;
+        const int p = p0 + threadIdx.x + u * kBlock;
+        const int row = row_lo + (p < raw_n ? p : 0);
+        rw[u] = segs.of(row) - seg_lo;
+        re[u] = row - segs.start(seg_lo + rw[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        if (p0 + u * kBlock >= raw_n) break;
+        rc[u] = s_cnt[rw[u]];
+        ro[u] = s_off[rw[u]];
+      }
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        if (p0 + u * kBlock >= raw_n) break;
+        if (p0 + threadIdx.x + u * kBlock < raw_n && re[u] < rc[u]) {
+          l_idx[ro[u] + re[u]] = ri[u];
+          l_z[ro[u] + re[u]] = rz[u];
+        }
       }
     }
     __syncthreads();
+    n = s_off[kWave];
   }
 
+  const Buf wb = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
+  const Buf sb = make_buf(s_down, 4u * (uint32_t)d_ff);
   const int q = lane % LG, g = lane / LG;
   const int ch = slice * LG + q;
   const bool cvalid = ch < C;
   float acc[EPC];
 #pragma unroll
   for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-  for (int k = wave * RG + g; k < n; k += kWaves * RG * U) {
+  // kb: the wave's first row of a round (wave-uniform); its lanes take rows kb + g + ...
+  for (int kb = wave * RG; kb < n; kb += kWaves * RG * U) {
     uint4 wv[U];
-    float zz[U];
+    float zz[U], sc[U];
+    int row[U];
+    bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kk = k + u * kWaves * RG;
-      const bool ok = kk < n;
-      int row;
+      const int kk = kb + g + u * kWaves * RG;
+      ok[u] = kk < n;
       if constexpr (DENSE) {
-        row = row_lo + kk;
-        zz[u] = ok ? seg_zval[row] : 0.f;
+        row[u] = row_lo + kk;
       } else {
-        row = ok ? l_idx[kk] : 0;
-        zz[u] = ok ? l_z[kk] : 0.f;
+        const int j = ok[u] ? kk : 0;  // n >= 1 here
+        row[u] = l_idx[j];
+        zz[u] = ok[u] ? l_z[j] : 0.f;
       }
-      // a zero gated value (the s_gated site) needs no W_down row
-      const bool need = ok && cvalid && (DENSE || zz[u] != 0.f);
-      wv[u] = need ? ld_weights(w_down_t + (size_t)row * C + ch) : make_uint4(0u, 0u, 0u, 0u);
-      if constexpr (is_quant<W>()) zz[u] *= ok ? s_down[row] : 0.f;  // the row's scale
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      // past the wave's last row: nothing left to unpack (wave-uniform: the wave's first
-      // row of this u is k - g + u kWaves RG)
-      if (k - g + u * kWaves * RG >= n) break;
+      if constexpr (DENSE) zz[u] = __int_as_float(ldb32(zb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
+      // a zero gated value (the s_gated site) needs no W_down row
+      const bool need = ok[u] && cvalid && (DENSE || zz[u] != 0.f);
+      wv[u] = ldb_nt(wb, need ? 16u * ((uint32_t)row[u] * (uint32_t)C + (uint32_t)ch) : kOOB);
+      if constexpr (is_quant<W>())  // the row's scale (0 for an unused slot)
+        sc[u] = __int_as_float(ldb32(sb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
+    }
+    issue_barrier();
+    auto fold = [&](int u) {
       float f[EPC];
       unpack(W{}, wv[u], f);
+      const float z = is_quant<W>() ? zz[u] * sc[u] : zz[u];
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[e] = fmaf(zz[u], f[e], acc[e]);
+      for (int e = 0; e < EPC; ++e) acc[e] = fmaf(z, f[e], acc[e]);
+    };
+    // A full round folds every slot.  The last round stops at the wave's last row (a
+    // wave-uniform test): unpacking the empty slots costs up to 96 ALU ops a slot.  Both
+    // branches use every load, so none of them is sunk behind a test.
+    if (kb + (U - 1) * kWaves * RG < n) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) fold(u);
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (kb + u * kWaves * RG >= n) break;
+        fold(u);
+      }
     }
   }
-  // the row groups of the wave (lanes q, q + LG, ...), then the waves
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) {
-    float a = acc[e];
-    if constexpr (RG >= 2) a += __shfl_xor(a, LG);
-    if constexpr (RG >= 4) a += __shfl_xor(a, 2 * LG);
-    if (g == 0) s_red[wave][e * (LG + 1) + q] = a;
-  }
+  for (int e = 0; e < EPC; ++e) s_red[wave * RG + g][e * (LG + 1) + q] = acc[e];
   __syncthreads();
   // consecutive threads, consecutive columns: each atomic instruction covers whole lines
   for (int o = threadIdx.x; o < LG * EPC; o += kBlock) {
     const int qq = o / EPC, e = o - qq * EPC;
-    float s = s_red[0][e * (LG + 1) + qq];
+    float sum = s_red[0][e * (LG + 1) + qq];
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) s += s_red[w][e * (LG + 1) + qq];
+    for (int w = 1; w < kWaves * RG; ++w) sum += s_red[w][e * (LG + 1) + qq];
     const int col = slice * LG * EPC + o;
-    if (col < d) unsafeAtomicAdd(y + col, s);
+    if (col < d) unsafeAtomicAdd(y + col, sum);
   }
 }
 
@@ -977,13 +1021,11 @@ hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void*
   return hipGetLastError();
 }
 
-// Down-projection grid for T = 1: S column slices x R row chunks, about
-// kDownWgPerCu workgroups per CU, at most 64 segments per chunk.
-constexpr int kDownWgPerCu = 2;
-
-void down_grid(int C, int lg, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
+// Down-projection grid for T = 1: S column slices x R row chunks, about wg_per_cu
+// workgroups per CU, at most 64 segments per chunk.
+void down_grid(int C, int lg, int wg_per_cu, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
   *S = (C + lg - 1) / lg;
-  int r = (kDownWgPerCu * cu_count() + *S - 1) / *S;
+  int r = (wg_per_cu * cu_count() + *S - 1) / *S;
   const int rmin = (nseg + kWave - 1) / kWave;
   if (r < rmin) r = rmin;
   if (r > nseg) r = nseg;
@@ -994,14 +1036,16 @@ void down_grid(int C, int lg, int nseg, int d_ff, int* S, int* R, size_t* shmem_
 
 template <class W, bool DENSE>
 hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
-  if (sh.T == 1 && sh.d % W::EPC == 0) {
+  // lanes a row and workgroups per CU, as measured best on the 8B shape: a bf16 slice of
+  // 512 columns at two workgroups per CU; int8 / int4 slices of 256 / 512 columns at one
+  constexpr int LG = is_quant<W>() ? 16 : 32, WG_PER_CU = is_quant<W>() ? 1 : 2;
+  int S = 0, R = 0;
+  size_t rows = 0;
+  if (sh.T == 1 && sh.d % W::EPC == 0) down_grid(sh.d / W::EPC, LG, WG_PER_CU, ws.nseg, sh.d_ff, &S, &R, &rows);
+  const size_t shmem = DENSE ? 0 : 2 * sizeof(int) * rows;
+  if (sh.T == 1 && sh.d % W::EPC == 0 && mat_bytes(sh.wdt, sh.d_ff, sh.d) < (int64_t(1) << 31) &&
+      shmem <= 96 * 1024) {
     const int C = sh.d / W::EPC;
-    int S, R;
-    size_t rows;
-    constexpr int LG = is_quant<W>() ? 16 : kWave;
-    down_grid(C, LG, ws.nseg, sh.d_ff, &S, &R, &rows);
-    const size_t shmem = DENSE ? 0 : 4 * sizeof(int) * rows;
-    if (shmem > 96 * 1024) return hipErrorInvalidValue;
     k_down_t1<W, DENSE, LG><<<S * R, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R,
                                                           static_cast<const uint4*>(w_down_t), C, sh.d, y,
                                                           sh.sc.down);

@@ -46,6 +46,7 @@ SMALL = [
     ("lopa_bf16_T70", 70, 264, 1000, 40, BF16, 1.3),        # a pre-split 64-token pass, then 6 tokens
     ("std_bf16_d4096", 1, 4096, 2056, 0, BF16, 1.2816),    # full-width rows, short d_ff
     ("std_bf16_d4096_odd", 1, 4096, 2052, 0, BF16, 1.2816),
+    ("std_bf16_long_chunks", 1, 4096, 40000, 0, BF16, 1.2816),  # down row chunks of over 1024 slots
     ("std_bf16_T4_odd_d", 4, 100, 77, 0, BF16, 0.5),       # batch with d not a multiple of 8: element-wise
     ("lopa_bf16_T3_odd_r", 3, 264, 1000, 36, BF16, 1.0),    # batch with r not a multiple of 8: element-wise
     ("very_small", 1, 8, 3, 0, BF16, 0.0),

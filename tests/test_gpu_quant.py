@@ -33,6 +33,8 @@ SMALL = [
     ("i4_t1_std_d4096", 1, 4096, 2056, 0, I4, 1.2816),  # 2 chunks a lane
     ("i4_t1_std_d8192", 1, 8192, 600, 0, I4, 1.2816),   # 4 chunks a lane
     ("i8_t1_ragged", 1, 272, 999, 0, I8, 0.9),          # 17 chunks: a partly filled lane group
+    ("i8_t1_long_chunks", 1, 4096, 40000, 0, I8, 1.2816),  # down row chunks of over 1024 slots
+    ("i4_t1_long_chunks", 1, 4096, 40000, 64, I4, 1.2816),
     ("i4_t1_ragged", 1, 288, 999, 0, I4, 0.9),          # 9 chunks
     ("i8_t1_lopa", 1, 256, 1000, 32, I8, 1.0),
     ("i4_t1_lopa", 1, 256, 1000, 64, I4, 1.0),
