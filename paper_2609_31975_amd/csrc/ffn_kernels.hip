@@ -60,29 +60,55 @@ __device__ __forceinline__ void load_vec(const float* __restrict__ v, int C, int
 // x u0), and the per-lane sums of the limbs correct the offsets exactly in 32-bit
 // integers; `scale` turns the sums back into the vector's units.  The workgroup converts
 // the vector once, each thread a share, into LDS (prepare_lane_vec, called by dot_rows
-// after its first weight loads); each lane then reads the words of its chunks.
+// after its first weight loads); each lane then reads the words of its chunks.  The
+// thread's share is loaded by make_lane_vec, ahead of the weights: loaded after them, its
+// first use waited for the weights too (the load counter is in order).
+// Q = false with quantized weights keeps the vector in fp32 and converts each code to
+// fp32 (one op an int8 element, two an int4 one): twice the ALU work of the limbs or more,
+// but no workgroup-wide conversion in front of the first row.  The kernels whose lanes
+// multiply one row each (LoPA's z = A x and the W_up dots after LoPA's gate) take it;
+// the gate streams, several rows a lane, keep the limbs (measured: fp32 z in LoPA's gate
+// stream cost 1.3 us at int8 and 5 us at int4 on the 8B shape).
 template <class W, int CPL, bool Q = is_quant<W>()>
 struct LaneVec {
   float f[CPL][W::EPC];
 };
+// the representation of a vector multiplied with one row a lane: fp32 while a lane holds at
+// most 64 elements
+template <class W, int CPL>
+constexpr bool limb_vec() {
+  return is_quant<W>() && CPL * W::EPC > 64;
+}
 template <class W, int CPL>
 struct LaneVec<W, CPL, true> {
-  static constexpr int WPC = W::EPC / 4;  // limb words per chunk
+  static constexpr int WPC = W::EPC / 4;                          // limb words per chunk
+  static constexpr int G = W::LB == 8 ? 4 : 8;                    // elements a thread converts at a time
+  static constexpr int GPT = 8192 / G / kBlock;                   // groups a thread converts (up to 8192 elements)
   uint32_t s2[CPL][WPC], u1[CPL][WPC], u0[CPL][WPC];
   int32_t ss2, su1, su0;  // sums over the lane's elements
   float scale;
-  const float* src;  // the vector, C chunks, until converted
+  float4 raw[GPT][G / 4];  // the thread's groups of the vector, until converted
   int C, q, lpr;
   bool ready;
 };
 
-template <class W, int CPL>
+template <class W, int CPL, bool Q>
 __device__ __forceinline__ void make_lane_vec(const float* __restrict__ v, int C, int q, int lpr,
-                                              LaneVec<W, CPL>& out) {
-  if constexpr (!is_quant<W>()) {
+                                              LaneVec<W, CPL, Q>& out) {
+  if constexpr (!Q) {
     load_vec<W, CPL>(v, C, q, lpr, out.f);
   } else {
-    out.src = v;
+    using LV = LaneVec<W, CPL, Q>;
+    constexpr int G = LV::G;
+    const int len = C * W::EPC, ngroups = len / G;
+    const Buf vb = make_buf(v, 4u * (uint32_t)len);
+#pragma unroll
+    for (int i = 0; i < LV::GPT; ++i) {  // group g = threadIdx.x + i kBlock
+      const int g = (int)threadIdx.x + i * kBlock;
+#pragma unroll
+      for (int h = 0; h < G / 4; ++h)
+        out.raw[i][h] = __builtin_bit_cast(float4, ldb(vb, g < ngroups ? 16u * (uint32_t)(g * (G / 4) + h) : kOOB));
+    }
     out.C = C;
     out.q = q;
     out.lpr = lpr;
@@ -94,27 +120,24 @@ __device__ __forceinline__ void make_lane_vec(const float* __restrict__ v, int C
 constexpr int kLimbWords = 2048;
 
 // Called by every thread of the workgroup at the same point (it has barriers).
-template <class W, int CPL>
-__device__ __forceinline__ void prepare_lane_vec(LaneVec<W, CPL>& out) {
-  if constexpr (is_quant<W>()) {
+template <class W, int CPL, bool Q>
+__device__ __forceinline__ void prepare_lane_vec(LaneVec<W, CPL, Q>& out) {
+  if constexpr (Q) {
     if (out.ready) return;
     out.ready = true;
     __shared__ uint32_t s_limb[3][kLimbWords];
     __shared__ float s_max[2][kBlock / kWave];
     constexpr float kFull = 127.f * 65536.f;
-    constexpr int G = W::LB == 8 ? 4 : 8;     // elements a thread converts at a time
-    constexpr int GPT = 8192 / G / kBlock;  // groups a thread holds (vectors of 8192 elements at most)
+    using LV = LaneVec<W, CPL, Q>;
+    constexpr int G = LV::G, GPT = LV::GPT;
     const int len = out.C * W::EPC, ngroups = len / G;
-    // the thread's groups: g = threadIdx.x + i * kBlock
-    float4 vals[GPT][G / 4];
+    // the thread's groups: g = threadIdx.x + i * kBlock (zeros past the vector)
+    const auto& vals = out.raw;
     float m = 0.f, nan = 0.f;
 #pragma unroll
     for (int i = 0; i < GPT; ++i) {
-      const int g = (int)threadIdx.x + i * kBlock;
 #pragma unroll
       for (int h = 0; h < G / 4; ++h) {
-        vals[i][h] = g < ngroups ? reinterpret_cast<const float4*>(out.src)[g * (G / 4) + h]
-                                 : make_float4(0.f, 0.f, 0.f, 0.f);
         const float4 f = vals[i][h];
         m = fmaxf(fmaxf(fmaxf(m, fabsf(f.x)), fmaxf(fabsf(f.y), fabsf(f.z))), fabsf(f.w));
         nan += ((f.x * 0.f + f.y * 0.f) + (f.z * 0.f + f.w * 0.f));  // NaN if any is NaN or infinite
@@ -188,9 +211,9 @@ __device__ __forceinline__ void prepare_lane_vec(LaneVec<W, CPL>& out) {
   }
 }
 
-template <class W, int CPL>
-__device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const LaneVec<W, CPL>& v) {
-  if constexpr (!is_quant<W>()) {
+template <class W, int CPL, bool Q>
+__device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const LaneVec<W, CPL, Q>& v) {
+  if constexpr (!Q) {
     float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
@@ -258,9 +281,9 @@ __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, 
   }
 }
 
-template <class W, int CPL, class RowOf, class Sink>
+template <class W, int CPL, bool Q, class RowOf, class Sink>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
-                                         int n, LaneVec<W, CPL>& v, RowOf row_of, Sink sink) {
+                                         int n, LaneVec<W, CPL, Q>& v, RowOf row_of, Sink sink) {
   constexpr int kWaves = kBlock / kWave;
   const Buf mb = make_buf(mat, bytes);
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
@@ -274,12 +297,12 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   };
   auto finish = [&](const uint4 (&b)[CPL], int pass) {
     const int k = pass * rpp + p;
-    const float sum = group_sum(lane_dot<W, CPL>(b, v), lpr);
+    const float sum = group_sum(lane_dot<W, CPL, Q>(b, v), lpr);
     if (q == 0 && k < n) sink(k, sum);
   };
   uint4 b0[CPL], b1[CPL];
   load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
-  prepare_lane_vec<W, CPL>(v);  // quantized: the whole workgroup converts the vector
+  prepare_lane_vec<W, CPL, Q>(v);  // limbs: the whole workgroup converts the vector
   if (wave >= npass) return;
   if (wave + kWaves >= npass) {  // a single pass: nothing to overlap
     finish(b0, wave);
@@ -350,7 +373,7 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ 
                                                       GWork gw, const float* __restrict__ s_a) {
   if (g_precompute(gw)) return;
   __shared__ float s_z[kBlock];  // quantized: the block's sums before their row scales
-  LaneVec<W, CPL> xr;
+  LaneVec<W, CPL, limb_vec<W, CPL>()> xr;
   make_lane_vec<W, CPL>(x, C, lane_id() & (lpr - 1), lpr, xr);
   const int rows_per_block = (kBlock / kWave) * (kWave >> lpr_log2);
   const int k0 = blockIdx.x * rows_per_block;
@@ -458,7 +481,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
       }
     }
     {
-      LaneVec<W, CPLG> zr;
+      LaneVec<W, CPLG> zr;  // limbs: the B stream gives a lane several rows
       make_lane_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
       dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
                         gate_sink);
@@ -488,7 +511,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
     }
     compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
-    LaneVec<W, CPLU> xr;
+    LaneVec<W, CPLU, limb_vec<W, CPLU>()> xr;
     make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
     dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   } else {

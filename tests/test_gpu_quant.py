@@ -105,10 +105,11 @@ def test_quant_degenerate_thresholds(gu, wdt):
     assert idx.tolist() == list(range(600)) and gu.rel_err(ys, yd) < 1e-6
 
 
-def test_quant_zero_and_nonfinite_tokens(gu):
-    """An all-zero token gives y = 0 with nothing active (its fixed-point scale is 0); a NaN
-    in the token makes every gate value NaN, so nothing is active either."""
-    inp = wl.make_inputs(305, 1, 4096, 600, r=0, wdt=I8)
+@pytest.mark.parametrize("r", [0, 64], ids=["standard", "lopa64"])
+def test_quant_zero_and_nonfinite_tokens(gu, r):
+    """An all-zero token gives y = 0 with nothing active (the fixed-point scale of x, or z,
+    is 0); a NaN in the token makes every gate value NaN, so nothing is active either."""
+    inp = wl.make_inputs(305, 1, 4096, 600, r=r, wdt=I8)
     z = wl.FFNInputs(**{**inp.__dict__, "x": np.zeros_like(inp.x)})
     y, idx, _, _ = gu.run_gpu_q(gu.DevInputs(z), 0.0)
     assert len(idx) == 0 and np.all(y == 0)
