@@ -694,9 +694,201 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
   }
 }
 
+// The same product for a batch of T tokens (up to kTokChunk), TG of them a workgroup
+// (blockIdx.y picks the token group): every listed row of the chunk (a neuron active for
+// any token of the batch) is read once per token group and folded into TG accumulator
+// sets.  Zero gated values add nothing; a row whose values are all zero for the group is
+// not read.  The lists and the group's gated values are staged in LDS as in the
+// single-token kernel.
+template <class W, bool DENSE, int LG, int TG>
+__global__ __launch_bounds__(kBlock) void k_down_tb(const int32_t* __restrict__ seg_count,
+                                                    const int32_t* __restrict__ seg_idx,
+                                                    const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
+                                                    int slots, int T, const uint4* __restrict__ w_down_t, int C,
+                                                    int d, float* __restrict__ y, const float* __restrict__ s_down) {
+  constexpr int EPC = W::EPC, U = 8, kWaves = kBlock / kWave, RG = kWave / LG, PT = kDownSlotsPerThread;
+  extern __shared__ int s_dyn[];  // the compacted list: row indices, then TG rows of gated values
+  __shared__ int s_cnt[kWave];
+  __shared__ int s_off[kWave + 1];
+  __shared__ float s_red[kWaves * RG][EPC * (LG + 1)];
+
+  const int S = (C + LG - 1) / LG;
+  const int chunk = blockIdx.x / S, slice = blockIdx.x % S;
+  const int t0 = blockIdx.y * TG, tn = min(TG, T - t0);
+  const Split chunks(nseg, R), segs(d_ff, nseg);
+  const int seg_lo = chunks.start(chunk), seg_hi = chunks.start(chunk + 1);
+  const int row_lo = segs.start(seg_lo), row_hi = segs.start(seg_hi);
+  const int raw_n = row_hi - row_lo;
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
+  const Buf zb = make_buf(seg_zval, 4u * (uint32_t)slots * (uint32_t)T);
+  int* l_idx = s_dyn;
+  float* l_z = reinterpret_cast<float*>(s_dyn + raw_n);  // [TG][raw_n]
+
+  int n = raw_n;
+  {
+    // one round trip: the chunk's slots and the group's gated values into registers, the
+    // segment counts into LDS; then each valid slot goes to its place in the list
+    const Buf ib = make_buf(seg_idx, 4u * (uint32_t)d_ff);
+    for (int p0 = 0; p0 < raw_n; p0 += kDownSlots) {
+      int ri[PT];
+      float rz[PT][TG];
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        const int p = p0 + threadIdx.x + u * kBlock;
+        const bool ok = p < raw_n;
+        const uint32_t slot = (uint32_t)(row_lo + p);
+        ri[u] = DENSE ? (int)slot : ldb32(ib, ok ? 4u * slot : kOOB);
+#pragma unroll
+        for (int v = 0; v < TG; ++v)
+          rz[u][v] = __int_as_float(ldb32(zb, ok && v < tn ? 4u * ((uint32_t)(t0 + v) * (uint32_t)slots + slot) : kOOB));
+      }
+      if constexpr (!DENSE) {
+        if (p0 == 0 && wave == 0) {
+          const int nsc = seg_hi - seg_lo;  // <= 64, guaranteed by the host
+          const Buf cb = make_buf(seg_count, 4u * (uint32_t)nseg);
+          const int c = ldb32(cb, lane < nsc ? 4u * (uint32_t)(seg_lo + lane) : kOOB);
+          const int v = wave_inclusive_scan(c);
+          s_cnt[lane] = c;
+          s_off[lane] = v - c;
+          if (lane == kWave - 1) s_off[kWave] = v;
+        }
+        __syncthreads();
+      }
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        const int p = p0 + threadIdx.x + u * kBlock;
+        if (p0 + u * kBlock >= raw_n) break;
+        int pos = p;
+        bool keep = p < raw_n;
+        if constexpr (!DENSE) {
+          const int row = row_lo + (keep ? p : 0);
+          const int w = segs.of(row) - seg_lo;
+          const int e = row - segs.start(seg_lo + w);
+          keep = keep && e < s_cnt[w];
+          pos = s_off[w] + e;
+        }
+        if (keep) {
+          l_idx[pos] = ri[u];
+#pragma unroll
+          for (int v = 0; v < TG; ++v) l_z[v * raw_n + pos] = rz[u][v];
+        }
+      }
+    }
+    __syncthreads();
+    if constexpr (!DENSE) n = s_off[kWave];
+  }
+
+  const Buf wb = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
+  const Buf sb = make_buf(s_down, 4u * (uint32_t)d_ff);
+  const int q = lane % LG, g = lane / LG;
+  const int ch = slice * LG + q;
+  const bool cvalid = ch < C;
+  float acc[TG][EPC];
+#pragma unroll
+  for (int v = 0; v < TG; ++v)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[v][e] = 0.f;
+  for (int kb = wave * RG; kb < n; kb += kWaves * RG * U) {
+    uint4 wv[U];
+    float zz[U][TG], sc[U];
+    int row[U];
+    bool ok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kk = kb + g + u * kWaves * RG;
+      ok[u] = kk < n;
+      const int j = ok[u] ? kk : 0;  // n >= 1 here
+      row[u] = l_idx[j];
+#pragma unroll
+      for (int v = 0; v < TG; ++v) zz[u][v] = ok[u] ? l_z[v * raw_n + j] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      bool any = false;
+#pragma unroll
+      for (int v = 0; v < TG; ++v) any = any || zz[u][v] != 0.f;
+      const bool need = ok[u] && cvalid && (DENSE || any);
+      wv[u] = ldb_nt(wb, need ? 16u * ((uint32_t)row[u] * (uint32_t)C + (uint32_t)ch) : kOOB);
+      if constexpr (is_quant<W>()) sc[u] = __int_as_float(ldb32(sb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
+    }
+    issue_barrier();
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (kb + u * kWaves * RG >= n) break;  // past the wave's last row (wave-uniform)
+      float f[EPC];
+      unpack(W{}, wv[u], f);
+#pragma unroll
+      for (int v = 0; v < TG; ++v) {
+        const float z = is_quant<W>() ? zz[u][v] * sc[u] : zz[u][v];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[v][e] = fmaf(z, f[e], acc[v][e]);
+      }
+    }
+  }
+  // one token at a time through the LDS tile: the row groups and waves in a fixed order,
+  // then one atomic per column
+  for (int v = 0; v < tn; ++v) {
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) s_red[wave * RG + g][e * (LG + 1) + q] = acc[v][e];
+    __syncthreads();
+    for (int o = threadIdx.x; o < LG * EPC; o += kBlock) {
+      const int qq = o / EPC, e = o - qq * EPC;
+      float sum = s_red[0][e * (LG + 1) + qq];
+#pragma unroll
+      for (int w = 1; w < kWaves * RG; ++w) sum += s_red[w][e * (LG + 1) + qq];
+      const int col = slice * LG * EPC + o;
+      if (col < d) unsafeAtomicAdd(y + (size_t)(t0 + v) * d + col, sum);
+    }
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------------------------ generic kernels
 // Any T <= kTokChunk, any d / d_ff / r, element-wise loads.  Used for shapes and
 // batches the specialised kernels do not cover.
+// <row `row` of a [rows][len] matrix, vec> for one wave (every lane gets the sum).
+// Rows of whole 16-byte chunks are read a chunk a lane (raw buffer loads, UF chunks of
+// a lane in flight together, the vector as float4); other rows element by element.
+template <class W>
+__device__ __forceinline__ float wave_row_dot(const void* __restrict__ mat, int row, int len,
+                                              const float* __restrict__ vec) {
+  constexpr int EPC = W::EPC, UF = 64 / EPC < 4 ? 64 / EPC : 4;
+  const int lane = lane_id();
+  float s = 0.f;
+  if (len % EPC == 0) {
+    const int C = len / EPC;
+    const Buf rb = make_buf(static_cast<const char*>(mat) + (size_t)row * (size_t)C * 16u, 16u * (uint32_t)C);
+    const Buf vb = make_buf(vec, 4u * (uint32_t)len);
+    for (int c0 = 0; c0 < C; c0 += UF * kWave) {
+      uint4 w[UF];
+      uint4 xv[UF][EPC / 4];
+#pragma unroll
+      for (int u = 0; u < UF; ++u) {
+        const int ch = c0 + u * kWave + lane;
+        const bool ok = ch < C;
+        w[u] = ldb(rb, ok ? 16u * (uint32_t)ch : kOOB);
+#pragma unroll
+        for (int i = 0; i < EPC / 4; ++i) xv[u][i] = ldb(vb, ok ? 16u * (uint32_t)(ch * (EPC / 4) + i) : kOOB);
+      }
+#pragma unroll
+      for (int u = 0; u < UF; ++u) {
+        float f[EPC];
+        unpack(W{}, w[u], f);
+#pragma unroll
+        for (int i = 0; i < EPC / 4; ++i) {
+          s = fmaf(f[4 * i], __uint_as_float(xv[u][i].x), s);
+          s = fmaf(f[4 * i + 1], __uint_as_float(xv[u][i].y), s);
+          s = fmaf(f[4 * i + 2], __uint_as_float(xv[u][i].z), s);
+          s = fmaf(f[4 * i + 3], __uint_as_float(xv[u][i].w), s);
+        }
+      }
+    }
+  } else {
+    for (int j = lane; j < len; j += kWave) s = fmaf(welem(W{}, mat, (size_t)row * len + j), vec[j], s);
+  }
+  return wave_sum(s);
+}
+
 template <class W>
 __global__ __launch_bounds__(kBlock) void k_lopa_z_generic(const float* __restrict__ x, const void* __restrict__ A,
                                                            int T, int d, int r, float* __restrict__ z,
@@ -705,9 +897,7 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_generic(const float* __restri
   if (k >= r) return;
   const int lane = lane_id();
   for (int tau = 0; tau < T; ++tau) {
-    float s = 0.f;
-    for (int j = lane; j < d; j += kWave) s = fmaf(welem(W{}, A, (size_t)k * d + j), x[(size_t)tau * d + j], s);
-    s = wave_sum(s);
+    float s = wave_row_dot<W>(A, k, d, x + (size_t)tau * d);
     if constexpr (is_quant<W>()) s *= s_a[k];
     if (lane == 0) z[(size_t)tau * r + k] = s;
   }
@@ -738,11 +928,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   clear_output(y, T * d, meta, nseg);
 
   for (int k = wave; k < nrows; k += kWaves) {
-    const size_t rowoff = (size_t)(row0 + k) * len;
     for (int tau = 0; tau < T; ++tau) {
-      float s = 0.f;
-      for (int j = lane; j < len; j += kWave) s = fmaf(welem(W{}, gate_w, rowoff + j), vec[(size_t)tau * len + j], s);
-      s = wave_sum(s);
+      float s = wave_row_dot<W>(gate_w, row0 + k, len, vec + (size_t)tau * len);
       if constexpr (is_quant<W>()) s *= s_g[row0 + k];
       if (lane == 0) s_h[k][tau] = s;
     }
@@ -786,11 +973,8 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   const int cnt = s_cnt;
   for (int e = wave; e < cnt; e += kWaves) {
     const int kr = s_list[e];
-    const size_t rowoff = (size_t)(row0 + kr) * d;
     for (int tau = 0; tau < T; ++tau) {
-      float s = 0.f;
-      for (int j = lane; j < d; j += kWave) s = fmaf(welem(W{}, w_up, rowoff + j), x[(size_t)tau * d + j], s);
-      s = wave_sum(s);
+      float s = wave_row_dot<W>(w_up, row0 + kr, d, x + (size_t)tau * d);
       if constexpr (is_quant<W>()) s *= s_up[row0 + kr];
       if (lane == 0) seg_zval[(size_t)tau * slots + row0 + e] = s_h[kr][tau] * (FULL ? up_value(form.silu_up, s) : s);
     }
@@ -1062,16 +1246,24 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
   // lanes a row and workgroups per CU, as measured best on the 8B shape: a bf16 slice of
   // 512 columns at two workgroups per CU; int8 / int4 slices of 256 / 512 columns at one
   constexpr int LG = is_quant<W>() ? 16 : 32, WG_PER_CU = is_quant<W>() ? 1 : 2;
+  // batches: TG tokens a workgroup (at most 64 accumulators a lane)
+  constexpr int TG = 64 / W::EPC < 4 ? 64 / W::EPC : 4;
+  const bool rows_ok = sh.d % W::EPC == 0 && mat_bytes(sh.wdt, sh.d_ff, sh.d) < (int64_t(1) << 31);
+  const int C = sh.d / W::EPC;
   int S = 0, R = 0;
   size_t rows = 0;
-  if (sh.T == 1 && sh.d % W::EPC == 0) down_grid(sh.d / W::EPC, LG, WG_PER_CU, ws.nseg, sh.d_ff, &S, &R, &rows);
-  const size_t shmem = DENSE ? 0 : 2 * sizeof(int) * rows;
-  if (sh.T == 1 && sh.d % W::EPC == 0 && mat_bytes(sh.wdt, sh.d_ff, sh.d) < (int64_t(1) << 31) &&
-      shmem <= 96 * 1024) {
-    const int C = sh.d / W::EPC;
-    k_down_t1<W, DENSE, LG><<<S * R, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff, R,
-                                                          static_cast<const uint4*>(w_down_t), C, sh.d, y,
-                                                          sh.sc.down);
+  if (rows_ok) down_grid(C, LG, WG_PER_CU, ws.nseg, sh.d_ff, &S, &R, &rows);
+  const size_t shmem_t1 = DENSE ? 0 : 2 * sizeof(int) * rows, shmem_tb = (1 + TG) * sizeof(int) * rows;
+  if (rows_ok && sh.T == 1 && shmem_t1 <= 96 * 1024) {
+    k_down_t1<W, DENSE, LG><<<S * R, kBlock, shmem_t1, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
+                                                             R, static_cast<const uint4*>(w_down_t), C, sh.d, y,
+                                                             sh.sc.down);
+  } else if (rows_ok && sh.T > 1 && shmem_tb <= 96 * 1024 && (int64_t)sh.T * ws.slots < (int64_t(1) << 29)) {
+    const dim3 grid(S * R, (sh.T + TG - 1) / TG);
+    k_down_tb<W, DENSE, LG, TG><<<grid, kBlock, shmem_tb, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg,
+                                                               sh.d_ff, R, ws.slots, sh.T,
+                                                               static_cast<const uint4*>(w_down_t), C, sh.d, y,
+                                                               sh.sc.down);
   } else {
     const size_t shmem = DENSE ? 0 : sizeof(int) * (size_t)(ws.nseg + 1);
     const int grid = (sh.d + kBlock - 1) / kBlock;
