@@ -826,8 +826,10 @@ __global__ __launch_bounds__(kBlock) void k_down_tb(const int32_t* __restrict__ 
     }
   }
   // one token at a time through the LDS tile: the row groups and waves in a fixed order,
-  // then one atomic per column
-  for (int v = 0; v < tn; ++v) {
+  // then one atomic per column (v runs to TG so that acc is indexed at compile time)
+#pragma unroll
+  for (int v = 0; v < TG; ++v) {
+    if (v >= tn) break;  // workgroup-uniform
 #pragma unroll
     for (int e = 0; e < EPC; ++e) s_red[wave * RG + g][e * (LG + 1) + q] = acc[v][e];
     __syncthreads();
@@ -889,6 +891,65 @@ __device__ __forceinline__ float wave_row_dot(const void* __restrict__ mat, int 
   return wave_sum(s);
 }
 
+// Token vectors staged in LDS by the element-wise gate kernel: at most kVecTok of them
+// and kVecFloats floats in all.
+constexpr int kVecTok = 4, kVecFloats = 8192;
+
+// out[v] = <row `row` of a [rows][len] matrix, sv + v len> for v < tn <= kVecTok, the
+// vectors in LDS; one wave, every lane gets the sums.  The lane's chunks of the row are
+// loaded once for all the vectors.
+template <class W>
+__device__ __forceinline__ void wave_row_dots_lds(const void* __restrict__ mat, int row, int len, const float* sv,
+                                                  int tn, float (&out)[kVecTok]) {
+  constexpr int EPC = W::EPC, UF = 64 / EPC < 4 ? 64 / EPC : 4;
+  const int lane = lane_id();
+  float acc[kVecTok];
+#pragma unroll
+  for (int v = 0; v < kVecTok; ++v) acc[v] = 0.f;
+  if (len % EPC == 0) {
+    const int C = len / EPC;
+    const Buf rb = make_buf(static_cast<const char*>(mat) + (size_t)row * (size_t)C * 16u, 16u * (uint32_t)C);
+    for (int c0 = 0; c0 < C; c0 += UF * kWave) {
+      uint4 w[UF];
+#pragma unroll
+      for (int u = 0; u < UF; ++u) {
+        const int ch = c0 + u * kWave + lane;
+        w[u] = ldb(rb, ch < C ? 16u * (uint32_t)ch : kOOB);
+      }
+#pragma unroll
+      for (int u = 0; u < UF; ++u) {
+        const int ch = c0 + u * kWave + lane;
+        if (ch < C) {
+          float f[EPC];
+          unpack(W{}, w[u], f);
+#pragma unroll
+          for (int v = 0; v < kVecTok; ++v)
+            if (v < tn) {
+              const float4* xp = reinterpret_cast<const float4*>(sv + v * len + ch * EPC);
+#pragma unroll
+              for (int i = 0; i < EPC / 4; ++i) {
+                const float4 xv = xp[i];
+                acc[v] = fmaf(f[4 * i], xv.x, acc[v]);
+                acc[v] = fmaf(f[4 * i + 1], xv.y, acc[v]);
+                acc[v] = fmaf(f[4 * i + 2], xv.z, acc[v]);
+                acc[v] = fmaf(f[4 * i + 3], xv.w, acc[v]);
+              }
+            }
+        }
+      }
+    }
+  } else {
+    for (int j = lane; j < len; j += kWave) {
+      const float wj = welem(W{}, mat, (size_t)row * len + j);
+#pragma unroll
+      for (int v = 0; v < kVecTok; ++v)
+        if (v < tn) acc[v] = fmaf(wj, sv[v * len + j], acc[v]);
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < kVecTok; ++v) out[v] = wave_sum(acc[v]);
+}
+
 template <class W>
 __global__ __launch_bounds__(kBlock) void k_lopa_z_generic(const float* __restrict__ x, const void* __restrict__ A,
                                                            int T, int d, int r, float* __restrict__ z,
@@ -918,6 +979,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   __shared__ float s_h[kSegMax][kTokChunk];
   __shared__ int s_list[kSegMax];
   __shared__ int s_cnt;
+  __shared__ __align__(16) float s_vec[kVecFloats];
   const int seg = blockIdx.x;
   const Split segs(d_ff, nseg);
   const int row0 = segs.start(seg), nrows = segs.start(seg + 1) - row0;
@@ -927,13 +989,37 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   const float* vec = LOPA ? z : x;
   clear_output(y, T * d, meta, nseg);
 
-  for (int k = wave; k < nrows; k += kWaves) {
-    for (int tau = 0; tau < T; ++tau) {
-      float s = wave_row_dot<W>(gate_w, row0 + k, len, vec + (size_t)tau * len);
-      if constexpr (is_quant<W>()) s *= s_g[row0 + k];
-      if (lane == 0) s_h[k][tau] = s;
+  // rows `k` (k = wave, wave + 4, ... < n) dotted with every token's vector `v` (len
+  // floats a token), the vectors staged in LDS a group of tokens at a time when they fit,
+  // so that each row chunk is loaded once a group and the vectors come from LDS;
+  // put(k, tau, value) takes the results
+  auto rows_by_tokens = [&](const void* mat, auto row_of, int n, const float* v, int vlen, auto put) {
+    const int tg = vlen <= kVecFloats ? min(kVecTok, kVecFloats / vlen) : 0;
+    if (tg == 0) {  // too long for LDS: from memory, a token at a time
+      for (int k = wave; k < n; k += kWaves)
+        for (int tau = 0; tau < T; ++tau) put(k, tau, wave_row_dot<W>(mat, row_of(k), vlen, v + (size_t)tau * vlen));
+      return;
     }
-  }
+    for (int t0 = 0; t0 < T; t0 += tg) {
+      const int tn = min(tg, T - t0);
+      __syncthreads();  // the previous group's readers are done
+      for (int i = threadIdx.x; i < tn * vlen; i += kBlock) s_vec[i] = v[(size_t)t0 * vlen + i];
+      __syncthreads();
+      for (int k = wave; k < n; k += kWaves) {
+        float o[kVecTok];
+        wave_row_dots_lds<W>(mat, row_of(k), vlen, s_vec, tn, o);
+#pragma unroll
+        for (int u = 0; u < kVecTok; ++u)
+          if (u < tn) put(k, t0 + u, o[u]);
+      }
+    }
+  };
+
+  rows_by_tokens(
+      gate_w, [&](int k) { return row0 + k; }, nrows, vec, len, [&](int k, int tau, float s) {
+        if constexpr (is_quant<W>()) s *= s_g[row0 + k];
+        if (lane == 0) s_h[k][tau] = s;
+      });
   __syncthreads();
   if constexpr (FULL) {
     if (form.g_idx) {  // LoPA's fixed term: h += G x
@@ -971,14 +1057,12 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_generic(const float* __restr
   __syncthreads();
 
   const int cnt = s_cnt;
-  for (int e = wave; e < cnt; e += kWaves) {
-    const int kr = s_list[e];
-    for (int tau = 0; tau < T; ++tau) {
-      float s = wave_row_dot<W>(w_up, row0 + kr, d, x + (size_t)tau * d);
-      if constexpr (is_quant<W>()) s *= s_up[row0 + kr];
-      if (lane == 0) seg_zval[(size_t)tau * slots + row0 + e] = s_h[kr][tau] * (FULL ? up_value(form.silu_up, s) : s);
-    }
-  }
+  rows_by_tokens(
+      w_up, [&](int e) { return row0 + s_list[e]; }, cnt, x, d, [&](int e, int tau, float s) {
+        const int kr = s_list[e];
+        if constexpr (is_quant<W>()) s *= s_up[row0 + kr];
+        if (lane == 0) seg_zval[(size_t)tau * slots + row0 + e] = s_h[kr][tau] * (FULL ? up_value(form.silu_up, s) : s);
+      });
 }
 
 // thread per output column; tokens in groups of 8 accumulators; y written directly
