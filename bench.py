@@ -596,8 +596,9 @@ def main():
         del run
         shapes.clear()
         torch.cuda.empty_cache()
-        # quantized weights (8B shape, T = 1): sparse and dense in the same format, against
-        # the bf16 dense call and an fp32 dense call (the paper's full-precision baseline)
+        # quantized weights (8B shape): sparse and dense in the same format; single-token
+        # calls also against the bf16 dense call and an fp32 dense call (the paper's
+        # full-precision baseline)
         qw = [w for w in wl.workloads() if w.wdt in wl.QMAX and w.d == head.d]
         if qw:
             f32 = Shape(head.d, head.d_ff, [0], sets_for(algorithmic_bytes(head.d, head.d_ff, 0, 1, head.d_ff, True,
@@ -614,18 +615,23 @@ def main():
                 qdense = {}
                 for w in ws_:
                     rw = measure(shq, w.r, w.T, w.t, K, W, name=w.name)[0]
-                    if w.r not in qdense:
-                        qdense[w.r] = dense_time(shq, w.r, w.T, K, W)[0]
+                    if (w.r, w.T) not in qdense:
+                        qdense[(w.r, w.T)] = dense_time(shq, w.r, w.T, K, W)[0]
+                    qd = qdense[(w.r, w.T)]
                     rw.update(weights={wl.I8: "int8", wl.I4: "int4"}[wdt], path="sparse",
-                              dense_same_format_us_per_call=round(qdense[w.r], 3),
-                              speedup_vs_dense_same_format=round(qdense[w.r] / rw["us_per_call"], 3),
-                              dense_us_per_call=round(dense_us, 3),
-                              speedup_vs_dense=round(dense_us / rw["us_per_call"], 3),
-                              fp32_dense_us_per_call=round(f32_us, 3),
-                              speedup_vs_fp32_dense=round(f32_us / rw["us_per_call"], 3))
+                              dense_same_format_us_per_call=round(qd, 3),
+                              speedup_vs_dense_same_format=round(qd / rw["us_per_call"], 3))
+                    if w.T == 1:  # the bf16 and fp32 dense calls above are single-token ones
+                        rw.update(dense_us_per_call=round(dense_us, 3),
+                                  speedup_vs_dense=round(dense_us / rw["us_per_call"], 3),
+                                  fp32_dense_us_per_call=round(f32_us, 3),
+                                  speedup_vs_fp32_dense=round(f32_us / rw["us_per_call"], 3))
+                        log(f"[bench] {w.name}: {rw['us_per_call']} us, x{rw['speedup_vs_dense']} vs bf16 dense, "
+                            f"x{rw['speedup_vs_fp32_dense']} vs fp32 dense")
+                    else:
+                        log(f"[bench] {w.name}: {rw['us_per_call']} us, x{rw['speedup_vs_dense_same_format']} vs "
+                            f"dense in the same format")
                     sweep.append(rw)
-                    log(f"[bench] {w.name}: {rw['us_per_call']} us, x{rw['speedup_vs_dense']} vs bf16 dense, "
-                        f"x{rw['speedup_vs_fp32_dense']} vs fp32 dense")
                 del shq
                 torch.cuda.empty_cache()
         # LoPA approximation of the 8B gate (Section 3.3): one conversion, timed end to end

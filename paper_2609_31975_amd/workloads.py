@@ -221,6 +221,8 @@ def workloads() -> list[Workload]:
     for wdt, tag in ((I8, "i8"), (I4, "i4")):
         out.append(Workload(f"8b_std_s90_{tag}", 4096, 14336, 0, 1, wdt, THRESHOLD[0.90], 6000, 4))
         out.append(Workload(f"8b_lopa512_s90_{tag}", 4096, 14336, 512, 1, wdt, THRESHOLD[0.90], 7000, 4))
+        out.append(Workload(f"8b_std_s90_{tag}_T4", 4096, 14336, 0, 4, wdt, THRESHOLD[0.90], 6000, 4))
+        out.append(Workload(f"8b_lopa512_s90_{tag}_T4", 4096, 14336, 512, 4, wdt, THRESHOLD[0.90], 7000, 4))
     for T in (1, 16):
         out.append(Workload(f"8b_lopa512_full_s90_T{T}", 4096, 14336, 512, T, BF16,
                             round(THRESHOLD[0.90] * 2 ** 0.5, 4), 3000, 4, "full"))
