@@ -65,6 +65,47 @@ __device__ __forceinline__ void split8(const float (&v)[8], bf16x8_t& hi, bf16x8
   }
 }
 
+// Chunk j (elements 8j .. 8j + 7) of a loaded 16-byte chunk of W, as 8 bf16: the chunk
+// itself for bf16, the codes converted for int8 / int4 (exact: small integers), so that
+// quantized rows enter the same bf16 operand tiles.  The row scales are applied to the
+// products.
+template <class W, int J>
+__device__ __forceinline__ uint4 bf16_chunk(const uint4& v) {
+  if constexpr (W::EPC == 8) {
+    return v;
+  } else {
+    const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      float a, b;  // elements 8J + 2p and 8J + 2p + 1
+      if constexpr (W::EPC == 16) {
+        const uint32_t w = d[2 * J + (p >> 1)];
+        const int e = 2 * (p & 1);
+        a = (float)((int32_t)(w << (24 - 8 * e)) >> 24);
+        b = (float)((int32_t)(w << (16 - 8 * e)) >> 24);
+      } else {
+        const uint32_t w = d[J];
+        a = (float)((int32_t)(w << (28 - 8 * p)) >> 28);
+        b = (float)((int32_t)(w << (24 - 8 * p)) >> 28);
+      }
+      // the high halves of both (selector bytes 2, 3 of the second operand, then of the first)
+      o[p] = __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+// all W::EPC / 8 of them into consecutive 16-byte slots of an LDS row
+template <class W>
+__device__ __forceinline__ void put_bf16_chunks(uint4* dst, const uint4& v) {
+  dst[0] = bf16_chunk<W, 0>(v);
+  if constexpr (W::EPC >= 16) dst[1] = bf16_chunk<W, 1>(v);
+  if constexpr (W::EPC >= 32) {
+    dst[2] = bf16_chunk<W, 2>(v);
+    dst[3] = bf16_chunk<W, 3>(v);
+  }
+}
+
 // k-step range [ks0, ks1) of k part kp out of np for rows of C chunks (4 chunks a step)
 __device__ __forceinline__ void kpart(int C, int kp, int np, int* ks0, int* ks1) {
   const int nks = (C + 3) / 4;
@@ -81,25 +122,31 @@ __device__ __forceinline__ void kpart(int C, int kp, int np, int* ks0, int* ks1)
 // pad chunk per row keeping the operand reads free of bank conflicts.  (Loading the
 // operand layout directly reads 64 bytes of each of 16 rows per instruction, which
 // streams about 25% slower.)
-template <int RT, int KU>
+// Quantized rows (W = WI8 / WI4): a loaded 16-byte chunk holds R8 = 2 or 4 of the tile's
+// 8-element chunks, so a row takes 4 KU / R8 lanes; the codes are converted to bf16 as
+// they go to the tile, which keeps the bf16 layout.
+template <int RT, int KU, class W = WBf16>
 struct WStage {
-  static constexpr int LPR = 4 * KU;          // lanes per row of a load instruction
+  static constexpr int R8 = W::EPC / 8;       // tile chunks per loaded chunk
+  static constexpr int LPR = 4 * KU / R8;     // lanes per row of a load instruction
   static constexpr int RPI = kWave / LPR;     // rows per load instruction
-  static constexpr int NI = RT * KU;          // load instructions per group
-  static constexpr int PITCH = LPR + 1;       // 16-byte chunks per LDS row
+  static constexpr int NI = (16 * RT + RPI - 1) / RPI;  // load instructions per group
+  static constexpr int PITCH = 4 * KU + 1;    // 16-byte (8 bf16) chunks per LDS row
   static constexpr int WORDS = 16 * RT * PITCH;  // uint4 of one wave's tile
 };
 
-// Rows of this lane's load instructions: roff[i] = row_of(i RPI + lane / LPR) * C, or -1
-// where row_of gives no row (-1).
-template <int RT, int KU, class RowOf>
-__device__ __forceinline__ void stage_rows(int (&roff)[RT * KU], int C, RowOf row_of) {
-  using S = WStage<RT, KU>;
+// Rows of this lane's load instructions: roff[i] = row_of(i RPI + lane / LPR) times the
+// row's loaded chunks (C / R8 for rows of C tile chunks), or -1 where row_of gives no row
+// (-1) or the lane falls past the tile's 16 RT rows.
+template <int RT, int KU, class W = WBf16, class RowOf>
+__device__ __forceinline__ void stage_rows(int* roff, int C, RowOf row_of) {  // roff: WStage::NI entries
+  using S = WStage<RT, KU, W>;
   const int lane = lane_id();
 #pragma unroll
   for (int i = 0; i < S::NI; ++i) {
-    const int r = row_of(i * S::RPI + lane / S::LPR);
-    roff[i] = r >= 0 ? r * C : -1;
+    const int br = i * S::RPI + lane / S::LPR;
+    const int r = br < 16 * RT ? row_of(br) : -1;
+    roff[i] = r >= 0 ? r * (C / S::R8) : -1;
   }
 }
 
@@ -111,21 +158,22 @@ __device__ __forceinline__ void stage_rows(int (&roff)[RT * KU], int C, RowOf ro
 //  - PRE (pre-split, NP = 1): b[u][nt][0] = the hi and lo fragments of the lane, read from
 //    planes [k step][token tile][lane] of uint4 (k_split_tokens); the lo plane starts
 //    part_bytes after the hi plane; tn = the planes' token-tile count.
-template <int RT, int NT, int KU, int NP>
+template <int RT, int NT, int KU, int NP, class W = WBf16>
 struct Frags {
-  uint4 a[RT * KU];
+  uint4 a[WStage<RT, KU, W>::NI];
   uint4 b[KU][NT][NP][2];
 };
 
-template <int RT, int NT, int KU, int NP, bool PRE = false>
-__device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP>& f, const Buf& wb, int C,
-                                           const int (&roff)[RT * KU], const Buf& tb, uint32_t part_bytes,
-                                           int tn, int ks, int ks1) {
-  using S = WStage<RT, KU>;
+template <int RT, int NT, int KU, int NP, bool PRE = false, class W = WBf16>
+__device__ __forceinline__ void load_frags(Frags<RT, NT, KU, NP, W>& f, const Buf& wb, int C,
+                                           const int* roff, const Buf& tb, uint32_t part_bytes, int tn, int ks,
+                                           int ks1) {
+  using S = WStage<RT, KU, W>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
   {
-    const int gc = lane % S::LPR, c = 4 * ks + gc;
-    const bool cv = ks + (gc >> 2) < ks1 && c < C;
+    // the lane's loaded chunk gc of the group: tile chunks R8 gc .. R8 gc + R8 - 1
+    const int gc = lane % S::LPR, c = 4 * ks / S::R8 + gc;
+    const bool cv = ks + (gc * S::R8 >> 2) < ks1 && c < C / S::R8;
 #pragma unroll
     for (int i = 0; i < S::NI; ++i)
       f.a[i] = ldb_nt(wb, (cv && roff[i] >= 0) ? 16u * (uint32_t)(roff[i] + c) : kOOB);
@@ -189,12 +237,19 @@ __device__ __forceinline__ void sum_split(const uint4 (&b)[NP][2], bf16x8_t& hi,
   split8(v, hi, lo);
 }
 
-template <int RT, int NT, int KU, int NP, bool PRE = false>
-__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4* tile, f32x4_t (&acc)[RT][NT]) {
-  using S = WStage<RT, KU>;
+template <int RT, int NT, int KU, int NP, bool PRE = false, class W = WBf16>
+__device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP, W>& f, uint4* tile, f32x4_t (&acc)[RT][NT]) {
+  using S = WStage<RT, KU, W>;
   const int lane = lane_id(), m = lane & 15, g = lane >> 4;
 #pragma unroll
-  for (int i = 0; i < S::NI; ++i) tile[(i * S::RPI + lane / S::LPR) * S::PITCH + lane % S::LPR] = f.a[i];
+  for (int i = 0; i < S::NI; ++i) {
+    const int br = i * S::RPI + lane / S::LPR;
+    if constexpr (S::R8 == 1) {
+      tile[br * S::PITCH + lane % S::LPR] = f.a[i];
+    } else if (br < 16 * RT) {  // lanes past the tile's rows loaded nothing
+      put_bf16_chunks<W>(tile + br * S::PITCH + (lane % S::LPR) * S::R8, f.a[i]);
+    }
+  }
   __builtin_amdgcn_wave_barrier();  // LDS operations of a wave complete in order
 #pragma unroll
   for (int u = 0; u < KU; ++u)
@@ -223,24 +278,23 @@ __device__ __forceinline__ void mma_frags(const Frags<RT, NT, KU, NP>& f, uint4*
 // pair always multiplies both halves (a group past ks1 adds zeros) and the exit test
 // closes the pair, so no load sits on a conditional path: with an exit test between
 // the halves the compiler moved the loads next to their use and waited on them there.
-template <int RT, int NT, int KU, int NP, bool PRE = false>
-__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int (&roff)[RT * KU], uint4* tile,
-                                            const Buf& tb, uint32_t part_bytes, int tn, int ks0, int ks1,
-                                            f32x4_t (&acc)[RT][NT]) {
+template <int RT, int NT, int KU, int NP, bool PRE = false, class W = WBf16>
+__device__ __forceinline__ void stream_rows(const Buf& wb, int C, const int* roff, uint4* tile, const Buf& tb,
+                                            uint32_t part_bytes, int tn, int ks0, int ks1, f32x4_t (&acc)[RT][NT]) {
   if (ks0 >= ks1) return;
-  Frags<RT, NT, KU, NP> f0, f1;
-  load_frags<RT, NT, KU, NP, PRE>(f0, wb, C, roff, tb, part_bytes, tn, ks0, ks1);
+  Frags<RT, NT, KU, NP, W> f0, f1;
+  load_frags<RT, NT, KU, NP, PRE, W>(f0, wb, C, roff, tb, part_bytes, tn, ks0, ks1);
   if (ks0 + KU >= ks1) {  // a single group
-    mma_frags<RT, NT, KU, NP, PRE>(f0, tile, acc);
+    mma_frags<RT, NT, KU, NP, PRE, W>(f0, tile, acc);
     return;
   }
   for (int ks = ks0;; ks += 2 * KU) {
-    load_frags<RT, NT, KU, NP, PRE>(f1, wb, C, roff, tb, part_bytes, tn, ks + KU, ks1);
+    load_frags<RT, NT, KU, NP, PRE, W>(f1, wb, C, roff, tb, part_bytes, tn, ks + KU, ks1);
     issue_barrier();
-    mma_frags<RT, NT, KU, NP, PRE>(f0, tile, acc);
-    load_frags<RT, NT, KU, NP, PRE>(f0, wb, C, roff, tb, part_bytes, tn, ks + 2 * KU, ks1);
+    mma_frags<RT, NT, KU, NP, PRE, W>(f0, tile, acc);
+    load_frags<RT, NT, KU, NP, PRE, W>(f0, wb, C, roff, tb, part_bytes, tn, ks + 2 * KU, ks1);
     issue_barrier();
-    mma_frags<RT, NT, KU, NP, PRE>(f1, tile, acc);
+    mma_frags<RT, NT, KU, NP, PRE, W>(f1, tile, acc);
     if (ks + 2 * KU >= ks1) break;
   }
 }
@@ -294,28 +348,30 @@ __global__ __launch_bounds__(kBlock) void k_split_tokens(const float* __restrict
 constexpr int kZWaves = 16;
 constexpr int kZParts = 2;
 
-template <int NT>
+template <int NT, class W>
 __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __restrict__ x,
                                                                  const uint4* __restrict__ xs, int ntt,
                                                                  const uint4* __restrict__ A, int C, int T, int r,
-                                                                 int tc, float* __restrict__ zp, GWork gw) {
+                                                                 int tc, float* __restrict__ zp, GWork gw,
+                                                                 const float* __restrict__ s_a) {
   if (g_precompute(gw)) return;
   constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   __shared__ f32x4_t s_part[kZWaves][NT][kWave];
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   const int tile = blockIdx.x / kZParts, part = blockIdx.x % kZParts;
   constexpr int KU = NT == 1 ? 4 : NT == 2 ? 2 : 1;
-  __shared__ uint4 s_stage[kZWaves][WStage<1, KU>::WORDS];
-  int roff[KU];
-  stage_rows<1, KU>(roff, C, [&](int br) { return tile * 16 + br < r ? tile * 16 + br : -1; });
-  const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)C);
+  using S = WStage<1, KU, W>;
+  __shared__ uint4 s_stage[kZWaves][S::WORDS];
+  int roff[S::NI];
+  stage_rows<1, KU, W>(roff, C, [&](int br) { return tile * 16 + br < r ? tile * 16 + br : -1; });
+  const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)(C / S::R8));
   const TokSrc tok = token_source(PRE, x, xs, C, T, ntt);
   f32x4_t acc[1][NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[0][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   int ks0, ks1;
   kpart(C, part * kZWaves + wave, kZParts * kZWaves, &ks0, &ks1);
-  stream_rows<1, NT, KU, 1, PRE>(ab, C, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
+  stream_rows<1, NT, KU, 1, PRE, W>(ab, C, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[0][nt];
   __syncthreads();
@@ -330,6 +386,7 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < kZWaves; ++w) s += sp[(w * NT + nt) * kWave * 4 + src];
+    if constexpr (is_quant<W>()) s *= s_a[k];  // the row's scale
     zp[((size_t)part * tc + tok) * r + k] = s;
   }
 }
@@ -349,7 +406,7 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 // KU / KUU: k steps per load group of the gate rows / the W_up rows.
 // FORM (a FormKind): the paper's full form (`form`): the activation value, SiLU on the
 // W_up output and, with kFormLoPA, the fixed term G added to the gate before the union.
-template <bool LOPA, bool DENSE, int NT, int KU, int KUU, int FORM>
+template <class W, bool LOPA, bool DENSE, int NT, int KU, int KUU, int FORM>
 __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const float* __restrict__ zp,
                                              const uint4* __restrict__ gate_w, int Cg, const uint4* __restrict__ w_up,
                                              int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,
@@ -357,7 +414,10 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
                                              int32_t* __restrict__ seg_idx, float* __restrict__ seg_act,
                                              uint4* __restrict__ zf, float* __restrict__ y,
                                              const uint4* __restrict__ xs, int ntt, Form form,
-                                             const float* __restrict__ gx) {
+                                             const float* __restrict__ gx, const float* __restrict__ s_g,
+                                             const float* __restrict__ s_up, const float* __restrict__ s_down) {
+  constexpr bool Q = is_quant<W>();
+  constexpr int R8 = W::EPC / 8;
   constexpr bool FULL = FORM != kFormDefault, HAS_G = FORM == kFormLoPA;
   constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   // the W_up rows of a union of at most two row tiles go as two tiles with twice the k
@@ -376,7 +436,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
   const int m = lane & 15, g = lane >> 4;
   clear_output(y, T * d, meta, nseg);
   const TokSrc tok = token_source(PRE, x, xs, Cu, T, ntt);
-  const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu);
+  const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)(Cu / R8));
 
   // segments blockIdx.x, blockIdx.x + gridDim.x, ... (the host makes the counts equal)
   const Split segs(d_ff, nseg);
@@ -391,16 +451,17 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[rt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     {
-      int roff[kTiles * KU];
-      stage_rows<kTiles, KU>(roff, Cg, [&](int br) { return br < nrows ? row0 + br : -1; });
+      int roff[WStage<kTiles, KU, W>::NI];
+      stage_rows<kTiles, KU, W>(roff, Cg, [&](int br) { return br < nrows ? row0 + br : -1; });
       int ks0, ks1;
       kpart(Cg, wave, kParts, &ks0, &ks1);
-      const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg);
+      const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)(Cg / R8));
       if constexpr (LOPA) {
         const uint32_t part = 32u * (uint32_t)tc * (uint32_t)Cg;
-        stream_rows<kTiles, NT, KU, 2>(gb, Cg, roff, s_stage[wave], make_buf(zp, 2 * part), part, T, ks0, ks1, acc);
+        stream_rows<kTiles, NT, KU, 2, false, W>(gb, Cg, roff, s_stage[wave], make_buf(zp, 2 * part), part, T, ks0,
+                                                 ks1, acc);
       } else {
-        stream_rows<kTiles, NT, KU, 1, PRE>(gb, Cg, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
+        stream_rows<kTiles, NT, KU, 1, PRE, W>(gb, Cg, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
       }
     }
     // LoPA's fixed term (G x) of the rows and tokens this lane thresholds, written by the z
@@ -417,6 +478,16 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
           gxb[nt][i] = ldb32(xb, tok < T && rl < nrows ? 4u * ((uint32_t)tok * (uint32_t)d_ff + (uint32_t)(row0 + rl))
                                                         : kOOB);
         }
+    }
+    // quantized: the row scales of the rows this lane thresholds (likewise after the stream)
+    uint32_t sgb[Q ? 4 : 1] = {};
+    if constexpr (Q) {
+      const Buf qb = make_buf(s_g, 4u * (uint32_t)d_ff);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rl = 16 * wave + 4 * g + i;
+        sgb[i] = ldb32(qb, rl < nrows ? 4u * (uint32_t)(row0 + rl) : kOOB);
+      }
     }
 #pragma unroll
     for (int rt = 0; rt < kTiles; ++rt)
@@ -439,6 +510,7 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
         for (int nt = 0; nt < NT; ++nt) {
           const int tok = 16 * nt + m;
           float hv = h[nt][i];
+          if constexpr (Q) hv *= __builtin_bit_cast(float, sgb[i]);
           if constexpr (HAS_G) hv += __builtin_bit_cast(float, gxb[nt][i]);  // h += G x
           const bool on = tok < T && hv > t;
           if (tok < T && rl < nrows) s_act[rl][tok] = on ? (FULL ? gate_value(form.act, hv - t) : hv - t) : 0.f;
@@ -485,16 +557,16 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       kpart(Cu, wave, kParts, &ks0, &ks1);
       auto up_row = [&](int e) { return e < cnt ? row0 + s_list[e] : -1; };
       auto full = [&] {
-        int roff[kTiles * KUU];
-        stage_rows<kTiles, KUU>(roff, Cu, up_row);
-        stream_rows<kTiles, NT, KUU, 1, PRE>(ub, Cu, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
+        int roff[WStage<kTiles, KUU, W>::NI];
+        stage_rows<kTiles, KUU, W>(roff, Cu, up_row);
+        stream_rows<kTiles, NT, KUU, 1, PRE, W>(ub, Cu, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1, acc);
       };
       if constexpr (NARROW) {
         if (nut <= 2) {
-          int roff[2 * 2 * KUU];
-          stage_rows<2, 2 * KUU>(roff, Cu, up_row);
-          stream_rows<2, NT, 2 * KUU, 1>(ub, Cu, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1,
-                                          reinterpret_cast<f32x4_t(&)[2][NT]>(acc));
+          int roff[WStage<2, 2 * KUU, W>::NI];
+          stage_rows<2, 2 * KUU, W>(roff, Cu, up_row);
+          stream_rows<2, NT, 2 * KUU, 1, false, W>(ub, Cu, roff, s_stage[wave], tok.b, tok.part, tok.tn, ks0, ks1,
+                                                   reinterpret_cast<f32x4_t(&)[2][NT]>(acc));
         } else {
           full();
         }
@@ -511,6 +583,18 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
 
     // wave w: union entries 16 w .. 16 w + 15 = half (w & 1) of fragment group w >> 1
     const int gi = wave >> 1, half = wave & 1;
+    // quantized: the W_up scale of each entry's row, and its W_down scale folded into zval
+    float sue[4] = {1.f, 1.f, 1.f, 1.f}, sde[4] = {1.f, 1.f, 1.f, 1.f};
+    if constexpr (Q) {
+      const Buf ubs = make_buf(s_up, 4u * (uint32_t)d_ff), dbs = make_buf(s_down, 4u * (uint32_t)d_ff);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 16 * wave + 4 * g + i;
+        const uint32_t off = e < cnt ? 4u * (uint32_t)(row0 + s_list[e < cnt ? e : 0]) : kOOB;
+        sue[i] = __builtin_bit_cast(float, ldb32(ubs, off));
+        sde[i] = __builtin_bit_cast(float, ldb32(dbs, off));
+      }
+    }
     if (32 * gi < cnt) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -524,7 +608,9 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int e = 16 * wave + 4 * g + i;
-            const float zz = e < cnt ? s_act[s_list[e]][tok] * (FULL ? up_value(form.silu_up, v[i]) : v[i]) : 0.f;
+            const float vu = Q ? v[i] * sue[i] : v[i];
+            float zz = e < cnt ? s_act[s_list[e]][tok] * (FULL ? up_value(form.silu_up, vu) : vu) : 0.f;
+            if constexpr (Q) zz *= sde[i];
             const __bf16 hb = (__bf16)zz;
             const __bf16 lb = (__bf16)(zz - (float)hb);
             hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
@@ -545,26 +631,28 @@ __device__ __forceinline__ void gate_up_body(const float* __restrict__ x, const 
       const uint4 *__restrict__ w_up, int Cu, int T, int d, int d_ff, int nseg, float t, int slots, int tc,       \
       int32_t *__restrict__ meta, int32_t *__restrict__ seg_count, int32_t *__restrict__ seg_idx,                  \
       float *__restrict__ seg_act, uint4 *__restrict__ zf, float *__restrict__ y, const uint4 *__restrict__ xs,  \
-      int ntt, Form form, const float *__restrict__ gx
-#define FFN_GATE_UP_ARGS \
-  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt, form, gx
+      int ntt, Form form, const float *__restrict__ gx, const float *__restrict__ s_g,                            \
+      const float *__restrict__ s_up, const float *__restrict__ s_down
+#define FFN_GATE_UP_ARGS                                                                                            \
+  x, zp, gate_w, Cg, w_up, Cu, T, d, d_ff, nseg, t, slots, tc, meta, seg_count, seg_idx, seg_act, zf, y, xs, ntt, form, \
+      gx, s_g, s_up, s_down
 
 // One workgroup per CU: four k steps a group for one token tile (two for LoPA's short
 // gate rows and for wider token tiles; one for LoPA's gate rows with four token tiles,
 // whose fragments carry both partial copies of z).
-template <bool LOPA, bool DENSE, int NT, int FORM>
+template <class W, bool LOPA, bool DENSE, int NT, int FORM>
 __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(FFN_GATE_UP_PARAMS) {
   constexpr int KU = NT == 1 ? (LOPA ? 2 : 4) : (LOPA && NT == 4 ? 1 : 2);
-  gate_up_body<LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2, FORM>(FFN_GATE_UP_ARGS);
+  gate_up_body<W, LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2, FORM>(FFN_GATE_UP_ARGS);
 }
 
 // Standard gating, one token tile: two k steps a group, so that two workgroups fit a CU
 // (at most 256 registers a lane); one workgroup's phase changes (LDS reductions, union)
 // then overlap the other's streaming.
-template <bool DENSE, int FORM>
+template <class W, bool DENSE, int FORM>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) void k_gate_up_mfma2(
     FFN_GATE_UP_PARAMS) {
-  gate_up_body<false, DENSE, 1, 2, 2, FORM>(FFN_GATE_UP_ARGS);
+  gate_up_body<W, false, DENSE, 1, 2, 2, FORM>(FFN_GATE_UP_ARGS);
 }
 #undef FFN_GATE_UP_PARAMS
 #undef FFN_GATE_UP_ARGS
@@ -584,23 +672,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) voi
 // column (y was cleared by the gate kernel).
 constexpr int kDnSlots = 4096;  // most slot indices of one row chunk
 
-template <int NT>
+template <int NT, class W = WBf16>
 struct DnCfg {
   static constexpr int DT = NT == 1 ? 4 : 2;  // 32-column tiles per wave
   static constexpr int CW = NT == 4 ? 1 : 2;  // column slots per workgroup
   static constexpr int WCOLS = 32 * DT * CW;  // columns per workgroup
-  static constexpr int LPR = 4 * DT;          // lanes per row of a load instruction
+  static constexpr int R8 = W::EPC / 8;       // tile chunks (8 bf16) per loaded chunk
+  static constexpr int LPR = 4 * DT / R8;     // lanes per row of a load instruction
   static constexpr int RPI = kWave / LPR;     // rows per load instruction
   static constexpr int NI = 32 / RPI;         // load instructions per group
   // chunks per LDS row: two pad chunks put the 8 rows that a half-wave's transposing
   // reads touch on distinct banks
-  static constexpr int PITCH = LPR + 2;
+  static constexpr int PITCH = 4 * DT + 2;
 };
 
-template <int NT>
+template <int NT, class W = WBf16>
 struct DnFrags {
-  uint4 t[DnCfg<NT>::NI];  // W_down chunks as loaded: entry RPI i + lane / LPR, chunk lane % LPR
-  uint4 zh[NT], zl[NT];    // zval fragments (hi, lo) of the token tiles
+  uint4 t[DnCfg<NT, W>::NI];  // W_down chunks as loaded: entry RPI i + lane / LPR, chunk lane % LPR
+  uint4 zh[NT], zl[NT];       // zval fragments (hi, lo) of the token tiles
 };
 
 // A group's table entry: x = first slot (relative to the chunk's first row) | entries
@@ -608,17 +697,18 @@ struct DnFrags {
 // past the last group are empty, so every load of such a group reads nothing.
 constexpr int kDnPad = 4 * kParts;
 
-template <int NT>
+template <int NT, class W = WBf16>
 struct DnRows {
-  int row[DnCfg<NT>::NI];  // neuron of the entry this lane loads, -1 for none
+  int row[DnCfg<NT, W>::NI];  // neuron of the entry this lane loads, -1 for none
   int2 info;
 };
 
-template <int NT>
-__device__ __forceinline__ DnRows<NT> dn_rows(int2 info, const int* s_idx, int C, int ch) {
-  using K = DnCfg<NT>;
+// C: loaded chunks per row, ch: this lane's chunk
+template <int NT, class W>
+__device__ __forceinline__ DnRows<NT, W> dn_rows(int2 info, const int* s_idx, int C, int ch) {
+  using K = DnCfg<NT, W>;
   const int lane = lane_id(), base = info.x & 0xFFFF, cnt = info.x >> 16;
-  DnRows<NT> a;
+  DnRows<NT, W> a;
   a.info = info;
 #pragma unroll
   for (int i = 0; i < K::NI; ++i) {
@@ -630,10 +720,10 @@ __device__ __forceinline__ DnRows<NT> dn_rows(int2 info, const int* s_idx, int C
   return a;
 }
 
-template <int NT>
-__device__ __forceinline__ void dn_issue(DnFrags<NT>& f, const DnRows<NT>& a, const Buf& db, const Buf& zb, int C,
-                                         int ch, int T, int ntt) {
-  using K = DnCfg<NT>;
+template <int NT, class W>
+__device__ __forceinline__ void dn_issue(DnFrags<NT, W>& f, const DnRows<NT, W>& a, const Buf& db, const Buf& zb,
+                                         int C, int ch, int T, int ntt) {
+  using K = DnCfg<NT, W>;
   const int lane = lane_id(), m = lane & 15;
 #pragma unroll
   for (int i = 0; i < K::NI; ++i) f.t[i] = ldb_nt(db, a.row[i] >= 0 ? 16u * (uint32_t)(a.row[i] * C + ch) : kOOB);
@@ -660,13 +750,15 @@ __device__ __forceinline__ uint2 lds_read_tr16(const char* p) {
 // 4a + b pointing at entry 4q + a (then 16 + 4q + a), columns 4b .. 4b + 3 of a 16-column
 // block, lane n of the group ends with entries 4q .. 4q + 3 (then 16 + 4q ..) of column
 // n: the B operand in the entry order of the zval fragments.
-template <int NT>
-__device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, uint4* tile, f32x4_t (&acc)[DnCfg<NT>::DT][2][NT]) {
-  using K = DnCfg<NT>;
+template <int NT, class W>
+__device__ __forceinline__ void dn_mma(const DnFrags<NT, W>& f, uint4* tile,
+                                       f32x4_t (&acc)[DnCfg<NT, W>::DT][2][NT]) {
+  using K = DnCfg<NT, W>;
   constexpr int ROWB = 16 * K::PITCH;  // bytes per tile row
   const int lane = lane_id();
 #pragma unroll
-  for (int i = 0; i < K::NI; ++i) tile[(K::RPI * i + lane / K::LPR) * K::PITCH + lane % K::LPR] = f.t[i];
+  for (int i = 0; i < K::NI; ++i)  // quantized rows: the codes as bf16, R8 tile chunks a loaded chunk
+    put_bf16_chunks<W>(tile + (K::RPI * i + lane / K::LPR) * K::PITCH + (lane % K::LPR) * K::R8, f.t[i]);
   __builtin_amdgcn_wave_barrier();  // LDS operations of a wave complete in order
   const char* src = reinterpret_cast<const char*>(tile) + (4 * (lane >> 4) + ((lane >> 2) & 3)) * ROWB + 8 * (lane & 3);
 #pragma unroll
@@ -685,13 +777,15 @@ __device__ __forceinline__ void dn_mma(const DnFrags<NT>& f, uint4* tile, f32x4_
   __builtin_amdgcn_wave_barrier();
 }
 
-template <int NT>
+// C: loaded chunks per row of w_down_t (d / W::EPC); the W_down row scales of quantized
+// weights are folded into zval by the gate kernel.
+template <int NT, class W>
 __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict__ seg_count,
                                                       const int32_t* __restrict__ seg_idx,
                                                       const uint4* __restrict__ zf, int nseg, int d_ff, int R, int tc,
                                                       const uint4* __restrict__ w_down_t, int C, int d, int T,
                                                       float* __restrict__ y) {
-  using K = DnCfg<NT>;
+  using K = DnCfg<NT, W>;
   constexpr int CW = K::CW, GS = kParts / CW, WCOLS = K::WCOLS;
   const Buf db = make_buf(w_down_t, 16u * (uint32_t)d_ff * (uint32_t)C);
   const int ntt = (tc + 15) / 16;
@@ -708,7 +802,7 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
   int* const s_idx = reinterpret_cast<int*>(s_big + STAGE_U4);
   f32x4_t* const s_part = reinterpret_cast<f32x4_t*>(s_big);
 
-  const int S = (C * 8 + WCOLS - 1) / WCOLS;
+  const int S = (d + WCOLS - 1) / WCOLS;
   const int chunk = blockIdx.x / S, cgrp = blockIdx.x % S;
   const Split chunks(nseg, R), segs(d_ff, nseg);
   const int seg_lo = chunks.start(chunk), seg_hi = chunks.start(chunk + 1);
@@ -768,26 +862,26 @@ __global__ __launch_bounds__(kBlock) void k_down_mfma(const int32_t* __restrict_
       for (int nt = 0; nt < NT; ++nt) acc[ct][h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   // this lane's 16-byte chunk of the wave's columns
-  const int ch = (cgrp * WCOLS + slot_w * 32 * K::DT) / 8 + lane % K::LPR;
+  const int ch = (cgrp * WCOLS + slot_w * 32 * K::DT) / W::EPC + lane % K::LPR;
   if (phase < ngrp) {
     // two register sets alternate, one group each per half-iteration; the table entry of
     // group j + 3 GS and the slot indices of group j + 2 GS are read while group j is
     // multiplied.  A pair always multiplies both halves (a group past the last one loads
     // nothing and adds zeros), so no load sits on a conditional path.
-    DnFrags<NT> f0, f1;
-    DnRows<NT> a = dn_rows<NT>(s_ginfo[phase], s_idx, C, ch);
+    DnFrags<NT, W> f0, f1;
+    DnRows<NT, W> a = dn_rows<NT, W>(s_ginfo[phase], s_idx, C, ch);
     dn_issue(f0, a, db, zb, C, ch, T, ntt);
-    a = dn_rows<NT>(s_ginfo[phase + GS], s_idx, C, ch);
+    a = dn_rows<NT, W>(s_ginfo[phase + GS], s_idx, C, ch);
     int2 info = s_ginfo[phase + 2 * GS];
     for (int j = phase;; j += 2 * GS) {
       dn_issue(f1, a, db, zb, C, ch, T, ntt);
       issue_barrier();
-      a = dn_rows<NT>(info, s_idx, C, ch);
+      a = dn_rows<NT, W>(info, s_idx, C, ch);
       info = s_ginfo[j + 3 * GS];
       dn_mma(f0, s_stage + wave * 32 * K::PITCH, acc);
       dn_issue(f0, a, db, zb, C, ch, T, ntt);
       issue_barrier();
-      a = dn_rows<NT>(info, s_idx, C, ch);
+      a = dn_rows<NT, W>(info, s_idx, C, ch);
       info = s_ginfo[j + 4 * GS];
       dn_mma(f1, s_stage + wave * 32 * K::PITCH, acc);
       if (j + 2 * GS >= ngrp) break;
@@ -829,15 +923,15 @@ hipError_t split_tokens(const Shape& sh, const float* x, const Workspace& ws, hi
   k_split_tokens<<<(n + kBlock - 1) / kBlock, kBlock, 0, s>>>(x, C, sh.T, nks, ntt, ws.xs);
   return hipGetLastError();
 }
-template <int NT>
+template <class W, int NT>
 hipError_t z_mfma(const Shape& sh, const Form& form, const float* x, const void* lopa_a, const Workspace& ws,
                   hipStream_t s) {
   const int C = sh.d / 8, grid = ((sh.r + 15) / 16) * kZParts;
   // with G, extra workgroups write G x for the gate kernel
   const GWork gw{form, x, ws.gx, sh.T, sh.d, sh.d_ff, grid};
   const int g = grid + (form.g_idx ? (g_items(sh.d_ff, sh.T) + kZWaves * kWave - 1) / (kZWaves * kWave) : 0);
-  k_lopa_z_mfma<NT><<<g, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a), C,
-                                                   sh.T, sh.r, ws.tc, ws.z, gw);
+  k_lopa_z_mfma<NT, W><<<g, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a),
+                                                      C, sh.T, sh.r, ws.tc, ws.z, gw, sh.sc.a);
   return hipGetLastError();
 }
 
@@ -848,7 +942,7 @@ int segments_for(int d_ff, int grid) {
   return n > 128 ? (n + grid - 1) / grid * grid : n;
 }
 
-template <bool LOPA, bool DENSE, int NT, int FORM>
+template <class W, bool LOPA, bool DENSE, int NT, int FORM>
 hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up, float t,
                      Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
@@ -858,32 +952,32 @@ hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const vo
   const int g = ws.nseg < grid ? ws.nseg : grid;
   auto kernel = [&] {
     if constexpr (two)
-      return k_gate_up_mfma2<DENSE, FORM>;
+      return k_gate_up_mfma2<W, DENSE, FORM>;
     else
-      return k_gate_up_mfma<LOPA, DENSE, NT, FORM>;
+      return k_gate_up_mfma<W, LOPA, DENSE, NT, FORM>;
   }();
   return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                             static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
                             ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form,
-                            (const float*)ws.gx);
+                            (const float*)ws.gx, LOPA ? sh.sc.b : sh.sc.gate, sh.sc.up, sh.sc.down);
 }
 
-template <bool LOPA, bool DENSE, int FORM>
+template <class W, bool LOPA, bool DENSE, int FORM>
 hipError_t gate_nt(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
                    Workspace& ws, float* y, hipStream_t s) {
-  if (sh.T <= 16) return gate_mfma<LOPA, DENSE, 1, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
-  if (sh.T <= 32) return gate_mfma<LOPA, DENSE, 2, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
-  return gate_mfma<LOPA, DENSE, 4, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  if (sh.T <= 16) return gate_mfma<W, LOPA, DENSE, 1, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  if (sh.T <= 32) return gate_mfma<W, LOPA, DENSE, 2, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  return gate_mfma<W, LOPA, DENSE, 4, FORM>(sh, f, x, gate_w, w_up, t, ws, y, s);
 }
 
-template <bool LOPA, bool DENSE>
+template <class W, bool LOPA, bool DENSE>
 hipError_t gate_form(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
                      Workspace& ws, float* y, hipStream_t s) {
   // the norm runs before this kernel, so only G needs the LoPA form here
   if constexpr (LOPA)
-    if (f.g_idx) return gate_nt<LOPA, DENSE, kFormLoPA>(sh, f, x, gate_w, w_up, t, ws, y, s);
-  return f.full() ? gate_nt<LOPA, DENSE, kFormAct>(sh, f, x, gate_w, w_up, t, ws, y, s)
-                  : gate_nt<LOPA, DENSE, kFormDefault>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (f.g_idx) return gate_nt<W, LOPA, DENSE, kFormLoPA>(sh, f, x, gate_w, w_up, t, ws, y, s);
+  return f.full() ? gate_nt<W, LOPA, DENSE, kFormAct>(sh, f, x, gate_w, w_up, t, ws, y, s)
+                  : gate_nt<W, LOPA, DENSE, kFormDefault>(sh, f, x, gate_w, w_up, t, ws, y, s);
 }
 
 // Down grid: S column groups x R row chunks, about kDnWgTarget workgroups, at most
@@ -892,10 +986,10 @@ hipError_t gate_form(const Shape& sh, const Form& f, const float* x, const void*
 constexpr int kDnWgTarget = 512;
 constexpr int64_t kDnAtomicsMax = 1 << 20;
 
-template <int NT>
+template <class W, int NT>
 hipError_t down_mfma(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
-  const int C = sh.d / 8;
-  const int64_t wcols = DnCfg<NT>::WCOLS;
+  const int C = sh.d / W::EPC;
+  const int64_t wcols = DnCfg<NT, W>::WCOLS;
   const int64_t S = ((int64_t)sh.d + wcols - 1) / wcols;
   int64_t R = (kDnWgTarget + S - 1) / S;
   const int64_t amax = kDnAtomicsMax / ((int64_t)sh.T * sh.d);
@@ -907,20 +1001,52 @@ hipError_t down_mfma(const Shape& sh, const void* w_down_t, const Workspace& ws,
   const int64_t rows_per_seg = (sh.d_ff + ws.nseg - 1) / ws.nseg;
   while (R < ws.nseg && ((ws.nseg + R - 1) / R) * rows_per_seg > kDnSlots) ++R;
   if (((ws.nseg + R - 1) / R) * rows_per_seg > kDnSlots || S * R > INT32_MAX) return hipErrorInvalidValue;
-  k_down_mfma<NT><<<(int)(S * R), kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.zf, ws.nseg, sh.d_ff, (int)R, ws.tc,
-                                                  static_cast<const uint4*>(w_down_t), C, sh.d, sh.T, y);
+  k_down_mfma<NT, W><<<(int)(S * R), kBlock, 0, s>>>(ws.seg_count, ws.seg_idx, ws.zf, ws.nseg, sh.d_ff, (int)R,
+                                                     ws.tc, static_cast<const uint4*>(w_down_t), C, sh.d, sh.T, y);
   return hipGetLastError();
+}
+
+// One call of the path for weights of format W (after the tokens are split, if they are).
+template <class W>
+hipError_t batched_format(const Shape& sh, Gate g, bool dense, const Form& form, const float* x, const void* lopa_a,
+                          const void* gate_w, const void* w_up, const void* w_down_t, float t, Workspace& ws,
+                          float* y, hipStream_t s) {
+  const bool lopa = g == Gate::LoPA;
+  hipError_t e = hipSuccess;
+  if (lopa) {
+    e = sh.T <= 16 ? z_mfma<W, 1>(sh, form, x, lopa_a, ws, s)
+                   : sh.T <= 32 ? z_mfma<W, 2>(sh, form, x, lopa_a, ws, s) : z_mfma<W, 4>(sh, form, x, lopa_a, ws, s);
+    if (e != hipSuccess) return e;
+    // RMSNorm between A and B: the two partial copies of z become one normalised copy
+    if (form.rms_eps > 0.f &&
+        (e = launch_rms_norm(ws.z, 2, ws.tc, sh.T, sh.r, form.rms_gain, form.rms_eps, s)) != hipSuccess)
+      return e;
+  }
+  if (lopa)
+    e = dense ? gate_form<W, true, true>(sh, form, x, gate_w, w_up, t, ws, y, s)
+              : gate_form<W, true, false>(sh, form, x, gate_w, w_up, t, ws, y, s);
+  else
+    e = dense ? gate_form<W, false, true>(sh, form, x, gate_w, w_up, t, ws, y, s)
+              : gate_form<W, false, false>(sh, form, x, gate_w, w_up, t, ws, y, s);
+  if (e != hipSuccess) return e;
+  if (sh.T <= 16) return down_mfma<W, 1>(sh, w_down_t, ws, y, s);
+  if (sh.T <= 32) return down_mfma<W, 2>(sh, w_down_t, ws, y, s);
+  return down_mfma<W, 4>(sh, w_down_t, ws, y, s);
 }
 
 }  // namespace
 
 // The matrix-core path addresses every operand with 32-bit byte offsets below 2^31.
+// bf16 weights, and int8 / int4 codes (converted to bf16 on their way into the operand
+// tiles): rows of whole 16-byte chunks, so d (and LoPA's r) a multiple of 16 / 32.
 bool batched_ok(const Shape& sh, Gate g) {
-  if (sh.wdt != 1 || sh.T < 2 || sh.T > kTokChunk || sh.d % 8 != 0) return false;
+  if (sh.wdt < 1 || sh.wdt > 3 || sh.T < 2 || sh.T > kTokChunk) return false;
+  const int q = sh.wdt == 1 ? 8 : sh.wdt == 2 ? 16 : 32;  // elements a 16-byte chunk
+  if (sh.d % q != 0) return false;
   const int64_t lim = int64_t(1) << 31;
   if (2 * (int64_t)sh.d_ff * sh.d >= lim || 4 * (int64_t)kTokChunk * sh.d >= lim) return false;
   if ((int64_t)segments_for(sh.d_ff, kSegGrid2) * 256 * kTokChunk >= lim) return false;
-  if (g == Gate::LoPA && (sh.r % 8 != 0 || 2 * (int64_t)sh.d_ff * sh.r >= lim || 2 * (int64_t)sh.r * sh.d >= lim ||
+  if (g == Gate::LoPA && (sh.r % q != 0 || 2 * (int64_t)sh.d_ff * sh.r >= lim || 2 * (int64_t)sh.r * sh.d >= lim ||
                           4 * (int64_t)kTokChunk * sh.d_ff >= lim))  // G x, read through a buffer
     return false;
   return true;
@@ -932,29 +1058,13 @@ int batched_segments(int d_ff) { return segments_for(d_ff, kSegGrid2); }
 hipError_t launch_batched(const Shape& sh, Gate g, bool dense, const Form& form, const float* x,
                           const void* lopa_a, const void* gate_w, const void* w_up, const void* w_down_t, float t,
                           Workspace& ws, float* y, hipStream_t s) {
-  const bool lopa = g == Gate::LoPA;
   hipError_t e = hipSuccess;
   // more than one token tile: the kernels read the tokens pre-split
   if (sh.T > 16 && (e = split_tokens(sh, x, ws, s)) != hipSuccess) return e;
-  if (lopa) {
-    e = sh.T <= 16 ? z_mfma<1>(sh, form, x, lopa_a, ws, s)
-                   : sh.T <= 32 ? z_mfma<2>(sh, form, x, lopa_a, ws, s) : z_mfma<4>(sh, form, x, lopa_a, ws, s);
-    if (e != hipSuccess) return e;
-    // RMSNorm between A and B: the two partial copies of z become one normalised copy
-    if (form.rms_eps > 0.f &&
-        (e = launch_rms_norm(ws.z, 2, ws.tc, sh.T, sh.r, form.rms_gain, form.rms_eps, s)) != hipSuccess)
-      return e;
-  }
-  if (lopa)
-    e = dense ? gate_form<true, true>(sh, form, x, gate_w, w_up, t, ws, y, s)
-              : gate_form<true, false>(sh, form, x, gate_w, w_up, t, ws, y, s);
-  else
-    e = dense ? gate_form<false, true>(sh, form, x, gate_w, w_up, t, ws, y, s)
-              : gate_form<false, false>(sh, form, x, gate_w, w_up, t, ws, y, s);
-  if (e != hipSuccess) return e;
-  if (sh.T <= 16) return down_mfma<1>(sh, w_down_t, ws, y, s);
-  if (sh.T <= 32) return down_mfma<2>(sh, w_down_t, ws, y, s);
-  return down_mfma<4>(sh, w_down_t, ws, y, s);
+  if (sh.wdt == 2) return batched_format<WI8>(sh, g, dense, form, x, lopa_a, gate_w, w_up, w_down_t, t, ws, y, s);
+  if (sh.wdt == 3) return batched_format<WI4>(sh, g, dense, form, x, lopa_a, gate_w, w_up, w_down_t, t, ws, y, s);
+  return batched_format<WBf16>(sh, g, dense, form, x, lopa_a, gate_w, w_up, w_down_t, t, ws, y, s);
 }
+
 
 }  // namespace ffn

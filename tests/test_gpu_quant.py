@@ -43,9 +43,16 @@ SMALL = [
     ("i8_gen_lopa_r40", 1, 256, 1000, 40, I8, 1.0),     # r not a multiple of 16: element-wise
     ("i8_gen_odd_d", 1, 100, 77, 0, I8, 0.5),
     ("i4_gen_even_d", 1, 102, 77, 0, I4, 0.5),          # d even, not a multiple of 32
-    ("i8_T3", 3, 256, 1000, 0, I8, 1.0),                # batches: element-wise
+    ("i8_T3", 3, 256, 1000, 0, I8, 1.0),                # batches: matrix cores, codes as bf16
     ("i4_T5_lopa", 5, 256, 1000, 32, I4, 1.0),
     ("i8_T70", 70, 64, 200, 0, I8, 1.0),                # two token passes
+    ("i8_T16_lopa", 16, 256, 1000, 32, I8, 1.0),
+    ("i8_T2_lopa_r48", 2, 256, 1000, 48, I8, 1.0),      # r = 48: three 16-element chunks a B row
+    ("i4_T20", 20, 288, 999, 0, I4, 0.9),               # two token tiles; 9 chunks a row
+    ("i8_T40_ragged", 40, 272, 999, 0, I8, 0.9),        # pre-split tokens; a half k step at the end
+    ("i4_T64_lopa", 64, 256, 1000, 64, I4, 1.0),        # four token tiles
+    ("i8_T4_gen_odd_d", 4, 100, 77, 0, I8, 0.5),        # d not a multiple of 16: element-wise
+    ("i4_T6_gen_d48", 6, 48, 77, 0, I4, 0.5),           # d not a multiple of 32: element-wise
 ]
 
 
