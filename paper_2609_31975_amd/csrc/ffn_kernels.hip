@@ -328,13 +328,112 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   }
 }
 
+// Standard gating with one row per wave a pass (64 lanes a row): the gate rows and the W_up
+// rows of the active neurons go through one stream.  A step finishes the row in one buffer
+// and reloads that buffer: with the W_up row of the same neuron when its gate value exceeds
+// t, else with the wave's next gate row.  The W_up reads of a segment thus overlap its gate
+// stream instead of following its compaction, and only an active last gate row costs a
+// round trip after the stream.  Every step issues the same loads (a buffer with nothing left
+// to load gets out-of-range offsets), so the load-counter waits stay exact; what a step does
+// next is uniform over the wave (all lanes hold the same group sum).  Gate values go to
+// s_h[k]; an active row's zval (activation value times the W_up dot, SiLU'd with
+// form.silu_up) goes to s_zv[k].  gate_w and w_up are both [d_ff][C] chunks of `bytes`.
+// The wave's first gate row is requested before x and its second after it, so that the weight
+// stream starts ahead of the vector loads of all the waves on a CU.
+template <class W, int CPL, bool FULL>
+__device__ __forceinline__ void gate_up_stream(const float* __restrict__ x, const uint4* __restrict__ gate_w,
+                                               const uint4* __restrict__ w_up, uint32_t bytes, int C, int row0, int n,
+                                               float t, const Form& form, float* s_h, float* s_zv) {
+  constexpr int kWaves = kBlock / kWave;
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
+  const int act = FULL ? form.act : 0;
+  int next_gate = wave;
+  LaneVec<W, CPL, false> v;
+  // a buffer's work: kind 1 the gate row k, kind 2 the W_up row k with activation value a,
+  // kind 0 nothing
+  struct Item {
+    int kind, k;
+    float a;
+  };
+  auto take_gate = [&](Item& it) {
+    it.kind = next_gate < n ? 1 : 0;
+    it.k = next_gate;
+    next_gate += kWaves;
+  };
+  auto load = [&](uint4 (&b)[CPL], const Item& it) {
+    const Buf mb = make_buf(it.kind == 2 ? w_up : gate_w, bytes);
+    load_pass<W, CPL>(mb, C, lane, kWave, it.kind != 0, row0 + it.k, b);
+  };
+  auto finish = [&](const uint4 (&b)[CPL], Item& it) {
+    if (it.kind == 0) return;
+    const float s = group_sum(lane_dot<W, CPL, false>(b, v), kWave);
+    if (it.kind == 1) {
+      if (lane == 0) s_h[it.k] = s;
+      if (uniform(s > t ? 1 : 0)) {  // NaN compares false: inactive
+        it.kind = 2;
+        it.a = gate_value(act, s - t);
+        return;
+      }
+    } else if (lane == 0) {
+      s_zv[it.k] = it.a * (FULL ? up_value(form.silu_up, s) : s);
+    }
+    take_gate(it);
+  };
+  uint4 b0[CPL];
+  Item i0, i1;
+  take_gate(i0);
+  load(b0, i0);
+  issue_barrier();
+  {  // x through raw buffer loads (zeros past C chunks), in this order among the stream's loads
+    constexpr int F4 = W::EPC / 4;  // float4s of x a chunk
+    const Buf xb = make_buf(x, 16u * F4 * (uint32_t)C);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int ch = lane + c * kWave;
+#pragma unroll
+      for (int e4 = 0; e4 < F4; ++e4) {
+        const float4 f = __builtin_bit_cast(float4, ldb(xb, ch < C ? 16u * (uint32_t)(ch * F4 + e4) : kOOB));
+        v.f[c][4 * e4 + 0] = f.x;
+        v.f[c][4 * e4 + 1] = f.y;
+        v.f[c][4 * e4 + 2] = f.z;
+        v.f[c][4 * e4 + 3] = f.w;
+      }
+    }
+  }
+  issue_barrier();
+  if constexpr (CPL <= 8) {
+    uint4 b1[CPL];
+    take_gate(i1);
+    load(b1, i1);
+    issue_barrier();
+    while (true) {
+      finish(b0, i0);
+      load(b0, i0);
+      issue_barrier();
+      finish(b1, i1);
+      load(b1, i1);
+      issue_barrier();
+      if (i0.kind == 0 && i1.kind == 0) break;
+    }
+  } else {
+    while (true) {
+      finish(b0, i0);
+      if (i0.kind == 0) break;
+      load(b0, i0);
+      issue_barrier();
+    }
+  }
+}
+
 // Ballot compaction of one segment (run by the first wave): neurons whose gate value
 // exceeds t (all neurons if `all`) get ascending ranks; their activation value (h - t,
 // or its R-S+ with act = 1) is kept in LDS for the W_up phase and published with the
 // neuron index.
+// With s_zv, the zval of each selected neuron is already in s_zv[row] and is published too.
 __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int row0, int seg, float t, bool all,
                                                 int act, int* s_list, float* s_act, int* s_cnt, int32_t* seg_count,
-                                                int32_t* seg_idx, float* seg_act) {
+                                                int32_t* seg_idx, float* seg_act, const float* s_zv = nullptr,
+                                                float* seg_zval = nullptr) {
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
     const bool valid = lane < nrows;
@@ -349,6 +448,7 @@ __device__ __forceinline__ void compact_segment(const float* s_h, int nrows, int
       s_act[rank] = a;
       seg_idx[row0 + rank] = row0 + lane;
       seg_act[row0 + rank] = a;
+      if (s_zv) seg_zval[row0 + rank] = s_zv[lane];
     }
     if (lane == 0) {
       const int cnt = __popcll(m);
@@ -516,6 +616,17 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
     dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   } else {
     static_assert(CPLG == CPLU, "standard gating shares the x registers");
+    if constexpr (!DENSE && !is_quant<W>()) {
+      if (lpru == kWave) {  // one row a wave: the W_up rows join the gate stream
+        __shared__ float s_zv[kSegMax];
+        gate_up_stream<W, CPLU, FULL>(x, gate_w, w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, row0, nrows, t, form,
+                                      s_h, s_zv);
+        __syncthreads();
+        compact_segment(s_h, nrows, row0, seg, t, false, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act,
+                        s_zv, seg_zval);
+        return;
+      }
+    }
     LaneVec<W, CPLU> xr;
     make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
     dot_rows<W, CPLU>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, xr, gate_row,

@@ -47,6 +47,12 @@ SMALL = [
     ("std_bf16_d4096", 1, 4096, 2056, 0, BF16, 1.2816),    # full-width rows, short d_ff
     ("std_bf16_d4096_odd", 1, 4096, 2052, 0, BF16, 1.2816),
     ("std_bf16_long_chunks", 1, 4096, 40000, 0, BF16, 1.2816),  # down row chunks of over 1024 slots
+    # one row per wave: W_up rows of active neurons interleaved with the gate stream
+    ("std_bf16_d4096_half_active", 1, 4096, 2056, 0, BF16, 0.0),   # runs of consecutive active rows
+    ("std_bf16_d4096_all_active", 1, 4096, 300, 0, BF16, -100.0),  # every gate row followed by its W_up row
+    ("std_bf16_d4096_one_row_segs", 1, 4096, 100, 0, BF16, 0.0),   # segments of one row: idle waves
+    ("std_bf16_d8192", 1, 8192, 1500, 0, BF16, 1.2816),            # one buffer a wave (16 chunks a lane)
+    ("std_f32_d2048", 1, 2048, 1500, 0, F32, 1.2816),
     ("std_bf16_T4_odd_d", 4, 100, 77, 0, BF16, 0.5),       # batch with d not a multiple of 8: element-wise
     ("lopa_bf16_T3_odd_r", 3, 264, 1000, 36, BF16, 1.0),    # batch with r not a multiple of 8: element-wise
     ("very_small", 1, 8, 3, 0, BF16, 0.0),
