@@ -51,6 +51,27 @@ __device__ __forceinline__ void load_vec(const float* __restrict__ v, int C, int
   }
 }
 
+// load_vec through raw buffer loads (zeros past C chunks): branch-free, and kept where it
+// stands among the weight loads around it.
+template <class W, int CPL>
+__device__ __forceinline__ void load_vec_buf(const float* __restrict__ v, int C, int q, int lpr,
+                                             float (&r)[CPL][W::EPC]) {
+  constexpr int F4 = W::EPC / 4;  // float4s a chunk
+  const Buf vb = make_buf(v, 16u * F4 * (uint32_t)C);
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = q + c * lpr;
+#pragma unroll
+    for (int e4 = 0; e4 < F4; ++e4) {
+      const float4 f = __builtin_bit_cast(float4, ldb(vb, ch < C ? 16u * (uint32_t)(ch * F4 + e4) : kOOB));
+      r[c][4 * e4 + 0] = f.x;
+      r[c][4 * e4 + 1] = f.y;
+      r[c][4 * e4 + 2] = f.z;
+      r[c][4 * e4 + 3] = f.w;
+    }
+  }
+}
+
 // The vector a lane multiplies its chunks of a row with.  fp32 / bf16 weights: the fp32
 // elements.  Quantized weights: X = rint(v * 127 * 2^16 / max |v|), a 24-bit fixed-point
 // copy, kept as its three bytes: the signed top byte s2 and the unsigned bytes u1, u0,
@@ -281,9 +302,16 @@ __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, 
   }
 }
 
-template <class W, int CPL, bool Q, class RowOf, class Sink>
+// LATE (fp32 vectors only): v is loaded here from `vec`, after the first pass's row loads,
+// so that the weight stream starts ahead of the vector loads of all the waves on a CU.  It
+// pays for long streams (the standard gate); for a stream of one pass (LoPA's z and gate,
+// the W_up dots after LoPA's gate) the in-order load counter makes the first use of the
+// vector wait for all the rows, and the call measured slower.
+template <class W, int CPL, bool LATE = false, bool Q, class RowOf, class Sink>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
-                                         int n, LaneVec<W, CPL, Q>& v, RowOf row_of, Sink sink) {
+                                         int n, LaneVec<W, CPL, Q>& v, RowOf row_of, Sink sink,
+                                         const float* __restrict__ vec = nullptr) {
+  static_assert(!(LATE && Q), "a late vector is an fp32 one");
   constexpr int kWaves = kBlock / kWave;
   const Buf mb = make_buf(mat, bytes);
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
@@ -302,6 +330,11 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   };
   uint4 b0[CPL], b1[CPL];
   load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
+  if constexpr (LATE) {
+    issue_barrier();
+    load_vec_buf<W, CPL>(vec, C, q, lpr, v.f);
+    issue_barrier();
+  }
   prepare_lane_vec<W, CPL, Q>(v);  // limbs: the whole workgroup converts the vector
   if (wave >= npass) return;
   if (wave + kWaves >= npass) {  // a single pass: nothing to overlap
@@ -384,22 +417,7 @@ __device__ __forceinline__ void gate_up_stream(const float* __restrict__ x, cons
   take_gate(i0);
   load(b0, i0);
   issue_barrier();
-  {  // x through raw buffer loads (zeros past C chunks), in this order among the stream's loads
-    constexpr int F4 = W::EPC / 4;  // float4s of x a chunk
-    const Buf xb = make_buf(x, 16u * F4 * (uint32_t)C);
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      const int ch = lane + c * kWave;
-#pragma unroll
-      for (int e4 = 0; e4 < F4; ++e4) {
-        const float4 f = __builtin_bit_cast(float4, ldb(xb, ch < C ? 16u * (uint32_t)(ch * F4 + e4) : kOOB));
-        v.f[c][4 * e4 + 0] = f.x;
-        v.f[c][4 * e4 + 1] = f.y;
-        v.f[c][4 * e4 + 2] = f.z;
-        v.f[c][4 * e4 + 3] = f.w;
-      }
-    }
-  }
+  load_vec_buf<W, CPL>(x, C, lane, kWave, v.f);
   issue_barrier();
   if constexpr (CPL <= 8) {
     uint4 b1[CPL];
@@ -628,9 +646,10 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
       }
     }
     LaneVec<W, CPLU> xr;
-    make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
-    dot_rows<W, CPLU>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, xr, gate_row,
-                      gate_sink);
+    constexpr bool kLate = !is_quant<W>();
+    if constexpr (!kLate) make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
+    dot_rows<W, CPLU, kLate>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, xr, gate_row,
+                             gate_sink, x);
     __syncthreads();
     apply_scales();
     compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
