@@ -417,13 +417,44 @@ __device__ __forceinline__ void gate_up_stream(const float* __restrict__ x, cons
   take_gate(i0);
   load(b0, i0);
   issue_barrier();
-  load_vec_buf<W, CPL>(x, C, lane, kWave, v.f);
+  // x is loaded once per workgroup (each thread a share, zeros past its C chunks) and staged
+  // in LDS, from where every lane reads its chunks
+  constexpr int F4 = W::EPC / 4, kXF4 = CPL * kWave * F4, kXPT = kXF4 / kBlock;
+  static_assert(kXPT * kBlock == kXF4, "x shares");
+  __shared__ float4 s_x[kXF4];
+  float4 xs[kXPT];
+  {
+    const int nf4 = C * F4;
+    const Buf xb = make_buf(x, 16u * (uint32_t)nf4);
+#pragma unroll
+    for (int k = 0; k < kXPT; ++k) {
+      const int j = (int)threadIdx.x + k * kBlock;
+      xs[k] = __builtin_bit_cast(float4, ldb(xb, j < nf4 ? 16u * (uint32_t)j : kOOB));
+    }
+  }
   issue_barrier();
+  auto stage_x = [&] {
+#pragma unroll
+    for (int k = 0; k < kXPT; ++k) s_x[threadIdx.x + k * kBlock] = xs[k];
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+#pragma unroll
+      for (int e4 = 0; e4 < F4; ++e4) {
+        const float4 f = s_x[(lane + c * kWave) * F4 + e4];
+        v.f[c][4 * e4 + 0] = f.x;
+        v.f[c][4 * e4 + 1] = f.y;
+        v.f[c][4 * e4 + 2] = f.z;
+        v.f[c][4 * e4 + 3] = f.w;
+      }
+    }
+  };
   if constexpr (CPL <= 8) {
     uint4 b1[CPL];
     take_gate(i1);
     load(b1, i1);
     issue_barrier();
+    stage_x();
     while (true) {
       finish(b0, i0);
       load(b0, i0);
@@ -434,6 +465,7 @@ __device__ __forceinline__ void gate_up_stream(const float* __restrict__ x, cons
       if (i0.kind == 0 && i1.kind == 0) break;
     }
   } else {
+    stage_x();
     while (true) {
       finish(b0, i0);
       if (i0.kind == 0) break;
