@@ -555,6 +555,43 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_t1(const float* __restrict__ 
   }
 }
 
+// z = A x for one token with fp32 / bf16 rows, one row a workgroup: thread i takes chunks
+// i, i + 256, ... (CPL of them) of the row and of x, and the wave sums meet in LDS.  Each
+// thread keeps a handful of loads in flight, and the rows spread over every CU (the
+// one-row-a-wave kernel above gives 4 rows a workgroup and half the CUs at r = 512).
+template <class W, int CPL, bool NORM>
+__global__ __launch_bounds__(kBlock) void k_lopa_z_row(const float* __restrict__ x, const uint4* __restrict__ A,
+                                                       int C, int r, float* __restrict__ z,
+                                                       const float* __restrict__ gain, float* __restrict__ zsq,
+                                                       GWork gw) {
+  if (g_precompute(gw)) return;
+  __shared__ float s_p[kBlock / kWave];
+  const int k = blockIdx.x;
+  LaneVec<W, CPL, false> v;
+  load_vec_buf<W, CPL>(x, C, threadIdx.x, kBlock, v.f);
+  const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)C);
+  uint4 b[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = (int)threadIdx.x + c * kBlock;
+    b[c] = ldb_nt(ab, ch < C ? 16u * ((uint32_t)k * (uint32_t)C + (uint32_t)ch) : kOOB);
+  }
+  const float part = wave_sum(lane_dot<W, CPL, false>(b, v));
+  if (lane_id() == 0) s_p[threadIdx.x / kWave] = part;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kBlock / kWave; ++w) sum += s_p[w];
+    if constexpr (NORM) {
+      z[k] = gain ? sum * gain[k] : sum;
+      zsq[k] = sum * sum;
+    } else {
+      z[k] = sum;
+    }
+  }
+}
+
 // One segment: gate values, compaction, W_up dots of the selected neurons.
 // LOPA: the gate rows are B [d_ff][r] against z; otherwise W_gate [d_ff][d] against x.
 // DENSE: every neuron of the segment is selected (act = max(h - t, 0)).
@@ -1443,9 +1480,36 @@ __global__ __launch_bounds__(kBlock) void k_rms_norm(float* __restrict__ z, int 
   }
 }
 
+template <class W, int CPL>
+void launch_z_row(const Shape& sh, const Form& form, const float* x, const void* A, const Workspace& ws,
+                  hipStream_t s) {
+  const GWork gw{form, x, ws.gx, 1, sh.d, sh.d_ff, sh.r};
+  const int g = sh.r + (form.g_idx ? (g_items(sh.d_ff, 1) + kBlock - 1) / kBlock : 0);
+  const int C = sh.d / W::EPC;
+  const uint4* a = static_cast<const uint4*>(A);
+  if (form.rms_eps > 0.f)
+    k_lopa_z_row<W, CPL, true><<<g, kBlock, 0, s>>>(x, a, C, sh.r, ws.z, form.rms_gain, ws.zsq, gw);
+  else
+    k_lopa_z_row<W, CPL, false><<<g, kBlock, 0, s>>>(x, a, C, sh.r, ws.z, nullptr, nullptr, gw);
+}
+
 template <class W>
 hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void* A, const Workspace& ws,
                   hipStream_t s) {
+  if constexpr (!is_quant<W>()) {  // one row a workgroup
+    const int C = sh.d / W::EPC;
+    if (fast_ok(sh, Gate::LoPA) && C <= 8 * kBlock) {
+      if (C <= kBlock)
+        launch_z_row<W, 1>(sh, form, x, A, ws, s);
+      else if (C <= 2 * kBlock)
+        launch_z_row<W, 2>(sh, form, x, A, ws, s);
+      else if (C <= 4 * kBlock)
+        launch_z_row<W, 4>(sh, form, x, A, ws, s);
+      else
+        launch_z_row<W, 8>(sh, form, x, A, ws, s);
+      return hipGetLastError();
+    }
+  }
   if (fast_ok(sh, Gate::LoPA)) {
     constexpr int L = cpl_lo<W>(), H = 2 * L;
     const int C = sh.d / W::EPC;
