@@ -1496,9 +1496,12 @@ void launch_z_row(const Shape& sh, const Form& form, const float* x, const void*
 template <class W>
 hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void* A, const Workspace& ws,
                   hipStream_t s) {
-  if constexpr (!is_quant<W>()) {  // one row a workgroup
+  // one row a workgroup when the one-row-a-wave kernel (four rows a workgroup) would leave
+  // compute units idle (measured: 8B r = 512, 4.0 -> 3.7 us; at 70B r = 1024, where the
+  // latter fills the GPU, the row kernel took 6.2 us against 5.7)
+  if constexpr (!is_quant<W>()) {
     const int C = sh.d / W::EPC;
-    if (fast_ok(sh, Gate::LoPA) && C <= 8 * kBlock) {
+    if (fast_ok(sh, Gate::LoPA) && C <= 8 * kBlock && sh.r < (kBlock / kWave) * cu_count()) {
       if (C <= kBlock)
         launch_z_row<W, 1>(sh, form, x, A, ws, s);
       else if (C <= 2 * kBlock)
