@@ -281,6 +281,23 @@ __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const LaneVec<W
   }
 }
 
+// The sum over the 64 lanes, the same in every lane: the rows of 16 lanes reduce by DPP and
+// their four sums are read with v_readlane, with no LDS round trip (group_sum's last two
+// steps are lane shuffles through LDS).  The same additions in the same order as
+// group_sum(v, 64), so the result is bit-identical.  Every lane must be active.
+__device__ __forceinline__ float wave_sum_uniform(float r) {
+  r += dpp_move<kDppXor1>(r);
+  r += dpp_move<kDppXor2>(r);
+  r += dpp_move<kDppHalfMirror>(r);
+  r += dpp_move<kDppMirror>(r);
+  const int ri = __float_as_int(r);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(ri, 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(ri, 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(ri, 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(ri, 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
 // Dot products <rows, v> for rows picked by `row_of(k)`, k in [0, n), of a matrix of
 // `bytes` bytes (< 2^31): each wave takes passes of 64/lpr rows (passes wave, wave + 4,
 // ...).  For rows of at most 8 chunks per lane and more than one pass per wave, two
@@ -325,7 +342,8 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   };
   auto finish = [&](const uint4 (&b)[CPL], int pass) {
     const int k = pass * rpp + p;
-    const float sum = group_sum(lane_dot<W, CPL, Q>(b, v), lpr);
+    const float dot = lane_dot<W, CPL, Q>(b, v);
+    const float sum = lpr == kWave ? wave_sum_uniform(dot) : group_sum(dot, lpr);
     if (q == 0 && k < n) sink(k, sum);
   };
   uint4 b0[CPL], b1[CPL];
@@ -399,10 +417,10 @@ __device__ __forceinline__ void gate_up_stream(const float* __restrict__ x, cons
   };
   auto finish = [&](const uint4 (&b)[CPL], Item& it) {
     if (it.kind == 0) return;
-    const float s = group_sum(lane_dot<W, CPL, false>(b, v), kWave);
+    const float s = wave_sum_uniform(lane_dot<W, CPL, false>(b, v));
     if (it.kind == 1) {
       if (lane == 0) s_h[it.k] = s;
-      if (uniform(s > t ? 1 : 0)) {  // NaN compares false: inactive
+      if (s > t) {  // NaN compares false: inactive
         it.kind = 2;
         it.a = gate_value(act, s - t);
         return;
@@ -576,7 +594,7 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_row(const float* __restrict__
     const int ch = (int)threadIdx.x + c * kBlock;
     b[c] = ldb_nt(ab, ch < C ? 16u * ((uint32_t)k * (uint32_t)C + (uint32_t)ch) : kOOB);
   }
-  const float part = wave_sum(lane_dot<W, CPL, false>(b, v));
+  const float part = wave_sum_uniform(lane_dot<W, CPL, false>(b, v));
   if (lane_id() == 0) s_p[threadIdx.x / kWave] = part;
   __syncthreads();
   if (threadIdx.x == 0) {
