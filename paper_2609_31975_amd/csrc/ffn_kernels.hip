@@ -319,15 +319,16 @@ __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, 
   }
 }
 
+// LATE = 2: the same, from the float4s of an LDS copy `lds_vec` (zeros past C chunks).
 // LATE (fp32 vectors only): v is loaded here from `vec`, after the first pass's row loads,
 // so that the weight stream starts ahead of the vector loads of all the waves on a CU.  It
 // pays for long streams (the standard gate); for a stream of one pass (LoPA's z and gate,
 // the W_up dots after LoPA's gate) the in-order load counter makes the first use of the
 // vector wait for all the rows, and the call measured slower.
-template <class W, int CPL, bool LATE = false, bool Q, class RowOf, class Sink>
+template <class W, int CPL, int LATE = 0, bool Q, class RowOf, class Sink>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
                                          int n, LaneVec<W, CPL, Q>& v, RowOf row_of, Sink sink,
-                                         const float* __restrict__ vec = nullptr) {
+                                         const float* __restrict__ vec = nullptr, const float4* lds_vec = nullptr) {
   static_assert(!(LATE && Q), "a late vector is an fp32 one");
   constexpr int kWaves = kBlock / kWave;
   const Buf mb = make_buf(mat, bytes);
@@ -348,10 +349,23 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   };
   uint4 b0[CPL], b1[CPL];
   load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
-  if constexpr (LATE) {
+  if constexpr (LATE == 1) {
     issue_barrier();
     load_vec_buf<W, CPL>(vec, C, q, lpr, v.f);
     issue_barrier();
+  } else if constexpr (LATE == 2) {
+    constexpr int F4 = W::EPC / 4;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+#pragma unroll
+      for (int e4 = 0; e4 < F4; ++e4) {
+        const float4 f = lds_vec[(q + c * lpr) * F4 + e4];
+        v.f[c][4 * e4 + 0] = f.x;
+        v.f[c][4 * e4 + 1] = f.y;
+        v.f[c][4 * e4 + 2] = f.z;
+        v.f[c][4 * e4 + 3] = f.w;
+      }
+    }
   }
   prepare_lane_vec<W, CPL, Q>(v);  // limbs: the whole workgroup converts the vector
   if (wave >= npass) return;
@@ -665,6 +679,25 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
   const int act = FULL ? form.act : 0;
 
   if constexpr (LOPA) {
+    // x for the W_up dots (fp32 vectors, one row a wave): loaded once per workgroup, each
+    // thread a share, ahead of the gate stream, and staged in LDS during the compaction, so
+    // that the W_up rows go out right after it (every wave reading 16 KB of x there had put
+    // 50 MB of L2 reads in front of the 12 MB of W_up rows)
+    constexpr bool kXLds = !limb_vec<W, CPLU>() && CPLU <= 8 && !DENSE;
+    constexpr int XF4 = W::EPC / 4, kXF4 = kXLds ? CPLU * kWave * XF4 : kBlock, kXPT = kXF4 / kBlock;
+    static_assert(kXPT * kBlock == kXF4, "x shares");
+    __shared__ float4 s_xu[kXLds ? kXF4 : 1];
+    const bool xlds = kXLds && lpru == kWave;
+    float4 xs[kXPT];
+    if constexpr (kXLds) {
+      const int nf4 = Cu * XF4;
+      const Buf xb = make_buf(x, 16u * (uint32_t)nf4);
+#pragma unroll
+      for (int k = 0; k < kXPT; ++k) {
+        const int j = (int)threadIdx.x + k * kBlock;
+        xs[k] = __builtin_bit_cast(float4, ldb(xb, xlds && j < nf4 ? 16u * (uint32_t)j : kOOB));
+      }
+    }
     // LoPA's fixed term (G x)_i of this thread's row (written by the z kernel's extra
     // workgroups) and the squares of z for RMSNorm: loaded before the gate stream, used
     // after it, branch-free so that nothing waits for them in front of the stream
@@ -714,9 +747,22 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
         __syncthreads();
       }
     }
+    if constexpr (kXLds) {
+      if (xlds) {
+#pragma unroll
+        for (int k = 0; k < kXPT; ++k) s_xu[threadIdx.x + k * kBlock] = xs[k];
+      }
+    }
     compact_segment(s_h, nrows, row0, seg, t, DENSE, act, s_list, s_act, &s_cnt, seg_count, seg_idx, seg_act);
     __syncthreads();
     LaneVec<W, CPLU, limb_vec<W, CPLU>()> xr;
+    if constexpr (kXLds) {
+      if (xlds) {
+        dot_rows<W, CPLU, 2>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row,
+                             up_sink, nullptr, s_xu);
+        return;
+      }
+    }
     make_lane_vec<W, CPLU>(x, Cu, lane_id() & (lpru - 1), lpru, xr);
     dot_rows<W, CPLU>(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu, Cu, lpru, lpru_log2, s_cnt, xr, up_row, up_sink);
   } else {
