@@ -325,10 +325,16 @@ __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, 
 // pays for long streams (the standard gate); for a stream of one pass (LoPA's z and gate,
 // the W_up dots after LoPA's gate) the in-order load counter makes the first use of the
 // vector wait for all the rows, and the call measured slower.
-template <class W, int CPL, int LATE = 0, bool Q, class RowOf, class Sink>
+// `stage` runs right after the first pass's row loads, in every thread of the workgroup
+// (LATE = 2: it may fill lds_vec, and ends with a barrier then).
+struct NoStage {
+  __device__ void operator()() const {}
+};
+template <class W, int CPL, int LATE = 0, bool Q, class RowOf, class Sink, class Stage = NoStage>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
                                          int n, LaneVec<W, CPL, Q>& v, RowOf row_of, Sink sink,
-                                         const float* __restrict__ vec = nullptr, const float4* lds_vec = nullptr) {
+                                         const float* __restrict__ vec = nullptr, const float4* lds_vec = nullptr,
+                                         Stage stage = Stage{}) {
   static_assert(!(LATE && Q), "a late vector is an fp32 one");
   constexpr int kWaves = kBlock / kWave;
   const Buf mb = make_buf(mat, bytes);
@@ -349,6 +355,7 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
   };
   uint4 b0[CPL], b1[CPL];
   load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
+  stage();
   if constexpr (LATE == 1) {
     issue_barrier();
     load_vec_buf<W, CPL>(vec, C, q, lpr, v.f);
@@ -720,9 +727,34 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
     }
     {
       LaneVec<W, CPLG> zr;  // limbs: the B stream gives a lane several rows
-      make_lane_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
-      dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
-                        gate_sink);
+      // fp32 z: loaded once per workgroup (each thread a share) ahead of the B rows and
+      // staged in LDS once the rows are requested, instead of 16 KB of z reads a wave
+      constexpr bool kZLds = !is_quant<W>() && CPLG <= 8;
+      if constexpr (kZLds) {
+        constexpr int ZF4 = W::EPC / 4, kZF4 = CPLG * kWave * ZF4, kZPT = kZF4 / kBlock;
+        static_assert(kZPT * kBlock == kZF4, "z shares");
+        __shared__ float4 s_zs[kZF4];
+        float4 zs[kZPT];
+        const int nf4 = Cg * ZF4;
+        const Buf zb = make_buf(z, 16u * (uint32_t)nf4);
+#pragma unroll
+        for (int k = 0; k < kZPT; ++k) {
+          const int j = (int)threadIdx.x + k * kBlock;
+          zs[k] = __builtin_bit_cast(float4, ldb(zb, j < nf4 ? 16u * (uint32_t)j : kOOB));
+        }
+        issue_barrier();
+        auto stage = [&] {
+#pragma unroll
+          for (int k = 0; k < kZPT; ++k) s_zs[threadIdx.x + k * kBlock] = zs[k];
+          __syncthreads();
+        };
+        dot_rows<W, CPLG, 2>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
+                             gate_sink, nullptr, s_zs, stage);
+      } else {
+        make_lane_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
+        dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
+                          gate_sink);
+      }
     }
     const float gv = __builtin_bit_cast(float, gbits);
     __syncthreads();
