@@ -210,6 +210,27 @@ int ffn_lopa_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, int r, con
 int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
                    float* act_host, hipStream_t stream);
 
+/* The active set of the last forward call as DEVICE pointers into the workspace (the
+ * compaction of Section 3.1's skip rule; calls of T <= 64 tokens, FFN_ERR_SHAPE above, since
+ * larger batches run in passes of 64 that reuse the workspace).  Pure pointer arithmetic on the
+ * host: nothing is enqueued, read or synchronized, so it may be called at any time, also
+ * while a stream is being captured into a graph; the data behind the pointers is valid once
+ * the forward call's work on its stream has completed, and device work ordered after the call
+ * (later kernels on the stream, or nodes after it in a graph) may read it directly.
+ *   *meta       int32[64]: meta[0] = nseg, the number of row segments the call used
+ *   *seg_count  int32[nseg]: active neurons of segment w (for T > 1 the union over tokens)
+ *   *idx        int32[d_ff]: segment w covers rows [start(w), start(w + 1)) with
+ *               start(w) = w q + min(w, m), q = d_ff / nseg, m = d_ff mod nseg; its active
+ *               neurons are idx[start(w)], ..., idx[start(w) + seg_count[w] - 1], ascending
+ *   *act        fp32[T][d_ff]: act[tau][start(w) + e] is the activation value of entry e of
+ *               segment w for token tau (h - t for the default form), 0 where that token is
+ *               inactive
+ * Slots past a segment's count hold stale data.  For a dense call every row is listed.
+ * Arguments (ws, T, d, d_ff, r) must be those of the forward call.  Returns FFN_OK, FFN_ERR_NULL
+ * or FFN_ERR_SHAPE. */
+int ffn_workspace_active(const void* ws, int T, int d, int d_ff, int r, const int32_t** meta,
+                         const int32_t** seg_count, const int32_t** idx, const float** act);
+
 /* Benchmark hook (eager launches only, not for graph capture): the next forward call
  * made by this host thread launches its gate kernel -- gate GEMV, threshold,
  * compaction and the W_up dot products of the active neurons, the call's dominant

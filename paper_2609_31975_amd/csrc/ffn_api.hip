@@ -122,17 +122,27 @@ int check_scales(const Call& c, bool lopa, Scales* out) {
   return FFN_OK;
 }
 
-int run(const Call& c) {
+// The host-side checks of a call's pointers, dtype and shape (not of the workspace when
+// `with_ws` is false: the no-allocation entry point supplies its own).
+int check_call(const Call& c, bool with_ws) {
   const bool lopa = c.r > 0;
-  if (!c.x || !c.gate || !c.w_up || !c.w_down_t || !c.y || !c.ws || (lopa && !c.lopa_a)) return FFN_ERR_NULL;
+  if (!c.x || !c.gate || !c.w_up || !c.w_down_t || !c.y || (with_ws && !c.ws) || (lopa && !c.lopa_a))
+    return FFN_ERR_NULL;
   const bool quant = c.wdt == FFN_I8 || c.wdt == FFN_I4;
   if ((c.wdt != FFN_F32 && c.wdt != FFN_BF16 && !quant) || (quant && !c.quant_call)) return FFN_ERR_DTYPE;
   const int sc = check_shape(c.T, c.d, c.d_ff, c.r, lopa);
   if (sc != FFN_OK) return sc;
   if (c.wdt == FFN_I4 && (c.d % 2 != 0 || (lopa && c.r % 2 != 0))) return FFN_ERR_SHAPE;
   if (!aligned(c.x) || !aligned(c.gate) || !aligned(c.w_up) || !aligned(c.w_down_t) || !aligned(c.y) ||
-      !aligned(c.ws) || (lopa && !aligned(c.lopa_a)))
+      (with_ws && !aligned(c.ws)) || (lopa && !aligned(c.lopa_a)))
     return FFN_ERR_ALIGN;
+  return FFN_OK;
+}
+
+int run(const Call& c) {
+  const bool lopa = c.r > 0;
+  const int cc = check_call(c, true);
+  if (cc != FFN_OK) return cc;
   Form form;
   const int so = check_options(c.opt, lopa, &form);
   if (so != FFN_OK) return so;
@@ -297,6 +307,19 @@ int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_uni
     }
   }
   *n_union = n;
+  return FFN_OK;
+}
+
+int ffn_workspace_active(const void* ws, int T, int d, int d_ff, int r, const int32_t** meta,
+                         const int32_t** seg_count, const int32_t** idx, const float** act) {
+  if (!ws || !meta || !seg_count || !idx || !act) return FFN_ERR_NULL;
+  if (r < 0 || ffn::check_shape(T, d, d_ff, r, r > 0) != FFN_OK || T > ffn::kTokChunk) return FFN_ERR_SHAPE;
+  ffn::Workspace w;
+  ffn::workspace_layout(T, d, d_ff, r, const_cast<void*>(ws), &w);
+  *meta = w.meta;
+  *seg_count = w.seg_count;
+  *idx = w.seg_idx;
+  *act = w.seg_act;
   return FFN_OK;
 }
 

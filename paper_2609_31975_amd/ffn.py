@@ -1,8 +1,8 @@
 """Thin ctypes binding of ``include/ffn_sparse.h`` (argument marshalling only).
 
-Every function takes torch device tensors, checks nothing the library does not
-check itself beyond dtype/shape bookkeeping, and passes raw device pointers plus
-the current HIP stream to the C ABI.  All arithmetic runs in the gfx950 kernels of
+Every function takes torch device tensors, checks the dtypes, shapes and devices the
+C ABI cannot see (it receives bare pointers and sizes), and passes raw device pointers
+plus the current HIP stream to the C ABI.  All arithmetic runs in the gfx950 kernels of
 ``libffn_sparse.so``; there is no fallback: if the library is missing this module
 raises on first use.
 """
@@ -79,6 +79,9 @@ def lib() -> ctypes.CDLL:
             getattr(L, name).argtypes = args
         L.ffn_active_set.restype = i
         L.ffn_active_set.argtypes = [vp, i, i, i, i, vp, vp, vp, vp]
+        pp = ctypes.POINTER(ctypes.c_void_p)
+        L.ffn_workspace_active.restype = i
+        L.ffn_workspace_active.argtypes = [vp, i, i, i, i, pp, pp, pp, pp]
         L.ffn_time_next_gate_kernel.restype = i
         L.ffn_time_next_gate_kernel.argtypes = [vp, vp]
         L.ffn_lopa_approx_workspace_bytes.restype = sz
@@ -172,9 +175,40 @@ def _opt(opt):
     return None if opt is None else ctypes.byref(opt)
 
 
+def _check_args(x, y, ws, weights, cols_of):
+    """Validate what the C ABI cannot see: x and y are float32 [T, d] on one device, every
+    weight has w_up's dtype and its expected [rows, cols] shape (``weights`` maps a name to
+    (tensor, rows, logical cols)), and the workspace is on the same device.  cols_of(n)
+    gives the stored row length of n logical elements (n / 2 bytes for int4 codes)."""
+    torch = _torch()
+    if x.dim() != 2 or x.dtype != torch.float32:
+        raise ValueError(f"x must be a float32 [T, d] tensor, got {x.dtype} {tuple(x.shape)}")
+    if y.dtype != torch.float32 or tuple(y.shape) != tuple(x.shape):
+        raise ValueError(f"y must be float32 of x's shape {tuple(x.shape)}, got {y.dtype} {tuple(y.shape)}")
+    dev = x.device
+    if y.device != dev or ws.device != dev:
+        raise ValueError("x, y and the workspace must be on one device")
+    wdtype = weights["w_up"][0].dtype
+    for name, (w, rows, cols) in weights.items():
+        if w is None:
+            raise ValueError(f"{name} is required")
+        if w.dtype != wdtype:
+            raise ValueError(f"{name} is {w.dtype}, w_up is {wdtype}: every weight must have one dtype")
+        if w.device != dev:
+            raise ValueError(f"{name} must be on x's device")
+        if tuple(w.shape) != (rows, cols_of(cols)):
+            raise ValueError(f"{name} must be [{rows}, {cols_of(cols)}], got {tuple(w.shape)}")
+
+
+def _same(n):
+    return n
+
+
 def _std_call(name, x, w_gate, w_up, w_down_t, t, y, ws, stream, opt=()):
     T, d = x.shape
     d_ff = w_up.shape[0]
+    _check_args(x, y, ws, {"w_up": (w_up, d_ff, d), "w_gate": (w_gate, d_ff, d), "w_down_t": (w_down_t, d_ff, d)},
+                _same)
     rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, _dev(x, "x"), _dev(w_gate, "w_gate"),
                               _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t), *opt,
                               _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
@@ -185,6 +219,8 @@ def _std_call(name, x, w_gate, w_up, w_down_t, t, y, ws, stream, opt=()):
 def _lopa_call(name, x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream, opt=()):
     T, d = x.shape
     d_ff, r = lopa_b.shape
+    _check_args(x, y, ws, {"w_up": (w_up, d_ff, d), "lopa_a": (lopa_a, r, d), "lopa_b": (lopa_b, d_ff, r),
+                           "w_down_t": (w_down_t, d_ff, d)}, _same)
     rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, r, _dev(x, "x"), _dev(lopa_a, "lopa_a"),
                               _dev(lopa_b, "lopa_b"), _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"),
                               ctypes.c_float(t), *opt, _dev(y, "y"), _dev(ws, "ws"),
@@ -233,6 +269,15 @@ def _q_call(name, x, gate, lopa_a, w_up, w_down_t, sc, t, opt, y, ws, stream, r)
     d_ff = w_up.shape[0]
     wdt = quant_dtype(w_up, d) if w_up.dtype != _torch().float32 and w_up.dtype != _torch().bfloat16 \
         else weight_dtype(w_up)
+    cols_of = (lambda n: n // 2) if wdt == FFN_I4 else _same
+    if wdt == FFN_I4 and (d % 2 or r % 2):
+        raise ValueError("int4 codes need an even d (and r)")
+    ws_ = {"w_up": (w_up, d_ff, d), "w_down_t": (w_down_t, d_ff, d)}
+    if r:
+        ws_.update(lopa_a=(lopa_a, r, d), lopa_b=(gate, d_ff, r))
+    else:
+        ws_.update(w_gate=(gate, d_ff, d))
+    _check_args(x, y, ws, ws_, cols_of)
     head = [wdt, T, d, d_ff] + ([r] if r else [])
     ptrs = [_dev(x, "x")] + ([_dev(lopa_a, "lopa_a")] if r else []) + [_dev(gate, "gate"), _dev(w_up, "w_up"),
                                                                        _dev(w_down_t, "w_down_t")]
@@ -271,6 +316,28 @@ def ffn_active_set(ws, T, d, d_ff, r=0, stream=None, with_act=True):
     _check("ffn_active_set", rc)
     k = n.value
     return idx[:k].copy(), (None if act is None else act[:, :k].copy())
+
+
+def ffn_workspace_active(ws, T, d, d_ff, r=0):
+    """Device views of the last call's active set (no synchronization, nothing enqueued):
+    returns (meta, seg_count, idx, act) as tensors aliasing the workspace ``ws``: meta int32
+    [64] (meta[0] = nseg), seg_count int32 [d_ff] (the first nseg entries are the segment
+    counts), idx int32 [d_ff], act float32 [T, d_ff]."""
+    torch = _torch()
+    if ws.dtype != torch.uint8 or not ws.is_contiguous():
+        raise ValueError("ws must be a contiguous uint8 tensor")
+    ptrs = [ctypes.c_void_p() for _ in range(4)]
+    rc = lib().ffn_workspace_active(_dev(ws, "ws"), T, d, d_ff, r, *(ctypes.byref(p) for p in ptrs))
+    _check("ffn_workspace_active", rc)
+    base = ws.data_ptr()
+    views = []
+    for p, n, dt in zip(ptrs, (64, d_ff, d_ff, T * d_ff), (torch.int32, torch.int32, torch.int32, torch.float32)):
+        off = p.value - base
+        nbytes = 4 * n
+        if off < 0 or off + nbytes > ws.numel():
+            raise FFNError("ffn_workspace_active", -5)
+        views.append(ws[off:off + nbytes].view(dt))
+    return views[0], views[1], views[2], views[3].view(T, d_ff)
 
 
 def ffn_time_next_gate_kernel(start, stop):

@@ -175,6 +175,20 @@ def make_form(seed: int, d: int, d_ff: int, r: int) -> FormInputs:
     return FormInputs(g_idx=g_idx, g_sign=g_sign, rms_gain=rms_gain)
 
 
+def g_repeated_diagonal(d: int, d_ff: int, sign: int = 1):
+    """LoPA's fixed term as the repeated diagonal of the appendix on the fixed-matrix
+    ablation: row i holds `sign` in column floor(i / k) with k = d_ff / d, read as
+    floor(i d / d_ff) when k is not an integer.  Returns (g_idx int32 [d_ff], g_sign int8)."""
+    i = np.arange(d_ff, dtype=np.int64)
+    return (i * d // d_ff).astype(np.int32), np.full(d_ff, sign, np.int8)
+
+
+def g_tiled_identity(d: int, d_ff: int):
+    """LoPA's fixed term as identity matrices I_d stacked over the d_ff rows (the tiled
+    identity of the same ablation): row i holds +1 in column i mod d."""
+    return (np.arange(d_ff, dtype=np.int64) % d).astype(np.int32), np.ones(d_ff, np.int8)
+
+
 def make_tokens_correlated(seed: int, T: int, d: int, rho: float) -> np.ndarray:
     """T tokens sharing a common part: x_tau = sqrt(rho) c + sqrt(1 - rho) n_tau, c and the
     n_tau iid N(0, 1) (each token stays N(0, 1); two tokens correlate by rho)."""

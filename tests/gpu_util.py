@@ -4,7 +4,8 @@ entry point through the C ABI, and compare against the oracle with the parity ru
 * active sets: bit-exact for every neuron whose oracle gate value is at least
   BAND = 1e-3 away from the threshold (inside the band both decisions are valid);
 * outputs: ||y - y_ref|| / ||y_ref|| <= 1e-5 (fp32 weights) or 2e-3 (bf16 weights),
-  per token; an all-zero reference requires an exactly zero output.
+  per token, and element-wise max |y - y_ref| <= the same tolerance times max |y_ref|;
+  an all-zero reference requires an exactly zero output.
 """
 from __future__ import annotations
 
@@ -170,6 +171,12 @@ def check_parity(res, y, idx, act, t, wdt, dense=False, what="", act_value=None)
         e = rel_err(y[tau], res.y[tau])
         assert e <= tol, f"{what}: token {tau} relative error {e:.3e} > {tol}"
         out["max_rel_err"] = max(out["max_rel_err"], e)
+        # element-wise: no column may carry an error the norm would average away
+        ref = np.asarray(res.y[tau], np.float64)
+        if np.isfinite(ref).all():
+            worst = float(np.max(np.abs(np.asarray(y[tau], np.float64) - ref))) if ref.size else 0.0
+            scale = float(np.max(np.abs(ref))) if ref.size else 0.0
+            assert worst <= tol * scale, f"{what}: token {tau} max abs error {worst:.3e} > {tol} x {scale:.3e}"
     if idx is None:
         return out
     assert np.all(np.diff(idx) > 0), f"{what}: active list not strictly ascending"

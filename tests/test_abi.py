@@ -200,3 +200,24 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(ffn, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         ffn.lib()
+
+
+def test_workspace_active_pointers():
+    """ffn_workspace_active is pointer arithmetic on the host: no device access, so it runs
+    here; the views lie inside the workspace, in layout order, 256-byte aligned."""
+    vp = ctypes.c_void_p
+    for T, d, d_ff, r in ((1, 4096, 14336, 0), (4, 264, 1000, 40), (64, 136, 300, 0)):
+        out = [vp() for _ in range(4)]
+        assert L.ffn_workspace_active(A, T, d, d_ff, r, *(ctypes.byref(p) for p in out)) == 0
+        meta, cnt, idx, act = (p.value for p in out)
+        n = ffn.workspace_bytes(T, d, d_ff, r)
+        assert A <= meta < cnt < idx < act and act + 4 * T * d_ff <= A + n
+        assert cnt - meta >= 4 * 64 and idx - cnt >= 4 * d_ff and act - idx >= 4 * d_ff
+        assert all((p - A) % 256 == 0 for p in (meta, cnt, idx, act))
+    out = [vp() for _ in range(4)]
+    refs = [ctypes.byref(p) for p in out]
+    assert L.ffn_workspace_active(None, 1, 64, 128, 0, *refs) == -1
+    assert L.ffn_workspace_active(A, 1, 64, 128, 0, None, *refs[1:]) == -1
+    assert L.ffn_workspace_active(A, 0, 64, 128, 0, *refs) == -2
+    assert L.ffn_workspace_active(A, 65, 64, 128, 0, *refs) == -2
+    assert L.ffn_workspace_active(A, 1, 64, 128, -1, *refs) == -2

@@ -52,6 +52,8 @@ CASES = [
     ("mc_std_bf16_T40", 40, 136, 300, 0, BF16, 1.5, ACT),
     ("mc_lopa_bf16_T64_all", 64, 264, 1000, 40, BF16, 1.6 * S2, ALL),
     ("mc_lopa_bf16_T70_g", 70, 264, 1000, 40, BF16, 1.3 * S2, dict(act=1, use_g=True)),
+    ("mc_lopa_bf16_T90_all", 90, 264, 1000, 40, BF16, 1.6 * S2, ALL),   # 64 + 26: a pre-split two-tile tail
+    ("mc_std_bf16_T100_act", 100, 264, 1000, 0, BF16, 1.6, ACT),
 ]
 
 
@@ -140,3 +142,23 @@ def test_zero_gated_value_rows_not_read(gu, shape, silu_up):
     res = gu.run_oracle(inp, t, form=form)
     assert np.isfinite(res.y).all()
     gu.check_parity(res, y, idx, act, t, wdt, what=f"s_gated {shape}")
+
+
+# ---------------------------------------------------------------- the fixed matrices of the LoPA ablation
+# (appendix on the ablation of W1's design: the repeated diagonal, its negative, the tiled identity)
+@pytest.mark.parametrize("kind", ["diagonal", "minus_diagonal", "tiled"])
+@pytest.mark.parametrize("T,d,d_ff,r", [(1, 264, 1000, 40), (1, 4096, 14336, 512), (4, 264, 1000, 40),
+                                        (20, 264, 1000, 40)], ids=lambda v: str(v))
+def test_fixed_matrix_variants(gu, kind, T, d, d_ff, r):
+    inp = wl.make_inputs(206, T, d, d_ff, r=r, wdt=BF16)
+    if kind == "tiled":
+        g_idx, g_sign = wl.g_tiled_identity(d, d_ff)
+    else:
+        g_idx, g_sign = wl.g_repeated_diagonal(d, d_ff, -1 if kind == "minus_diagonal" else 1)
+    fi = wl.FormInputs(g_idx=g_idx, g_sign=g_sign, rms_gain=np.ones(r, np.float32))
+    form = gu.Form(act=1, silu_up=True, form=fi, use_g=True)
+    t = 1.2816 * S2
+    y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(inp), t, form)
+    res = gu.run_oracle(inp, t, form=form)
+    fig = gu.check_parity(res, y, idx, act, t, BF16, what=f"{kind} T={T}", act_value=form.act_value)
+    assert 0 < fig["n_union"] < d_ff

@@ -93,3 +93,44 @@ def test_full_size_gate_properties(dev):
     Uref = (W64 - M) @ V64.T
     assert float((U64 - Uref).norm() / Uref.norm()) < 1e-5
     print("8b gate approx:", it, obj, flush=True)
+
+
+@pytest.mark.parametrize("planted_w", [True, False], ids=["planted", "gaussian"])
+def test_architecture_casting(dev, planted_w):
+    """Architecture casting (Section 3.4): a standard gate W is replaced by its LoPA
+    approximation (M, U, V) from ffn_lopa_approx, and the sparse FFN runs with LoPA gating
+    h = M x + U (V x) (the _ex call with G = M, no norm, no activation on W_up).  The
+    cast call matches the oracle on the same factors, and its gate differs from the
+    standard gate on W by at most the approximation error: |h_cast - h_std| <= ||row of
+    (W - M - U V)|| ||x|| per neuron.  A planted W = M + U V is recovered, so the cast call
+    then equals standard gating on W itself."""
+    torch, ffn = dev
+    from tests import gpu_util as gu
+    from paper_2609_31975_amd import workloads as wl
+    H, D, r, T, t = 1000, 256, 32, 4, 1.0
+    if planted_w:
+        W, _, _, _ = planted(17, H, D, r)   # gate values x[g_idx] g_sign plus a small U V x
+    else:
+        W = (np.random.default_rng(18).standard_normal((H, D)) * D ** -0.5).astype(np.float32)
+    base = wl.make_inputs(19, T, D, H, r=0, wdt=wl.F32)
+    gi, gs, U, V, it, obj = run(dev, W, r)
+    U32, V32 = U.astype(np.float32), V.astype(np.float32)
+    cast = wl.FFNInputs(x=base.x, w_up=base.w_up, w_down_t=base.w_down_t, lopa_a=V32, lopa_b=U32, wdt=wl.F32)
+    form = gu.Form(form=wl.FormInputs(g_idx=gi, g_sign=gs, rms_gain=np.ones(r, np.float32)), use_g=True)
+    y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(cast), t, form)
+    res_cast = gu.run_oracle(cast, t, form=form)
+    gu.check_parity(res_cast, y, idx, act, t, wl.F32, what="cast")
+    std = wl.FFNInputs(x=base.x, w_up=base.w_up, w_down_t=base.w_down_t, w_gate=W, wdt=wl.F32)
+    res_std = gu.run_oracle(std, t)
+    E = W.astype(np.float64) - la.dense_m(gi, gs, D) - U32.astype(np.float64) @ V32.astype(np.float64)
+    bound = np.linalg.norm(E, axis=1)[None, :] * np.linalg.norm(base.x.astype(np.float64), axis=1)[:, None]
+    assert np.all(np.abs(res_cast.h - res_std.h) <= bound + 1e-9)
+    if planted_w:
+        assert obj < 1e-9 * H * D
+        ys, _, _, _ = gu.run_gpu(gu.DevInputs(std), t)
+        gu.check_parity(res_std, y, None, None, t, wl.F32, what="cast vs standard")
+        assert gu.rel_err(y, ys) < 1e-4
+    else:
+        assert obj > 0
+        frac = np.mean(np.abs(res_cast.h - res_std.h) <= bound)
+        assert frac == 1.0

@@ -44,6 +44,9 @@ SMALL = [
     ("std_bf16_T64", 64, 264, 1000, 0, BF16, 1.6),
     ("std_bf16_T17", 17, 136, 300, 0, BF16, 1.2),           # pre-split tokens, second tile nearly empty
     ("lopa_bf16_T70", 70, 264, 1000, 40, BF16, 1.3),        # a pre-split 64-token pass, then 6 tokens
+    ("std_bf16_T100", 100, 264, 1000, 0, BF16, 1.6),        # 64 + 36: the tail pass is pre-split (three tiles)
+    ("lopa_bf16_T100", 100, 264, 1000, 40, BF16, 1.6),
+    ("lopa_bf16_T81", 81, 264, 1000, 40, BF16, 1.6),        # 64 + 17: a tail pass of two tiles, one token in the second
     ("std_bf16_d4096", 1, 4096, 2056, 0, BF16, 1.2816),    # full-width rows, short d_ff
     ("std_bf16_d4096_odd", 1, 4096, 2052, 0, BF16, 1.2816),
     ("std_bf16_long_chunks", 1, 4096, 40000, 0, BF16, 1.2816),  # down row chunks of over 1024 slots
@@ -271,3 +274,86 @@ def test_correlated_batches(gu, rho, T, r):
     if rho == 1.0:
         assert fig["n_union"] == round(n1)
     print(f"rho={rho} T={T} r={r}: union {fig['n_union']} of {d_ff}, per token {n1:.0f}", flush=True)
+
+
+# ---------------------------------------------------------------- NaN gate values
+NAN_GATE = [(1, 264, 1000, 0, BF16), (1, 260, 999, 0, F32), (4, 264, 1000, 0, BF16), (4, 264, 1000, 0, F32),
+            (1, 264, 1000, 40, BF16), (1, 256, 1024, 32, F32), (4, 264, 1000, 40, BF16), (4, 264, 1000, 40, F32),
+            (1, 4096, 2056, 0, BF16)]
+
+
+@pytest.mark.parametrize("shape", NAN_GATE, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
+def test_nan_gate_rows_are_inactive(gu, shape):
+    """NaN in a few W_gate rows (or B rows for LoPA) makes those gate values NaN: the
+    neurons are inactive (h > t is false), the rest of the call is unaffected and y is
+    finite."""
+    T, d, d_ff, r, wdt = shape
+    inp = wl.make_inputs(108, T, d, d_ff, r=r, wdt=wdt)
+    nan = np.uint16(0x7FC0) if wdt == BF16 else np.float32(np.nan)
+    rows = np.arange(3, d_ff, 97)
+    if r:
+        inp.lopa_b = inp.lopa_b.copy()
+        inp.lopa_b[rows] = nan
+    else:
+        inp.w_gate = inp.w_gate.copy()
+        inp.w_gate[rows] = nan
+    t = 0.9
+    res = gu.run_oracle(inp, t)
+    assert np.isnan(res.h[:, rows]).all() and not res.active[:, rows].any()
+    y, idx, act, _ = gu.run_gpu(gu.DevInputs(inp), t)
+    assert np.isfinite(y).all()
+    assert not np.isin(rows, idx).any(), "a NaN gate value was listed as active"
+    gu.check_parity(res, y, idx, act, t, wdt, what=f"nan gate {shape}")
+
+
+# ---------------------------------------------------------------- device views of the active set
+@pytest.mark.parametrize("shape", [(1, 4096, 2056, 0), (1, 264, 1000, 40), (4, 264, 1000, 40), (20, 264, 1000, 0)],
+                         ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}")
+def test_workspace_active_under_graph_capture(gu, shape):
+    """ffn_workspace_active gives device pointers into the workspace without synchronizing:
+    a graph that holds the call and copies of those views (device work reading them right
+    after the call) replays, for new tokens each time, to the active set that the
+    synchronizing host hook reports."""
+    import torch
+    from paper_2609_31975_amd import ffn
+    T, d, d_ff, r = shape
+    t = 1.2816
+    inp = wl.make_inputs(109, T, d, d_ff, r=r, wdt=BF16)
+    dev = gu.DevInputs(inp)
+    ws = ffn.alloc_workspace(T, d, d_ff, r)
+    y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+    x = dev.x.clone()
+    meta, cnt, idx, act = ffn.ffn_workspace_active(ws, T, d, d_ff, r)
+
+    def call():
+        if r:
+            ffn.ffn_lopa_sparse_forward(x, dev.lopa_a, dev.lopa_b, dev.w_up, dev.w_down_t, t, y, ws)
+        else:
+            ffn.ffn_sparse_forward(x, dev.w_gate, dev.w_up, dev.w_down_t, t, y, ws)
+
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        call()   # eager warm-up (kernel loading, occupancy queries)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        call()
+        got = [v.clone() for v in (meta, cnt, idx, act)]
+    for rep in range(3):
+        x.copy_(torch.from_numpy(wl.make_tokens(110 + rep, T, d)).to("cuda"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        m, c, ix, a = (v.cpu().numpy() for v in got)
+        nseg = int(m[0])
+        assert 1 <= nseg <= d_ff
+        q, rem = divmod(d_ff, nseg)
+        starts = [w * q + min(w, rem) for w in range(nseg)]
+        listed = np.concatenate([ix[s:s + c[w]] for w, s in enumerate(starts)])
+        acts = np.concatenate([a[:, s:s + c[w]] for w, s in enumerate(starts)], axis=1)
+        ref_idx, ref_act = ffn.ffn_active_set(ws, T, d, d_ff, r)
+        assert np.array_equal(listed, ref_idx), f"replay {rep}"
+        assert np.array_equal(acts.view(np.uint32), ref_act.view(np.uint32)), f"replay {rep}"
+        res = gu.run_oracle(inp, t, x=x.cpu().numpy())
+        gu.check_parity(res, y.cpu().numpy(), listed, acts, t, BF16, what=f"graph replay {rep}")
+    del graph

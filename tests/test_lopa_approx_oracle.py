@@ -84,3 +84,21 @@ def test_rank_deficient_residual():
 def test_bad_rank():
     with pytest.raises(ValueError):
         la.lopa_approx(np.zeros((4, 3)), 4)
+
+
+@pytest.mark.parametrize("seed", [8, 9])
+def test_factor_convention(seed):
+    """The factors' convention (reading: U carries the singular values): V has orthonormal
+    rows, U = (W - M) V^T, and U's columns are orthogonal with norms equal to the top r
+    singular values of W - M, largest first.  Moving the singular values onto V fails the
+    first two; a transposed or unsorted V fails the last."""
+    rng = np.random.default_rng(seed)
+    W = rng.standard_normal((60, 36))
+    r = 7
+    res = la.lopa_approx(W, r)
+    R = W - la.dense_m(res.g_idx, res.g_sign, W.shape[1])
+    assert np.allclose(res.V @ res.V.T, np.eye(r), atol=1e-12)
+    assert np.allclose(res.U, R @ res.V.T, atol=1e-12)
+    s = np.linalg.svd(R, compute_uv=False)
+    gram = res.U.T @ res.U
+    assert np.allclose(gram, np.diag(s[:r] ** 2), atol=1e-9 * s[0] ** 2)

@@ -529,6 +529,60 @@ def test_fixed_term_is_the_matrix_G_plus_BA():
     assert not np.allclose(no_sign.h, std.h, rtol=0, atol=1e-5)   # the sign is part of G
 
 
+# The fixed matrices of the appendix on the LoPA ablation.  With B = 0 the gate is G x
+#   alone: the repeated diagonal (k = d_ff / d rows per column) gives x with every element
+#   repeated k times, the tiled identity gives x repeated as a whole.
+@pytest.mark.parametrize("kind", ["diagonal", "minus_diagonal", "tiled"])
+def test_fixed_matrix_variants(kind):
+    d, d_ff, r = 8, 24, 2
+    x = np.array([[1, -2, 3, 0.5, -0.25, 4, -3, 2]], np.float32)
+    if kind == "tiled":
+        g_idx, g_sign = wl.g_tiled_identity(d, d_ff)
+        want = np.tile(x[0], 3)
+    else:
+        sign = -1 if kind == "minus_diagonal" else 1
+        g_idx, g_sign = wl.g_repeated_diagonal(d, d_ff, sign)
+        want = sign * np.repeat(x[0], 3)
+    inp = wl.make_inputs(24, 1, d, d_ff, r=r, wdt=wl.F32)
+    res = ffn_oracle.ffn(x, lopa_a=inp.lopa_a, lopa_b=np.zeros((d_ff, r), np.float32), w_up=inp.w_up,
+                         w_down_t=inp.w_down_t, t=0.7, wdt=wl.F32, g_idx=g_idx, g_sign=g_sign)
+    assert res.h[0].tolist() == want.tolist()
+
+
+def test_fixed_matrix_generators():
+    """Every column gets floor(k) or ceil(k) consecutive rows of the diagonal, in order."""
+    for d, d_ff in ((4096, 14336), (8, 24), (5, 13), (7, 7)):
+        g_idx, g_sign = wl.g_repeated_diagonal(d, d_ff)
+        assert np.all(np.diff(g_idx) >= 0) and g_idx[0] == 0 and g_idx[-1] == d - 1
+        counts = np.bincount(g_idx, minlength=d)
+        assert counts.min() >= d_ff // d and counts.max() <= -(-d_ff // d)
+        assert np.all(g_sign == 1)
+        t_idx, t_sign = wl.g_tiled_identity(d, d_ff)
+        assert np.array_equal(t_idx[:d], np.arange(min(d, d_ff))) and np.all(t_sign == 1)
+
+
+def test_diagonal_and_tiled_identity_agree_up_to_a_permutation():
+    """The appendix notes the two fixed matrices are the same up to a permutation of the
+    hidden neurons: permuting the rows of B, W_up and W_down^T along with G leaves the
+    FFN output unchanged (only the order of the sum over neurons differs)."""
+    d, d_ff, r, T, t = 16, 48, 4, 3, 0.9
+    k = d_ff // d
+    inp = wl.make_inputs(25, T, d, d_ff, r=r, wdt=wl.F32)
+    di, ds = wl.g_repeated_diagonal(d, d_ff)
+    ti, ts = wl.g_tiled_identity(d, d_ff)
+    # tiled row q d + j and diagonal row j k + q both hold column j
+    q, j = np.divmod(np.arange(d_ff), d)
+    perm = j * k + q
+    assert np.array_equal(di[perm], ti)
+    diag = ffn_oracle.ffn(inp.x, lopa_a=inp.lopa_a, lopa_b=inp.lopa_b, w_up=inp.w_up, w_down_t=inp.w_down_t, t=t,
+                          wdt=wl.F32, g_idx=di, g_sign=ds)
+    tiled = ffn_oracle.ffn(inp.x, lopa_a=inp.lopa_a, lopa_b=inp.lopa_b[perm], w_up=inp.w_up[perm],
+                           w_down_t=inp.w_down_t[perm], t=t, wdt=wl.F32, g_idx=ti, g_sign=ts)
+    assert np.array_equal(tiled.h, diag.h[:, perm])
+    assert np.allclose(tiled.y, diag.y, rtol=1e-12, atol=1e-13)
+    assert diag.active.any() and not diag.active.all()
+
+
 # RMSNorm between the factors (Section 3.3): A picks z = (x2, 8 x3) = (3, 4) from
 #   x = (1, -2, 3, 0.5); mean(z^2) = 12.5, so RMSNorm(z) = (3, 4) / sqrt(12.5)
 #   = (3 sqrt2 / 5, 4 sqrt2 / 5).  B rows (1,0), (0,1), (1,1), (-1,0), (0,0), (2,-1).
@@ -549,6 +603,24 @@ def test_rms_norm_worked(wdt):
     res_g = ffn_oracle.ffn(x, rms_gain=gain, **kw)
     assert np.allclose(res_g.h[0], [2 * z0, z1 / 4, 2 * z0 + z1 / 4, -2 * z0, 0, 4 * z0 - z1 / 4], rtol=1e-14,
                        atol=1e-15)
+
+
+# Where eps sits (Section 3.3's norm, reading: inside the root).  The same z = (3, 4) with
+#   eps = 12.5 = mean(z^2): 1 / sqrt(12.5 + 12.5) = 1/5, so RMSNorm(z) = (3/5, 4/5).  eps
+#   outside the root, 1 / (sqrt(12.5) + 12.5), would give about (0.187, 0.249) instead.
+@pytest.mark.parametrize("wdt", [wl.F32, wl.BF16])
+def test_rms_norm_eps_inside_the_root(wdt):
+    x, _, up, dn = _worked_standard()
+    up = np.nan_to_num(up, nan=0.0)
+    dn = np.nan_to_num(dn, nan=0.0)
+    A = np.array([[0, 0, 1, 0], [0, 0, 0, 8]])
+    B = np.array([[1, 0], [0, 1], [1, 1], [-1, 0], [0, 0], [2, -1]])
+    res = ffn_oracle.ffn(x, lopa_a=_enc(A, wdt), lopa_b=_enc(B, wdt), w_up=_enc(up, wdt), w_down_t=_enc(dn, wdt),
+                         t=0.5, wdt=wdt, rms_norm=True, rms_eps=12.5)
+    z0, z1 = 0.6, 0.8
+    assert np.allclose(res.h[0], [z0, z1, z0 + z1, -z0, 0, 2 * z0 - z1], rtol=1e-14, atol=1e-15)
+    # h > 0.5 for neurons 0, 1, 2 only; a = h - 0.5; v = (W_up x) = (0, 0.5, -1) on them
+    assert np.flatnonzero(res.active[0]).tolist() == [0, 1, 2]
 
 
 def test_rms_norm_is_scale_invariant():
