@@ -94,6 +94,20 @@ int ffn_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, 
                        const void* w_up, const void* w_down_t, float t, float* y, void* ws,
                        size_t ws_bytes, hipStream_t stream);
 
+/* ffn_sparse_forward without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  The call allocates nothing: its workspace is a 16 MiB array inside the
+ * library, one per GPU, set up on the first call made with that GPU current (the stream must
+ * belong to the current device) and kept until the process ends.  Shapes whose
+ * ffn_workspace_bytes(T, d, d_ff, 0) exceeds 16 MiB return FFN_ERR_WORKSPACE (T = 1 fits any
+ * shape the other calls take; 70B-shaped batches up to 37 tokens, 8B-shaped ones up to 62).
+ * Every call on one GPU shares that array, so calls that overlap in time on one GPU (other
+ * streams, other host threads) race and give wrong results: order them.  ffn_active_set and
+ * ffn_workspace_active cannot see this workspace.  Arguments and errors otherwise as for
+ * ffn_sparse_forward; FFN_ERR_HIP if the runtime cannot give the array's address. */
+int ffn_sparse_forward_noalloc(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                               const void* w_up, const void* w_down_t, float t, float* y, hipStream_t stream);
+
 /* Sparse method, LoPA gating h = B (A x) (Section 3.3). */
 int ffn_lopa_sparse_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const float* x,
                             const void* lopa_a, const void* lopa_b, const void* w_up,

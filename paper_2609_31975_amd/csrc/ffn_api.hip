@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "ffn_internal.h"
@@ -171,6 +172,31 @@ int run(const Call& c) {
   return FFN_OK;
 }
 
+// ------------------------------------------------------------------ the no-allocation entry point
+// Its workspace: a file-scope device array, one copy per GPU the library runs on, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, so its device
+// address is taken once per device with hipGetSymbolAddress and kept in g_scratch.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The scratch array's device address on the current device (set up on the first call made
+// with that device current), or null if the runtime cannot give it.
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    g_scratch[dev] = p;
+  }
+  return g_scratch[dev];
+}
+
 }  // namespace
 }  // namespace ffn
 
@@ -211,6 +237,18 @@ int ffn_lopa_dense_forward(ffn_dtype_t wdt, int T, int d, int d_ff, int r, const
   if (r < 1) return FFN_ERR_SHAPE;
   return ffn::run(
       Call{wdt, T, d, d_ff, r, true, x, lopa_b, lopa_a, w_up, w_down_t, t, nullptr, y, ws, ws_bytes, stream});
+}
+
+int ffn_sparse_forward_noalloc(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
+                               const void* w_up, const void* w_down_t, float t, float* y, hipStream_t stream) {
+  Call c{wdt, T, d, d_ff, 0, false, x, w_gate, nullptr, w_up, w_down_t, t, nullptr, y, nullptr, 0, stream};
+  const int cc = ffn::check_call(c, false);
+  if (cc != FFN_OK) return cc;
+  if (ffn::workspace_layout(T, d, d_ff, 0, nullptr, nullptr) > ffn::kScratchBytes) return FFN_ERR_WORKSPACE;
+  c.ws = ffn::scratch_on_current_device();
+  if (!c.ws) return FFN_ERR_HIP;
+  c.ws_bytes = ffn::kScratchBytes;
+  return ffn::run(c);
 }
 
 int ffn_dense_forward_ex(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,

@@ -79,6 +79,8 @@ def lib() -> ctypes.CDLL:
             getattr(L, name).argtypes = args
         L.ffn_active_set.restype = i
         L.ffn_active_set.argtypes = [vp, i, i, i, i, vp, vp, vp, vp]
+        L.ffn_sparse_forward_noalloc.restype = i
+        L.ffn_sparse_forward_noalloc.argtypes = [i, i, i, i, vp, vp, vp, vp, f, vp, vp]
         pp = ctypes.POINTER(ctypes.c_void_p)
         L.ffn_workspace_active.restype = i
         L.ffn_workspace_active.argtypes = [vp, i, i, i, i, pp, pp, pp, pp]
@@ -236,6 +238,20 @@ def ffn_dense_forward(x, w_gate, w_up, w_down_t, t, y, ws, stream=None):
 
 def ffn_sparse_forward(x, w_gate, w_up, w_down_t, t, y, ws, stream=None):
     return _std_call("ffn_sparse_forward", x, w_gate, w_up, w_down_t, t, y, ws, stream)
+
+
+def ffn_sparse_forward_noalloc(x, w_gate, w_up, w_down_t, t, y, stream=None):
+    """ffn_sparse_forward with the library's own per-GPU workspace (no allocation; calls that
+    overlap on one GPU race)."""
+    T, d = x.shape
+    d_ff = w_up.shape[0]
+    _check_args(x, y, y, {"w_up": (w_up, d_ff, d), "w_gate": (w_gate, d_ff, d), "w_down_t": (w_down_t, d_ff, d)},
+                _same)
+    rc = lib().ffn_sparse_forward_noalloc(weight_dtype(w_up), T, d, d_ff, _dev(x, "x"), _dev(w_gate, "w_gate"),
+                                          _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t),
+                                          _dev(y, "y"), _stream(stream))
+    _check("ffn_sparse_forward_noalloc", rc)
+    return y
 
 
 def ffn_lopa_sparse_forward(x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream=None):

@@ -221,3 +221,17 @@ def test_workspace_active_pointers():
     assert L.ffn_workspace_active(A, 0, 64, 128, 0, *refs) == -2
     assert L.ffn_workspace_active(A, 65, 64, 128, 0, *refs) == -2
     assert L.ffn_workspace_active(A, 1, 64, 128, -1, *refs) == -2
+
+
+def test_noalloc_argument_errors():
+    """The no-allocation entry point checks its arguments and its workspace limit before it
+    touches the GPU."""
+    f = L.ffn_sparse_forward_noalloc
+    c = ctypes.c_float(0.5)
+    assert f(1, 1, 64, 128, None, A, A, A, c, A, None) == -1
+    assert f(1, 1, 64, 128, A, A, A, A, c, None, None) == -1
+    assert f(7, 1, 64, 128, A, A, A, A, c, A, None) == -3
+    assert f(1, 0, 64, 128, A, A, A, A, c, A, None) == -2
+    assert f(1, 1, 64, 128, MIS, A, A, A, c, A, None) == -4
+    assert ffn.workspace_bytes(64, 8192, 28672, 0) > 16 << 20
+    assert f(1, 64, 8192, 28672, A, A, A, A, c, A, None) == -5
