@@ -25,7 +25,11 @@
  *   lopa_b     [d_ff][r]   weights (LoPA U factor)
  *   w_up       [d_ff][d]   weights
  *   w_down_t   [d_ff][d]   weights, W2 transposed: row i = output vector of neuron i
- *   ws         workspace of at least ffn_workspace_bytes(...) bytes
+ *   ws         workspace of at least ffn_workspace_bytes(...) bytes, zero-filled once before
+ *              its first use (a memset after allocation); every call leaves it ready for the
+ *              next one.  The single-token LoPA calls hand z = A x between workgroups of one
+ *              kernel through tagged words in it, which must not start out tagged; a call that
+ *              returned FFN_ERR_HIP may leave it unusable until it is zero-filled again.
  * Weights are fp32 (FFN_F32) or bfloat16 (FFN_BF16, raw 16-bit patterns); x, y and
  * every accumulation are fp32.  t is a host fp32 scalar.
  *

@@ -36,6 +36,9 @@ size_t workspace_layout(int T, int d, int d_ff, int r, void* base, Workspace* ou
     return p;
   };
   w.meta = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 64));
+  // right after meta, so that calls of any token count with one rank find their slots in the
+  // same place
+  w.zslot = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)(r > 0 ? r : 1)));
   w.seg_count = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)d_ff));
   w.seg_idx = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.slots));
   w.seg_act = reinterpret_cast<float*>(take(sizeof(float) * (size_t)w.tc * w.slots));
@@ -163,9 +166,12 @@ int run(const Call& c) {
     if (batched_ok(sh, g)) {
       e = launch_batched(sh, g, c.dense, form, x, c.lopa_a, c.gate, c.w_up, c.w_down_t, c.t, ws, y, c.stream);
     } else {
-      if (lopa) e = launch_lopa_z(sh, form, x, c.lopa_a, ws, c.stream);
-      if (e == hipSuccess) e = launch_gate_up(sh, g, c.dense, form, x, c.gate, c.w_up, c.t, ws, y, c.stream);
-      if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream);
+      // z = A x: in the gate kernel where it can (its down kernel then clears the z slots)
+      const bool fz = lopa && lopa_fuses_z(sh, form);
+      if (lopa && !fz) e = launch_lopa_z(sh, form, x, c.lopa_a, ws, c.stream);
+      if (e == hipSuccess)
+        e = launch_gate_up(sh, g, c.dense, form, x, c.gate, c.w_up, c.t, ws, y, c.stream, fz ? c.lopa_a : nullptr);
+      if (e == hipSuccess) e = launch_down(sh, c.dense, c.w_down_t, ws, y, c.stream, fz);
     }
     if (e != hipSuccess) return FFN_ERR_HIP;
   }

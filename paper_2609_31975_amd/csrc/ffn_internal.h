@@ -15,6 +15,14 @@ constexpr int kBlock = 256;       // threads per workgroup for every kernel
 constexpr int kTokChunk = 64;     // tokens per pass; a larger batch runs as several passes
 constexpr int kListWindow = 1024; // active entries staged in LDS at a time by the down kernel
 constexpr int kPreSplitMin = 17;  // batches of more than one 16-token tile get their tokens pre-split
+// Tag of a published z value (a signalling-NaN bit pattern, which no arithmetic produces and
+// none of the workspace's other data holds), and the most z components the single-token gate
+// kernel computes itself (8 a thread).
+constexpr uint32_t kZTag = 0x7FA5A5A5u;
+constexpr int kFusedZMax = 8 * 256;
+// How long a gate workgroup waits for the z components of the others before it computes the
+// missing ones itself: 100 us of the 100 MHz constant clock (wall_clock64).
+constexpr uint64_t kZWaitTicks = 10000;
 
 // Balanced split of n items into `parts` ranges; range w is [start(w), start(w + 1)).
 // The first n % parts ranges hold n / parts + 1 items, the others n / parts.  32-bit
@@ -47,6 +55,9 @@ struct Workspace {
   int tc;
   int r;
   int32_t* meta;       // [64]             meta[0] = nseg of the last call
+  uint64_t* zslot;     // [r]              LoPA z of one token as published by the gate kernel that
+                       //                  computes it (kZTag in the high word, the fp32 value in
+                       //                  the low one); all-zero tags between calls (LoPA only)
   int32_t* seg_count;  // [d_ff]           (at most d_ff segments)
   int32_t* seg_idx;    // [slots]          neuron index
   float* seg_act;      // [tc][slots]      h - t for the token, 0 where inactive
@@ -121,10 +132,15 @@ hipError_t launch_rms_norm(float* z, int parts, int tc, int T, int r, const floa
 // Also clears y[0 .. T*d) and sets ws.nseg / meta[0] for the down kernel.  With
 // form.rms_eps > 0 (LoPA) z is normalised first: inside the single-token gate kernel,
 // else by launch_rms_norm.
+// lopa_a (only where lopa_fuses_z holds): the gate kernel computes z = A x itself.
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x,
-                          const void* gate_w, const void* w_up, float t, Workspace& ws, float* y, hipStream_t s);
+                          const void* gate_w, const void* w_up, float t, Workspace& ws, float* y, hipStream_t s,
+                          const void* lopa_a = nullptr);
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
-                       hipStream_t s);
+                       hipStream_t s, bool clear_zslots = false);
+// The single-token LoPA gate kernel computes z = A x itself (no z kernel before it; the down
+// kernel then clears ws.zslot): fp32 / bf16 rows of the single-token kernels, r <= kFusedZMax.
+bool lopa_fuses_z(const Shape& sh, const Form& form);
 
 // Matrix-core path for batches of 2..64 tokens with bf16 weights (ffn_batched.hip):
 // the whole call (LoPA z, gate + union + W_up, down), clearing y first.

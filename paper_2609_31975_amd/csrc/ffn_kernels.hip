@@ -330,11 +330,13 @@ __device__ __forceinline__ void load_pass(const Buf& mb, int C, int q, int lpr, 
 struct NoStage {
   __device__ void operator()() const {}
 };
-template <class W, int CPL, int LATE = 0, bool Q, class RowOf, class Sink, class Stage = NoStage>
+// `pre` runs before the first pass's row loads (loads it issues are ahead of them in the
+// in-order load counter, so that `stage` can wait for them without waiting for the rows).
+template <class W, int CPL, int LATE = 0, bool Q, class RowOf, class Sink, class Stage = NoStage, class Pre = NoStage>
 __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t bytes, int C, int lpr, int lpr_log2,
                                          int n, LaneVec<W, CPL, Q>& v, RowOf row_of, Sink sink,
                                          const float* __restrict__ vec = nullptr, const float4* lds_vec = nullptr,
-                                         Stage stage = Stage{}) {
+                                         Stage stage = Stage{}, Pre pre = Pre{}) {
   static_assert(!(LATE && Q), "a late vector is an fp32 one");
   constexpr int kWaves = kBlock / kWave;
   const Buf mb = make_buf(mat, bytes);
@@ -354,7 +356,13 @@ __device__ __forceinline__ void dot_rows(const uint4* __restrict__ mat, uint32_t
     if (q == 0 && k < n) sink(k, sum);
   };
   uint4 b0[CPL], b1[CPL];
+  constexpr bool kPre = !__is_same(Pre, NoStage);
+  if constexpr (kPre) {
+    pre();
+    issue_barrier();
+  }
   load(b0, wave);  // a wave without passes loads nothing (out-of-range offsets)
+  if constexpr (kPre) issue_barrier();
   stage();
   if constexpr (LATE == 1) {
     issue_barrier();
@@ -636,7 +644,16 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_row(const float* __restrict__
 // DENSE: every neuron of the segment is selected (act = max(h - t, 0)).
 // FORM (a FormKind): the paper's full form (`form`): the activation value, SiLU on the
 // W_up output and, with kFormLoPA, the fixed term G and RMSNorm of z.
-template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU, int FORM>
+// CPLA > 0 (LoPA, fp32 / bf16 rows): z = A x is computed inside this kernel instead of by a
+// kernel before it.  Workgroup w computes the z components of range w of Split(r, nseg) (the
+// first r workgroups one each when r <= nseg), CPLA chunks of an A row (and of x) a thread,
+// and publishes each with one 64-bit store, the value and kZTag together; it then reads all
+// r components back, each with one 64-bit load, until every tag is there.  The loads of the
+// A rows go out first, then the workgroup's B rows, so that the rows stream while z is formed
+// and handed over, and the wait for z covers only the A rows.  The down kernel of the call
+// clears the tags.  A workgroup that has not seen every component after kZWaitTicks computes
+// the missing ones itself, so the kernel finishes whatever the residency of its workgroups.
+template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU, int FORM, int CPLA = 0>
 __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__ x, const float* __restrict__ z,
                                                        const uint4* __restrict__ gate_w, int Cg, int lprg,
                                                        int lprg_log2, const uint4* __restrict__ w_up, int Cu,
@@ -646,8 +663,11 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
                                                        float* __restrict__ seg_zval, float* __restrict__ y, int d,
                                                        Form form, const float* __restrict__ zsq,
                                                        const float* __restrict__ gx, const float* __restrict__ s_g,
-                                                       const float* __restrict__ s_up) {
+                                                       const float* __restrict__ s_up, const uint4* __restrict__ A,
+                                                       uint64_t* __restrict__ zslot) {
   constexpr bool FULL = FORM != kFormDefault, EXTRA = LOPA && FORM == kFormLoPA;
+  constexpr bool FZ = LOPA && CPLA > 0;
+  static_assert(!FZ || (!is_quant<W>() && CPLG <= 8), "z is computed in the gate kernel for fp32 / bf16 rows");
   __shared__ float s_h[kSegMax];
   __shared__ float s_ss[kBlock / kWave];
   __shared__ int s_list[kSegMax];
@@ -706,18 +726,21 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
       }
     }
     // LoPA's fixed term (G x)_i of this thread's row (written by the z kernel's extra
-    // workgroups) and the squares of z for RMSNorm: loaded before the gate stream, used
-    // after it, branch-free so that nothing waits for them in front of the stream
+    // workgroups, or gathered here when z is computed here) and the squares of z for RMSNorm:
+    // loaded before the gate stream, used after it, branch-free so that nothing waits for
+    // them in front of the stream
     const bool has_g = EXTRA && form.g_idx;
-    const uint32_t gbits =
-        EXTRA ? ldb32(make_buf(gx, 4u * (uint32_t)d_ff), has_g && (int)threadIdx.x < nrows
-                                                               ? 4u * (uint32_t)(row0 + (int)threadIdx.x)
-                                                               : kOOB)
-              : 0u;
+    const bool own_row = (int)threadIdx.x < nrows;
+    uint32_t gbits = 0u;
+    GEntry gent{0u, 0.f};
+    if constexpr (EXTRA && !FZ)
+      gbits = ldb32(make_buf(gx, 4u * (uint32_t)d_ff), has_g && own_row ? 4u * (uint32_t)(row0 + (int)threadIdx.x)
+                                                                        : kOOB);
+    if constexpr (EXTRA && FZ) gent = g_fetch(form, d_ff, has_g && own_row ? row0 + (int)threadIdx.x : -1);
     const bool norm = EXTRA && form.rms_eps > 0.f;
     const int r = Cg * W::EPC;
-    uint32_t sq[EXTRA ? kNormRegs : 1] = {};
-    if constexpr (EXTRA) {
+    uint32_t sq[EXTRA && !FZ ? kNormRegs : 1] = {};
+    if constexpr (EXTRA && !FZ) {
       const Buf qb = make_buf(zsq, 4u * (uint32_t)r);
 #pragma unroll
       for (int j = 0; j < kNormRegs; ++j) {
@@ -725,6 +748,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
         sq[j] = ldb32(qb, norm && k < r ? 4u * (uint32_t)k : kOOB);
       }
     }
+    float inv = 1.f;  // RMSNorm's 1 / sqrt(mean z^2 + eps) (fused z: found while z is staged)
     {
       LaneVec<W, CPLG> zr;  // limbs: the B stream gives a lane several rows
       // fp32 z: loaded once per workgroup (each thread a share) ahead of the B rows and
@@ -734,34 +758,200 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
         constexpr int ZF4 = W::EPC / 4, kZF4 = CPLG * kWave * ZF4, kZPT = kZF4 / kBlock;
         static_assert(kZPT * kBlock == kZF4, "z shares");
         __shared__ float4 s_zs[kZF4];
-        float4 zs[kZPT];
-        const int nf4 = Cg * ZF4;
-        const Buf zb = make_buf(z, 16u * (uint32_t)nf4);
+        if constexpr (FZ) {
+          // z = A x here (see above the kernel).  Components of this workgroup: [zk0, zk0 + nz)
+          constexpr int ZR = 2, AF4 = W::EPC / 4, kZC = kFusedZMax / kBlock;
+          const int Ca = d / W::EPC;
+          const Split zsp(r, nseg);
+          const int zk0 = zsp.start(seg), nz = zsp.start(seg + 1) - zk0;
+          const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)Ca);
+          uint4 ar[ZR][CPLA];
+          LaneVec<W, CPLA, false> xa;
+          auto load_a = [&](int zb) {
 #pragma unroll
-        for (int k = 0; k < kZPT; ++k) {
-          const int j = (int)threadIdx.x + k * kBlock;
-          zs[k] = __builtin_bit_cast(float4, ldb(zb, j < nf4 ? 16u * (uint32_t)j : kOOB));
+            for (int zr_ = 0; zr_ < ZR; ++zr_)
+#pragma unroll
+              for (int c = 0; c < CPLA; ++c) {
+                const int ch = (int)threadIdx.x + c * kBlock;
+                ar[zr_][c] = ldb_nt(ab, zb + zr_ < nz && ch < Ca ? 16u * ((uint32_t)(zk0 + zb + zr_) * (uint32_t)Ca +
+                                                                          (uint32_t)ch)
+                                                                 : kOOB);
+              }
+          };
+          __shared__ float s_zp[ZR][kBlock / kWave];
+          float* const s_zf = reinterpret_cast<float*>(s_zs);
+          // components zb .. zb + ZR - 1 of the workgroup, their A rows loaded: partial sums of the
+          // thread's chunks, the 64 lanes, then the four waves in order, as the z kernel adds
+          // them; each goes out with one 64-bit store, its tag in the high word
+          auto publish = [&](int zb) {
+            const int wave = threadIdx.x / kWave;
+            float part[ZR];
+#pragma unroll
+            for (int zr_ = 0; zr_ < ZR; ++zr_) part[zr_] = wave_sum_uniform(lane_dot<W, CPLA, false>(ar[zr_], xa));
+            if (lane_id() == 0)
+#pragma unroll
+              for (int zr_ = 0; zr_ < ZR; ++zr_) s_zp[zr_][wave] = part[zr_];
+            __syncthreads();
+            if ((int)threadIdx.x < min(ZR, nz - zb)) {
+              const float s = ((s_zp[threadIdx.x][0] + s_zp[threadIdx.x][1]) + s_zp[threadIdx.x][2]) +
+                              s_zp[threadIdx.x][3];
+              const uint64_t word = ((uint64_t)kZTag << 32) | (uint64_t)__float_as_uint(s);
+              __hip_atomic_store(zslot + zk0 + zb + threadIdx.x, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            __syncthreads();
+          };
+          // A workgroup that computes components does so before it requests its B rows: its A
+          // rows then share the memory system with the other workgroups' B rows only, and z is
+          // out about a round trip after the kernel starts (measured: with the B rows requested
+          // first, the last component went out 6.5 us into the kernel and z was complete
+          // everywhere at 9 us)
+          auto pre = [&] {
+            load_a(0);
+            const Buf xb = make_buf(x, 16u * AF4 * (uint32_t)Ca);
+#pragma unroll
+            for (int c = 0; c < CPLA; ++c) {
+              const int ch = (int)threadIdx.x + c * kBlock;
+#pragma unroll
+              for (int e4 = 0; e4 < AF4; ++e4) {
+                const float4 f = __builtin_bit_cast(
+                    float4, ldb(xb, nz > 0 && ch < Ca ? 16u * (uint32_t)(ch * AF4 + e4) : kOOB));
+                xa.f[c][4 * e4 + 0] = f.x;
+                xa.f[c][4 * e4 + 1] = f.y;
+                xa.f[c][4 * e4 + 2] = f.z;
+                xa.f[c][4 * e4 + 3] = f.w;
+              }
+            }
+            if (nz > 0) publish(0);  // workgroup-uniform
+          };
+          auto stage = [&] {
+            const int wave = threadIdx.x / kWave;
+            if constexpr (EXTRA) gbits = g_gather_bits(gent, x, d, has_g && own_row);
+            // 1) components past the first ZR (r > ZR nseg): after the B rows
+            for (int zb = ZR; zb < nz; zb += ZR) {  // workgroup-uniform
+              load_a(zb);
+              publish(zb);
+            }
+            // 2) every component, through its tag: thread i holds components i, i + 256, ...
+            float zv[kZC];
+            bool have[kZC];
+#pragma unroll
+            for (int i = 0; i < kZC; ++i) {
+              zv[i] = 0.f;
+              have[i] = (int)threadIdx.x + i * kBlock >= r;
+            }
+            const uint64_t t0 = wall_clock64();
+            bool late = false;
+            for (;;) {
+              bool all = true;
+#pragma unroll
+              for (int i = 0; i < kZC; ++i) {
+                if (!have[i]) {
+                  const uint64_t v = __hip_atomic_load(zslot + threadIdx.x + i * kBlock, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                  if ((uint32_t)(v >> 32) == kZTag) {
+                    have[i] = true;
+                    zv[i] = __uint_as_float((uint32_t)v);
+                  } else {
+                    all = false;
+                  }
+                }
+              }
+              if (__syncthreads_and(all)) break;
+              if (__syncthreads_or(wall_clock64() - t0 > kZWaitTicks)) {
+                late = true;
+                break;
+              }
+              __builtin_amdgcn_s_sleep(2);
+            }
+            // 3) into LDS (zeros past r, which the lanes' last chunks may read); a component
+            // still missing is marked with the tag pattern and computed here, a wave a row
+#pragma unroll
+            for (int i = 0; i < kZF4 * 4 / kBlock; ++i) {
+              const int j = (int)threadIdx.x + i * kBlock;
+              s_zf[j] = i < kZC && j < r ? (have[i] ? zv[i] : __uint_as_float(kZTag)) : 0.f;
+            }
+            __syncthreads();
+            if (late) {  // workgroup-uniform
+              const Buf xb = make_buf(x, 16u * AF4 * (uint32_t)Ca);
+              for (int k = wave; k < r; k += kBlock / kWave) {
+                if (__float_as_uint(s_zf[k]) != kZTag) continue;  // wave-uniform (one LDS word)
+                float s = 0.f;
+                for (int ch = lane_id(); ch < Ca; ch += kWave) {
+                  float f[W::EPC];
+                  unpack(W{}, ldb(ab, 16u * ((uint32_t)k * (uint32_t)Ca + (uint32_t)ch)), f);
+#pragma unroll
+                  for (int e4 = 0; e4 < AF4; ++e4) {
+                    const float4 xv = __builtin_bit_cast(float4, ldb(xb, 16u * (uint32_t)(ch * AF4 + e4)));
+                    s = fmaf(f[4 * e4], xv.x, fmaf(f[4 * e4 + 1], xv.y, fmaf(f[4 * e4 + 2], xv.z,
+                                                                              fmaf(f[4 * e4 + 3], xv.w, s))));
+                  }
+                }
+                s = wave_sum(s);
+                if (lane_id() == 0) s_zf[k] = s;
+              }
+              __syncthreads();
+#pragma unroll
+              for (int i = 0; i < kZC; ++i)
+                if ((int)threadIdx.x + i * kBlock < r) zv[i] = s_zf[threadIdx.x + i * kBlock];
+              __syncthreads();
+            }
+            // 4) RMSNorm: the scale from every component's square; z goes to LDS times the gains
+            if constexpr (EXTRA) {
+              if (norm) {  // workgroup-uniform
+                float ss = 0.f;
+#pragma unroll
+                for (int i = 0; i < kZC; ++i) ss += zv[i] * zv[i];
+                ss = wave_sum(ss);
+                if (lane_id() == 0) s_ss[wave] = ss;
+                __syncthreads();
+                float tot = 0.f;
+#pragma unroll
+                for (int w = 0; w < kBlock / kWave; ++w) tot += s_ss[w];
+                inv = 1.f / sqrtf(tot / (float)r + form.rms_eps);
+                if (form.rms_gain) {
+#pragma unroll
+                  for (int i = 0; i < kZC; ++i) {
+                    const int j = (int)threadIdx.x + i * kBlock;
+                    if (j < r) s_zf[j] = zv[i] * form.rms_gain[j];
+                  }
+                }
+                __syncthreads();
+              }
+            }
+          };
+          dot_rows<W, CPLG, 2>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
+                               gate_sink, nullptr, s_zs, stage, pre);
+        } else {
+          float4 zs[kZPT];
+          const int nf4 = Cg * ZF4;
+          const Buf zb = make_buf(z, 16u * (uint32_t)nf4);
+#pragma unroll
+          for (int k = 0; k < kZPT; ++k) {
+            const int j = (int)threadIdx.x + k * kBlock;
+            zs[k] = __builtin_bit_cast(float4, ldb(zb, j < nf4 ? 16u * (uint32_t)j : kOOB));
+          }
+          issue_barrier();
+          auto stage = [&] {
+#pragma unroll
+            for (int k = 0; k < kZPT; ++k) s_zs[threadIdx.x + k * kBlock] = zs[k];
+            __syncthreads();
+          };
+          dot_rows<W, CPLG, 2>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr,
+                               gate_row, gate_sink, nullptr, s_zs, stage);
         }
-        issue_barrier();
-        auto stage = [&] {
-#pragma unroll
-          for (int k = 0; k < kZPT; ++k) s_zs[threadIdx.x + k * kBlock] = zs[k];
-          __syncthreads();
-        };
-        dot_rows<W, CPLG, 2>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
-                             gate_sink, nullptr, s_zs, stage);
       } else {
         make_lane_vec<W, CPLG>(z, Cg, lane_id() & (lprg - 1), lprg, zr);
         dot_rows<W, CPLG>(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg, Cg, lprg, lprg_log2, nrows, zr, gate_row,
                           gate_sink);
       }
     }
-    const float gv = __builtin_bit_cast(float, gbits);
+    // G x: the z kernel's extra workgroups stored g_sign x[g_idx]; gathered here, the sign
+    // is applied now
+    const float gv = FZ ? g_value(gent, gbits) : __builtin_bit_cast(float, gbits);
     __syncthreads();
     apply_scales();
     if constexpr (EXTRA) {
-      float inv = 1.f;
-      if (norm) {  // 1 / sqrt(mean z^2 + eps)
+      if (norm && !FZ) {  // 1 / sqrt(mean z^2 + eps)
         float ss = 0.f;
 #pragma unroll
         for (int j = 0; j < kNormRegs; ++j) ss += __builtin_bit_cast(float, sq[j]);
@@ -838,13 +1028,22 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
 // guarantees w_down_t < 2^31 bytes.
 constexpr int kDownSlotsPerThread = 4, kDownSlots = kDownSlotsPerThread * kBlock;
 
+// The z slots of a single-token LoPA call whose gate kernel computed z: their tags go back to
+// zero for the next call (the gate kernel, which read them, has finished).
+__device__ __forceinline__ void clear_zslots(uint64_t* zslot, int n) {
+  if (blockIdx.x == 0)
+    for (int j = threadIdx.x; j < n; j += kBlock) zslot[j] = 0;
+}
+
 template <class W, bool DENSE, int LG>
 __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ seg_count,
                                                     const int32_t* __restrict__ seg_idx,
                                                     const float* __restrict__ seg_zval, int nseg, int d_ff, int R,
                                                     const uint4* __restrict__ w_down_t, int C, int d,
-                                                    float* __restrict__ y, const float* __restrict__ s_down) {
+                                                    float* __restrict__ y, const float* __restrict__ s_down,
+                                                    uint64_t* __restrict__ zslot, int nzclear) {
   constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave, RG = kWave / LG, PT = kDownSlotsPerThread;
+  clear_zslots(zslot, nzclear);
   extern __shared__ int s_dyn[];  // the compacted list (sparse only): indices, then values
   __shared__ int s_cnt[kWave];
   __shared__ int s_off[kWave + 1];
@@ -1366,8 +1565,10 @@ __global__ __launch_bounds__(kBlock) void k_down_generic(const int32_t* __restri
                                                          const int32_t* __restrict__ seg_idx,
                                                          const float* __restrict__ seg_zval, int nseg, int d_ff,
                                                          int slots, const void* __restrict__ w_down_t, int T, int d,
-                                                         float* __restrict__ y, const float* __restrict__ s_down) {
+                                                         float* __restrict__ y, const float* __restrict__ s_down,
+                                                         uint64_t* __restrict__ zslot, int nzclear) {
   extern __shared__ int s_pre[];  // [nseg + 1] list offsets (sparse only)
+  clear_zslots(zslot, nzclear);
   __shared__ int s_slot[kListWindow];
   const int col = blockIdx.x * kBlock + threadIdx.x;
   const bool cvalid = col < d;
@@ -1493,27 +1694,49 @@ bool fast_ok(const Shape& sh, Gate g) {
   return true;
 }
 
-template <class W, bool LOPA, bool DENSE, int FORM, int CPLG, int CPLU>
+template <class W, bool LOPA, bool DENSE, int FORM, int CPLG, int CPLU, int CPLA = 0>
 hipError_t go_gate_up_t1(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up,
-                         float t, Workspace& ws, float* y, hipStream_t s) {
+                         float t, Workspace& ws, float* y, hipStream_t s, const void* lopa_a = nullptr) {
   const int Cu = sh.d / W::EPC, Cg = LOPA ? sh.r / W::EPC : Cu;
   const int lpru = lanes_per_row(Cu, CPLU), lprg = lanes_per_row(Cg, CPLG);
-  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU, FORM>;
+  auto kernel = k_gate_up_t1<W, LOPA, DENSE, CPLG, CPLU, FORM, CPLA>;
   static int per_cu = 0;  // one cache per instantiation
   ws.nseg = resident_segments(kernel, &per_cu, sh.d_ff);
   return launch_gate_kernel(kernel, ws.nseg, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg, lprg,
                             ilog2(lprg), static_cast<const uint4*>(w_up), Cu, lpru, ilog2(lpru), sh.d_ff, ws.nseg, t,
                             ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.seg_zval, y, sh.d, form,
-                            (const float*)ws.zsq, (const float*)ws.gx, LOPA ? sh.sc.b : sh.sc.gate, sh.sc.up);
+                            (const float*)ws.zsq, (const float*)ws.gx, LOPA ? sh.sc.b : sh.sc.gate, sh.sc.up,
+                            static_cast<const uint4*>(lopa_a), ws.zslot);
+}
+
+// Whether the single-token LoPA gate kernel computes z itself: fp32 / bf16 rows whose B rows
+// take at most the lower chunk count a lane (z staged in LDS), and r within kFusedZMax.
+template <class W>
+bool fuses_z(const Shape& sh) {
+  if constexpr (is_quant<W>()) {
+    return false;
+  } else {
+    return sh.T == 1 && sh.r >= 1 && sh.r <= kFusedZMax && fast_ok(sh, Gate::LoPA) &&
+           cpl_pick(sh.r / W::EPC, cpl_lo<W>()) == cpl_lo<W>();
+  }
 }
 
 template <class W, bool LOPA, bool DENSE, int FORM>
 hipError_t gate_up_fast(const Shape& sh, const Form& f, const float* x, const void* gate_w, const void* w_up, float t,
-                        Workspace& ws, float* y, hipStream_t s) {
+                        Workspace& ws, float* y, hipStream_t s, const void* lopa_a) {
   constexpr int L = cpl_lo<W>(), H = 2 * L;
   const int cplu = cpl_pick(sh.d / W::EPC, L);
   if constexpr (LOPA) {
     const int cplg = cpl_pick(sh.r / W::EPC, L);
+    if constexpr (!is_quant<W>()) {
+      // z computed in the gate kernel: an A row's chunks spread over the 256 threads, 2 a
+      // thread while the row fits (rows of up to 512 chunks), else 4
+      if (lopa_a && fuses_z<W>(sh)) {
+        if (cplu == L)
+          return go_gate_up_t1<W, true, DENSE, FORM, L, L, 2>(sh, f, x, gate_w, w_up, t, ws, y, s, lopa_a);
+        return go_gate_up_t1<W, true, DENSE, FORM, L, H, 4>(sh, f, x, gate_w, w_up, t, ws, y, s, lopa_a);
+      }
+    }
     if (cplg == L && cplu == L) return go_gate_up_t1<W, true, DENSE, FORM, L, L>(sh, f, x, gate_w, w_up, t, ws, y, s);
     if (cplg == L && cplu == H) return go_gate_up_t1<W, true, DENSE, FORM, L, H>(sh, f, x, gate_w, w_up, t, ws, y, s);
     if (cplg == H && cplu == L) return go_gate_up_t1<W, true, DENSE, FORM, H, L>(sh, f, x, gate_w, w_up, t, ws, y, s);
@@ -1651,7 +1874,7 @@ void down_grid(int C, int lg, int wg_per_cu, int nseg, int d_ff, int* S, int* R,
 }
 
 template <class W, bool DENSE>
-hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s) {
+hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, float* y, hipStream_t s, int nzclear) {
   // lanes a row and workgroups per CU, as measured best on the 8B shape: a bf16 slice of
   // 512 columns at two workgroups per CU; int8 / int4 slices of 256 / 512 columns at one
   constexpr int LG = is_quant<W>() ? 16 : 32, WG_PER_CU = is_quant<W>() ? 1 : 2;
@@ -1666,7 +1889,7 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
   if (rows_ok && sh.T == 1 && shmem_t1 <= 96 * 1024) {
     k_down_t1<W, DENSE, LG><<<S * R, kBlock, shmem_t1, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
                                                              R, static_cast<const uint4*>(w_down_t), C, sh.d, y,
-                                                             sh.sc.down);
+                                                             sh.sc.down, ws.zslot, nzclear);
   } else if (rows_ok && sh.T > 1 && shmem_tb <= 96 * 1024 && (int64_t)sh.T * ws.slots < (int64_t(1) << 29)) {
     const dim3 grid(S * R, (sh.T + TG - 1) / TG);
     k_down_tb<W, DENSE, LG, TG><<<grid, kBlock, shmem_tb, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg,
@@ -1677,7 +1900,8 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
     const size_t shmem = DENSE ? 0 : sizeof(int) * (size_t)(ws.nseg + 1);
     const int grid = (sh.d + kBlock - 1) / kBlock;
     k_down_generic<W, DENSE><<<grid, kBlock, shmem, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
-                                                        ws.slots, w_down_t, sh.T, sh.d, y, sh.sc.down);
+                                                        ws.slots, w_down_t, sh.T, sh.d, y, sh.sc.down, ws.zslot,
+                                                        nzclear);
   }
   return hipGetLastError();
 }
@@ -1686,14 +1910,15 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
 // flag of the element-wise one (G and the norm need LoPA; the options check enforces it)
 template <class W, bool LOPA, bool DENSE>
 hipError_t gate_up_form(const Shape& sh, bool fast, const Form& f, const float* x, const void* gate_w,
-                        const void* w_up, float t, Workspace& ws, float* y, hipStream_t s) {
+                        const void* w_up, float t, Workspace& ws, float* y, hipStream_t s, const void* lopa_a) {
   if (!fast)
     return f.full() ? gate_up_generic<W, LOPA, DENSE, true>(sh, f, x, gate_w, w_up, t, ws, y, s)
                     : gate_up_generic<W, LOPA, DENSE, false>(sh, f, x, gate_w, w_up, t, ws, y, s);
   if constexpr (LOPA)
-    if (f.kind() == kFormLoPA) return gate_up_fast<W, LOPA, DENSE, kFormLoPA>(sh, f, x, gate_w, w_up, t, ws, y, s);
-  return f.full() ? gate_up_fast<W, LOPA, DENSE, kFormAct>(sh, f, x, gate_w, w_up, t, ws, y, s)
-                  : gate_up_fast<W, LOPA, DENSE, kFormDefault>(sh, f, x, gate_w, w_up, t, ws, y, s);
+    if (f.kind() == kFormLoPA)
+      return gate_up_fast<W, LOPA, DENSE, kFormLoPA>(sh, f, x, gate_w, w_up, t, ws, y, s, lopa_a);
+  return f.full() ? gate_up_fast<W, LOPA, DENSE, kFormAct>(sh, f, x, gate_w, w_up, t, ws, y, s, lopa_a)
+                  : gate_up_fast<W, LOPA, DENSE, kFormDefault>(sh, f, x, gate_w, w_up, t, ws, y, s, lopa_a);
 }
 
 }  // namespace
@@ -1720,8 +1945,13 @@ hipError_t launch_lopa_z(const Shape& sh, const Form& form, const float* x, cons
   return by_format(sh.wdt, [&](auto w) { return lopa_z<decltype(w)>(sh, form, x, lopa_a, ws, s); });
 }
 
+bool lopa_fuses_z(const Shape& sh, const Form&) {
+  return by_format(sh.wdt, [&](auto w) { return fuses_z<decltype(w)>(sh) ? hipSuccess : hipErrorNotSupported; }) ==
+         hipSuccess;
+}
+
 hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form, const float* x, const void* gate_w,
-                          const void* w_up, float t, Workspace& ws, float* y, hipStream_t s) {
+                          const void* w_up, float t, Workspace& ws, float* y, hipStream_t s, const void* lopa_a) {
   const bool lopa = g == Gate::LoPA;
   const bool fast = fast_ok(sh, g);
   if (lopa && !fast && form.rms_eps > 0.f) {  // the single-token kernel normalises z itself
@@ -1730,18 +1960,19 @@ hipError_t launch_gate_up(const Shape& sh, Gate g, bool dense, const Form& form,
   }
   return by_format(sh.wdt, [&](auto w) {
     using W = decltype(w);
-    if (lopa) return dense ? gate_up_form<W, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
-                           : gate_up_form<W, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
-    return dense ? gate_up_form<W, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s)
-                 : gate_up_form<W, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s);
+    if (lopa) return dense ? gate_up_form<W, true, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s, lopa_a)
+                           : gate_up_form<W, true, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s, lopa_a);
+    return dense ? gate_up_form<W, false, true>(sh, fast, form, x, gate_w, w_up, t, ws, y, s, nullptr)
+                 : gate_up_form<W, false, false>(sh, fast, form, x, gate_w, w_up, t, ws, y, s, nullptr);
   });
 }
 
 hipError_t launch_down(const Shape& sh, bool dense, const void* w_down_t, const Workspace& ws, float* y,
-                       hipStream_t s) {
+                       hipStream_t s, bool clear_zslots) {
+  const int nz = clear_zslots ? sh.r : 0;
   return by_format(sh.wdt, [&](auto w) {
     using W = decltype(w);
-    return dense ? down<W, true>(sh, w_down_t, ws, y, s) : down<W, false>(sh, w_down_t, ws, y, s);
+    return dense ? down<W, true>(sh, w_down_t, ws, y, s, nz) : down<W, false>(sh, w_down_t, ws, y, s, nz);
   });
 }
 

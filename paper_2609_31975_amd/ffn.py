@@ -158,11 +158,12 @@ def workspace_bytes(T: int, d: int, d_ff: int, r: int = 0) -> int:
 
 
 def alloc_workspace(T: int, d: int, d_ff: int, r: int = 0, device="cuda"):
+    """A zero-filled workspace (the header asks for zeros before the first call)."""
     torch = _torch()
     n = workspace_bytes(T, d, d_ff, r)
     if n == 0:
         raise FFNError("ffn_workspace_bytes", -2)
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    return torch.zeros(n, dtype=torch.uint8, device=device)
 
 
 def options(act=FFN_ACT_RELU, silu_up=False, g_idx=None, g_sign=None, rms_norm=False, rms_gain=None,
