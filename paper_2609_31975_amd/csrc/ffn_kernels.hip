@@ -1026,7 +1026,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
 // every LDS read of the list is unconditional, so that the loads of a round issue back to
 // back: with predicated loads each one sat behind its own branch and LDS wait.  The host
 // guarantees w_down_t < 2^31 bytes.
-constexpr int kDownSlotsPerThread = 4, kDownSlots = kDownSlotsPerThread * kBlock;
+constexpr int kDownSlotsPerThread = 8, kDownSlots = kDownSlotsPerThread * kBlock;
 
 // The z slots of a single-token LoPA call whose gate kernel computed z: their tags go back to
 // zero for the next call (the gate kernel, which read them, has finished).
@@ -1042,7 +1042,7 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
                                                     const uint4* __restrict__ w_down_t, int C, int d,
                                                     float* __restrict__ y, const float* __restrict__ s_down,
                                                     uint64_t* __restrict__ zslot, int nzclear) {
-  constexpr int EPC = W::EPC, U = 16, kWaves = kBlock / kWave, RG = kWave / LG, PT = kDownSlotsPerThread;
+  constexpr int EPC = W::EPC, U = 8, kWaves = kBlock / kWave, RG = kWave / LG, PT = kDownSlotsPerThread;
   clear_zslots(zslot, nzclear);
   extern __shared__ int s_dyn[];  // the compacted list (sparse only): indices, then values
   __shared__ int s_cnt[kWave];
@@ -1125,10 +1125,15 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
   float acc[EPC];
 #pragma unroll
   for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-  // kb: the wave's first row of a round (wave-uniform); its lanes take rows kb + g + ...
-  for (int kb = wave * RG; kb < n; kb += kWaves * RG * U) {
+  // A round: U slots of each of the wave's row groups, rows kb + g + u kWaves RG (kb the
+  // wave's first row, wave-uniform).  Two register sets alternate, so that the next round's
+  // rows are in flight while a round is folded (a chunk of more rows than one round had
+  // waited a whole round trip per round).  Rows past n load nothing and fold nothing.
+  struct Round {
     uint4 wv[U];
     float zz[U], sc[U];
+  };
+  auto issue = [&](Round& rd, int kb) {
     int row[U];
     bool ok[U];
 #pragma unroll
@@ -1140,37 +1145,58 @@ __global__ __launch_bounds__(kBlock) void k_down_t1(const int32_t* __restrict__ 
       } else {
         const int j = ok[u] ? kk : 0;  // n >= 1 here
         row[u] = l_idx[j];
-        zz[u] = ok[u] ? l_z[j] : 0.f;
+        rd.zz[u] = ok[u] ? l_z[j] : 0.f;
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if constexpr (DENSE) zz[u] = __int_as_float(ldb32(zb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
+      if constexpr (DENSE) rd.zz[u] = __int_as_float(ldb32(zb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
       // a zero gated value (the s_gated site) needs no W_down row
-      const bool need = ok[u] && cvalid && (DENSE || zz[u] != 0.f);
-      wv[u] = ldb_nt(wb, need ? 16u * ((uint32_t)row[u] * (uint32_t)C + (uint32_t)ch) : kOOB);
+      const bool need = ok[u] && cvalid && (DENSE || rd.zz[u] != 0.f);
+      rd.wv[u] = ldb_nt(wb, need ? 16u * ((uint32_t)row[u] * (uint32_t)C + (uint32_t)ch) : kOOB);
       if constexpr (is_quant<W>())  // the row's scale (0 for an unused slot)
-        sc[u] = __int_as_float(ldb32(sb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
+        rd.sc[u] = __int_as_float(ldb32(sb, ok[u] ? 4u * (uint32_t)row[u] : kOOB));
     }
-    issue_barrier();
-    auto fold = [&](int u) {
-      float f[EPC];
-      unpack(W{}, wv[u], f);
-      const float z = is_quant<W>() ? zz[u] * sc[u] : zz[u];
+  };
+  auto fold = [&](const Round& rd, int u) {
+    float f[EPC];
+    unpack(W{}, rd.wv[u], f);
+    const float z = is_quant<W>() ? rd.zz[u] * rd.sc[u] : rd.zz[u];
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) acc[e] = fmaf(z, f[e], acc[e]);
-    };
-    // A full round folds every slot.  The last round stops at the wave's last row (a
-    // wave-uniform test): unpacking the empty slots costs up to 96 ALU ops a slot.  Both
-    // branches use every load, so none of them is sunk behind a test.
+    for (int e = 0; e < EPC; ++e) acc[e] = fmaf(z, f[e], acc[e]);
+  };
+  // A full round folds every slot.  A round with the wave's last row stops there (a
+  // wave-uniform test): unpacking the empty slots costs up to 96 ALU ops a slot.  Both
+  // branches use every load, so none of them is sunk behind a test.
+  auto fold_round = [&](const Round& rd, int kb) {
     if (kb + (U - 1) * kWaves * RG < n) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) fold(u);
+      for (int u = 0; u < U; ++u) fold(rd, u);
     } else {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         if (kb + u * kWaves * RG >= n) break;
-        fold(u);
+        fold(rd, u);
+      }
+    }
+  };
+  constexpr int kStride = kWaves * RG * U;  // rows of one round of the workgroup
+  if (wave * RG < n) {
+    Round r0, r1;
+    int kb = wave * RG;
+    issue(r0, kb);
+    issue_barrier();
+    if (kb + kStride >= n) {
+      fold_round(r0, kb);
+    } else {
+      for (;; kb += 2 * kStride) {
+        issue(r1, kb + kStride);
+        issue_barrier();
+        fold_round(r0, kb);
+        issue(r0, kb + 2 * kStride);
+        issue_barrier();
+        fold_round(r1, kb + kStride);
+        if (kb + 2 * kStride >= n) break;
       }
     }
   }
