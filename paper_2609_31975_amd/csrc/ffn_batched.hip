@@ -341,31 +341,38 @@ __global__ __launch_bounds__(kBlock) void k_split_tokens(const float* __restrict
 }
 
 // ------------------------------------------------------------------ LoPA z = A x
-// Workgroup b: 16-row tile b / kZParts of A over half b % kZParts of the d range, each
-// of its waves a sixteenth of that half.  The waves' sums are added in LDS (fixed order)
-// and stored as partial copy b % kZParts of z: zp[part][tc][r]; the gate kernel adds
-// the two copies.
+// Workgroup b: 16-row tile of A over one half (kZParts) of the d range, each of its waves a
+// sixteenth of that half, for NT token tiles; with pre-split tokens each group of NT token
+// tiles has workgroups of its own (at 64 tokens, r = 512: 256 workgroups instead of 64 that
+// each read every token's fragments).  The waves' sums are added in LDS (fixed order) and
+// stored as partial copy `part` of z: zp[part][tc][r]; the gate kernel adds the two copies.
 constexpr int kZWaves = 16;
 constexpr int kZParts = 2;
 
-template <int NT, class W>
+template <int NT, bool PRE, class W>
 __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __restrict__ x,
                                                                  const uint4* __restrict__ xs, int ntt,
                                                                  const uint4* __restrict__ A, int C, int T, int r,
                                                                  int tc, float* __restrict__ zp, GWork gw,
                                                                  const float* __restrict__ s_a) {
   if (g_precompute(gw)) return;
-  constexpr bool PRE = NT > 1;  // tokens pre-split by k_split_tokens
   __shared__ f32x4_t s_part[kZWaves][NT][kWave];
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
-  const int tile = blockIdx.x / kZParts, part = blockIdx.x % kZParts;
+  // blockIdx.x = (tile kZParts + part) ngrp + tg: tg the group of NT token tiles
+  const int ngrp = PRE ? ntt / NT : 1;
+  const int tg = (int)blockIdx.x % ngrp, tp = (int)blockIdx.x / ngrp;
+  const int tile = tp / kZParts, part = tp % kZParts;
   constexpr int KU = NT == 1 ? 4 : NT == 2 ? 2 : 1;
   using S = WStage<1, KU, W>;
   __shared__ uint4 s_stage[kZWaves][S::WORDS];
   int roff[S::NI];
   stage_rows<1, KU, W>(roff, C, [&](int br) { return tile * 16 + br < r ? tile * 16 + br : -1; });
   const Buf ab = make_buf(A, 16u * (uint32_t)r * (uint32_t)(C / S::R8));
-  const TokSrc tok = token_source(PRE, x, xs, C, T, ntt);
+  TokSrc tok = token_source(PRE, x, xs, C, T, ntt);
+  if constexpr (PRE) {  // the group's first token tile at entry 0 of each k step's row of tiles
+    const uint32_t skip = 16u * (uint32_t)(tg * NT * kWave);
+    tok.b = make_buf(xs + (size_t)tg * NT * kWave, 2 * tok.part - skip);
+  }
   f32x4_t acc[1][NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[0][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -375,14 +382,16 @@ __global__ __launch_bounds__(kZWaves * kWave) void k_lopa_z_mfma(const float* __
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) s_part[wave][nt][lane] = acc[0][nt];
   __syncthreads();
-  // thread o: token o / 16, row tile * 16 + o % 16 (16 consecutive floats of z a token);
-  // that value sits in lane 16 (kk / 4) + tok % 16, element kk % 4, of token tile tok / 16
+  // thread o: local token o / 16 of the group, row tile * 16 + o % 16 (16 consecutive floats
+  // of z a token); that value sits in lane 16 (kk / 4) + tl % 16, element kk % 4, of the
+  // group's token tile tl / 16
   const float* sp = reinterpret_cast<const float*>(s_part);
-  for (int o = threadIdx.x; o < T * 16; o += kZWaves * kWave) {
-    const int tok = o >> 4, kk = o & 15;
+  const int tok0 = 16 * NT * tg;
+  for (int o = threadIdx.x; o < 16 * NT * 16; o += kZWaves * kWave) {
+    const int tl = o >> 4, kk = o & 15, tok = tok0 + tl;
     const int k = tile * 16 + kk;
-    if (k >= r) continue;
-    const int nt = tok >> 4, src = ((16 * (kk >> 2) + (tok & 15)) << 2) + (kk & 3);
+    if (k >= r || tok >= T) continue;
+    const int nt = tl >> 4, src = ((16 * (kk >> 2) + (tl & 15)) << 2) + (kk & 3);
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < kZWaves; ++w) s += sp[(w * NT + nt) * kWave * 4 + src];
@@ -923,14 +932,14 @@ hipError_t split_tokens(const Shape& sh, const float* x, const Workspace& ws, hi
   k_split_tokens<<<(n + kBlock - 1) / kBlock, kBlock, 0, s>>>(x, C, sh.T, nks, ntt, ws.xs);
   return hipGetLastError();
 }
-template <class W, int NT>
+template <class W, int NT, bool PRE>
 hipError_t z_mfma(const Shape& sh, const Form& form, const float* x, const void* lopa_a, const Workspace& ws,
                   hipStream_t s) {
-  const int C = sh.d / 8, grid = ((sh.r + 15) / 16) * kZParts;
+  const int C = sh.d / 8, ngrp = PRE ? token_tiles(ws) / NT : 1, grid = ((sh.r + 15) / 16) * kZParts * ngrp;
   // with G, extra workgroups write G x for the gate kernel
   const GWork gw{form, x, ws.gx, sh.T, sh.d, sh.d_ff, grid};
   const int g = grid + (form.g_idx ? (g_items(sh.d_ff, sh.T) + kZWaves * kWave - 1) / (kZWaves * kWave) : 0);
-  k_lopa_z_mfma<NT, W><<<g, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a),
+  k_lopa_z_mfma<NT, PRE, W><<<g, kZWaves * kWave, 0, s>>>(x, ws.xs, token_tiles(ws), static_cast<const uint4*>(lopa_a),
                                                       C, sh.T, sh.r, ws.tc, ws.z, gw, sh.sc.a);
   return hipGetLastError();
 }
@@ -1014,8 +1023,8 @@ hipError_t batched_format(const Shape& sh, Gate g, bool dense, const Form& form,
   const bool lopa = g == Gate::LoPA;
   hipError_t e = hipSuccess;
   if (lopa) {
-    e = sh.T <= 16 ? z_mfma<W, 1>(sh, form, x, lopa_a, ws, s)
-                   : sh.T <= 32 ? z_mfma<W, 2>(sh, form, x, lopa_a, ws, s) : z_mfma<W, 4>(sh, form, x, lopa_a, ws, s);
+    // pre-split tokens (more than 16): one token tile a workgroup
+    e = sh.T <= 16 ? z_mfma<W, 1, false>(sh, form, x, lopa_a, ws, s) : z_mfma<W, 1, true>(sh, form, x, lopa_a, ws, s);
     if (e != hipSuccess) return e;
     // RMSNorm between A and B: the two partial copies of z become one normalised copy
     if (form.rms_eps > 0.f &&

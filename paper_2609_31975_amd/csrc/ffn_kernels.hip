@@ -102,11 +102,14 @@ constexpr bool limb_vec() {
 }
 template <class W, int CPL>
 struct LaneVec<W, CPL, true> {
-  static constexpr int WPC = W::EPC / 4;                          // limb words per chunk
+  // int8: three byte limbs of X, four elements a word (limb 0 the signed top byte); int4: six
+  // nibble limbs, eight elements a word, nibble k of a word holding element k as the codes do
+  // (limb 0 the signed top nibble).  Either way four words a limb for a 16-byte chunk of codes.
+  static constexpr int NL = W::LB == 8 ? 3 : 6;                   // limbs
   static constexpr int G = W::LB == 8 ? 4 : 8;                    // elements a thread converts at a time
   static constexpr int GPT = 8192 / G / kBlock;                   // groups a thread converts (up to 8192 elements)
-  uint32_t s2[CPL][WPC], u1[CPL][WPC], u0[CPL][WPC];
-  int32_t ss2, su1, su0;  // sums over the lane's elements
+  uint32_t limb[NL][CPL][4];
+  int32_t lsum[NL];  // sums of each limb's values over the lane's elements
   float scale;
   float4 raw[GPT][G / 4];  // the thread's groups of the vector, until converted
   int C, q, lpr;
@@ -137,8 +140,9 @@ __device__ __forceinline__ void make_lane_vec(const float* __restrict__ v, int C
   }
 }
 
-// The quantized vector's limb words, [3][kLimbWords]: s2, u1, u0 (vectors up to 8192).
-constexpr int kLimbWords = 2048;
+// The quantized vector's limb words: kLimbSpace words, limb l at l * (8192 / G) (vectors up
+// to 8192 elements; 24 KB for either format).
+constexpr int kLimbSpace = 6144;
 
 // Called by every thread of the workgroup at the same point (it has barriers).
 template <class W, int CPL, bool Q>
@@ -146,11 +150,11 @@ __device__ __forceinline__ void prepare_lane_vec(LaneVec<W, CPL, Q>& out) {
   if constexpr (Q) {
     if (out.ready) return;
     out.ready = true;
-    __shared__ uint32_t s_limb[3][kLimbWords];
+    __shared__ uint32_t s_limb[kLimbSpace];
     __shared__ float s_max[2][kBlock / kWave];
     constexpr float kFull = 127.f * 65536.f;
     using LV = LaneVec<W, CPL, Q>;
-    constexpr int G = LV::G, GPT = LV::GPT;
+    constexpr int G = LV::G, GPT = LV::GPT, NL = LV::NL, LW = 8192 / G;  // LW: words a limb
     const int len = out.C * W::EPC, ngroups = len / G;
     // the thread's groups: g = threadIdx.x + i * kBlock (zeros past the vector)
     const auto& vals = out.raw;
@@ -184,50 +188,62 @@ __device__ __forceinline__ void prepare_lane_vec(LaneVec<W, CPL, Q>& out) {
     for (int i = 0; i < GPT; ++i) {
       const int g = (int)threadIdx.x + i * kBlock;
       if (g < ngroups) {
-        const float e[8] = {vals[i][0].x, vals[i][0].y, vals[i][0].z, vals[i][0].w,
-                            vals[i][G / 4 - 1].x, vals[i][G / 4 - 1].y, vals[i][G / 4 - 1].z, vals[i][G / 4 - 1].w};
+        int X[G];
 #pragma unroll
-        for (int wi = 0; wi < G / 4; ++wi) {
-          // int8: the group's 4 elements; int4: its even (wi = 0) or odd (wi = 1) elements
-          int X[4];
+        for (int h = 0; h < G / 4; ++h) {  // |e k| <= kFull (NaN: clamped, the scale is NaN then)
+          const float e[4] = {vals[i][h].x, vals[i][h].y, vals[i][h].z, vals[i][h].w};
 #pragma unroll
-          for (int b = 0; b < 4; ++b)  // |e k| <= kFull (NaN: clamped, the scale is NaN then)
-            X[b] = (int)rintf(fminf(fmaxf(e[G == 4 ? b : 2 * b + wi] * k, -kFull), kFull));
+          for (int b = 0; b < 4; ++b) X[4 * h + b] = (int)rintf(fminf(fmaxf(e[b] * k, -kFull), kFull));
+        }
+        if constexpr (W::LB == 8) {
           // byte j of X0..X3 into one word per j (v_perm_b32: selector bytes 0-3 pick the
           // second operand's bytes, 4-7 the first's, 12 gives zero)
           const uint32_t lo = __builtin_amdgcn_perm((uint32_t)X[1], (uint32_t)X[0], 0x06020400u);  // X0.b0 X1.b0 X0.b2 X1.b2
           const uint32_t hi = __builtin_amdgcn_perm((uint32_t)X[3], (uint32_t)X[2], 0x06020400u);  // X2.b0 X3.b0 X2.b2 X3.b2
           const uint32_t mid = __builtin_amdgcn_perm((uint32_t)X[1], (uint32_t)X[0], 0x0c0c0501u);  // X0.b1 X1.b1 0 0
           const uint32_t mid2 = __builtin_amdgcn_perm((uint32_t)X[3], (uint32_t)X[2], 0x0c0c0501u); // X2.b1 X3.b1 0 0
-          const int word = g * (G / 4) + wi;
-          s_limb[0][word] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);     // byte 2 of X0..X3
-          s_limb[1][word] = __builtin_amdgcn_perm(mid2, mid, 0x05040100u);  // byte 1
-          s_limb[2][word] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);     // byte 0
+          s_limb[0 * LW + g] = __builtin_amdgcn_perm(hi, lo, 0x07060302u);     // byte 2 of X0..X3
+          s_limb[1 * LW + g] = __builtin_amdgcn_perm(mid2, mid, 0x05040100u);  // byte 1
+          s_limb[2 * LW + g] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);     // byte 0
+        } else {
+          // nibble 5 - l of X0..X7 into word l, nibble k of the word from X_k (X fits 24 bits
+          // signed, so its top nibble is the signed limb)
+#pragma unroll
+          for (int l = 0; l < 6; ++l) {
+            uint32_t wd = 0u;
+#pragma unroll
+            for (int b = 0; b < 8; ++b) wd |= (((uint32_t)X[b] >> (4 * (5 - l))) & 15u) << (4 * b);
+            s_limb[l * LW + g] = wd;
+          }
         }
       }
     }
     __syncthreads();
-    constexpr int WPC = W::EPC / 4;
-    int32_t ss2 = 0, su1 = 0, su0 = 0;
+    int32_t ls[NL];
+#pragma unroll
+    for (int l = 0; l < NL; ++l) ls[l] = 0;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int ch = out.q + c * out.lpr;
 #pragma unroll
-      for (int wi = 0; wi < WPC; ++wi) {
+      for (int wi = 0; wi < 4; ++wi) {
         const bool ok = ch < out.C;
-        const int word = ch * WPC + wi;
-        const uint32_t w2 = ok ? s_limb[0][word] : 0u, w1 = ok ? s_limb[1][word] : 0u, w0 = ok ? s_limb[2][word] : 0u;
-        out.s2[c][wi] = w2;
-        out.u1[c][wi] = w1;
-        out.u0[c][wi] = w0;
-        ss2 = __builtin_amdgcn_sdot4((int)w2, 0x01010101, ss2, false);
-        su1 = (int32_t)__builtin_amdgcn_udot4(w1, 0x01010101u, (uint32_t)su1, false);
-        su0 = (int32_t)__builtin_amdgcn_udot4(w0, 0x01010101u, (uint32_t)su0, false);
+        const int word = ch * 4 + wi;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+          const uint32_t wl = ok ? s_limb[l * LW + word] : 0u;
+          out.limb[l][c][wi] = wl;
+          if constexpr (W::LB == 8)
+            ls[l] = l == 0 ? __builtin_amdgcn_sdot4((int)wl, 0x01010101, ls[l], false)
+                           : (int32_t)__builtin_amdgcn_udot4(wl, 0x01010101u, (uint32_t)ls[l], false);
+          else
+            ls[l] = l == 0 ? __builtin_amdgcn_sdot8((int)wl, 0x11111111, ls[l], false)
+                           : (int32_t)__builtin_amdgcn_udot8(wl, 0x11111111u, (uint32_t)ls[l], false);
+        }
       }
     }
-    out.ss2 = ss2;
-    out.su1 = su1;
-    out.su0 = su0;
+#pragma unroll
+    for (int l = 0; l < NL; ++l) out.lsum[l] = ls[l];
     __syncthreads();  // the limb words are read before any later conversion overwrites them
   }
 }
@@ -247,37 +263,47 @@ __device__ __forceinline__ float lane_dot(const uint4 (&b)[CPL], const LaneVec<W
       }
     }
     return acc0 + acc1;
-  } else {
+  } else if constexpr (W::LB == 8) {
     int32_t a2 = 0;
     uint32_t a1 = 0u, a0 = 0u;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const uint32_t cw[4] = {b[c].x, b[c].y, b[c].z, b[c].w};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if constexpr (W::LB == 8) {  // signed codes w; w ^ 0x80 per byte = w + 128
-          const uint32_t off = cw[i] ^ 0x80808080u;
-          a2 = __builtin_amdgcn_sdot4((int)cw[i], (int)v.s2[c][i], a2, false);
-          a1 = __builtin_amdgcn_udot4(off, v.u1[c][i], a1, false);
-          a0 = __builtin_amdgcn_udot4(off, v.u0[c][i], a0, false);
-        } else {  // nibble n -> byte n + 8 (two's complement nibble xor 8), even then odd
-          const uint32_t ev = (cw[i] & 0x0F0F0F0Fu) ^ 0x08080808u;
-          const uint32_t od = ((cw[i] >> 4) & 0x0F0F0F0Fu) ^ 0x08080808u;
-          a2 = __builtin_amdgcn_sdot4((int)ev, (int)v.s2[c][2 * i], a2, false);
-          a2 = __builtin_amdgcn_sdot4((int)od, (int)v.s2[c][2 * i + 1], a2, false);
-          a1 = __builtin_amdgcn_udot4(ev, v.u1[c][2 * i], a1, false);
-          a1 = __builtin_amdgcn_udot4(od, v.u1[c][2 * i + 1], a1, false);
-          a0 = __builtin_amdgcn_udot4(ev, v.u0[c][2 * i], a0, false);
-          a0 = __builtin_amdgcn_udot4(od, v.u0[c][2 * i + 1], a0, false);
-        }
+      for (int i = 0; i < 4; ++i) {  // signed codes w; w ^ 0x80 per byte = w + 128
+        const uint32_t off = cw[i] ^ 0x80808080u;
+        a2 = __builtin_amdgcn_sdot4((int)cw[i], (int)v.limb[0][c][i], a2, false);
+        a1 = __builtin_amdgcn_udot4(off, v.limb[1][c][i], a1, false);
+        a0 = __builtin_amdgcn_udot4(off, v.limb[2][c][i], a0, false);
       }
     }
-    // remove the code offsets: int8 sum (w + 128) u = sum w u + 128 sum u; int4 likewise
-    // with 8, also on the signed limb
-    constexpr int kOff = W::LB == 8 ? 128 : 8;
-    const int32_t e2 = W::LB == 8 ? a2 : a2 - kOff * v.ss2;
-    const int32_t e1 = (int32_t)a1 - kOff * v.su1, e0 = (int32_t)a0 - kOff * v.su0;
+    // remove the code offsets: sum (w + 128) u = sum w u + 128 sum u
+    const int32_t e2 = a2;
+    const int32_t e1 = (int32_t)a1 - 128 * v.lsum[1], e0 = (int32_t)a0 - 128 * v.lsum[2];
     return fmaf((float)e2, 65536.f, fmaf((float)e1, 256.f, (float)e0)) * v.scale;
+  } else {
+    // int4: v_dot8 of eight nibbles at a time; the signed top limb against the signed codes,
+    // the five unsigned limbs against the codes + 8 (nibble ^ 8)
+    int32_t a5 = 0;
+    uint32_t au[5] = {0u, 0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const uint32_t cw[4] = {b[c].x, b[c].y, b[c].z, b[c].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t off = cw[i] ^ 0x88888888u;
+        a5 = __builtin_amdgcn_sdot8((int)cw[i], (int)v.limb[0][c][i], a5, false);
+#pragma unroll
+        for (int l = 1; l < 6; ++l) au[l - 1] = __builtin_amdgcn_udot8(off, v.limb[l][c][i], au[l - 1], false);
+      }
+    }
+    float r = 0.f;
+#pragma unroll
+    for (int l = 5; l >= 1; --l) {  // nibble 0 (l = 5) up to nibble 4 (l = 1), then the top one
+      const int32_t e = (int32_t)au[l - 1] - 8 * v.lsum[l];
+      r = fmaf((float)e, (float)(1 << (4 * (5 - l))), r);
+    }
+    return fmaf((float)a5, 1048576.f, r) * v.scale;
   }
 }
 
