@@ -43,6 +43,7 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kTiles = 4;                // 16-row tiles of a gate segment
 constexpr int kSegRowsB = 16 * kTiles;   // rows per gate segment (one 64-lane ballot)
@@ -663,6 +664,306 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) voi
     FFN_GATE_UP_PARAMS) {
   gate_up_body<W, false, DENSE, 1, 2, 2, FORM>(FFN_GATE_UP_ARGS);
 }
+// ------------------------------------------------------------------ batches of 2 .. 4 tokens
+// For at most four tokens the gate and the W_up dots run on v_mfma_f32_4x4x4_16b_bf16:
+// sixteen independent 4x4x4 products an instruction, in which lane 4b + i holds 4
+// consecutive k of row i of block b (A operand), lane 4b + j those of token j (B operand),
+// and element i of lane 4b + j receives D[b][i][j].  One load instruction of a quad (four
+// rows) gives lane 4b + i the 16-byte chunk b of 16 consecutive chunks of row i: 256
+// contiguous bytes a row, already in the A layout (its 8 bf16, or 16 / 32 codes converted
+// to bf16, feed 2 / 4 / 8 products), so rows need no reshaping through LDS and a quad of
+// union rows is any four rows.  The 16 blocks hold disjoint k ranges of the same 4 x 4
+// product and are summed once the quad is done.  The tokens sit in LDS, split once per
+// workgroup into bf16 hi + lo in the order the lanes read them, so the streams load nothing
+// but weights; sixteen waves a workgroup keep up to 128 KB a CU in flight.  Tokens past the
+// batch are zeros (a batch of 2 or 3 tokens leaves lanes idle).
+// Standard gating only: for LoPA, whose gate rows are short and whose time goes into the
+// W_up rows of the union, the 16x16x32 kernel measured faster (8B, r = 512, four tokens:
+// 37.7 against 39.7 us a call); for standard gating with int8 / int4 rows this kernel took
+// the 8B four-token call from 42.1 / 41.9 to 36.0 / 36.0 us.
+constexpr int kQ4Waves = 16;      // waves a workgroup (one workgroup a CU: four a SIMD)
+constexpr int kQ4Threads = kQ4Waves * kWave;
+constexpr int kQ4Depth = 8;       // weight loads in flight a wave
+constexpr int kQ4MaxX = 4096;     // elements a token (d padded to a whole step)
+constexpr int kQ4Quads = kSegRowsB / 4;
+
+__device__ __forceinline__ short4_t half4(const uint4& v, int h) {
+  return __builtin_bit_cast(short4_t, h ? make_uint2(v.z, v.w) : make_uint2(v.x, v.y));
+}
+__device__ __forceinline__ f32x4_t mfma4(short4_t a, short4_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// One step of a quad: the weight chunk v (8 elements a 16-byte group J) against the token
+// fragment at t: t[f kWave], f < FW / 2 the hi parts, then as many lo parts.  Four accumulators take the
+// hi and lo products of the two k halves of each group, so that no product waits on the
+// one before it.
+template <class W>
+__device__ __forceinline__ void q4_mma(const uint4& v, const uint4* __restrict__ t, f32x4_t (&acc)[4]) {
+  constexpr int G8 = W::EPC / 8, FW = W::EPC / 4;
+  auto one = [&](const uint4& w, const uint4& th, const uint4& tl) {
+    acc[0] = mfma4(half4(w, 0), half4(th, 0), acc[0]);
+    acc[1] = mfma4(half4(w, 0), half4(tl, 0), acc[1]);
+    acc[2] = mfma4(half4(w, 1), half4(th, 1), acc[2]);
+    acc[3] = mfma4(half4(w, 1), half4(tl, 1), acc[3]);
+  };
+  one(bf16_chunk<W, 0>(v), t[0], t[(FW / 2) * kWave]);
+  if constexpr (G8 > 1) one(bf16_chunk<W, 1>(v), t[kWave], t[(FW / 2 + 1) * kWave]);
+  if constexpr (G8 > 2) {
+    one(bf16_chunk<W, 2>(v), t[2 * kWave], t[(FW / 2 + 2) * kWave]);
+    one(bf16_chunk<W, 3>(v), t[3 * kWave], t[(FW / 2 + 3) * kWave]);
+  }
+}
+
+// Items [i0, i1) of a quad stream: item it is step it % ns of quad it / ns; a step is 16
+// chunks of a row (C chunks a row, ns = ceil(C / 16) steps).  row_of(q) is this lane's row
+// of quad q (row lane & 3 of the quad), or -1.  The weights of item it + kQ4Depth are
+// requested when item it has been multiplied; items past i1 load nothing.  deposit(q, s)
+// receives the quad's 4 x 4 sums in lanes 0..3 (lane j: s[i] = row i . token j) when the
+// stream leaves quad q.  stage() runs once the first loads are out, in every thread.
+template <class W, class RowOf, class Stage, class Deposit>
+__device__ __forceinline__ void q4_stream(const Buf& wb, int C, int ns, int i0, int i1,
+                                          const uint4* __restrict__ tok, RowOf row_of, Stage stage,
+                                          Deposit deposit) {
+  constexpr int D = kQ4Depth, FW = W::EPC / 4;
+  const int lane = lane_id(), b = lane >> 2;
+  uint4 wv[D];
+  int lq = i0 / ns, ls = i0 - lq * ns;
+  int lrow = row_of(lq);
+  auto issue = [&](int u, bool live) {
+    const int ch = 16 * ls + b;
+    wv[u] = ldb_nt(wb, live && lrow >= 0 && ch < C ? 16u * ((uint32_t)lrow * (uint32_t)C + (uint32_t)ch) : kOOB);
+    if (live && ++ls == ns) {
+      ls = 0;
+      lrow = row_of(++lq);
+    }
+  };
+  int cq = i0 / ns, cs = i0 - cq * ns;
+#pragma unroll
+  for (int u = 0; u < D; ++u) issue(u, i0 + u < i1);
+  stage();
+  f32x4_t acc[4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) acc[a] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto flush = [&] {
+    f32x4_t s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll
+    for (int o = 4; o < kWave; o <<= 1)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[i] += __shfl_xor(s[i], o);
+    deposit(cq, s);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) acc[a] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  };
+  for (int it = i0; it < i1; it += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      if (it + u < i1) {
+        q4_mma<W>(wv[u], tok + (size_t)cs * FW * kWave + lane, acc);
+        if (++cs == ns) {
+          flush();
+          cs = 0;
+          ++cq;
+        }
+      }
+      issue(u, it + u + D < i1);
+    }
+  }
+  if (cs != 0) flush();  // a quad cut by the end of the range
+}
+
+// Tokens into LDS: elements [0, K) of rows j < T of src (row stride `stride` floats),
+// split into bf16 hi + lo, for lane 4 ((k / EPC) % 16) + j of step k / (16 EPC): part f of a lane's fragment
+// (f < FW / 2 hi, then lo) at uint4 (step FW + f) kWave + lane, so that the lanes of a
+// wave read 16 consecutive bytes each.  Zeros up to Kp (a whole number of steps) and for
+// rows j >= T.  A region of Kp elements takes Kp uint4.  UMAX: the most 8-element units
+// a thread takes (4 Kp / 8 <= UMAX kQ4Threads).  The loads are issued by q4_load_tokens and
+// the values stored by q4_store_tokens, so that other loads can go out in between.
+template <class W, int UMAX>
+__device__ __forceinline__ void q4_load_tokens(const float* __restrict__ src, int T, int K, int Kp, int stride,
+                                               float4 (&v)[UMAX][2]) {
+  const Buf sb = make_buf(src, 4u * (uint32_t)T * (uint32_t)stride);
+  const int nu = 4 * (Kp / 8);
+#pragma unroll
+  for (int u = 0; u < UMAX; ++u) {
+    const int unit = threadIdx.x + u * kQ4Threads, j = unit % 4, k = 8 * (unit / 4);
+    const bool ok = unit < nu && j < T && k < K;
+    const uint32_t off = ok ? 4u * ((uint32_t)j * (uint32_t)stride + (uint32_t)k) : kOOB;
+    v[u][0] = __builtin_bit_cast(float4, ldb(sb, off));
+    v[u][1] = __builtin_bit_cast(float4, ldb(sb, off + 16));
+  }
+}
+template <class W, int UMAX>
+__device__ __forceinline__ void q4_store_tokens(const float4 (&v)[UMAX][2], int Kp, uint4* __restrict__ tok) {
+  constexpr int EPC = W::EPC, FW = EPC / 4;
+  const int nu = 4 * (Kp / 8);
+#pragma unroll
+  for (int u = 0; u < UMAX; ++u) {
+    const int unit = threadIdx.x + u * kQ4Threads, j = unit % 4, k = 8 * (unit / 4);
+    if (unit < nu) {
+      const float f[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w, v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
+      bf16x8_t hi, lo;
+      split8(f, hi, lo);
+      const int step = k / (16 * EPC), bb = (k / EPC) % 16, grp = (k % EPC) / 8;
+      uint4* p = tok + (size_t)step * FW * kWave + 4 * bb + j;
+      p[grp * kWave] = __builtin_bit_cast(uint4, hi);
+      p[(FW / 2 + grp) * kWave] = __builtin_bit_cast(uint4, lo);
+    }
+  }
+}
+
+// Gate, union and W_up dots of one segment for batches of at most four tokens (the same
+// outputs as gate_up_body with one token tile).  Every wave takes an equal share of the
+// segment's (quad, step) items, so a quad may be split between waves: each wave leaves its
+// partial sums in its own LDS slots and the slots are added in a fixed order.
+template <class W, bool DENSE, int FORM>
+__global__ __launch_bounds__(kQ4Threads) void k_gate_up_q4(FFN_GATE_UP_PARAMS) {
+  constexpr int EPC = W::EPC, STEP = 16 * EPC;
+  constexpr bool Q = is_quant<W>();
+  constexpr bool FULL = FORM != kFormDefault;
+  static_assert(FORM != kFormLoPA, "standard gating");
+  constexpr int UX = 4 * kQ4MaxX / 8 / kQ4Threads;
+  __shared__ uint4 s_tok[kQ4MaxX];
+  // partial sums [wave][quad][token] (element i: row i of the quad) of the gate and W_up
+  __shared__ f32x4_t s_pg[kQ4Waves][kQ4Quads][4], s_pu[kQ4Waves][kQ4Quads][4];
+  __shared__ float s_act[kSegRowsB][4];
+  __shared__ int s_list[kSegRowsB];
+  __shared__ int s_cnt;
+
+  const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
+  for (int j = blockIdx.x * kQ4Threads + threadIdx.x; j < T * d; j += gridDim.x * kQ4Threads) y[j] = 0.f;
+  if (blockIdx.x == 0 && threadIdx.x == 0) meta[0] = nseg;
+  const int Cu_ = Cu / (EPC / 8);  // 16-byte chunks a row (of W_gate and W_up)
+  const int nsu = (Cu_ + 15) / 16, Kpx = nsu * STEP;
+  const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cu_);
+  const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu_);
+  auto deposit_g = [&](int q, const f32x4_t& s) {
+    if (lane < 4) s_pg[wave][q][lane] = s;
+  };
+  auto deposit_u = [&](int q, const f32x4_t& s) {
+    if (lane < 4) s_pu[wave][q][lane] = s;
+  };
+
+  const Split segs(d_ff, nseg);
+  bool staged = false;
+  for (int seg = blockIdx.x; seg < nseg; seg += gridDim.x) {
+    __syncthreads();  // the previous segment's LDS reads are done
+    const int row0 = segs.start(seg);
+    const int nrows = segs.start(seg + 1) - row0;  // <= kSegRowsB, guaranteed by the host
+    for (int o = threadIdx.x; o < kQ4Waves * kQ4Quads * 4; o += kQ4Threads) {
+      (&s_pg[0][0][0])[o] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      (&s_pu[0][0][0])[o] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    __syncthreads();
+    {
+      const int n = ((nrows + 3) / 4) * nsu;
+      const int i0 = (int)((int64_t)n * wave / kQ4Waves), i1 = (int)((int64_t)n * (wave + 1) / kQ4Waves);
+      auto row_of = [&](int q) {
+        const int rl = 4 * q + (lane & 3);
+        return rl < nrows ? row0 + rl : -1;
+      };
+      auto stage = [&] {
+        if (staged) return;
+        staged = true;
+        float4 vx[UX][2];
+        q4_load_tokens<W, UX>(x, T, d, Kpx, d, vx);
+        q4_store_tokens<W, UX>(vx, Kpx, s_tok);
+        __syncthreads();
+      };
+      if (i0 < i1)
+        q4_stream<W>(gb, Cu_, nsu, i0, i1, s_tok, row_of, stage, deposit_g);
+      else
+        stage();
+    }
+    // the row scale of the row this lane of wave 0 thresholds
+    float sg = 1.f;
+    if constexpr (Q)
+      if (wave == 0)
+        sg = __int_as_float(ldb32(make_buf(s_g, 4u * (uint32_t)d_ff), lane < nrows ? 4u * (uint32_t)(row0 + lane) : kOOB));
+    __syncthreads();
+    if (wave == 0) {
+      // lane: row `lane` of the segment
+      const int q = lane >> 2, i = lane & 3;
+      bool any = false;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float hv = 0.f;
+#pragma unroll
+        for (int w = 0; w < kQ4Waves; ++w) hv += s_pg[w][q][j][i];
+        if constexpr (Q) hv *= sg;
+        const bool on = j < T && hv > t;
+        if (lane < nrows) s_act[lane][j] = on ? (FULL ? gate_value(form.act, hv - t) : hv - t) : 0.f;
+        any |= on;
+      }
+      const bool sel = lane < nrows && (DENSE || any);
+      const uint64_t bm = __ballot(sel);
+      const int rank = rank_in_mask(bm);
+      if (sel) {
+        s_list[rank] = lane;
+        seg_idx[row0 + rank] = row0 + lane;
+      }
+      if (lane == 0) {
+        s_cnt = __popcll(bm);
+        seg_count[seg] = __popcll(bm);
+      }
+    }
+    __syncthreads();
+    const int cnt = uniform(s_cnt);
+    for (int o = threadIdx.x; o < cnt * T; o += kQ4Threads) {
+      const int tk = o / cnt, e = o - tk * cnt;
+      seg_act[(size_t)tk * slots + row0 + e] = s_act[s_list[e]][tk];
+    }
+    {
+      const int n = ((cnt + 3) / 4) * nsu;
+      const int i0 = (int)((int64_t)n * wave / kQ4Waves), i1 = (int)((int64_t)n * (wave + 1) / kQ4Waves);
+      auto row_of = [&](int q) {
+        const int e = 4 * q + (lane & 3);
+        return e < cnt ? row0 + s_list[e] : -1;
+      };
+      if (i0 < i1) q4_stream<W>(ub, Cu_, nsu, i0, i1, s_tok, row_of, [] {}, deposit_u);
+    }
+    __syncthreads();
+
+    // wave w: union entries 16 w .. 16 w + 15 = half (w & 1) of fragment group w >> 1;
+    // lane m + 16 g: token m, entries 16 w + 4 g + i
+    const int m = lane & 15, g = lane >> 4;
+    const int gi = wave >> 1, half = wave & 1;
+    float sue[4] = {1.f, 1.f, 1.f, 1.f}, sde[4] = {1.f, 1.f, 1.f, 1.f};
+    if constexpr (Q) {
+      const Buf ubs = make_buf(s_up, 4u * (uint32_t)d_ff), dbs = make_buf(s_down, 4u * (uint32_t)d_ff);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 16 * (wave & 3) + 4 * g + i;
+        const uint32_t off = e < cnt ? 4u * (uint32_t)(row0 + s_list[e < cnt ? e : 0]) : kOOB;
+        sue[i] = __int_as_float(ldb32(ubs, off));
+        sde[i] = __int_as_float(ldb32(dbs, off));
+      }
+    }
+    if (wave < 4 && 32 * gi < cnt && m < T) {
+      const int qq = 4 * wave + g;  // the quad of entries 16 w + 4 g ..
+      f32x4_t v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < kQ4Waves; ++w) v += s_pu[w][qq][m];
+      uint32_t hw[2] = {0u, 0u}, lw[2] = {0u, 0u};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int e = 16 * wave + 4 * g + i;
+        const float vu = Q ? v[i] * sue[i] : v[i];
+        float zz = e < cnt ? s_act[s_list[e]][m] * (FULL ? up_value(form.silu_up, vu) : vu) : 0.f;
+        if constexpr (Q) zz *= sde[i];
+        const __bf16 hb = (__bf16)zz;
+        const __bf16 lb = (__bf16)(zz - (float)hb);
+        hw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, hb) << (16 * (i & 1));
+        lw[i >> 1] |= (uint32_t)__builtin_bit_cast(uint16_t, lb) << (16 * (i & 1));
+      }
+      // token tile 0: hi plane entry of lane m + 16 g, then the lo plane 64 entries on
+      uint4* frag = zf + (((size_t)seg * 2 + gi) * ntt * 2) * kWave + m + 16 * g;
+      reinterpret_cast<uint2*>(frag)[half] = make_uint2(hw[0], hw[1]);
+      reinterpret_cast<uint2*>(frag + kWave)[half] = make_uint2(lw[0], lw[1]);
+    }
+  }
+}
+
 #undef FFN_GATE_UP_PARAMS
 #undef FFN_GATE_UP_ARGS
 
@@ -747,7 +1048,6 @@ __device__ __forceinline__ void dn_issue(DnFrags<NT, W>& f, const DnRows<NT, W>&
   }
 }
 
-typedef short short4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint2 lds_read_tr16(const char* p) {
   const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t*)(p));
   return __builtin_bit_cast(uint2, v);
@@ -951,20 +1251,38 @@ int segments_for(int d_ff, int grid) {
   return n > 128 ? (n + grid - 1) / grid * grid : n;
 }
 
+// The 4x4x4 kernel takes standard gating for batches of at most four tokens whose rows,
+// padded to a whole step, fit its token LDS.
+template <class W>
+bool q4_fits(const Shape& sh) {
+  const int step = 16 * W::EPC;
+  return sh.T <= 4 && (sh.d + step - 1) / step * step <= kQ4MaxX;
+}
+
 template <class W, bool LOPA, bool DENSE, int NT, int FORM>
 hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up, float t,
                      Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
-  constexpr bool two = !LOPA && NT == 1;
+  if constexpr (NT == 1 && !LOPA)
+    if (q4_fits<W>(sh)) {
+      ws.nseg = segments_for(sh.d_ff, kSegGrid);
+      return launch_gate_kernel_n(k_gate_up_q4<W, DENSE, FORM>, ws.nseg < kSegGrid ? ws.nseg : kSegGrid,
+                                  kQ4Threads, s, x,
+                                (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
+                                static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
+                                ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form,
+                                (const float*)ws.gx, LOPA ? sh.sc.b : sh.sc.gate, sh.sc.up, sh.sc.down);
+    }
+  // two workgroups a CU only where their segments stay near 64 rows: halving 8B-shaped
+  // segments to 28 rows left the row tiles half empty (int8 / int4 at four tokens: 52.7 /
+  // 54.4 us a call, 42.1 / 41.9 us with one workgroup a CU)
+  const bool two = !LOPA && NT == 1 && sh.d_ff >= 48 * kSegGrid2;
   const int grid = two ? kSegGrid2 : kSegGrid;
   ws.nseg = segments_for(sh.d_ff, grid);
   const int g = ws.nseg < grid ? ws.nseg : grid;
-  auto kernel = [&] {
-    if constexpr (two)
-      return k_gate_up_mfma2<W, DENSE, FORM>;
-    else
-      return k_gate_up_mfma<W, LOPA, DENSE, NT, FORM>;
-  }();
+  auto kernel = k_gate_up_mfma<W, LOPA, DENSE, NT, FORM>;
+  if constexpr (!LOPA && NT == 1)
+    if (two) kernel = k_gate_up_mfma2<W, DENSE, FORM>;
   return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                             static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
                             ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form,
