@@ -673,18 +673,21 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) voi
 // contiguous bytes a row, already in the A layout (its 8 bf16, or 16 / 32 codes converted
 // to bf16, feed 2 / 4 / 8 products), so rows need no reshaping through LDS and a quad of
 // union rows is any four rows.  The 16 blocks hold disjoint k ranges of the same 4 x 4
-// product and are summed once the quad is done.  The tokens sit in LDS, split once per
-// workgroup into bf16 hi + lo in the order the lanes read them, so the streams load nothing
-// but weights; sixteen waves a workgroup keep up to 128 KB a CU in flight.  Tokens past the
-// batch are zeros (a batch of 2 or 3 tokens leaves lanes idle).
-// Standard gating only: for LoPA, whose gate rows are short and whose time goes into the
-// W_up rows of the union, the 16x16x32 kernel measured faster (8B, r = 512, four tokens:
-// 37.7 against 39.7 us a call); for standard gating with int8 / int4 rows this kernel took
-// the 8B four-token call from 42.1 / 41.9 to 36.0 / 36.0 us.
-constexpr int kQ4Waves = 16;      // waves a workgroup (one workgroup a CU: four a SIMD)
+// product and are summed once the quad is done.  The tokens (x, and LoPA's z: the sum of the
+// z kernel's two partial copies) sit in LDS, split once per workgroup into bf16 hi + lo in
+// the order the lanes read them, so the streams load nothing but weights.  Eight waves a workgroup with four loads in flight each (32 KB a CU) measured
+// fastest: at 8B int8 / int4 and four tokens the gate kernel took 22.6 / 22.5 us, against
+// 26.1 / 25.9 us with sixteen waves and eight loads, 30.2 / 28.2 us with sixteen and twelve,
+// and 33.3 / 28.2 us with four waves and four loads.  Tokens past the batch are zeros (a batch
+// of 2 or 3 tokens leaves lanes idle).
+// Against the 16x16x32 kernel at four tokens on the 8B shape: standard gating with int8 /
+// int4 rows 42.1 / 41.9 -> 32.6 / 32.1 us a call; LoPA (r = 512) with bf16 / int8 / int4 rows
+// 38.4 / 34.7 / 34.3 -> 37.7 / 31.8 / 31.5 us.
+constexpr int kQ4Waves = 8;       // waves a workgroup (one workgroup a CU: two a SIMD)
 constexpr int kQ4Threads = kQ4Waves * kWave;
-constexpr int kQ4Depth = 8;       // weight loads in flight a wave
-constexpr int kQ4MaxX = 4096;     // elements a token (d padded to a whole step)
+constexpr int kQ4Depth = 4;       // weight loads in flight a wave
+constexpr int kQ4MaxX = 4096;     // elements a token: x (d padded to a whole step) ...
+constexpr int kQ4MaxZ = 1024;     // ... and LoPA's z (r padded likewise)
 constexpr int kQ4Quads = kSegRowsB / 4;
 
 __device__ __forceinline__ short4_t half4(const uint4& v, int h) {
@@ -772,8 +775,8 @@ __device__ __forceinline__ void q4_stream(const Buf& wb, int C, int ns, int i0, 
   if (cs != 0) flush();  // a quad cut by the end of the range
 }
 
-// Tokens into LDS: elements [0, K) of rows j < T of src (row stride `stride` floats),
-// split into bf16 hi + lo, for lane 4 ((k / EPC) % 16) + j of step k / (16 EPC): part f of a lane's fragment
+// Tokens into LDS: elements [0, K) of rows j < T of src (row stride `stride` floats; with
+// copies = 2 the sum of two partial copies `part` floats apart), split into bf16 hi + lo, for lane 4 ((k / EPC) % 16) + j of step k / (16 EPC): part f of a lane's fragment
 // (f < FW / 2 hi, then lo) at uint4 (step FW + f) kWave + lane, so that the lanes of a
 // wave read 16 consecutive bytes each.  Zeros up to Kp (a whole number of steps) and for
 // rows j >= T.  A region of Kp elements takes Kp uint4.  UMAX: the most 8-element units
@@ -781,16 +784,23 @@ __device__ __forceinline__ void q4_stream(const Buf& wb, int C, int ns, int i0, 
 // the values stored by q4_store_tokens, so that other loads can go out in between.
 template <class W, int UMAX>
 __device__ __forceinline__ void q4_load_tokens(const float* __restrict__ src, int T, int K, int Kp, int stride,
-                                               float4 (&v)[UMAX][2]) {
-  const Buf sb = make_buf(src, 4u * (uint32_t)T * (uint32_t)stride);
+                                               float4 (&v)[UMAX][2], int copies = 1, uint32_t part = 0) {
+  const Buf sb = make_buf(src, 4u * (copies == 2 ? 2u * part : (uint32_t)T * (uint32_t)stride));
   const int nu = 4 * (Kp / 8);
 #pragma unroll
   for (int u = 0; u < UMAX; ++u) {
     const int unit = threadIdx.x + u * kQ4Threads, j = unit % 4, k = 8 * (unit / 4);
     const bool ok = unit < nu && j < T && k < K;
     const uint32_t off = ok ? 4u * ((uint32_t)j * (uint32_t)stride + (uint32_t)k) : kOOB;
-    v[u][0] = __builtin_bit_cast(float4, ldb(sb, off));
-    v[u][1] = __builtin_bit_cast(float4, ldb(sb, off + 16));
+    float4 a = __builtin_bit_cast(float4, ldb(sb, off)), c = __builtin_bit_cast(float4, ldb(sb, off + 16));
+    if (copies == 2) {
+      const float4 a2 = __builtin_bit_cast(float4, ldb(sb, ok ? off + 4u * part : kOOB));
+      const float4 c2 = __builtin_bit_cast(float4, ldb(sb, ok ? off + 4u * part + 16 : kOOB));
+      a = make_float4(a.x + a2.x, a.y + a2.y, a.z + a2.z, a.w + a2.w);
+      c = make_float4(c.x + c2.x, c.y + c2.y, c.z + c2.z, c.w + c2.w);
+    }
+    v[u][0] = a;
+    v[u][1] = c;
   }
 }
 template <class W, int UMAX>
@@ -816,14 +826,13 @@ __device__ __forceinline__ void q4_store_tokens(const float4 (&v)[UMAX][2], int 
 // outputs as gate_up_body with one token tile).  Every wave takes an equal share of the
 // segment's (quad, step) items, so a quad may be split between waves: each wave leaves its
 // partial sums in its own LDS slots and the slots are added in a fixed order.
-template <class W, bool DENSE, int FORM>
+template <class W, bool LOPA, bool DENSE, int FORM>
 __global__ __launch_bounds__(kQ4Threads) void k_gate_up_q4(FFN_GATE_UP_PARAMS) {
   constexpr int EPC = W::EPC, STEP = 16 * EPC;
   constexpr bool Q = is_quant<W>();
-  constexpr bool FULL = FORM != kFormDefault;
-  static_assert(FORM != kFormLoPA, "standard gating");
-  constexpr int UX = 4 * kQ4MaxX / 8 / kQ4Threads;
-  __shared__ uint4 s_tok[kQ4MaxX];
+  constexpr bool FULL = FORM != kFormDefault, HAS_G = FORM == kFormLoPA;
+  constexpr int UX = 4 * kQ4MaxX / 8 / kQ4Threads, UZ = LOPA ? (4 * kQ4MaxZ / 8 + kQ4Threads - 1) / kQ4Threads : 1;
+  __shared__ uint4 s_tok[kQ4MaxX + (LOPA ? kQ4MaxZ : 0)];
   // partial sums [wave][quad][token] (element i: row i of the quad) of the gate and W_up
   __shared__ f32x4_t s_pg[kQ4Waves][kQ4Quads][4], s_pu[kQ4Waves][kQ4Quads][4];
   __shared__ float s_act[kSegRowsB][4];
@@ -833,9 +842,10 @@ __global__ __launch_bounds__(kQ4Threads) void k_gate_up_q4(FFN_GATE_UP_PARAMS) {
   const int lane = lane_id(), wave = uniform(threadIdx.x / kWave);
   for (int j = blockIdx.x * kQ4Threads + threadIdx.x; j < T * d; j += gridDim.x * kQ4Threads) y[j] = 0.f;
   if (blockIdx.x == 0 && threadIdx.x == 0) meta[0] = nseg;
-  const int Cu_ = Cu / (EPC / 8);  // 16-byte chunks a row (of W_gate and W_up)
-  const int nsu = (Cu_ + 15) / 16, Kpx = nsu * STEP;
-  const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cu_);
+  const int Cu_ = Cu / (EPC / 8), Cg_ = Cg / (EPC / 8);
+  const int nsu = (Cu_ + 15) / 16, Kpx = nsu * STEP, nsg = (Cg_ + 15) / 16, Kpz = LOPA ? nsg * STEP : 0;
+  uint4* const tok_g = s_tok + (LOPA ? Kpx : 0);
+  const Buf gb = make_buf(gate_w, 16u * (uint32_t)d_ff * (uint32_t)Cg_);
   const Buf ub = make_buf(w_up, 16u * (uint32_t)d_ff * (uint32_t)Cu_);
   auto deposit_g = [&](int q, const f32x4_t& s) {
     if (lane < 4) s_pg[wave][q][lane] = s;
@@ -856,7 +866,7 @@ __global__ __launch_bounds__(kQ4Threads) void k_gate_up_q4(FFN_GATE_UP_PARAMS) {
     }
     __syncthreads();
     {
-      const int n = ((nrows + 3) / 4) * nsu;
+      const int n = ((nrows + 3) / 4) * nsg;
       const int i0 = (int)((int64_t)n * wave / kQ4Waves), i1 = (int)((int64_t)n * (wave + 1) / kQ4Waves);
       auto row_of = [&](int q) {
         const int rl = 4 * q + (lane & 3);
@@ -867,19 +877,30 @@ __global__ __launch_bounds__(kQ4Threads) void k_gate_up_q4(FFN_GATE_UP_PARAMS) {
         staged = true;
         float4 vx[UX][2];
         q4_load_tokens<W, UX>(x, T, d, Kpx, d, vx);
+        float4 vz[UZ][2];
+        if constexpr (LOPA) q4_load_tokens<W, UZ>(zp, T, Cg * 8, Kpz, Cg * 8, vz, 2, (uint32_t)tc * (uint32_t)Cg * 8u);
         q4_store_tokens<W, UX>(vx, Kpx, s_tok);
+        if constexpr (LOPA) q4_store_tokens<W, UZ>(vz, Kpz, tok_g);
         __syncthreads();
       };
       if (i0 < i1)
-        q4_stream<W>(gb, Cu_, nsu, i0, i1, s_tok, row_of, stage, deposit_g);
+        q4_stream<W>(gb, Cg_, nsg, i0, i1, tok_g, row_of, stage, deposit_g);
       else
         stage();
     }
     // the row scale of the row this lane of wave 0 thresholds
-    float sg = 1.f;
+    float sg = 1.f, gxv[4] = {0.f, 0.f, 0.f, 0.f};
     if constexpr (Q)
       if (wave == 0)
         sg = __int_as_float(ldb32(make_buf(s_g, 4u * (uint32_t)d_ff), lane < nrows ? 4u * (uint32_t)(row0 + lane) : kOOB));
+    if constexpr (HAS_G)
+      if (wave == 0) {
+        const Buf xb = make_buf(gx, 4u * (uint32_t)tc * (uint32_t)d_ff);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          gxv[j] = __int_as_float(
+              ldb32(xb, j < T && lane < nrows ? 4u * ((uint32_t)j * (uint32_t)d_ff + (uint32_t)(row0 + lane)) : kOOB));
+      }
     __syncthreads();
     if (wave == 0) {
       // lane: row `lane` of the segment
@@ -891,6 +912,7 @@ __global__ __launch_bounds__(kQ4Threads) void k_gate_up_q4(FFN_GATE_UP_PARAMS) {
 #pragma unroll
         for (int w = 0; w < kQ4Waves; ++w) hv += s_pg[w][q][j][i];
         if constexpr (Q) hv *= sg;
+        if constexpr (HAS_G) hv += gxv[j];
         const bool on = j < T && hv > t;
         if (lane < nrows) s_act[lane][j] = on ? (FULL ? gate_value(form.act, hv - t) : hv - t) : 0.f;
         any |= on;
@@ -1251,22 +1273,22 @@ int segments_for(int d_ff, int grid) {
   return n > 128 ? (n + grid - 1) / grid * grid : n;
 }
 
-// The 4x4x4 kernel takes standard gating for batches of at most four tokens whose rows,
-// padded to a whole step, fit its token LDS.
+// The 4x4x4 kernel takes batches of at most four tokens whose rows (and LoPA's r), padded to
+// a whole step, fit its token LDS.
 template <class W>
-bool q4_fits(const Shape& sh) {
+bool q4_fits(const Shape& sh, bool lopa) {
   const int step = 16 * W::EPC;
-  return sh.T <= 4 && (sh.d + step - 1) / step * step <= kQ4MaxX;
+  return sh.T <= 4 && (sh.d + step - 1) / step * step <= kQ4MaxX && (!lopa || (sh.r + step - 1) / step * step <= kQ4MaxZ);
 }
 
 template <class W, bool LOPA, bool DENSE, int NT, int FORM>
 hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const void* gate_w, const void* w_up, float t,
                      Workspace& ws, float* y, hipStream_t s) {
   const int Cu = sh.d / 8, Cg = LOPA ? sh.r / 8 : Cu;
-  if constexpr (NT == 1 && !LOPA)
-    if (q4_fits<W>(sh)) {
+  if constexpr (NT == 1)
+    if (q4_fits<W>(sh, LOPA)) {
       ws.nseg = segments_for(sh.d_ff, kSegGrid);
-      return launch_gate_kernel_n(k_gate_up_q4<W, DENSE, FORM>, ws.nseg < kSegGrid ? ws.nseg : kSegGrid,
+      return launch_gate_kernel_n(k_gate_up_q4<W, LOPA, DENSE, FORM>, ws.nseg < kSegGrid ? ws.nseg : kSegGrid,
                                   kQ4Threads, s, x,
                                 (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                                 static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,

@@ -45,6 +45,8 @@ CASES = [
     ("gen_lopa_f32_r1_T2", 2, 16, 40, 1, F32, 0.1, ALL),
     ("gen_std_f32_T70", 70, 64, 200, 0, F32, 1.0, ACT),
     ("mc_std_bf16_T2", 2, 264, 1000, 0, BF16, 1.0, ACT),
+    ("q4_std_bf16_T4_act_d4096", 4, 4096, 3000, 0, BF16, 1.2816, ACT),
+    ("q4_std_bf16_T3_silu", 3, 136, 77, 0, BF16, 0.5, dict(silu_up=True)),
     ("mc_std_bf16_T12", 12, 264, 1000, 0, BF16, 1.2, ACT),
     ("mc_lopa_bf16_T4_all", 4, 264, 1000, 40, BF16, 1.2 * S2, ALL),
     ("mc_lopa_bf16_T8_norm", 8, 264, 1000, 40, BF16, 1.2, NORM_ONLY),

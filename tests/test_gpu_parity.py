@@ -57,6 +57,13 @@ SMALL = [
     ("std_bf16_d8192", 1, 8192, 1500, 0, BF16, 1.2816),            # one buffer a wave (16 chunks a lane)
     ("std_f32_d2048", 1, 2048, 1500, 0, F32, 1.2816),
     ("std_bf16_T4_odd_d", 4, 100, 77, 0, BF16, 0.5),       # batch with d not a multiple of 8: element-wise
+    # 2..4 tokens, standard gating: the 4x4x4 matrix-core kernel (rows padded to 128 elements fit 4096)
+    ("std_bf16_T4_q4_d4096", 4, 4096, 3000, 0, BF16, 1.2816),  # the largest d it takes; 63-row segments
+    ("std_bf16_T3_q4_short", 3, 136, 77, 0, BF16, 0.5),        # 17 chunks: a step of one chunk; 2 segments
+    ("std_bf16_T2_d4104", 2, 4104, 500, 0, BF16, 1.0),         # one step past its token LDS: 16x16x32 kernel
+    ("lopa_bf16_T4_q4_r1024", 4, 4096, 3000, 1024, BF16, 1.2816),  # the largest r it takes
+    ("lopa_bf16_T2_q4_r48", 2, 264, 1000, 48, BF16, 1.0),          # 6 chunks of z: one partial step
+    ("lopa_bf16_T3_r1032", 3, 264, 500, 1032, BF16, 1.0),          # r past its z LDS: 16x16x32 kernel
     ("lopa_bf16_T3_odd_r", 3, 264, 1000, 36, BF16, 1.0),    # batch with r not a multiple of 8: element-wise
     ("very_small", 1, 8, 3, 0, BF16, 0.0),
     ("d_is_1", 1, 1, 5, 0, F32, 0.0),

@@ -44,6 +44,11 @@ SMALL = [
     ("i8_gen_odd_d", 1, 100, 77, 0, I8, 0.5),
     ("i4_gen_even_d", 1, 102, 77, 0, I4, 0.5),          # d even, not a multiple of 32
     ("i8_T3", 3, 256, 1000, 0, I8, 1.0),                # batches: matrix cores, codes as bf16
+    ("i4_T4_q4_d4096", 4, 4096, 3000, 0, I4, 1.2816),   # 4x4x4 kernel: 8 products a loaded chunk
+    ("i8_T2_q4_ragged", 2, 272, 999, 0, I8, 0.9),       # 17 chunks: a step of one chunk
+    ("i4_T3_q4_ragged", 3, 288, 999, 0, I4, 0.9),       # 9 chunks: one partial step
+    ("i4_T4_q4_lopa_r512", 4, 4096, 3000, 512, I4, 1.2816),
+    ("i8_T3_q4_lopa_r48", 3, 256, 1000, 48, I8, 1.0),   # three 16-code chunks of z
     ("i4_T5_lopa", 5, 256, 1000, 32, I4, 1.0),
     ("i8_T70", 70, 64, 200, 0, I8, 1.0),                # two token passes
     ("i8_T16_lopa", 16, 256, 1000, 32, I8, 1.0),
@@ -68,7 +73,8 @@ def test_quant_small(gu, case, dense):
 
 ALL = dict(act=1, silu_up=True, use_g=True, rms_norm=True, use_gain=True)
 FORM_CASES = [("i8_t1_lopa_all", 1, 4096, 3000, 512, I8), ("i4_t1_lopa_all", 1, 4096, 3000, 512, I4),
-              ("i8_t1_std_act", 1, 4096, 3000, 0, I8), ("i4_T3_lopa_all", 3, 256, 1000, 32, I4)]
+              ("i8_t1_std_act", 1, 4096, 3000, 0, I8), ("i4_T3_lopa_all", 3, 256, 1000, 32, I4),
+              ("i8_T4_std_act", 4, 4096, 3000, 0, I8)]
 
 
 @pytest.mark.parametrize("case", FORM_CASES, ids=[c[0] for c in FORM_CASES])
