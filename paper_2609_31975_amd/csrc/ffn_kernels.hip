@@ -1938,6 +1938,22 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
   size_t rows = 0;
   if (rows_ok) down_grid(C, LG, WG_PER_CU, ws.nseg, sh.d_ff, &S, &R, &rows);
   const size_t shmem_t1 = DENSE ? 0 : 2 * sizeof(int) * rows, shmem_tb = (1 + TG) * sizeof(int) * rows;
+  // bf16 rows of 1024 chunks or more (d >= 8192): 1 KB column slices, so that each workgroup
+  // stages half as many slots (70B: 12.6 -> 12.2 us; on d = 4096 the 512-byte slices are faster)
+  if constexpr (W::EPC == 8) {
+    if (rows_ok && sh.T == 1 && C >= 1024) {
+      int S2 = 0, R2 = 0;
+      size_t rows2 = 0;
+      down_grid(C, 64, WG_PER_CU, ws.nseg, sh.d_ff, &S2, &R2, &rows2);
+      const size_t shmem2 = DENSE ? 0 : 2 * sizeof(int) * rows2;
+      if (shmem2 <= 96 * 1024) {
+        k_down_t1<W, DENSE, 64><<<S2 * R2, kBlock, shmem2, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg,
+                                                                 sh.d_ff, R2, static_cast<const uint4*>(w_down_t), C,
+                                                                 sh.d, y, sh.sc.down, ws.zslot, nzclear);
+        return hipGetLastError();
+      }
+    }
+  }
   if (rows_ok && sh.T == 1 && shmem_t1 <= 96 * 1024) {
     k_down_t1<W, DENSE, LG><<<S * R, kBlock, shmem_t1, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg, sh.d_ff,
                                                              R, static_cast<const uint4*>(w_down_t), C, sh.d, y,
