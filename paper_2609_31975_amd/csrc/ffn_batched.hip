@@ -656,13 +656,13 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_mfma(FFN_GATE_UP_PARAMS) {
   gate_up_body<W, LOPA, DENSE, NT, KU, NT == 1 ? 4 : 2, FORM>(FFN_GATE_UP_ARGS);
 }
 
-// Standard gating, one token tile: two k steps a group, so that two workgroups fit a CU
-// (at most 256 registers a lane); one workgroup's phase changes (LDS reductions, union)
-// then overlap the other's streaming.
-template <class W, bool DENSE, int FORM>
+// One token tile: two k steps a group, so that two workgroups fit a CU (at most 256
+// registers a lane); one workgroup's phase changes (LDS reductions, union) then overlap the
+// other's streaming.  LoPA's gate rows keep two k steps a group as in k_gate_up_mfma.
+template <class W, bool LOPA, bool DENSE, int FORM>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) void k_gate_up_mfma2(
     FFN_GATE_UP_PARAMS) {
-  gate_up_body<W, false, DENSE, 1, 2, 2, FORM>(FFN_GATE_UP_ARGS);
+  gate_up_body<W, LOPA, DENSE, 1, 2, 2, FORM>(FFN_GATE_UP_ARGS);
 }
 // ------------------------------------------------------------------ batches of 2 .. 4 tokens
 // For at most four tokens the gate and the W_up dots run on v_mfma_f32_4x4x4_16b_bf16:
@@ -1297,14 +1297,16 @@ hipError_t gate_mfma(const Shape& sh, const Form& form, const float* x, const vo
     }
   // two workgroups a CU only where their segments stay near 64 rows: halving 8B-shaped
   // segments to 28 rows left the row tiles half empty (int8 / int4 at four tokens: 52.7 /
-  // 54.4 us a call, 42.1 / 41.9 us with one workgroup a CU)
-  const bool two = !LOPA && NT == 1 && sh.d_ff >= 48 * kSegGrid2;
+  // 54.4 us a call, 42.1 / 41.9 us with one workgroup a CU).  On the 70B shape LoPA gains
+  // too (eight tokens: gate kernel 76.1 -> 71.1 us), where one workgroup a CU walks two
+  // segments one after the other.
+  const bool two = NT == 1 && sh.d_ff >= 48 * kSegGrid2;
   const int grid = two ? kSegGrid2 : kSegGrid;
   ws.nseg = segments_for(sh.d_ff, grid);
   const int g = ws.nseg < grid ? ws.nseg : grid;
   auto kernel = k_gate_up_mfma<W, LOPA, DENSE, NT, FORM>;
-  if constexpr (!LOPA && NT == 1)
-    if (two) kernel = k_gate_up_mfma2<W, DENSE, FORM>;
+  if constexpr (NT == 1)
+    if (two) kernel = k_gate_up_mfma2<W, LOPA, DENSE, FORM>;
   return launch_gate_kernel(kernel, g, s, x, (const float*)ws.z, static_cast<const uint4*>(gate_w), Cg,
                             static_cast<const uint4*>(w_up), Cu, sh.T, sh.d, sh.d_ff, ws.nseg, t, ws.slots, ws.tc,
                             ws.meta, ws.seg_count, ws.seg_idx, ws.seg_act, ws.zf, y, ws.xs, token_tiles(ws), form,

@@ -56,6 +56,8 @@ CASES = [
     ("mc_lopa_bf16_T70_g", 70, 264, 1000, 40, BF16, 1.3 * S2, dict(act=1, use_g=True)),
     ("mc_lopa_bf16_T90_all", 90, 264, 1000, 40, BF16, 1.6 * S2, ALL),   # 64 + 26: a pre-split two-tile tail
     ("mc_std_bf16_T100_act", 100, 264, 1000, 0, BF16, 1.6, ACT),
+    ("mc2_lopa_bf16_T8_all", 8, 264, 24576, 40, BF16, 1.2 * S2, ALL),   # LoPA with two gate workgroups a CU
+    ("mc2_std_bf16_T5_act", 5, 264, 24576, 0, BF16, 1.2, ACT),
 ]
 
 

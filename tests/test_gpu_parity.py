@@ -44,6 +44,8 @@ SMALL = [
     ("std_bf16_T64", 64, 264, 1000, 0, BF16, 1.6),
     ("std_bf16_T17", 17, 136, 300, 0, BF16, 1.2),           # pre-split tokens, second tile nearly empty
     ("std_bf16_T8_dff24576", 8, 264, 24576, 0, BF16, 1.2),  # 512 segments: two halves a gate workgroup
+    ("lopa_bf16_T8_dff24576", 8, 264, 24576, 40, BF16, 1.2),  # LoPA with two gate workgroups a CU
+    ("lopa_bf16_T16_dff24600", 16, 264, 24600, 72, BF16, 1.4),  # ragged segments, 16 tokens
     ("lopa_bf16_T70", 70, 264, 1000, 40, BF16, 1.3),        # a pre-split 64-token pass, then 6 tokens
     ("std_bf16_T100", 100, 264, 1000, 0, BF16, 1.6),        # 64 + 36: the tail pass is pre-split (three tiles)
     ("lopa_bf16_T100", 100, 264, 1000, 40, BF16, 1.6),

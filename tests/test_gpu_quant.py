@@ -56,6 +56,8 @@ SMALL = [
     ("i4_T20", 20, 288, 999, 0, I4, 0.9),               # two token tiles; 9 chunks a row
     ("i8_T40_ragged", 40, 272, 999, 0, I8, 0.9),        # pre-split tokens; a half k step at the end
     ("i4_T64_lopa", 64, 256, 1000, 64, I4, 1.0),        # four token tiles
+    ("i8_T8_lopa_dff24576", 8, 256, 24576, 32, I8, 1.0),  # LoPA with two gate workgroups a CU
+    ("i4_T6_std_dff24600", 6, 288, 24600, 0, I4, 0.9),    # the same for standard gating
     ("i8_T4_gen_odd_d", 4, 100, 77, 0, I8, 0.5),        # d not a multiple of 16: element-wise
     ("i4_T6_gen_d48", 6, 48, 77, 0, I4, 0.5),           # d not a multiple of 32: element-wise
 ]
