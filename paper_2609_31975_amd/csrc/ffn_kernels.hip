@@ -1716,10 +1716,17 @@ int cu_count() {
   return cus[slot];
 }
 
+// At least kSegMinRows rows a segment, and at most d / kDnChunkCapDiv row chunks in the down
+// kernel: on a small FFN (d 256, d_ff 1024) one-row segments over 768 workgroups and 256 row
+// chunks, each chunk adding into the same few cache lines of y, left the call at 13.3 us; with
+// both limits it takes 7.8 us.  The 8B and 70B shapes are above both limits.
+constexpr int kSegMinRows = 16;
+constexpr int kDnChunkCapDiv = 16;
+
 // Segments for the T = 1 gate kernel: one row-balanced segment per workgroup slot the
 // GPU holds at once (so every CU gets the same number of rows; more segments than
-// resident slots measured slower), never more than kSegMax rows per segment.  `per_cu`
-// caches the kernel's occupancy.
+// resident slots measured slower), never more than kSegMax rows per segment nor fewer than
+// kSegMinRows (where d_ff allows).  `per_cu` caches the kernel's occupancy.
 template <class K>
 int resident_segments(K kernel, int* per_cu, int d_ff) {
   if (*per_cu == 0) {
@@ -1729,6 +1736,8 @@ int resident_segments(K kernel, int* per_cu, int d_ff) {
   }
   int g = cu_count() * *per_cu;
   const int lo = (d_ff + kSegMax - 1) / kSegMax;
+  const int hi = (d_ff + kSegMinRows - 1) / kSegMinRows;
+  if (g > hi) g = hi;
   if (g < lo) g = lo;
   if (g > d_ff) g = d_ff;
   return g;
@@ -1914,9 +1923,10 @@ hipError_t lopa_z(const Shape& sh, const Form& form, const float* x, const void*
 
 // Down-projection grid for T = 1: S column slices x R row chunks, about wg_per_cu
 // workgroups per CU, at most 64 segments per chunk.
-void down_grid(int C, int lg, int wg_per_cu, int nseg, int d_ff, int* S, int* R, size_t* shmem_rows) {
+void down_grid(int C, int lg, int wg_per_cu, int nseg, int d_ff, int d, int* S, int* R, size_t* shmem_rows) {
   *S = (C + lg - 1) / lg;
   int r = (wg_per_cu * cu_count() + *S - 1) / *S;
+  if (r > d / kDnChunkCapDiv) r = d / kDnChunkCapDiv > 1 ? d / kDnChunkCapDiv : 1;
   const int rmin = (nseg + kWave - 1) / kWave;
   if (r < rmin) r = rmin;
   if (r > nseg) r = nseg;
@@ -1936,7 +1946,7 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
   const int C = sh.d / W::EPC;
   int S = 0, R = 0;
   size_t rows = 0;
-  if (rows_ok) down_grid(C, LG, WG_PER_CU, ws.nseg, sh.d_ff, &S, &R, &rows);
+  if (rows_ok) down_grid(C, LG, WG_PER_CU, ws.nseg, sh.d_ff, sh.d, &S, &R, &rows);
   const size_t shmem_t1 = DENSE ? 0 : 2 * sizeof(int) * rows, shmem_tb = (1 + TG) * sizeof(int) * rows;
   // bf16 rows of 1024 chunks or more (d >= 8192): 1 KB column slices, so that each workgroup
   // stages half as many slots (70B: 12.6 -> 12.2 us; on d = 4096 the 512-byte slices are faster)
@@ -1944,7 +1954,7 @@ hipError_t down(const Shape& sh, const void* w_down_t, const Workspace& ws, floa
     if (rows_ok && sh.T == 1 && C >= 1024) {
       int S2 = 0, R2 = 0;
       size_t rows2 = 0;
-      down_grid(C, 64, WG_PER_CU, ws.nseg, sh.d_ff, &S2, &R2, &rows2);
+      down_grid(C, 64, WG_PER_CU, ws.nseg, sh.d_ff, sh.d, &S2, &R2, &rows2);
       const size_t shmem2 = DENSE ? 0 : 2 * sizeof(int) * rows2;
       if (shmem2 <= 96 * 1024) {
         k_down_t1<W, DENSE, 64><<<S2 * R2, kBlock, shmem2, s>>>(ws.seg_count, ws.seg_idx, ws.seg_zval, ws.nseg,
