@@ -19,7 +19,9 @@
 //   k_lopa_z_mfma  z = A x as two partial sums over halves of the d range;
 //   k_gate_up_mfma per segment of at most 64 rows: gate, union of the tokens' active rows,
 //                  ascending, W_up dots of the union rows; zval = act * v is left in
-//                  the A-operand fragment order of the down product;
+//                  the A-operand fragment order of the down product (k_gate_up_q4 does the
+//                  same for 2..4 tokens on 4x4x4 products, k_gate_up_mfma2 at two
+//                  workgroups a CU where d_ff is large);
 //   k_down_mfma    Y[tokens][cols] += Z[tokens][entries] D[entries][cols] over the
 //                  union rows, segment by segment.
 // A wave of the gate kernel multiplies four row tiles over a quarter of the k range, so
