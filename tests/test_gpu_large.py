@@ -1,5 +1,6 @@
-"""GPU parity on weight matrices larger than 2 GiB, the most the fast kernels address with
-32-bit byte offsets: such calls take the element-wise kernels, which address rows in 64 bits.
+"""GPU parity on weight matrices around 2 GiB, the most the fast kernels address with 32-bit
+byte offsets: just below it the fast kernels run at their largest offsets, past it the calls
+take the element-wise kernels, which address rows in 64 bits.
 
 Each large matrix is zero except for K rows spread over its whole address range (the first
 rows, rows on both sides of byte 2^31, the last row), which hold a seeded K-row weight set.  A
@@ -26,6 +27,11 @@ CASES = [
     # fp32 rows of 16 KB likewise
     ("std_f32_d4096_T1", 1, 4096, 131080, 0, wl.F32,
      [0, 1, 65536, 131071, 131072, 131073, 131076, 131079]),
+    # just below 2^31 bytes (2^31 - 128 KB): the single-token kernels, the two-workgroup batch
+    # kernel and LoPA's single-token kernel with z inside, at their largest row offsets
+    ("std_d8192_T1_fast_edge", 1, 8192, 131064, 0, wl.BF16, [0, 1, 65536, 131056, 131060, 131061, 131062, 131063]),
+    ("std_d8192_T8_fast_edge", 8, 8192, 131064, 0, wl.BF16, [0, 65536, 131059, 131060, 131062, 131063]),
+    ("lopa_d8192_T1_fast_edge", 1, 8192, 131064, 1024, wl.BF16, [0, 2, 98304, 131057, 131061, 131062, 131063]),
     # LoPA: B rows of 1032 bf16 (2064 bytes), the largest d_ff the calls take (2^20); row 1040448
     # is the first B row past byte 2^31; W_up / W_down are exactly 2 GiB
     ("lopa_dff2p20_T1", 1, 1024, 1 << 20, 1032, wl.BF16,
@@ -45,7 +51,7 @@ RUNS = [(c, False) for c in CASES] + [(CASES[0], True)]  # the dense baseline on
 
 
 @pytest.mark.parametrize("case,dense", RUNS, ids=[c[0] + ("-dense" if dn else "-sparse") for c, dn in RUNS])
-def test_matrices_beyond_2gib(gu, case, dense):
+def test_matrices_around_2gib(gu, case, dense):
     import torch
     from paper_2609_31975_amd import ffn
     name, T, d, d_ff, r, wdt, rows = case
