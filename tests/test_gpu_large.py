@@ -32,6 +32,10 @@ CASES = [
     ("std_d8192_T1_fast_edge", 1, 8192, 131064, 0, wl.BF16, [0, 1, 65536, 131056, 131060, 131061, 131062, 131063]),
     ("std_d8192_T8_fast_edge", 8, 8192, 131064, 0, wl.BF16, [0, 65536, 131059, 131060, 131062, 131063]),
     ("lopa_d8192_T1_fast_edge", 1, 8192, 131064, 1024, wl.BF16, [0, 2, 98304, 131057, 131061, 131062, 131063]),
+    # int8 codes just below 2^31 bytes (8 KB rows, the widest rows of the single-token integer-dot
+    # kernels); four tokens take the element-wise batch kernels with codes
+    ("i8_d8192_T1_fast_edge", 1, 8192, 262136, 0, wl.I8, [0, 1, 131072, 262128, 262133, 262134, 262135]),
+    ("i8_d8192_T4", 4, 8192, 262136, 0, wl.I8, [0, 100000, 262130, 262132, 262134, 262135]),
     # LoPA: B rows of 1032 bf16 (2064 bytes), the largest d_ff the calls take (2^20); row 1040448
     # is the first B row past byte 2^31; W_up / W_down are exactly 2 GiB
     ("lopa_dff2p20_T1", 1, 1024, 1 << 20, 1032, wl.BF16,
@@ -60,10 +64,17 @@ def test_matrices_around_2gib(gu, case, dense):
     inp = wl.make_inputs(seed=4242 + len(name), T=T, d=d, d_ff=K, r=r, wdt=wdt)
     where = torch.tensor(rows, dtype=torch.int64, device="cuda")
 
+    tdt = {wl.BF16: torch.bfloat16, wl.F32: torch.float32, wl.I8: torch.int8}[wdt]
+
     def big(cols, small):
-        m = torch.zeros((d_ff, cols), dtype=torch.bfloat16 if wdt == wl.BF16 else torch.float32, device="cuda")
+        m = torch.zeros((d_ff, cols), dtype=tdt, device="cuda")
         m[where] = gu.to_dev(small)
         return m
+
+    def big_scale(small):  # one fp32 scale a row; the zero rows' scales are 1
+        v = torch.ones(d_ff, dtype=torch.float32, device="cuda")
+        v[where] = gu.to_dev(small)
+        return v
 
     print(f"[large] {name} {'dense' if dense else 'sparse'}: d {d} d_ff {d_ff} r {r} T {T}", flush=True)
     x = gu.to_dev(inp.x)
@@ -71,11 +82,17 @@ def test_matrices_around_2gib(gu, case, dense):
     gate = (gu.to_dev(inp.lopa_a), big(r, inp.lopa_b)) if r else (big(d, inp.w_gate),)
     ws = ffn.alloc_workspace(T, d, d_ff, r)
     y = torch.full((T, d), float("nan"), dtype=torch.float32, device="cuda")
-    if r:
-        fn = ffn.ffn_lopa_dense_forward if dense else ffn.ffn_lopa_sparse_forward
+    if wdt == wl.I8:
+        assert r == 0 and not dense
+        sc = ffn.scales(gate=big_scale(inp.scales["gate"]), up=big_scale(inp.scales["up"]),
+                        down=big_scale(inp.scales["down"]))
+        ffn.ffn_sparse_forward_q(x, *gate, w_up, w_down_t, sc, T_GATE, None, y, ws)
     else:
-        fn = ffn.ffn_dense_forward if dense else ffn.ffn_sparse_forward
-    fn(x, *gate, w_up, w_down_t, T_GATE, y, ws)
+        if r:
+            fn = ffn.ffn_lopa_dense_forward if dense else ffn.ffn_lopa_sparse_forward
+        else:
+            fn = ffn.ffn_dense_forward if dense else ffn.ffn_sparse_forward
+        fn(x, *gate, w_up, w_down_t, T_GATE, y, ws)
     torch.cuda.synchronize()
     y_gpu = y.cpu().numpy()
     res = gu.run_oracle(inp, T_GATE, dense=dense)
