@@ -258,6 +258,15 @@ int ffn_workspace_active(const void* ws, int T, int d, int d_ff, int r, const in
  * or FFN_ERR_NULL if exactly one event is NULL. */
 int ffn_time_next_gate_kernel(hipEvent_t start, hipEvent_t stop);
 
+/* Test hook.  The single-token LoPA gate kernel shares z = A x (Section 3.3, Eq. (lopaapprox))
+ * between its workgroups: each computes some components and publishes them, then waits for
+ * the others' components for at most `ticks` of the 100 MHz constant clock (10000 = 100 us by
+ * default) and computes any still missing itself, so the kernel ends whatever the residency
+ * of its workgroups.  This sets that bound for the calls that follow, on every thread; a small
+ * value sends most workgroups down the self-computing path, which lets tests check it.  The
+ * results stay within the parity tolerances either way.  Returns FFN_OK. */
+int ffn_set_z_wait_ticks(uint64_t ticks);
+
 /* Human-readable text for a status code. */
 const char* ffn_status_string(int status);
 

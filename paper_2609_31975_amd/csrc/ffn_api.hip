@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -14,6 +15,8 @@
 namespace ffn {
 
 thread_local GateTiming g_gate_timing;
+std::atomic<uint64_t> g_z_wait{kZWaitTicks};
+uint64_t z_wait_ticks() { return g_z_wait.load(std::memory_order_relaxed); }
 
 namespace {
 constexpr size_t kAlign = 256;
@@ -92,6 +95,7 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 // norm's gain and eps (eps 0: no norm).
 int check_options(const ffn_options_t* o, bool lopa, Form* form) {
   *form = Form{};
+  form->z_wait = z_wait_ticks();
   if (!o) return FFN_OK;
   if ((o->act != FFN_ACT_RELU && o->act != FFN_ACT_RSPLUS) || (o->silu_up != 0 && o->silu_up != 1) ||
       (o->rms_norm != 0 && o->rms_norm != 1))
@@ -370,6 +374,11 @@ int ffn_workspace_active(const void* ws, int T, int d, int d_ff, int r, const in
 int ffn_time_next_gate_kernel(hipEvent_t start, hipEvent_t stop) {
   if ((start == nullptr) != (stop == nullptr)) return FFN_ERR_NULL;
   ffn::g_gate_timing = ffn::GateTiming{start, stop};
+  return FFN_OK;
+}
+
+int ffn_set_z_wait_ticks(uint64_t ticks) {
+  ffn::g_z_wait.store(ticks, std::memory_order_relaxed);
   return FFN_OK;
 }
 

@@ -108,6 +108,7 @@ struct Form {
   const int8_t* g_sign = nullptr;  // G's value per row
   const float* rms_gain = nullptr;  // RMSNorm gains over z (null: ones)
   float rms_eps = 0.f;              // > 0: RMSNorm between the LoPA factors
+  uint64_t z_wait = kZWaitTicks;    // single-token LoPA: the gate workgroups' bounded wait for z
   bool full() const { return act != 0 || silu_up != 0 || g_idx != nullptr || rms_eps > 0.f; }
   int kind() const { return g_idx != nullptr || rms_eps > 0.f ? kFormLoPA : full() ? kFormAct : kFormDefault; }
 };
@@ -118,6 +119,9 @@ struct GateTiming {
   hipEvent_t stop = nullptr;
 };
 extern thread_local GateTiming g_gate_timing;
+
+// The bounded wait for z of the calls that follow (ffn_set_z_wait_ticks; kZWaitTicks unless set).
+uint64_t z_wait_ticks();
 
 // Launchers (return hipSuccess or the launch error).  Every launcher enqueues on `s`.
 // With form.rms_eps > 0 on the single-token path, z is stored times the RMSNorm gains and

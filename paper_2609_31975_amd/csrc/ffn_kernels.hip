@@ -677,8 +677,9 @@ __global__ __launch_bounds__(kBlock) void k_lopa_z_row(const float* __restrict__
 // r components back, each with one 64-bit load, until every tag is there.  The loads of the
 // A rows go out first, then the workgroup's B rows, so that the rows stream while z is formed
 // and handed over, and the wait for z covers only the A rows.  The down kernel of the call
-// clears the tags.  A workgroup that has not seen every component after kZWaitTicks computes
-// the missing ones itself, so the kernel finishes whatever the residency of its workgroups.
+// clears the tags.  A workgroup that has not seen every component after form.z_wait ticks
+// (kZWaitTicks unless a test shortens it) computes the missing ones itself, so the kernel
+// finishes whatever the residency of its workgroups.
 template <class W, bool LOPA, bool DENSE, int CPLG, int CPLU, int FORM, int CPLA = 0>
 __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__ x, const float* __restrict__ z,
                                                        const uint4* __restrict__ gate_w, int Cg, int lprg,
@@ -883,7 +884,7 @@ __global__ __launch_bounds__(kBlock) void k_gate_up_t1(const float* __restrict__
                 }
               }
               if (__syncthreads_and(all)) break;
-              if (__syncthreads_or(wall_clock64() - t0 > kZWaitTicks)) {
+              if (__syncthreads_or(wall_clock64() - t0 > form.z_wait)) {
                 late = true;
                 break;
               }

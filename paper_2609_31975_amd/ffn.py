@@ -86,6 +86,8 @@ def lib() -> ctypes.CDLL:
         L.ffn_workspace_active.argtypes = [vp, i, i, i, i, pp, pp, pp, pp]
         L.ffn_time_next_gate_kernel.restype = i
         L.ffn_time_next_gate_kernel.argtypes = [vp, vp]
+        L.ffn_set_z_wait_ticks.restype = i
+        L.ffn_set_z_wait_ticks.argtypes = [ctypes.c_uint64]
         L.ffn_lopa_approx_workspace_bytes.restype = sz
         L.ffn_lopa_approx_workspace_bytes.argtypes = [i, i, i]
         L.ffn_lopa_approx.restype = i
@@ -361,6 +363,14 @@ def ffn_time_next_gate_kernel(start, stop):
     """Arm torch.cuda.Event pair (enable_timing=True) for the next call's gate kernel."""
     rc = lib().ffn_time_next_gate_kernel(ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event))
     _check("ffn_time_next_gate_kernel", rc)
+
+
+def ffn_set_z_wait_ticks(ticks: int):
+    """Set the single-token LoPA gate kernel's bounded wait for z (100 MHz ticks; test hook)."""
+    _check("ffn_set_z_wait_ticks", lib().ffn_set_z_wait_ticks(int(ticks)))
+
+
+Z_WAIT_TICKS_DEFAULT = 10000  # 100 us, the library's default
 
 
 def ffn_lopa_approx(w, r: int, max_iters: int = 20, stream=None):

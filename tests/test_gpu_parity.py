@@ -367,3 +367,43 @@ def test_workspace_active_under_graph_capture(gu, shape):
         res = gu.run_oracle(inp, t, x=x.cpu().numpy())
         gu.check_parity(res, y.cpu().numpy(), listed, acts, t, BF16, what=f"graph replay {rep}")
     del graph
+
+
+# ---------------------------------------------------------------- LoPA's z, computed by each workgroup
+# The single-token LoPA gate kernel shares z = A x between its workgroups and, past a bounded
+# wait, has a workgroup compute the components it has not seen itself.  A wait of 0 ticks (set
+# from the host; every kernel still ends normally) sends most workgroups down that path.
+Z_SELF = [
+    ("bf16_small", 264, 1000, 40, BF16, 1.0, False),
+    ("f32_small", 256, 1024, 32, F32, 1.2816, False),
+    ("bf16_8b_r512", 4096, 14336, 512, BF16, 1.2816, False),
+    ("bf16_70b_r1024", 8192, 2048, 1024, BF16, 1.2816, False),
+    ("bf16_norm_g", 264, 1000, 40, BF16, 1.0 * 2 ** 0.5, True),   # RMSNorm and G after the wait
+]
+
+
+@pytest.mark.parametrize("case", Z_SELF, ids=[c[0] for c in Z_SELF])
+def test_lopa_z_computed_by_each_workgroup(gu, case):
+    from paper_2609_31975_amd import ffn
+    name, d, d_ff, r, wdt, t, full = case
+    inp = wl.make_inputs(303, 1, d, d_ff, r=r, wdt=wdt)
+    dev = gu.DevInputs(inp)
+    form = None
+    if full:
+        form = gu.Form(act=1, silu_up=True, form=wl.make_form(304, d, d_ff, r), use_g=True, rms_norm=True,
+                       use_gain=True)
+    ffn.ffn_set_z_wait_ticks(0)
+    try:
+        if form is None:
+            y, idx, act, _ = gu.run_gpu(dev, t)
+        else:
+            y, idx, act, _ = gu.run_gpu_ex(dev, t, form)
+    finally:
+        ffn.ffn_set_z_wait_ticks(ffn.Z_WAIT_TICKS_DEFAULT)
+    res = gu.run_oracle(inp, t, form=form)
+    gu.check_parity(res, y, idx, act, t, wdt, what=f"z computed by each workgroup, {name}",
+                    act_value=None if form is None else form.act_value)
+    # and the default wait again on the same inputs
+    y2, idx2, act2, _ = gu.run_gpu(dev, t) if form is None else gu.run_gpu_ex(dev, t, form)
+    gu.check_parity(res, y2, idx2, act2, t, wdt, what=f"default wait, {name}",
+                    act_value=None if form is None else form.act_value)
