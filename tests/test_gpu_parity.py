@@ -238,16 +238,20 @@ def test_graph_replay(gu, shape):
 
 
 # ---------------------------------------------------------------- random shapes
-def _random_cases(n=12, seed=2026):
-    """Seeded shapes across every dispatch path: token counts 1..70, d and r multiples
-    of 8 (fast and matrix-core kernels) or not (element-wise), short and ragged d_ff."""
+def _random_cases(n=40, seed=2026):
+    """Seeded shapes across every dispatch path: token counts 1..130 (several passes of 64),
+    d and r multiples of 8 (fast and matrix-core kernels) or not (element-wise), short and
+    ragged d_ff, at most about 2e8 multiply-adds for the oracle."""
     rng = np.random.default_rng(seed)
     cases = []
-    for i in range(n):
-        T = int(rng.choice([1, 1, 2, 3, 5, 8, 13, 16, 17, 33, 64, 70]))
-        d = int(rng.choice([8, 64, 136, 264, 520, 1032, 100, 250]))
-        d_ff = int(rng.integers(3, 1500))
-        r = int(rng.choice([0, 0, 8, 16, 40, 24, 36]))
+    while len(cases) < n:
+        i = len(cases)
+        T = int(rng.choice([1, 1, 1, 2, 3, 4, 5, 8, 13, 16, 17, 33, 64, 70, 130]))
+        d = int(rng.choice([8, 64, 136, 264, 520, 1032, 2056, 4096, 100, 250]))
+        d_ff = int(rng.integers(3, 5000))
+        r = int(rng.choice([0, 0, 0, 8, 16, 40, 24, 36, 128, 520]))
+        if T * d * (d_ff + r) > 2e8:
+            continue
         wdt = BF16 if rng.random() < 0.75 else F32
         t = float(rng.choice([0.0, 0.8416, 1.2816, 1.6449]))
         cases.append((f"rand{i}_T{T}_d{d}_dff{d_ff}_r{r}_{'bf16' if wdt == BF16 else 'f32'}", T, d, d_ff, r, wdt, t))
