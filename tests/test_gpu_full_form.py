@@ -166,3 +166,41 @@ def test_fixed_matrix_variants(gu, kind, T, d, d_ff, r):
     res = gu.run_oracle(inp, t, form=form)
     fig = gu.check_parity(res, y, idx, act, t, BF16, what=f"{kind} T={T}", act_value=form.act_value)
     assert 0 < fig["n_union"] < d_ff
+
+
+def _random_form_cases(n=24, seed=2028):
+    """Seeded shapes and option sets of the full form across the dispatch paths (single
+    token, element-wise, matrix-core batches of one to four token tiles, several passes)."""
+    rng = np.random.default_rng(seed)
+    flag_sets = [ACT, ALL, G_ONLY, NORM_ONLY, dict(act=1), dict(silu_up=True), dict(use_g=True, act=1),
+                 dict(rms_norm=True, use_gain=True, silu_up=True)]
+    cases = []
+    while len(cases) < n:
+        i = len(cases)
+        T = int(rng.choice([1, 1, 1, 2, 3, 4, 7, 16, 17, 40, 64, 70]))
+        d = int(rng.choice([64, 136, 264, 1032, 4096, 100, 250]))
+        d_ff = int(rng.integers(5, 4000))
+        r = int(rng.choice([0, 16, 40, 128, 520, 36]))
+        wdt = BF16 if rng.random() < 0.75 else F32
+        flags = flag_sets[int(rng.integers(len(flag_sets)))]
+        if r == 0:  # G and the norm are LoPA's
+            flags = {k: v for k, v in flags.items() if k in ("act", "silu_up")} or dict(act=1)
+        if T * d * (d_ff + r) > 2e8:
+            continue
+        t = 1.2816 * (S2 if flags.get("use_g") else 1.0)
+        tag = f"frand{i}_T{T}_d{d}_dff{d_ff}_r{r}_{'bf16' if wdt == BF16 else 'f32'}_" + "+".join(sorted(flags))
+        cases.append((tag, T, d, d_ff, r, wdt, t, flags))
+    return cases
+
+
+FRANDOM = _random_form_cases()
+
+
+@pytest.mark.parametrize("case", FRANDOM, ids=[c[0] for c in FRANDOM])
+def test_full_form_random_shapes(gu, case):
+    name, T, d, d_ff, r, wdt, t, flags = case
+    inp = wl.make_inputs(206, T, d, d_ff, r=r, wdt=wdt)
+    form = _form(gu, inp, flags)
+    y, idx, act, _ = gu.run_gpu_ex(gu.DevInputs(inp), t, form)
+    res = gu.run_oracle(inp, t, form=form)
+    gu.check_parity(res, y, idx, act, t, wdt, what=name, act_value=form.act_value)

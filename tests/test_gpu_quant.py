@@ -147,3 +147,42 @@ def test_quant_workloads(gu, w):
     frac = np.mean(fig["n_active"]) / w.d_ff
     assert 0.05 < frac < 0.15
     print(w.name, fig["max_rel_err"], fig["n_union"], flush=True)
+
+
+def _random_quant_cases(n=24, seed=2027):
+    """Seeded shapes for int8 / int4 codes across the dispatch paths: d and r multiples of
+    the chunk width (16 / 32 codes: integer-dot and matrix-core kernels) or only even
+    (element-wise), 1..70 tokens, with and without the full form."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        i = len(cases)
+        wdt = I8 if rng.random() < 0.5 else I4
+        T = int(rng.choice([1, 1, 1, 2, 3, 4, 5, 8, 16, 17, 40, 70]))
+        d = int(rng.choice([32, 64, 256, 512, 1024, 4096, 96, 100, 258]))
+        d_ff = int(rng.integers(5, 4000))
+        r = int(rng.choice([0, 0, 32, 64, 128, 512, 96, 34]))
+        full = bool(rng.random() < 0.3)
+        if T * d * (d_ff + r) > 2e8:
+            continue
+        tag = f"qrand{i}_{'i8' if wdt == I8 else 'i4'}_T{T}_d{d}_dff{d_ff}_r{r}{'_form' if full else ''}"
+        cases.append((tag, T, d, d_ff, r, wdt, full))
+    return cases
+
+
+QRANDOM = _random_quant_cases()
+
+
+@pytest.mark.parametrize("case", QRANDOM, ids=[c[0] for c in QRANDOM])
+def test_quant_random_shapes(gu, case):
+    name, T, d, d_ff, r, wdt, full = case
+    inp = wl.make_inputs(305, T, d, d_ff, r=r, wdt=wdt)
+    form = None
+    t = 1.2816
+    if full:
+        flags = ALL if r else dict(act=1, silu_up=True)
+        form = gu.Form(form=wl.make_form(10, d, d_ff, r), **flags)
+        t *= math.sqrt(2) if r else 1.0
+    y, idx, act, _ = gu.run_gpu_q(gu.DevInputs(inp), t, form=form)
+    res = gu.run_oracle(inp, t, form=form)
+    gu.check_parity(res, y, idx, act, t, wdt, what=name, act_value=None if form is None else form.act_value)
