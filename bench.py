@@ -608,6 +608,10 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
+        # the paper's own FFN-only GPU speedups (Section 5.3), context only: its 5.8B-parameter
+        # model on a GPU the paper does not name, not this workload or machine
+        "paper_context": {"speedup_vs_dense": {"standard_s90": 2.06, "lopa_s90": 3.31, "lopa_s95": 3.90},
+                          "model": "5.8B parameters (FFN only)", "gpu": "not stated in the paper"},
         "dtype": "f32",
         "weight_dtype": {0: "f32", 1: "bf16", 2: "int8", 3: "int4"}[head.wdt],
         "data": "synthetic: seeded Gaussian weights (N(0,1/d), W_down N(0,1/d_ff)), iid N(0,1) tokens",
