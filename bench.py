@@ -546,7 +546,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the sparse FFN hot path here is a single-GPU kernel "
-              "sequence and this build runs no collectives; use --gpus 1", file=sys.stderr)
+              "sequence and the library runs no collectives; use --gpus 1", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2609_31975_amd import ffn
