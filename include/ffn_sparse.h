@@ -197,10 +197,12 @@ typedef struct {
  * (else FFN_ERR_SHAPE).  Errors as for the other calls; FFN_ERR_NULL for a missing
  * scales struct or array, FFN_ERR_ALIGN for a misaligned scale array, FFN_ERR_OPTION for
  * scales with fp32 / bf16 weights.  Quantized weights take the single-token kernels
- * (T = 1, d a multiple of 16 (int8) or 32 (int4), up to 8192) or the element-wise kernels
- * (any other shape or batch).  The single-token kernels form their dot products with
- * the integer dot instructions against a 24-bit fixed-point copy of x (or z): relative
- * to the vector's largest magnitude, each element is exact to 2^-24. */
+ * (T = 1, d a multiple of 16 (int8) or 32 (int4), up to 8192), the matrix-core batch
+ * kernels (2..64 tokens a pass, d and r multiples of 16 / 32; the codes enter the bf16
+ * products unchanged, being small integers) or the element-wise kernels (any other shape).
+ * The single-token kernels form their dot products with the integer dot instructions
+ * against a 24-bit fixed-point copy of x (or z): relative to the vector's largest
+ * magnitude, each element is exact to 2^-24. */
 int ffn_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, const float* x, const void* w_gate,
                         const void* w_up, const void* w_down_t, const ffn_scales_t* scales, float t,
                         const ffn_options_t* opt, float* y, void* ws, size_t ws_bytes, hipStream_t stream);
