@@ -193,7 +193,10 @@ def test_repeatable(gu, r):
     assert gu.rel_err(y2, y1) < 1e-6
 
 
-GRAPH_SHAPES = [(1, 4096, 2056, 0), (4, 264, 1000, 40), (20, 264, 1000, 40), (64, 264, 1000, 0)]
+GRAPH_SHAPES = [(1, 4096, 2056, 0), (4, 264, 1000, 40), (20, 264, 1000, 40), (64, 264, 1000, 0),
+                (1, 4096, 2056, 512),     # LoPA's z handed between gate workgroups through tagged words
+                (3, 4096, 2056, 0), (3, 4096, 2056, 512),   # the 4x4x4 batch kernel
+                (8, 1024, 24576, 0), (8, 1024, 24576, 64)]  # two gate workgroups a CU
 
 
 @pytest.mark.parametrize("shape", GRAPH_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}")
@@ -411,3 +414,57 @@ def test_lopa_z_computed_by_each_workgroup(gu, case):
     y2, idx2, act2, _ = gu.run_gpu(dev, t) if form is None else gu.run_gpu_ex(dev, t, form)
     gu.check_parity(res, y2, idx2, act2, t, wdt, what=f"default wait, {name}",
                     act_value=None if form is None else form.act_value)
+
+
+# ---------------------------------------------------------------- graph replay: full form, int8 codes
+@pytest.mark.parametrize("kind,T,r", [("form", 1, 512), ("form", 4, 512), ("form", 20, 40), ("int8", 1, 0),
+                                      ("int8", 1, 512), ("int8", 4, 512), ("int4", 16, 64)])
+def test_graph_replay_form_and_codes(gu, kind, T, r):
+    """The full form (G, RMSNorm, R-S+, SiLU) and int8 / int4 codes captured in a HIP graph:
+    every replay gives the eager result, with y filled with NaN and other work in between."""
+    import torch
+    from paper_2609_31975_amd import ffn
+    d, d_ff = (4096, 2056) if T <= 4 else (264, 1000)
+    wdt = {"form": BF16, "int8": wl.I8, "int4": wl.I4}[kind]
+    inp = wl.make_inputs(108, T, d, d_ff, r=r, wdt=wdt)
+    dev = gu.DevInputs(inp)
+    form = None
+    t = 1.2816
+    if kind == "form":
+        form = gu.Form(act=1, silu_up=True, form=wl.make_form(109, d, d_ff, r), use_g=True, rms_norm=True,
+                       use_gain=True)
+        t *= 2 ** 0.5
+    ws = ffn.alloc_workspace(T, d, d_ff, r)
+    y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+    opt = None if form is None else form.options()
+    sc = None if kind == "form" else dev.scales_struct()
+    gate = (dev.lopa_a, dev.lopa_b) if r else (dev.w_gate,)
+
+    def call():
+        if kind == "form":
+            fn = ffn.ffn_lopa_sparse_forward_ex if r else ffn.ffn_sparse_forward_ex
+            fn(dev.x, *gate, dev.w_up, dev.w_down_t, t, opt, y, ws)
+        else:
+            fn = ffn.ffn_lopa_sparse_forward_q if r else ffn.ffn_sparse_forward_q
+            fn(dev.x, *gate, dev.w_up, dev.w_down_t, sc, t, opt, y, ws)
+
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        call()
+    torch.cuda.synchronize()
+    y_eager = y.cpu().numpy()
+    gu.check_parity(gu.run_oracle(inp, t, form=form), y_eager, None, None, t, wdt, what=f"{kind} eager")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        call()
+    other = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):
+        y.fill_(float("nan"))
+        other.mul_(1.0001)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        y_rep = y.cpu().numpy()
+        assert np.isfinite(y_rep).all(), f"replay {rep} left entries unwritten"
+        assert gu.rel_err(y_rep, y_eager) < 1e-6, f"replay {rep}"
+    del graph
