@@ -468,3 +468,46 @@ def test_graph_replay_form_and_codes(gu, kind, T, r):
         assert np.isfinite(y_rep).all(), f"replay {rep} left entries unwritten"
         assert gu.rel_err(y_rep, y_eager) < 1e-6, f"replay {rep}"
     del graph
+
+
+# ---------------------------------------------------------------- concurrent calls
+@pytest.mark.parametrize("r", [0, 512], ids=["standard", "lopa512"])
+def test_concurrent_streams(gu, r):
+    """Calls with distinct workspaces on two streams at once (the header allows it): each
+    stream's results equal a call made alone.  With LoPA, the two single-token gate kernels
+    share the GPU, so their workgroups are not all resident together and the bounded wait
+    for z (each workgroup computing what it has not seen) keeps both finite."""
+    import torch
+    from paper_2609_31975_amd import ffn
+    d, d_ff, t = 4096, 14336, 1.2816
+    inps = [wl.make_inputs(110 + k, 1, d, d_ff, r=r, wdt=BF16) for k in range(2)]
+    devs = [gu.DevInputs(i) for i in inps]
+    wss = [ffn.alloc_workspace(1, d, d_ff, r) for _ in range(2)]
+    ys = [torch.empty((1, d), dtype=torch.float32, device="cuda") for _ in range(2)]
+
+    def call(k):
+        dv = devs[k]
+        if r:
+            ffn.ffn_lopa_sparse_forward(dv.x, dv.lopa_a, dv.lopa_b, dv.w_up, dv.w_down_t, t, ys[k], wss[k])
+        else:
+            ffn.ffn_sparse_forward(dv.x, dv.w_gate, dv.w_up, dv.w_down_t, t, ys[k], wss[k])
+
+    alone = []
+    for k in range(2):
+        call(k)
+        torch.cuda.synchronize()
+        alone.append(ys[k].cpu().numpy())
+        gu.check_parity(gu.run_oracle(inps[k], t), alone[k], None, None, t, BF16, what=f"alone {k}")
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(20):
+        for k in range(2):
+            ys[k].fill_(float("nan"))
+        torch.cuda.synchronize()
+        for k in range(2):
+            with torch.cuda.stream(streams[k]):
+                call(k)
+        torch.cuda.synchronize()
+        for k in range(2):
+            got = ys[k].cpu().numpy()
+            assert np.isfinite(got).all(), f"rep {rep} stream {k}: entries unwritten"
+            assert gu.rel_err(got, alone[k]) < 1e-5, f"rep {rep} stream {k}"
