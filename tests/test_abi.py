@@ -235,3 +235,11 @@ def test_noalloc_argument_errors():
     assert f(1, 1, 64, 128, MIS, A, A, A, c, A, None) == -4
     assert ffn.workspace_bytes(64, 8192, 28672, 0) > 16 << 20
     assert f(1, 64, 8192, 28672, A, A, A, A, c, A, None) == -5
+
+
+def test_z_wait_hook():
+    """The test hook for the single-token LoPA kernel's bounded wait takes any tick count
+    (host state only; nothing is launched)."""
+    for ticks in (0, 1, 10000, (1 << 64) - 1):
+        assert L.ffn_set_z_wait_ticks(ctypes.c_uint64(ticks)) == 0
+    ffn.ffn_set_z_wait_ticks(ffn.Z_WAIT_TICKS_DEFAULT)
