@@ -21,6 +21,9 @@ sparsity, T = 1), with
                        call-level fraction of peak is ``hbm_frac_touched``)
 * ``roofline``         the dominant (gate) kernel alone: algorithmic bytes per launch /
                        its average duration from hipExtLaunchKernel start/stop events
+* ``us_per_call_mall_flushed``  the same call eager, each after a 1 GiB write that evicts
+                       the Infinity Cache and the L2s (median of 20; also on the sweep's
+                       single-token rows)
 * ``cpu_baseline``     the fp64 oracle on one host core for a bounded sample of the
                        headline workload (and the dense oracle on three calls)
 * ``sweep``            the other workloads (70B LoPA and 8-token batches; 8B standard
@@ -268,6 +271,29 @@ def time_graph(run: Runner, K: int, W: int):
         w1 = time.perf_counter()
     del graph
     return (w1 - w0) * 1e6 / K, e0.elapsed_time(e1) * 1e3 / K
+
+
+FLUSH_BYTES = 1 << 30
+
+
+def time_flushed(run: Runner, n: int = 20):
+    """Median µs of n eager calls, each after a 1 GiB write that evicts the 256 MB Infinity
+    Cache and the L2s: its own event pair around the call only.  The host enqueues the call
+    while the write runs, so the call's kernels follow one another as in the graph."""
+    torch = run.torch
+    buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    run(0)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        buf.fill_(i & 0xFF)
+        a.record(stream)
+        run(i)
+        b.record(stream)
+    torch.cuda.synchronize()
+    del buf
+    return float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
 
 
 def time_gate_kernel(run: Runner, K: int):
@@ -590,6 +616,7 @@ def main():
     rec, run, nlist = measure(sh, r0, T0, head.t, K, W, dense_us=dense_us, name=head.name, exact=True, form=hform,
                               rho=head.rho)
     gate_mean, gate_med = time_gate_kernel(run, K)
+    flushed = time_flushed(run)
     gbytes = np.mean([gate_kernel_bytes(head.d, head.d_ff, r0, T0, k, False, head.wdt) for k in nlist])
     par = parity_sample(sh, r0, T0, head.t, form=hform, form_seed=head.seed)
     traffic, traffic_src = recorded_traffic(head.name)
@@ -632,6 +659,8 @@ def main():
                      "call_level_frac": rec["hbm_frac_touched"]},
         "parity_sample": par,
         "us_per_call_events": rec["us_per_call_events"],
+        # eager calls, each after a 1 GiB write (Infinity Cache and L2 cold), median
+        "us_per_call_mall_flushed": round(flushed, 3),
     }
 
     # ---- sweep
@@ -646,7 +675,10 @@ def main():
         tdense = {}
         for w in works:
             form = full_form(shp, w.r, w.seed) if w.form == "full" else None
-            rw = measure(shp, w.r, w.T, w.t, k, w_, name=w.name, form=form, rho=w.rho)[0]
+            rw, rrun, _ = measure(shp, w.r, w.T, w.t, k, w_, name=w.name, form=form, rho=w.rho)
+            if w.T == 1:
+                rw["us_per_call_mall_flushed"] = round(time_flushed(rrun), 3)
+            del rrun
             if w.rho:
                 rw["token_correlation"] = w.rho
                 base = [q for q in sweep if q.get("workload") == f"8b_lopa512_s90_T{w.T}"]
