@@ -47,9 +47,10 @@
  * Faults during execution surface at the caller's next synchronization of `stream`.
  *
  * Semantics of special values: a NaN gate value is inactive (h > t is false).
- * Inf/NaN in the w_up / w_down_t rows of a neuron that is active for any token of
- * the batch propagate into every token's output (the row is read for the union).
- * Rows of neurons inactive for every token are never read.
+ * Inf/NaN in the w_up / w_down_t rows of an active neuron propagate, as Inf or NaN, into
+ * the output of every token that activates it, and may reach the other tokens of a batch
+ * (the row is read for the union).  Rows of neurons inactive for every token are never
+ * read.
  */
 #ifndef FFN_SPARSE_H
 #define FFN_SPARSE_H

@@ -168,6 +168,66 @@ def test_inactive_rows_are_never_read(gu, shape):
     gu.check_parity(res, y, idx, act, t, wdt, what="poisoned")
 
 
+# Inf / NaN in the rows of an active neuron, on each dispatch path: the single-token kernels
+# (bf16 standard, fp32 LoPA), the 4x4x4 and 16x16 matrix-core batches (the latter with
+# pre-split tokens) and the element-wise batch kernels (d not a multiple of 8)
+NONFINITE_SHAPES = [(1, 4096, 1000, 0, BF16), (1, 256, 1024, 32, F32), (4, 1024, 2000, 0, BF16),
+                    (20, 512, 1500, 64, BF16), (3, 100, 700, 0, BF16)]
+
+
+@pytest.mark.parametrize("where", ["down_inf", "up_nan"])
+@pytest.mark.parametrize("shape", NONFINITE_SHAPES, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}")
+def test_nonfinite_rows_of_active_neurons(gu, shape, where):
+    """Non-finite values in a W_up / W_down^T row of a neuron that token 0 activates reach
+    token 0's output: +Inf at one W_down^T entry makes that column non-finite (sign(zval) x
+    Inf for one token), NaN across the W_up row makes the whole output row NaN.  A token that does not activate the
+    neuron gets the oracle's value or a non-finite one there (a batch reads the row for the
+    union); every other entry matches the oracle."""
+    T, d, d_ff, r, wdt = shape
+    inp = wl.make_inputs(107, T, d, d_ff, r=r, wdt=wdt)
+    t = 1.0
+    res = gu.run_oracle(inp, t)
+    near = (np.abs(res.h - t) < gu.BAND).any(0)
+    cand = np.flatnonzero(res.active[0] & ~near)
+    assert cand.size, "no active neuron clear of the band"
+    i, c = int(cand[cand.size // 2]), d // 3
+    # zval of neuron i for every token, from the oracle: W_down^T with row i all ones, the rest 0
+    ones = np.uint16(0x3F80) if wdt == BF16 else np.float32(1.0)
+    dz = np.zeros_like(inp.w_down_t)
+    dz[i] = ones
+    zval = gu.run_oracle(wl.FFNInputs(**{**inp.__dict__, "w_down_t": dz}), t).y[:, 0]
+    if where == "down_inf":
+        dn = inp.w_down_t.copy()
+        dn[i, c] = np.uint16(0x7F80) if wdt == BF16 else np.float32(np.inf)
+        pinp = wl.FFNInputs(**{**inp.__dict__, "w_down_t": dn})
+    else:
+        up = inp.w_up.copy()
+        up[i] = np.uint16(0x7FC0) if wdt == BF16 else np.float32(np.nan)
+        pinp = wl.FFNInputs(**{**inp.__dict__, "w_up": up})
+    y, idx, act, _ = gu.run_gpu(gu.DevInputs(pinp), t)
+    tol = gu.TOL[wdt]
+    on = res.active[:, i]
+    assert on[0]
+    for tau in range(T):
+        ref = np.asarray(res.y[tau], np.float64)
+        scale = float(np.max(np.abs(ref)))
+        row = np.asarray(y[tau], np.float64)
+        if where == "down_inf":
+            rest = np.arange(d) != c
+            if on[tau] and T == 1:  # fp32 products: zval x Inf
+                assert row[c] == np.sign(zval[tau]) * np.inf, f"token {tau}: column {c} is {row[c]}"
+            elif on[tau]:  # a batch may multiply Inf with zval's bf16 hi and lo parts: Inf or NaN
+                assert not np.isfinite(row[c]), f"token {tau}: column {c} is {row[c]}"
+            else:
+                assert not np.isfinite(row[c]) or abs(row[c] - ref[c]) <= tol * scale
+            assert np.isfinite(row[rest]).all(), f"token {tau}: non-finite outside column {c}"
+            assert np.max(np.abs(row[rest] - ref[rest])) <= tol * scale
+        elif on[tau]:
+            assert np.isnan(row).all(), f"token {tau}: {np.isfinite(row).sum()} finite entries"
+        else:
+            assert np.isnan(row).all() or np.max(np.abs(row - ref)) <= tol * scale
+
+
 @pytest.mark.parametrize("wdt", [F32, BF16])
 def test_worked_example_on_gpu(gu, wdt):
     """The hand-worked example of the oracle pins (exact arithmetic; neuron 0 sits on the threshold)."""
