@@ -2,7 +2,7 @@
 
 Every function takes torch device tensors, checks the dtypes, shapes and devices the
 C ABI cannot see (it receives bare pointers and sizes), and passes raw device pointers
-plus the current HIP stream to the C ABI.  All arithmetic runs in the gfx950 kernels of
+plus a HIP stream (by default the current stream of the tensors' device) to the C ABI.  All arithmetic runs in the gfx950 kernels of
 ``libffn_sparse.so``; there is no fallback: if the library is missing this module
 raises on first use.
 """
@@ -144,9 +144,13 @@ def _dev(t, what):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream):
+def _stream(stream, device):
+    """The HIP stream to enqueue on: `stream`, or the current stream of the tensors' device
+    (not of the current device, which may be another one)."""
     torch = _torch()
-    s = torch.cuda.current_stream() if stream is None else stream
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    if s.device != device:
+        raise ValueError(f"stream is on {s.device}, the tensors on {device}")
     return ctypes.c_void_p(s.cuda_stream)
 
 
@@ -216,7 +220,7 @@ def _std_call(name, x, w_gate, w_up, w_down_t, t, y, ws, stream, opt=()):
                 _same)
     rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, _dev(x, "x"), _dev(w_gate, "w_gate"),
                               _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t), *opt,
-                              _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+                              _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream, x.device))
     _check(name, rc)
     return y
 
@@ -229,7 +233,7 @@ def _lopa_call(name, x, lopa_a, lopa_b, w_up, w_down_t, t, y, ws, stream, opt=()
     rc = getattr(lib(), name)(weight_dtype(w_up), T, d, d_ff, r, _dev(x, "x"), _dev(lopa_a, "lopa_a"),
                               _dev(lopa_b, "lopa_b"), _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"),
                               ctypes.c_float(t), *opt, _dev(y, "y"), _dev(ws, "ws"),
-                              ws.numel() * ws.element_size(), _stream(stream))
+                              ws.numel() * ws.element_size(), _stream(stream, x.device))
     _check(name, rc)
     return y
 
@@ -252,7 +256,7 @@ def ffn_sparse_forward_noalloc(x, w_gate, w_up, w_down_t, t, y, stream=None):
                 _same)
     rc = lib().ffn_sparse_forward_noalloc(weight_dtype(w_up), T, d, d_ff, _dev(x, "x"), _dev(w_gate, "w_gate"),
                                           _dev(w_up, "w_up"), _dev(w_down_t, "w_down_t"), ctypes.c_float(t),
-                                          _dev(y, "y"), _stream(stream))
+                                          _dev(y, "y"), _stream(stream, x.device))
     _check("ffn_sparse_forward_noalloc", rc)
     return y
 
@@ -301,7 +305,7 @@ def _q_call(name, x, gate, lopa_a, w_up, w_down_t, sc, t, opt, y, ws, stream, r)
     ptrs = [_dev(x, "x")] + ([_dev(lopa_a, "lopa_a")] if r else []) + [_dev(gate, "gate"), _dev(w_up, "w_up"),
                                                                        _dev(w_down_t, "w_down_t")]
     rc = getattr(lib(), name)(*head, *ptrs, None if sc is None else ctypes.byref(sc), ctypes.c_float(t), _opt(opt),
-                              _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream))
+                              _dev(y, "y"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream, x.device))
     _check(name, rc)
     return y
 
@@ -331,7 +335,8 @@ def ffn_active_set(ws, T, d, d_ff, r=0, stream=None, with_act=True):
     idx = np.empty(d_ff, np.int32)
     act = np.empty((T, d_ff), np.float32) if with_act else None
     rc = lib().ffn_active_set(_dev(ws, "ws"), T, d, d_ff, r, ctypes.byref(n), idx.ctypes.data_as(ctypes.c_void_p),
-                              None if act is None else act.ctypes.data_as(ctypes.c_void_p), _stream(stream))
+                              None if act is None else act.ctypes.data_as(ctypes.c_void_p),
+                              _stream(stream, ws.device))
     _check("ffn_active_set", rc)
     k = n.value
     return idx[:k].copy(), (None if act is None else act[:, :k].copy())
@@ -390,7 +395,7 @@ def ffn_lopa_approx(w, r: int, max_iters: int = 20, stream=None):
     it, obj = ctypes.c_int(0), ctypes.c_double(0.0)
     rc = lib().ffn_lopa_approx(H, D, r, _dev(w, "w"), max_iters, _dev(g_idx, "g_idx"), _dev(g_sign, "g_sign"),
                                _dev(U, "lopa_b"), _dev(V, "lopa_a"), ctypes.byref(it), ctypes.byref(obj),
-                               _dev(ws, "ws"), n, _stream(stream))
+                               _dev(ws, "ws"), n, _stream(stream, w.device))
     _check("ffn_lopa_approx", rc)
     return g_idx, g_sign, U, V, it.value, obj.value
 
