@@ -168,6 +168,30 @@ def test_inactive_rows_are_never_read(gu, shape):
     gu.check_parity(res, y, idx, act, t, wdt, what="poisoned")
 
 
+# ---------------------------------------------------------------- degenerate shapes
+# d = 1, one neuron, r = 1 and the like: y rests on a handful of neurons, so it is checked
+# against the fp64 rebuild from the kernel's own activation values (gu.check_rebuilt), and the
+# active sets and activation values against the oracle as everywhere else.
+DEGENERATE = [(1, 1, 1, 0, F32, -1.0), (1, 1, 64, 0, BF16, 0.0), (5, 1, 300, 0, F32, 0.5),
+              (1, 64, 1, 0, BF16, -1.0), (3, 32, 1, 1, F32, 0.0), (4, 264, 5, 1, BF16, 0.0),
+              (64, 1, 100, 0, BF16, 0.0), (1, 8, 1000, 1, F32, 0.5), (16, 8, 64, 8, BF16, 0.0),
+              (1, 4096, 1, 0, BF16, -1.0), (2, 16, 1, 0, wl.I8, -1.0), (3, 2, 7, 2, wl.I4, 0.0),
+              (1, 1, 5000, 1, BF16, 1.2816), (33, 3, 7, 3, F32, 0.0)]
+
+
+@pytest.mark.parametrize("shape", DEGENERATE, ids=lambda s: f"T{s[0]}_d{s[1]}_dff{s[2]}_r{s[3]}_w{s[4]}_t{s[5]}")
+def test_degenerate_shapes(gu, shape):
+    T, d, d_ff, r, wdt, t = shape
+    inp = wl.make_inputs(108, T, d, d_ff, r=r, wdt=wdt)
+    dev = gu.DevInputs(inp)
+    y, idx, act, _ = gu.run_gpu_q(dev, t) if wdt in (wl.I8, wl.I4) else gu.run_gpu(dev, t)
+    res = gu.run_oracle(inp, t)
+    name = f"degenerate T{T} d{d} d_ff{d_ff} r{r}"
+    assert np.isfinite(y).all(), f"{name}: non-finite output"
+    gu.check_parity(res, y, idx, act, t, wdt, what=name, check_y=False)
+    gu.check_rebuilt(inp, y, idx, act, wdt, what=name)
+
+
 # Inf / NaN in the rows of an active neuron, on each dispatch path: the single-token kernels
 # (bf16 standard, fp32 LoPA), the 4x4x4 and 16x16 matrix-core batches (the latter with
 # pre-split tokens) and the element-wise batch kernels (d not a multiple of 8)

@@ -138,3 +138,26 @@ def test_nothing_active_needs_exact_zeros():
     tiny[1, 3] = 1e-30
     with pytest.raises(AssertionError):
         gu.check_parity(res, tiny, empty, np.zeros((2, 0), np.float32), 1e30, wl.F32, what="not zero")
+
+
+def test_rebuilt_rule_passes_oracle_activations_and_catches_a_missing_term():
+    """check_rebuilt: y formed from the oracle's own activations passes; dropping one listed
+    neuron's term, or moving one column by 1e-3 of its value, fails."""
+    inp = wl.make_inputs(614, 2, 48, 40, wdt=wl.F32)
+    res = gu.run_oracle(inp, 0.5)
+    idx = np.flatnonzero(res.active.any(0)).astype(np.int32)
+    act = np.where(res.active[:, idx], res.h[:, idx] - np.float64(np.float32(0.5)), 0.0).astype(np.float32)
+    y = res.y.astype(np.float32)
+    gu.check_rebuilt(inp, y, idx, act, wl.F32, what="exact")
+    wu = gu.decode_rows(inp.w_up, wl.F32)[idx]
+    wd = gu.decode_rows(inp.w_down_t, wl.F32)[idx]
+    k = int(np.flatnonzero(act[0])[0])
+    missing = y.copy()
+    missing[0] -= np.float32(act[0, k] * (inp.x[0].astype(np.float64) @ wu[k])) * wd[k].astype(np.float32)
+    with pytest.raises(AssertionError, match="token 0"):
+        gu.check_rebuilt(inp, missing, idx, act, wl.F32, what="missing term")
+    col = y.copy()
+    j = int(np.argmax(np.abs(y[1])))
+    col[1, j] *= np.float32(1.001)
+    with pytest.raises(AssertionError, match="token 1"):
+        gu.check_rebuilt(inp, col, idx, act, wl.F32, what="one column")
