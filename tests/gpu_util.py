@@ -231,7 +231,7 @@ def decode_rows(w, wdt, scale=None) -> np.ndarray:
 EPS32 = 2.0 ** -24
 
 
-def check_rebuilt(inp: wl.FFNInputs, y, idx, act, wdt, what=""):
+def check_rebuilt(inp: wl.FFNInputs, y, idx, act, wdt, what="", silu_up=False):
     """Outputs of shapes whose y rests on a few neurons (a fixed relative bound does not hold
     there: one activation just past the band, or a cancelling dot, carries its rounding into y).
     y must match, column by column, the fp64 sum over the listed neurons of the kernel's own
@@ -240,7 +240,9 @@ def check_rebuilt(inp: wl.FFNInputs, y, idx, act, wdt, what=""):
     reduction level on the sums of the terms' magnitudes), of the token operands' bf16 hi / lo
     split in the matrix-core batch kernels (2^-16 of each element; bf16 weights and codes), and
     of the 24-bit fixed-point copy of x in the single-token integer dot products (codes).  The
-    activation values themselves are checked against the oracle by check_parity (check_y=False)."""
+    activation values themselves are checked against the oracle by check_parity (check_y=False).
+    silu_up: the full form's SiLU on the W_up output (its slope stays within 1.1, so the same
+    allowance serves)."""
     T = y.shape[0]
     tol = TOL[wdt]
     sc = inp.scales or {}
@@ -260,6 +262,10 @@ def check_rebuilt(inp: wl.FFNInputs, y, idx, act, wdt, what=""):
         vmag_q = np.zeros_like(v)
     levels_up = np.ceil(x.shape[1] / 64) + 8
     levels_dn = np.ceil(len(idx) / 64) + 8
+    if silu_up:
+        v = v / (1.0 + np.exp(-v))
+        vmag = 1.1 * vmag
+        vmag_q = 1.1 * vmag_q
     ref = (np.asarray(act, np.float64) * v) @ wd
     mag = np.abs(a * v) @ np.abs(wd)
     mag_v = (a * vmag) @ np.abs(wd)
