@@ -168,6 +168,43 @@ def test_inactive_rows_are_never_read(gu, shape):
     gu.check_parity(res, y, idx, act, t, wdt, what="poisoned")
 
 
+# ---------------------------------------------------------------- one workspace, many shapes
+# The header lets one workspace (zero-filled once, large enough) serve every later call: each
+# call leaves it ready for the next, whatever the next one's shape.  The layout moves with the
+# shape, so the regions of one call lie over other regions of the next; the single-token LoPA
+# calls' tagged z words must still never read as published when they are not.
+SHARED_WS = [(1, 1024, 3000, 512, BF16), (1, 1024, 3000, 0, BF16), (4, 1024, 3000, 512, BF16),
+             (1, 1024, 3000, 256, BF16), (20, 1024, 3000, 0, BF16), (1, 1024, 3000, 1024, BF16),
+             (1, 264, 1000, 40, F32), (70, 264, 1000, 40, BF16), (1, 1024, 3000, 512, wl.I8),
+             (8, 1024, 3000, 512, BF16), (1, 1024, 3000, 512, BF16)]
+
+
+def test_workspace_shared_across_shapes(gu):
+    import torch
+    from paper_2609_31975_amd import ffn
+    t = 1.2816
+    cases = [(shape, wl.make_inputs(120 + k, *shape[:3], r=shape[3], wdt=shape[4])) for k, shape in enumerate(SHARED_WS)]
+    nbytes = max(ffn.workspace_bytes(T, d, d_ff, r) for (T, d, d_ff, r, _), _ in cases)
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    devs = [gu.DevInputs(inp) for _, inp in cases]
+    refs = [gu.run_oracle(inp, t) for _, inp in cases]
+    for rnd in range(2):
+        for k, ((T, d, d_ff, r, wdt), inp) in enumerate(cases):
+            dv = devs[k]
+            y = torch.full((T, d), float("nan"), dtype=torch.float32, device="cuda")
+            if wdt == wl.I8:
+                sc = dv.scales_struct()
+                ffn.ffn_lopa_sparse_forward_q(dv.x, dv.lopa_a, dv.lopa_b, dv.w_up, dv.w_down_t, sc, t, None, y, ws)
+            elif r:
+                ffn.ffn_lopa_sparse_forward(dv.x, dv.lopa_a, dv.lopa_b, dv.w_up, dv.w_down_t, t, y, ws)
+            else:
+                ffn.ffn_sparse_forward(dv.x, dv.w_gate, dv.w_up, dv.w_down_t, t, y, ws)
+            torch.cuda.synchronize()
+            idx, act = ffn.ffn_active_set(ws, T, d, d_ff, r) if T <= 64 else (None, None)
+            gu.check_parity(refs[k], y.cpu().numpy(), idx, act, t, wdt,
+                            what=f"shared workspace, round {rnd}, call {k} (T{T} d{d} d_ff{d_ff} r{r})")
+
+
 # ---------------------------------------------------------------- degenerate shapes
 # d = 1, one neuron, r = 1 and the like: y rests on a handful of neurons, so it is checked
 # against the fp64 rebuild from the kernel's own activation values (gu.check_rebuilt), and the
