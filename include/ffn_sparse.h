@@ -227,7 +227,9 @@ int ffn_lopa_dense_forward_q(ffn_dtype_t wdt, int T, int d, int d_ff, int r, con
  *   act_host        [T][d_ff] fp32 (may be NULL): act_host[tau][k] = the activation value
  *                   (h - t for the default form) of neuron idx_host[k] for token tau, or 0
  *                   where that token is inactive
- * For a dense call every neuron is listed.  Returns FFN_OK or an error code. */
+ * For a dense call every neuron is listed.  T is at most 64: a larger call runs as passes of
+ * 64 tokens, and the workspace keeps the lists of its last pass only (FFN_ERR_SHAPE).
+ * Returns FFN_OK or an error code. */
 int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_union, int32_t* idx_host,
                    float* act_host, hipStream_t stream);
 
@@ -247,8 +249,8 @@ int ffn_active_set(const void* ws, int T, int d, int d_ff, int r, int32_t* n_uni
  *               segment w for token tau (h - t for the default form), 0 where that token is
  *               inactive
  * Slots past a segment's count hold stale data.  For a dense call every row is listed.
- * Arguments (ws, T, d, d_ff, r) must be those of the forward call.  Returns FFN_OK, FFN_ERR_NULL
- * or FFN_ERR_SHAPE. */
+ * Arguments (ws, T, d, d_ff, r) must be those of the forward call, T at most 64 (as for
+ * ffn_active_set).  Returns FFN_OK, FFN_ERR_NULL or FFN_ERR_SHAPE. */
 int ffn_workspace_active(const void* ws, int T, int d, int d_ff, int r, const int32_t** meta,
                          const int32_t** seg_count, const int32_t** idx, const float** act);
 
